@@ -1,0 +1,10 @@
+"""Float64 CPU oracle for the H2O chunk step.
+
+TEST INFRASTRUCTURE ONLY: imported by ``tests/``, ``__graft_entry__.smoke()``
+and the ``cpu_baseline`` leg of ``bench.py``, never by the library.
+"""
+from .h2o_oracle import (accumulate_scores, bottomk, decode, evict_insert,
+                         h2o_step, rel_err, sdpa_chunk, visible)
+
+__all__ = ["accumulate_scores", "bottomk", "decode", "evict_insert",
+           "h2o_step", "rel_err", "sdpa_chunk", "visible"]

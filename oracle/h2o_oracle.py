@@ -1,0 +1,214 @@
+"""Float64 CPU oracle for the H2O chunk step.
+
+TEST INFRASTRUCTURE ONLY. Only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` may import this module. The HIP library
+never calls it and shares no code with it.
+
+What it computes is the plain definition of each step, one attention head at a
+time, with numpy float64 matrix products as the only library primitive:
+
+1. SDPA of the chunk's T queries against [cache keys || chunk keys]
+   (Sec. "Sparse Attention. Key-Value Caching", Eq. main-sdpa and
+   Eq. main-sdpa-comp): ``A = d^-1/2 Q K^T`` masked, ``M = softmax(A)`` along
+   keys, ``Y = M V``. Every cache token precedes the chunk, so a query sees all
+   cache slots; chunk key t is visible to chunk query i iff t <= i (the causal
+   rule of Sec. "Discussion: SDPA Kernels for Sparse Attention").
+2. The log-sum-exp of each query row, lambda = log(exp(A) 1)
+   (Sec. "FlashAttention for Summed Attention Weights").
+3. Summed attention weights sum_i m_{i,j} per key (Sec. "Variants of
+   Heavy-Hitter Oracle", the H2O score increment; Sec. "Computing Summed
+   Attention Weights in SDPA"), additionally summed over the q_g query heads
+   that share one KV head (GQA, Sec. "Sparse Attention. Key-Value Caching"),
+   because the score and the eviction are per KV head.
+4. Score accumulation phi <- phi + sum_i m_{i,j} (Eq. h2o-score as a running
+   sum over chunks), held in float32 storage: one IEEE float32 addition.
+5. Eviction: per (b, kv-head), the k slots with the smallest score
+   (Sec. "Variants of Heavy-Hitter Oracle"), ties broken by the lower slot
+   index, returned in ascending slot order.
+6. Insert: scatter of the chunk's keys/values into the evicted slots along the
+   slot axis (Sec. "Fine-Tuning for Sparse Attention", the linear recurrence;
+   Sec. "Buffer Read/Write Access by torch.scatter, torch.gather"); new key i
+   goes to the i-th smallest evicted slot, its score starts at its own summed
+   weight from this chunk, its token position is pos0 + i.
+
+Readings of points the paper leaves open are listed in the repository's design
+notes; the ones that change results are repeated at the functions below.
+"""
+from __future__ import annotations
+
+from typing import Iterable, Optional, Sequence, Tuple
+
+import numpy as np
+
+F64 = np.float64
+
+
+# ----------------------------------------------------------------- step 1: mask
+def visible(M: int, T: int) -> np.ndarray:
+    """Boolean [T, M+T]: may chunk query i attend key column j?
+
+    Columns j < M are cache slots (all tokens precede the chunk: always
+    visible). Column M+t is chunk key t, visible iff t <= i: the mask
+    -inf * 1{P + i < t(j)} with t(j) = P + t.
+    """
+    i = np.arange(T)[:, None]
+    j = np.arange(M + T)[None, :]
+    return (j < M) | ((j - M) <= i)
+
+
+# --------------------------------------------------------- steps 1-3 per head
+def _head(Qh: np.ndarray, K: np.ndarray, V: np.ndarray, allowed: np.ndarray,
+          scale: float) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """One query head: returns (Y [T,d], lambda [T], column sums [M+T])."""
+    A = scale * (Qh @ K.T)                         # d^-1/2 Q K^T
+    A = np.where(allowed, A, -np.inf)              # mask
+    amax = A.max(axis=1, keepdims=True)            # finite: every row sees the cache
+    lam = amax[:, 0] + np.log(np.exp(A - amax).sum(axis=1))
+    Mw = np.exp(A - lam[:, None])                  # softmax rows; masked -> 0
+    Y = Mw @ V
+    return Y, lam, Mw.sum(axis=0)
+
+
+def sdpa_chunk(q, k_cache, v_cache, k_new, v_new, scale: Optional[float] = None,
+               heads: Optional[Iterable[Tuple[int, int]]] = None):
+    """Attention of the chunk over [cache || chunk] with summed weights.
+
+    Shapes: q [B,Hq,T,d]; k_cache, v_cache [B,Hkv,M,d]; k_new, v_new [B,Hkv,T,d].
+    Query head hq uses KV head hq // (Hq/Hkv).
+
+    Returns float64 (out [B,Hq,T,d], lse [B,Hq,T], wsum [B,Hkv,M+T]) where
+    ``wsum[b,h,j] = sum over the group's query heads g and queries i of
+    m^{(g)}_{i,j}``. With ``heads`` (a list of (b, kv-head)) only those heads
+    are computed; the other entries are NaN.
+    """
+    q = np.asarray(q)
+    B, Hq, T, d = q.shape
+    Hkv, M = k_cache.shape[1], k_cache.shape[2]
+    if Hq % Hkv:
+        raise ValueError("Hq must be a multiple of Hkv")
+    G = Hq // Hkv
+    if scale is None:
+        scale = 1.0 / np.sqrt(d)
+    scale = float(scale)
+    allowed = visible(M, T)
+    out = np.full((B, Hq, T, d), np.nan, F64)
+    lse = np.full((B, Hq, T), np.nan, F64)
+    wsum = np.full((B, Hkv, M + T), np.nan, F64)
+    if heads is None:
+        heads = [(b, h) for b in range(B) for h in range(Hkv)]
+    for b, h in heads:
+        K = np.concatenate([k_cache[b, h], k_new[b, h]]).astype(F64)
+        V = np.concatenate([v_cache[b, h], v_new[b, h]]).astype(F64)
+        acc = np.zeros(M + T, F64)
+        for g in range(G):
+            hq = h * G + g
+            Y, lam, col = _head(q[b, hq].astype(F64), K, V, allowed, scale)
+            out[b, hq] = Y
+            lse[b, hq] = lam
+            acc += col
+        wsum[b, h] = acc
+    return out, lse, wsum
+
+
+# ------------------------------------------------------------ step 4: scores
+def accumulate_scores(scores, wsum) -> np.ndarray:
+    """phi <- phi + summed weights of this chunk, for the M cache slots.
+
+    Scores are stored in float32 and the update is one IEEE float32 addition
+    of the stored score and the float32 value of the summed weight.
+    """
+    scores = np.asarray(scores, np.float32)
+    M = scores.shape[-1]
+    return scores + np.asarray(wsum)[..., :M].astype(np.float32)
+
+
+# ---------------------------------------------------------- step 5: eviction
+def bottomk(scores, k: int) -> np.ndarray:
+    """Indices of the k smallest scores per row (last axis), ascending slots.
+
+    Order is lexicographic on (score, slot): at equal scores the lower slot is
+    evicted first. -0.0 and +0.0 compare equal. Scores must not be NaN.
+    """
+    s = np.asarray(scores, np.float32)
+    lead, M = s.shape[:-1], s.shape[-1]
+    if not 0 <= k <= M:
+        raise ValueError("need 0 <= k <= M")
+    flat = s.reshape(-1, M)
+    res = np.empty((flat.shape[0], k), np.int32)
+    slots = np.arange(M)
+    for r in range(flat.shape[0]):
+        row = flat[r].astype(F64) + 0.0                  # -0.0 -> +0.0
+        order = np.lexsort((slots, row))                 # primary key: score
+        res[r] = np.sort(order[:k])
+    return res.reshape(*lead, k)
+
+
+# ------------------------------------------------------------ step 6: insert
+def evict_insert(k_cache, v_cache, scores, token_pos, k_new, v_new, wsum,
+                 k: int, pos0: int):
+    """Evict the k lowest-score slots per (b, kv-head) and insert the chunk.
+
+    ``scores`` are the accumulated float32 scores. Returns new copies
+    (k_cache, v_cache, scores, token_pos, evict_idx); token_pos may be None.
+    """
+    T = k_new.shape[2]
+    if k != T:
+        raise ValueError("every chunk key is inserted: k must equal T")
+    idx = bottomk(scores, k)
+    kc, vc = k_cache.copy(), v_cache.copy()
+    sc = np.asarray(scores, np.float32).copy()
+    tp = None if token_pos is None else token_pos.copy()
+    M = sc.shape[-1]
+    B, H = sc.shape[0], sc.shape[1]
+    newsc = np.asarray(wsum)[..., M:M + T].astype(np.float32)
+    for b in range(B):
+        for h in range(H):
+            e = idx[b, h]
+            kc[b, h, e] = k_new[b, h, :k]
+            vc[b, h, e] = v_new[b, h, :k]
+            sc[b, h, e] = newsc[b, h, :k]
+            if tp is not None:
+                tp[b, h, e] = pos0 + np.arange(k, dtype=np.int32)
+    return kc, vc, sc, tp, idx
+
+
+# --------------------------------------------------------------- whole step
+def h2o_step(k_cache, v_cache, scores, token_pos, q, k_new, v_new, pos0: int,
+             scale: Optional[float] = None):
+    """One chunk step: attend, accumulate, evict, insert.
+
+    Returns dict with out, lse, wsum (float64), scores_acc (float32 scores after
+    accumulation), evict_idx and the new cache state.
+    """
+    out, lse, wsum = sdpa_chunk(q, k_cache, v_cache, k_new, v_new, scale)
+    acc = accumulate_scores(scores, wsum)
+    T = q.shape[2]
+    kc, vc, sc, tp, idx = evict_insert(k_cache, v_cache, acc, token_pos,
+                                       k_new, v_new, wsum, T, pos0)
+    return dict(out=out, lse=lse, wsum=wsum, scores_acc=acc, evict_idx=idx,
+                k_cache=kc, v_cache=vc, scores=sc, token_pos=tp)
+
+
+def decode(k_cache, v_cache, scores, token_pos, q_steps, k_new_steps,
+           v_new_steps, pos0: int, scale: Optional[float] = None):
+    """Token generation: ``len(q_steps)`` chunk steps of length T (usually 1),
+    positions pos0, pos0+T, ... Returns the list of per-step results."""
+    res = []
+    state = (k_cache, v_cache, scores, token_pos)
+    for s in range(len(q_steps)):
+        T = q_steps[s].shape[2]
+        r = h2o_step(*state, q_steps[s], k_new_steps[s], v_new_steps[s],
+                     pos0 + s * T, scale)
+        res.append(r)
+        state = (r["k_cache"], r["v_cache"], r["scores"], r["token_pos"])
+    return res
+
+
+# ------------------------------------------------------------------ metrics
+def rel_err(x, ref, axes: Sequence[int]) -> float:
+    """Max over slices of ||x - ref||_2 / ||ref||_2, the norm taken over `axes`."""
+    x = np.asarray(x, F64)
+    ref = np.asarray(ref, F64)
+    num = np.sqrt(((x - ref) ** 2).sum(axis=tuple(axes)))
+    den = np.sqrt((ref ** 2).sum(axis=tuple(axes)))
+    return float((num / np.maximum(den, np.finfo(F64).tiny)).max())

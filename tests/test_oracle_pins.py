@@ -1,0 +1,381 @@
+"""Pins of the float64 oracle against computations that are not the oracle.
+
+CPU only. Each pin is a different route to the same numbers (brute force,
+torch's SDPA, the paper's two alternative summed-weight algorithms), a closed
+form, or an invariant the mathematics fixes. ``test_planted_mistakes`` shows
+that plausible mistakes in the oracle are caught by at least one pin.
+"""
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import h2o_oracle as O
+from paper_2608_19920_amd import workloads as W
+import _pins as P
+
+TINY = [  # B, Hq, Hkv, d, M, T
+    (1, 1, 1, 4, 3, 1),
+    (1, 2, 1, 8, 5, 3),
+    (2, 4, 2, 4, 7, 4),
+    (1, 3, 1, 6, 0, 4),      # no cache slots: plain causal attention
+    (1, 2, 2, 5, 16, 2),
+]
+
+
+def _inputs(B, Hq, Hkv, d, M, T, seed=0, dtype="f32", heavy=0.0):
+    w = W.custom(B=B, Hq=Hq, Hkv=Hkv, d=d, M=M, T=T, dtype=dtype, heavy_frac=heavy)
+    return W.make_inputs(w, seed)
+
+
+def _args(x):
+    return x["q"], x["k_cache"], x["v_cache"], x["k_new"], x["v_new"]
+
+
+# --------------------------------------------------------------- attention
+@pytest.mark.parametrize("shape", TINY)
+def test_brute_force(shape):
+    x = _inputs(*shape, seed=sum(shape))
+    o, l, w = oracle.sdpa_chunk(*_args(x), x["scale"])
+    bo, bl, bw = P.brute_sdpa(*_args(x), x["scale"])
+    np.testing.assert_allclose(o, bo, rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(l, bl, rtol=1e-13, atol=1e-13)
+    np.testing.assert_allclose(w, bw, rtol=1e-12, atol=1e-13)
+
+
+def test_brute_force_bf16_heavy_hitters():
+    x = _inputs(1, 4, 2, 8, 12, 3, seed=7, dtype="bf16", heavy=0.25)
+    o, l, w = oracle.sdpa_chunk(*_args(x), x["scale"])
+    bo, bl, bw = P.brute_sdpa(*_args(x), x["scale"])
+    np.testing.assert_allclose(o, bo, rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(l, bl, rtol=1e-13)
+    np.testing.assert_allclose(w, bw, rtol=1e-12, atol=1e-13)
+
+
+@pytest.mark.parametrize("shape", [(2, 6, 2, 16, 40, 9), (1, 7, 1, 32, 70, 33),
+                                   (1, 4, 4, 64, 130, 17)])
+def test_torch_sdpa(shape):
+    x = _inputs(*shape, seed=3, dtype="bf16", heavy=0.05)
+    o, l, _ = oracle.sdpa_chunk(*_args(x), x["scale"])
+    to, tl = P.torch_sdpa(*_args(x), x["scale"])
+    np.testing.assert_allclose(o, to, rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(l, tl, rtol=1e-13)
+
+
+def test_special_case_no_cache_is_causal_attention():
+    x = _inputs(1, 2, 1, 16, 0, 11, seed=5)
+    o, _, _ = oracle.sdpa_chunk(*_args(x), x["scale"])
+    F = torch.nn.functional
+    K = torch.from_numpy(x["k_new"][0, 0].astype(np.float64))
+    V = torch.from_numpy(x["v_new"][0, 0].astype(np.float64))
+    for g in range(2):
+        Q = torch.from_numpy(x["q"][0, g].astype(np.float64))
+        ref = F.scaled_dot_product_attention(Q[None], K[None], V[None], is_causal=True,
+                                             scale=float(x["scale"]))[0]
+        np.testing.assert_allclose(o[0, g], ref.numpy(), rtol=1e-12, atol=1e-13)
+
+
+def test_special_case_single_query_is_unmasked_attention():
+    x = _inputs(1, 4, 2, 16, 50, 1, seed=6)
+    o, _, _ = oracle.sdpa_chunk(*_args(x), x["scale"])
+    F = torch.nn.functional
+    for hq in range(4):
+        h = hq // 2
+        K = torch.from_numpy(np.concatenate([x["k_cache"][0, h], x["k_new"][0, h]]).astype(np.float64))
+        V = torch.from_numpy(np.concatenate([x["v_cache"][0, h], x["v_new"][0, h]]).astype(np.float64))
+        Q = torch.from_numpy(x["q"][0, hq].astype(np.float64))
+        ref = F.scaled_dot_product_attention(Q[None], K[None], V[None], scale=float(x["scale"]))[0]
+        np.testing.assert_allclose(o[0, hq], ref.numpy(), rtol=1e-12, atol=1e-13)
+
+
+@pytest.mark.parametrize("G,M,T", [(1, 10, 4), (3, 37, 9), (7, 5, 5)])
+def test_closed_form_zero_keys(G, M, T):
+    x = _inputs(1, 2 * G, 2, 8, M, T, seed=11)
+    kc = np.zeros_like(x["k_cache"])
+    kn = np.zeros_like(x["k_new"])
+    o, l, w = oracle.sdpa_chunk(x["q"], kc, x["v_cache"], kn, x["v_new"], x["scale"])
+    for h in range(2):
+        V = np.concatenate([x["v_cache"][0, h], x["v_new"][0, h]]).astype(np.float64)
+        for i in range(T):
+            for g in range(G):
+                np.testing.assert_allclose(o[0, h * G + g, i], V[:M + i + 1].mean(axis=0),
+                                           rtol=1e-12, atol=1e-13)
+                assert abs(l[0, h * G + g, i] - np.log(M + i + 1)) < 1e-13
+        inv = np.array([1.0 / (M + i + 1) for i in range(T)])
+        np.testing.assert_allclose(w[0, h, :M], G * inv.sum(), rtol=1e-13)
+        for t in range(T):
+            np.testing.assert_allclose(w[0, h, M + t], G * inv[t:].sum(), rtol=1e-13)
+
+
+@pytest.mark.parametrize("shape", [(2, 8, 2, 16, 64, 16), (1, 7, 1, 32, 33, 20)])
+def test_invariants(shape):
+    B, Hq, Hkv, d, M, T = shape
+    G = Hq // Hkv
+    x = _inputs(*shape, seed=12, dtype="bf16", heavy=0.1)
+    o, l, w = oracle.sdpa_chunk(*_args(x), x["scale"])
+    # every query row's weights sum to one  =>  per KV head, sum_j w = T*G
+    np.testing.assert_allclose(w.sum(axis=-1), T * G, rtol=1e-13)
+    assert (w >= 0).all()
+    assert (w[..., :M] <= G * T * (1 + 1e-13)).all()
+    for t in range(T):                    # chunk key t is seen by queries t..T-1
+        assert (w[..., M + t] <= G * (T - t) * (1 + 1e-13)).all()
+    assert np.isfinite(o).all() and np.isfinite(l).all()
+
+
+@pytest.mark.parametrize("rt,ct", [(1, 1), (2, 3), (3, 7), (5, 64), (64, 5)])
+def test_mapreduce_algorithm(rt, ct):
+    x = _inputs(1, 4, 2, 8, 23, 6, seed=13, dtype="bf16", heavy=0.1)
+    o, _, w = oracle.sdpa_chunk(*_args(x), x["scale"])
+    mo, mw = P.mapreduce_wsum(*_args(x), x["scale"], rt, ct)
+    np.testing.assert_allclose(mw, w, rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(mo, o, rtol=1e-12, atol=1e-13)
+
+
+@pytest.mark.parametrize("shape", [(1, 4, 2, 8, 23, 6), (2, 3, 1, 16, 50, 12)])
+def test_transposed_identity(shape):
+    x = _inputs(*shape, seed=14, dtype="bf16", heavy=0.1)
+    _, _, w = oracle.sdpa_chunk(*_args(x), x["scale"])
+    tw = P.transposed_wsum(*_args(x), x["scale"])
+    np.testing.assert_allclose(tw, w, rtol=1e-11, atol=1e-12)
+
+
+def test_cache_slot_permutation():
+    x = _inputs(1, 4, 2, 16, 31, 7, seed=15, dtype="bf16", heavy=0.1)
+    o, l, w = oracle.sdpa_chunk(*_args(x), x["scale"])
+    perm = np.random.default_rng(0).permutation(31)
+    o2, l2, w2 = oracle.sdpa_chunk(x["q"], x["k_cache"][:, :, perm], x["v_cache"][:, :, perm],
+                                   x["k_new"], x["v_new"], x["scale"])
+    np.testing.assert_allclose(o2, o, rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(l2, l, rtol=1e-13)
+    np.testing.assert_allclose(w2[..., :31], w[..., perm], rtol=1e-12, atol=1e-14)
+    np.testing.assert_allclose(w2[..., 31:], w[..., 31:], rtol=1e-12, atol=1e-14)
+
+
+def test_gqa_equals_sum_of_replicated_heads():
+    """Group of G query heads on one KV head == G separate heads (G=1) whose
+    KV head is a copy, summed: pins the contiguous hq // G mapping and the
+    group sum of the per-head (B, Hq, N_k) arrays."""
+    G, Hkv = 3, 2
+    x = _inputs(2, G * Hkv, Hkv, 8, 19, 5, seed=16)
+    o, l, w = oracle.sdpa_chunk(*_args(x), x["scale"])
+    rep = lambda a: np.repeat(a, G, axis=1)           # KV head h -> q heads hG..hG+G-1
+    o1, l1, w1 = oracle.sdpa_chunk(x["q"], rep(x["k_cache"]), rep(x["v_cache"]),
+                                   rep(x["k_new"]), rep(x["v_new"]), x["scale"])
+    np.testing.assert_allclose(o1, o, rtol=1e-13, atol=1e-14)
+    np.testing.assert_allclose(w1.reshape(2, Hkv, G, -1).sum(axis=2), w, rtol=1e-13)
+    bo, bl, bw = P.brute_sdpa(x["q"][:1, :G], x["k_cache"][:1, :1], x["v_cache"][:1, :1],
+                              x["k_new"][:1, :1], x["v_new"][:1, :1], x["scale"])
+    np.testing.assert_allclose(w[:1, :1], bw, rtol=1e-12)
+
+
+# ---------------------------------------------------------------- scores
+def _f32_round_exact(fr: Fraction) -> np.float32:
+    """Round an exact rational to float32, nearest with ties to even."""
+    c = np.float32(float(fr))
+    cands = {c, np.nextafter(c, np.float32(np.inf)), np.nextafter(c, np.float32(-np.inf))}
+    best = min(cands, key=lambda v: (abs(Fraction(float(v)) - fr),
+                                     int(np.array(v).view(np.uint32)) & 1))
+    return np.float32(best)
+
+
+def test_accumulate_is_one_float32_rounding():
+    rng = np.random.default_rng(1)
+    s = rng.standard_exponential((3, 2, 200)).astype(np.float32)
+    s[0, 0, :5] = [0.0, 1e-30, 3.0e38, 1.0, 2 ** -20]
+    w = rng.standard_exponential((3, 2, 210)) * 10 ** rng.uniform(-8, 3, (3, 2, 210))
+    w = w.astype(np.float32)
+    acc = oracle.accumulate_scores(s, w)
+    assert acc.dtype == np.float32 and acc.shape == s.shape
+    for idx in np.ndindex(s.shape):
+        exact = Fraction(float(s[idx])) + Fraction(float(w[idx[:-1] + (idx[-1],)]))
+        assert acc[idx] == _f32_round_exact(exact), idx
+
+
+@pytest.mark.parametrize("M,k,quant", [(50, 7, None), (300, 64, None), (300, 64, 4),
+                                       (33, 1, None), (33, 1, 1), (40, 40, 2), (40, 0, None),
+                                       (1000, 999, 3)])
+def test_bottomk_brute_force(M, k, quant):
+    rng = np.random.default_rng(M + k)
+    s = rng.standard_exponential((3, 4, M)).astype(np.float32)
+    if quant is not None:                       # many exact ties: multiples of 2^-quant
+        s = (np.floor(s * 2 ** quant) / 2 ** quant).astype(np.float32)
+    e = oracle.bottomk(s, k)
+    np.testing.assert_array_equal(e, P.brute_bottomk(s, k))
+    for r in np.ndindex(s.shape[:-1]):
+        sel = e[r]
+        assert len(set(sel.tolist())) == k and (np.diff(sel) > 0).all()
+        if 0 < k < M:
+            rest = np.setdiff1d(np.arange(M), sel)
+            assert s[r][sel].max() <= s[r][rest].min()
+            tau = s[r][sel].max()                   # ties at the threshold: lower slots first
+            if (s[r][rest] == tau).any():
+                assert sel[s[r][sel] == tau].max() < rest[s[r][rest] == tau].min()
+
+
+def test_bottomk_signed_zero_is_a_tie():
+    s = np.array([[1.0, -0.0, 0.0, 2.0, -0.0]], np.float32)
+    np.testing.assert_array_equal(oracle.bottomk(s, 2), [[1, 2]])
+    np.testing.assert_array_equal(oracle.bottomk(s, 3), [[1, 2, 4]])
+
+
+# ---------------------------------------------------------------- insert
+def _scatter_torch(buf, idx, src):
+    """buf.scatter(2, index broadcast along d, src) as stated for the cache buffers."""
+    t = torch.from_numpy(buf.copy())
+    ix = torch.from_numpy(idx.astype(np.int64))
+    if t.dim() == 4:
+        ix = ix.unsqueeze(-1).expand(-1, -1, -1, t.shape[-1])
+    return t.scatter(2, ix, torch.from_numpy(src.copy())).numpy()
+
+
+def _gather_torch(buf, idx):
+    t = torch.from_numpy(buf.copy())
+    ix = torch.from_numpy(idx.astype(np.int64))
+    if t.dim() == 4:
+        ix = ix.unsqueeze(-1).expand(-1, -1, -1, t.shape[-1])
+    return t.gather(2, ix).numpy()
+
+
+def test_insert_is_scatter_and_round_trips():
+    x = _inputs(2, 4, 2, 8, 40, 9, seed=21, dtype="bf16")
+    out, lse, w = oracle.sdpa_chunk(*_args(x), x["scale"])
+    acc = oracle.accumulate_scores(x["scores"], w)
+    kc, vc, sc, tp, e = oracle.evict_insert(x["k_cache"], x["v_cache"], acc, x["token_pos"],
+                                            x["k_new"], x["v_new"], w, 9, int(x["pos0"]))
+    np.testing.assert_array_equal(e, P.brute_bottomk(acc, 9))
+    np.testing.assert_array_equal(kc, _scatter_torch(x["k_cache"], e, x["k_new"]))
+    np.testing.assert_array_equal(vc, _scatter_torch(x["v_cache"], e, x["v_new"]))
+    # inverse recurrence: keys = scatter(keys', index, gather(keys, index))
+    delta = _gather_torch(x["k_cache"], e)
+    np.testing.assert_array_equal(_scatter_torch(kc, e, delta), x["k_cache"])
+    # untouched slots keep their accumulated score; inserted ones start at w[M+i]
+    newsc = w[..., 40:].astype(np.float32)
+    np.testing.assert_array_equal(sc, _scatter_torch(acc, e, newsc))
+    np.testing.assert_array_equal(
+        tp, _scatter_torch(x["token_pos"], e,
+                           np.broadcast_to(int(x["pos0"]) + np.arange(9, dtype=np.int32),
+                                           (2, 2, 9)).copy()))
+    lhs = sc.astype(np.float64).sum(axis=-1)
+    rhs = (acc.astype(np.float64).sum(axis=-1)
+           - np.take_along_axis(acc, e, -1).astype(np.float64).sum(axis=-1)
+           + newsc.astype(np.float64).sum(axis=-1))
+    np.testing.assert_allclose(lhs, rhs, rtol=1e-12)
+
+
+def test_insert_requires_k_equal_T():
+    x = _inputs(1, 2, 1, 4, 10, 3, seed=1)
+    _, _, w = oracle.sdpa_chunk(*_args(x), x["scale"])
+    with pytest.raises(ValueError):
+        oracle.evict_insert(x["k_cache"], x["v_cache"], x["scores"], None,
+                            x["k_new"], x["v_new"], w, 2, 10)
+
+
+def test_decode_trajectory_runs_step_by_step():
+    w = W.custom(B=1, Hq=4, Hkv=2, d=8, M=12, T=1, dtype="bf16", heavy_frac=0.1, steps=4)
+    x = W.make_inputs(w, 2)
+    res = oracle.decode(x["k_cache"], x["v_cache"], x["scores"], x["token_pos"],
+                        x["q_steps"], x["k_new_steps"], x["v_new_steps"], int(x["pos0"]),
+                        x["scale"])
+    assert len(res) == 4
+    for s, r in enumerate(res):
+        np.testing.assert_allclose(r["wsum"].sum(-1), 2.0, rtol=1e-13)   # T*G = 1*2
+        for b, h in np.ndindex(1, 2):
+            slot = r["evict_idx"][b, h, 0]
+            assert r["token_pos"][b, h, slot] == int(x["pos0"]) + s
+            np.testing.assert_array_equal(r["k_cache"][b, h, slot], x["k_new_steps"][s, b, h, 0])
+
+
+# ------------------------------------------------------- planted mistakes
+def _pin_failures(monkeypatch_ctx):
+    """Run a small battery of pins; return the names of those that fail."""
+    fails = []
+    x = _inputs(1, 4, 2, 6, 9, 4, seed=31, dtype="bf16", heavy=0.2)
+    try:
+        o, l, w = oracle.sdpa_chunk(*_args(x), x["scale"])
+        bo, bl, bw = P.brute_sdpa(*_args(x), x["scale"])
+        if not (np.allclose(o, bo, rtol=1e-10, atol=1e-12) and np.allclose(l, bl, rtol=1e-10)
+                and np.allclose(w, bw, rtol=1e-10, atol=1e-12)):
+            fails.append("brute")
+        if not np.allclose(w.sum(-1), 4 * 2, rtol=1e-12):
+            fails.append("rowsum")
+    except Exception:
+        fails.append("attention-crash")
+    s = np.floor(np.random.default_rng(3).standard_exponential((2, 30)) * 4).astype(np.float32) / 4
+    try:
+        if not np.array_equal(oracle.bottomk(s, 9), P.brute_bottomk(s, 9)):
+            fails.append("bottomk")
+    except Exception:
+        fails.append("bottomk-crash")
+    return fails
+
+
+def test_planted_mistakes_are_caught(monkeypatch):
+    assert _pin_failures(None) == []
+    mutants = {}
+
+    def off_by_one(M, T):                    # chunk key t visible only for t < i
+        i = np.arange(T)[:, None]
+        j = np.arange(M + T)[None, :]
+        return (j < M) | ((j - M) < i)
+    mutants["mask off by one"] = ("visible", off_by_one)
+
+    def head_drop_max(Qh, K, V, allowed, scale):   # lse missing its max term
+        A = np.where(allowed, scale * (Qh @ K.T), -np.inf)
+        amax = A.max(axis=1, keepdims=True)
+        lam = np.log(np.exp(A - amax).sum(axis=1))
+        Mw = np.exp(A - lam[:, None])
+        return Mw @ V, lam, Mw.sum(axis=0)
+    mutants["dropped max in lse"] = ("_head", head_drop_max)
+
+    def head_no_scale(Qh, K, V, allowed, scale):   # forgot d^-1/2
+        return O.__dict__["_orig_head"](Qh, K, V, allowed, 1.0)
+    mutants["missing scale"] = ("_head", head_no_scale)
+
+    def head_transposed_sum(Qh, K, V, allowed, scale):   # sums over keys, not queries
+        Y, lam, col = O.__dict__["_orig_head"](Qh, K, V, allowed, scale)
+        A = np.where(allowed, scale * (Qh @ K.T), -np.inf)
+        Mw = np.exp(A - lam[:, None])
+        s = np.zeros_like(col)
+        s[:Mw.shape[0]] = Mw.sum(axis=1)
+        return Y, lam, s
+    mutants["summed along the wrong axis"] = ("_head", head_transposed_sum)
+
+    def bottomk_largest(scores, k):
+        return O.__dict__["_orig_bottomk"](-np.asarray(scores, np.float32), k)
+    mutants["evicts largest"] = ("bottomk", bottomk_largest)
+
+    def bottomk_high_index_ties(scores, k):
+        s = np.asarray(scores, np.float32)
+        M = s.shape[-1]
+        out = []
+        for row in s.reshape(-1, M):
+            order = np.lexsort((-np.arange(M), row))
+            out.append(np.sort(order[:k]))
+        return np.array(out, np.int32).reshape(*s.shape[:-1], k)
+    mutants["ties evict higher slot"] = ("bottomk", bottomk_high_index_ties)
+
+    monkeypatch.setitem(O.__dict__, "_orig_head", O._head)
+    monkeypatch.setitem(O.__dict__, "_orig_bottomk", O.bottomk)
+    for name, (attr, fn) in mutants.items():
+        with monkeypatch.context() as m:
+            m.setattr(O, attr, fn)
+            if attr == "bottomk":
+                m.setattr(oracle, "bottomk", fn)
+            fails = _pin_failures(None)
+        assert fails, f"planted mistake not caught: {name}"
+
+    # a wrong GQA head mapping (strided instead of contiguous) is caught too
+    orig = O.sdpa_chunk
+
+    def strided(q, *a, **k):
+        B, Hq, T, d = q.shape
+        Hkv = a[0].shape[1]
+        G = Hq // Hkv
+        perm = np.array([(hq % G) * Hkv + hq // G for hq in range(Hq)])
+        o, l, w = orig(q[:, perm], *a, **k)
+        return o, l, w
+    with monkeypatch.context() as m:
+        m.setattr(oracle, "sdpa_chunk", strided)
+        assert _pin_failures(None), "strided head mapping not caught"

@@ -1,0 +1,146 @@
+/*
+ * h2o.h - C ABI of libh2o.so, the MI355X (gfx950) H2O chunk step.
+ *
+ * One chunk step of sparse attention with the heavy-hitter-oracle (H2O) cache
+ * policy, as stated in "Learning how to Forget: Fine-tuning for Long-Context
+ * Sparse Attention":
+ *
+ *   1. h2o_sdpa_chunk: scaled dot-product attention of the chunk's T queries
+ *      over [M cache slots || the chunk's T keys] (Eq. main-sdpa,
+ *      Eq. main-sdpa-comp), causal inside the chunk (the token-position mask of
+ *      Sec. "Discussion: SDPA Kernels for Sparse Attention"; every cache token
+ *      precedes the chunk), returning the output, the per-row log-sum-exp and
+ *      the summed attention weights sum_i m_{i,j} per key column (Sec.
+ *      "Variants of Heavy-Hitter Oracle", Sec. "Computing Summed Attention
+ *      Weights in SDPA"), summed over the query heads of each GQA group.
+ *   2. h2o_accumulate_scores: the running H2O score phi += sum_i m_{i,j}
+ *      (Eq. h2o-score) for the M cache slots.
+ *   3. h2o_evict_insert: per (batch, KV head) overwrite the k slots with the
+ *      smallest score (Sec. "Variants of Heavy-Hitter Oracle") by the chunk's
+ *      keys and values - the scatter of Sec. "Fine-Tuning for Sparse
+ *      Attention" along the slot axis (Sec. "Buffer Read/Write Access by
+ *      torch.scatter, torch.gather").
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Pointers are device pointers (HIP global memory) unless stated. All
+ *    tensors are dense, C-contiguous, 16-byte aligned, and owned by the
+ *    caller; the library never keeps a pointer after the call returns.
+ *  - Shapes (row-major):
+ *        q, out            [B, Hq,  T, d]       dtype
+ *        k_cache, v_cache  [B, Hkv, M, d]       dtype
+ *        k_new, v_new      [B, Hkv, T, d]       dtype
+ *        lse               [B, Hq,  T]          float32
+ *        wsum              [B, Hkv, M + T]      float32
+ *        scores            [B, Hkv, M]          float32
+ *        token_pos         [B, Hkv, M]          int32
+ *        evict_idx         [B, Hkv, k]          int32
+ *    Query head hq belongs to KV head hq / (Hq / Hkv) (contiguous groups).
+ *    Key column j < M is cache slot j; column M + t is chunk key t.
+ *  - dtype: H2O_F32 (float32) or H2O_BF16 (bfloat16). lse, wsum and scores
+ *    are float32 in both modes.
+ *  - stream: a hipStream_t passed as void* (NULL = the null stream). Work is
+ *    only enqueued; nothing synchronises. A device fault surfaces at the
+ *    caller's next synchronisation.
+ *  - Errors: every function returns an h2o_status. Arguments are validated
+ *    on the host before anything is enqueued, so on error no buffer is
+ *    touched. h2o_last_error() returns a message for the calling thread's
+ *    last non-OK status.
+ *  - Calls that share buffers must be ordered by the caller (same stream).
+ */
+#ifndef H2O_H
+#define H2O_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  H2O_OK = 0,
+  H2O_EINVAL = 1,      /* null pointer, k != T, T < 1, M < k, bad scale     */
+  H2O_ESHAPE = 2,      /* Hq % Hkv != 0, d not in {64,128}, sizes <= 0 or
+                          too large for 32-bit element counts per head        */
+  H2O_EDTYPE = 3,      /* dtype not H2O_F32 / H2O_BF16                        */
+  H2O_EALIGN = 4,      /* a tensor pointer is not 16-byte aligned             */
+  H2O_EWORKSPACE = 5,  /* workspace smaller than h2o_workspace_bytes()        */
+  H2O_ENODEVICE = 6,   /* no usable gfx950 device                             */
+  H2O_ELAUNCH = 7      /* a kernel launch failed                              */
+} h2o_status;
+
+typedef enum { H2O_F32 = 0, H2O_BF16 = 1 } h2o_dtype;
+
+/* Bytes of device scratch h2o_sdpa_chunk needs for this shape (0 on invalid
+ * arguments). The workspace holds partial row statistics and per-row-tile
+ * partial column sums; its contents on entry are ignored. */
+size_t h2o_workspace_bytes(int B, int Hq, int Hkv, int T, int M, int d,
+                           int dtype);
+
+/* SDPA of the chunk over [cache || chunk] plus summed attention weights.
+ *
+ *   out[b,hq,i,:] = sum_j m_{i,j} V_j,  m_{i,j} = exp(s_{i,j} - lse[b,hq,i])
+ *   s_{i,j} = scale * <q[b,hq,i], K_j>  for visible (i,j), where
+ *            K_j = k_cache[b,h,j] (j < M, always visible) or
+ *                  k_new[b,h,j-M] (visible iff j-M <= i), h = hq / (Hq/Hkv)
+ *   lse[b,hq,i]  = log sum_{visible j} exp(s_{i,j})        (natural log)
+ *   wsum[b,h,j]  = sum_{hq in group h} sum_i m_{i,j}         (written, not
+ *                  accumulated; invisible pairs contribute 0)
+ *
+ * scale is usually 1/sqrt(d) and must be finite and > 0. T >= 1, M >= 0.
+ * With dtype H2O_BF16 the products run on bf16 MFMA with float32
+ * accumulation, the softmax and all sums are float32 and out is rounded to
+ * bf16 (nearest even). out must not alias any input. */
+int h2o_sdpa_chunk(const void* q, const void* k_cache, const void* v_cache,
+                   const void* k_new, const void* v_new, void* out, float* lse,
+                   float* wsum, void* workspace, size_t workspace_bytes, int B,
+                   int Hq, int Hkv, int T, int M, int d, float scale,
+                   int dtype, void* stream);
+
+/* scores[b,h,j] += wsum[b,h,j] for j < M: one IEEE float32 addition per slot
+ * (Eq. h2o-score as a running sum over chunks). wsum has M + T columns; only
+ * the first M are read. scores and wsum must not overlap. */
+int h2o_accumulate_scores(float* scores, const float* wsum, int B, int Hkv,
+                          int M, int T, void* stream);
+
+/* Eviction and insert for one chunk (k == T: every chunk key is inserted).
+ * Per (b,h): E = the k slots j < M with the smallest (scores[j], j) in
+ * lexicographic order (score first, lower slot wins ties, -0.0 == +0.0;
+ * scores must not be NaN), written to evict_idx in ascending slot order.
+ * Then for i < k, with slot = E[i]:
+ *   k_cache[b,h,slot,:] = k_new[b,h,i,:],  v_cache[b,h,slot,:] = v_new[b,h,i,:]
+ *   scores[b,h,slot]    = wsum[b,h,M+i]    (the new key's own summed weight)
+ *   token_pos[b,h,slot] = pos0 + i         (skipped when token_pos is NULL)
+ * All other slots are unchanged. Inputs k_new/v_new/wsum must not overlap
+ * the buffers written. */
+int h2o_evict_insert(void* k_cache, void* v_cache, float* scores,
+                     int32_t* token_pos, const void* k_new, const void* v_new,
+                     const float* wsum, int32_t* evict_idx, int B, int Hkv,
+                     int M, int T, int d, int k, int32_t pos0, int dtype,
+                     void* stream);
+
+/* The selection of h2o_evict_insert alone: for each of `rows` rows of M
+ * float32 scores, the k smallest by (score, index), ascending indices, into
+ * idx_out [rows, k]. 0 <= k <= M. */
+int h2o_bottomk(const float* scores, int rows, int M, int k, int32_t* idx_out,
+                void* stream);
+
+/* Message for the calling thread's last non-OK status ("" if none). The
+ * pointer stays valid until the thread's next call into the library. */
+const char* h2o_last_error(void);
+
+/* Testing hook, not needed in normal use: force the bf16 SDPA kernel path of
+ * h2o_sdpa_chunk for every later call in the process (-1 automatic, 0 the
+ * generic VALU kernels, 1 the MFMA prefill kernels, 2 the decode kernels,
+ * which need T == 1). float32 always uses the generic kernels. Returns
+ * H2O_EINVAL for other values. */
+int h2o_debug_force_path(int path);
+
+/* Library version string. */
+const char* h2o_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* H2O_H */

@@ -1,0 +1,256 @@
+// C ABI of libh2o.so: argument validation, workspace plan, kernel dispatch.
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+
+#include "../../include/h2o.h"
+#include "internal.h"
+
+namespace h2o {
+namespace {
+
+thread_local std::string g_last_error;
+std::atomic<int> g_forced_path{-1};
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return code;
+}
+
+int ok() {
+  g_last_error.clear();
+  return H2O_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Checks that a usable gfx950 device is current. Cached per device id.
+int check_device() {
+  int n = 0;
+  if (hipGetDeviceCount(&n) != hipSuccess || n <= 0) {
+    (void)hipGetLastError();
+    return fail(H2O_ENODEVICE, "no HIP device visible");
+  }
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return fail(H2O_ENODEVICE, "hipGetDevice failed");
+  static std::mutex mu;
+  static int known[64] = {0};   // 0 unknown, 1 ok, 2 bad
+  std::lock_guard<std::mutex> lk(mu);
+  if (dev >= 0 && dev < 64 && known[dev] == 0) {
+    hipDeviceProp_t prop;
+    if (hipGetDeviceProperties(&prop, dev) != hipSuccess)
+      return fail(H2O_ENODEVICE, "hipGetDeviceProperties failed");
+    known[dev] = std::strncmp(prop.gcnArchName, "gfx950", 6) == 0 ? 1 : 2;
+  }
+  if (dev < 0 || dev >= 64 || known[dev] != 1)
+    return fail(H2O_ENODEVICE, "device %d is not a gfx950 (MI355X) GPU", dev);
+  return H2O_OK;
+}
+
+int check_shape(int B, int Hq, int Hkv, int T, int M, int d) {
+  if (B < 1 || Hq < 1 || Hkv < 1) return fail(H2O_ESHAPE, "B, Hq, Hkv must be >= 1");
+  if (Hq % Hkv) return fail(H2O_ESHAPE, "Hq (%d) must be a multiple of Hkv (%d)", Hq, Hkv);
+  if (d != 64 && d != 128) return fail(H2O_ESHAPE, "head dim d=%d not supported (64 or 128)", d);
+  if (T < 1) return fail(H2O_EINVAL, "chunk length T must be >= 1");
+  if (M < 0) return fail(H2O_EINVAL, "cache length M must be >= 0");
+  const long long nk = (long long)M + T;
+  const long long rows = (long long)(Hq / Hkv) * T;
+  if (nk * d >= (1ll << 31) || rows * d >= (1ll << 31) || (long long)B * Hq >= (1 << 24))
+    return fail(H2O_ESHAPE, "shape too large for 32-bit per-head indexing");
+  return H2O_OK;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+}  // namespace
+
+Plan make_plan(const Shape& s, int dtype) {
+  Plan p{};
+  const size_t BH = s.BH(), R = s.R(), Nk = s.Nk();
+  int path = dtype == H2O_BF16 ? 1 : 0;
+  if (dtype == H2O_BF16 && s.T == 1 && decode_supports(s.d, s.G())) path = 2;
+  const int forced = g_forced_path.load();
+  if (dtype == H2O_BF16 && forced >= 0) path = forced;
+  // the decode kernels need one query per head and an instantiated (d, G)
+  if (path == 2 && (s.T != 1 || !decode_supports(s.d, s.G()))) path = 1;
+  p.path = path;
+  p.nsplit = 1;
+  if (path == 1) {
+    // Split the key range of each row tile when there are too few blocks to
+    // give every CU two workgroups; keep at least 8 key tiles per split.
+    const int rows_blk = mfma_rows_per_block();
+    const long long nrt = (R + rows_blk - 1) / rows_blk;
+    const long long blocks = nrt * (long long)BH;
+    const long long ntiles = (Nk + 31) / 32;
+    long long ns = (512 + blocks - 1) / blocks;
+    long long cap = ntiles / 8;
+    if (ns > cap) ns = cap;
+    if (ns > 8) ns = 8;
+    if (ns < 1) ns = 1;
+    p.nsplit = (int)ns;
+    p.rows_per_part = mfma_rows_per_part();
+    p.nparts = (int)(nrt * (rows_blk / p.rows_per_part));
+  } else if (path == 2) {
+    p.nsplit = decode_nsplit(s.M);
+    p.rows_per_part = 0;
+    p.nparts = 0;
+    size_t off = 0;
+    p.off_stats = off;
+    off = align256(off + (size_t)p.nsplit * BH * s.G() * sizeof(float) * 2);
+    p.off_opart = off;
+    off = align256(off + (size_t)p.nsplit * BH * s.G() * s.d * sizeof(float));
+    p.off_logits = off;
+    off = align256(off + BH * s.G() * (size_t)s.M * sizeof(float));
+    p.off_parts = off;
+    p.bytes = off;
+    return p;
+  } else {
+    p.rows_per_part = 64;
+    p.nparts = (int)((R + 63) / 64);
+  }
+  size_t off = 0;
+  p.off_stats = off;
+  off = align256(off + (size_t)p.nsplit * BH * R * sizeof(float) * 2);
+  p.off_parts = off;
+  off = align256(off + (size_t)p.nparts * BH * Nk * sizeof(float));
+  p.off_opart = off;
+  if (p.nsplit > 1) off = align256(off + (size_t)p.nsplit * BH * R * s.d * sizeof(float));
+  p.off_logits = off;
+  p.bytes = off;
+  return p;
+}
+
+}  // namespace h2o
+
+using namespace h2o;
+
+extern "C" {
+
+const char* h2o_version(void) { return "h2o-mi355x 0.1 (gfx950)"; }
+
+const char* h2o_last_error(void) { return g_last_error.c_str(); }
+
+// Testing hook (not part of the stable ABI): force the SDPA kernel path for
+// bf16 inputs. -1 = automatic, 0 = generic VALU, 1 = MFMA prefill, 2 = decode.
+int h2o_debug_force_path(int path) {
+  if (path < -1 || path > 2) return fail(H2O_EINVAL, "path must be -1..2");
+  g_forced_path.store(path);
+  return ok();
+}
+
+size_t h2o_workspace_bytes(int B, int Hq, int Hkv, int T, int M, int d, int dtype) {
+  if (dtype != H2O_F32 && dtype != H2O_BF16) return 0;
+  if (check_shape(B, Hq, Hkv, T, M, d) != H2O_OK) return 0;
+  Shape s{B, Hq, Hkv, T, M, d};
+  return make_plan(s, dtype).bytes;
+}
+
+int h2o_sdpa_chunk(const void* q, const void* k_cache, const void* v_cache, const void* k_new,
+                   const void* v_new, void* out, float* lse, float* wsum, void* workspace,
+                   size_t workspace_bytes, int B, int Hq, int Hkv, int T, int M, int d,
+                   float scale, int dtype, void* stream) {
+  if (dtype != H2O_F32 && dtype != H2O_BF16) return fail(H2O_EDTYPE, "dtype %d unknown", dtype);
+  int rc = check_shape(B, Hq, Hkv, T, M, d);
+  if (rc) return rc;
+  if (!q || !k_new || !v_new || !out || !lse || !wsum || (M > 0 && (!k_cache || !v_cache)))
+    return fail(H2O_EINVAL, "null tensor pointer");
+  if (!(std::isfinite(scale) && scale > 0.f)) return fail(H2O_EINVAL, "scale must be finite > 0");
+  const void* ptrs[] = {q, k_new, v_new, out, lse, wsum, workspace};
+  for (const void* p : ptrs)
+    if (p && !aligned16(p)) return fail(H2O_EALIGN, "tensor pointer not 16-byte aligned");
+  if (M > 0 && (!aligned16(k_cache) || !aligned16(v_cache)))
+    return fail(H2O_EALIGN, "cache pointer not 16-byte aligned");
+  Shape s{B, Hq, Hkv, T, M, d};
+  Plan p = make_plan(s, dtype);
+  if (workspace_bytes < p.bytes || (p.bytes > 0 && !workspace))
+    return fail(H2O_EWORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, p.bytes);
+  rc = check_device();
+  if (rc) return rc;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  char* ws = reinterpret_cast<char*>(workspace);
+  hipError_t e;
+  switch (p.path) {
+    case 1:
+      e = launch_sdpa_mfma(s, p, q, k_cache, v_cache, k_new, v_new, out, lse, wsum, ws, scale,
+                           st);
+      break;
+    case 2:
+      e = launch_sdpa_decode(s, p, q, k_cache, v_cache, k_new, v_new, out, lse, wsum, ws,
+                             scale, st);
+      break;
+    default:
+      e = launch_sdpa_generic(s, p, dtype, q, k_cache, v_cache, k_new, v_new, out, lse, wsum,
+                              ws, scale, st);
+  }
+  if (e != hipSuccess) return fail(H2O_ELAUNCH, "kernel launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int h2o_accumulate_scores(float* scores, const float* wsum, int B, int Hkv, int M, int T,
+                          void* stream) {
+  if (B < 1 || Hkv < 1 || M < 0 || T < 0) return fail(H2O_ESHAPE, "bad sizes");
+  if ((long long)B * Hkv * ((long long)M + T) >= (1ll << 40)) return fail(H2O_ESHAPE, "too large");
+  if (M > 0 && (!scores || !wsum)) return fail(H2O_EINVAL, "null tensor pointer");
+  if ((scores && !aligned16(scores)) || (wsum && !aligned16(wsum)))
+    return fail(H2O_EALIGN, "tensor pointer not 16-byte aligned");
+  int rc = check_device();
+  if (rc) return rc;
+  hipError_t e = launch_accumulate(scores, wsum, B * Hkv, M, T,
+                                   reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(H2O_ELAUNCH, "kernel launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int h2o_bottomk(const float* scores, int rows, int M, int k, int32_t* idx_out, void* stream) {
+  if (rows < 0 || M < 0 || k < 0 || k > M) return fail(H2O_EINVAL, "need rows >= 0, 0 <= k <= M");
+  if ((long long)rows * M >= (1ll << 40)) return fail(H2O_ESHAPE, "too large");
+  if (rows > 0 && k > 0 && (!scores || !idx_out)) return fail(H2O_EINVAL, "null tensor pointer");
+  if ((scores && !aligned16(scores)) || (idx_out && !aligned16(idx_out)))
+    return fail(H2O_EALIGN, "tensor pointer not 16-byte aligned");
+  int rc = check_device();
+  if (rc) return rc;
+  hipError_t e = launch_bottomk(scores, rows, M, k, idx_out, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(H2O_ELAUNCH, "kernel launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int h2o_evict_insert(void* k_cache, void* v_cache, float* scores, int32_t* token_pos,
+                     const void* k_new, const void* v_new, const float* wsum, int32_t* evict_idx,
+                     int B, int Hkv, int M, int T, int d, int k, int32_t pos0, int dtype,
+                     void* stream) {
+  if (dtype != H2O_F32 && dtype != H2O_BF16) return fail(H2O_EDTYPE, "dtype %d unknown", dtype);
+  if (B < 1 || Hkv < 1) return fail(H2O_ESHAPE, "B, Hkv must be >= 1");
+  if (d != 64 && d != 128) return fail(H2O_ESHAPE, "head dim d=%d not supported (64 or 128)", d);
+  if (T < 1) return fail(H2O_EINVAL, "chunk length T must be >= 1");
+  if (k != T) return fail(H2O_EINVAL, "k (%d) must equal T (%d): every chunk key is inserted", k, T);
+  if (M < k) return fail(H2O_EINVAL, "cache length M (%d) must be >= k (%d)", M, k);
+  if ((long long)B * Hkv * ((long long)M + T) * d >= (1ll << 40))
+    return fail(H2O_ESHAPE, "too large");
+  if (!k_cache || !v_cache || !scores || !k_new || !v_new || !wsum || !evict_idx)
+    return fail(H2O_EINVAL, "null tensor pointer");
+  const void* ptrs[] = {k_cache, v_cache, scores, token_pos, k_new, v_new, wsum, evict_idx};
+  for (const void* p : ptrs)
+    if (p && !aligned16(p)) return fail(H2O_EALIGN, "tensor pointer not 16-byte aligned");
+  int rc = check_device();
+  if (rc) return rc;
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  hipError_t e = launch_bottomk(scores, B * Hkv, M, k, evict_idx, st);
+  if (e == hipSuccess)
+    e = launch_insert(k_cache, v_cache, scores, token_pos, k_new, v_new, wsum, evict_idx,
+                      B * Hkv, M, T, d, k, pos0, dtype == H2O_F32 ? 4 : 2, st);
+  if (e != hipSuccess) return fail(H2O_ELAUNCH, "kernel launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+}  // extern "C"

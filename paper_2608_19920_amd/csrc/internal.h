@@ -1,0 +1,94 @@
+// Internal declarations shared by the libh2o translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace h2o {
+
+// ------------------------------------------------------------ element types
+typedef uint16_t bf16_t;   // raw bfloat16 bits
+
+__device__ __forceinline__ float bf16_to_f32(bf16_t h) {
+  return __uint_as_float(static_cast<uint32_t>(h) << 16);
+}
+// Round-to-nearest-even; inputs are finite here.
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return static_cast<bf16_t>(u >> 16);
+}
+__device__ __forceinline__ float load_elem(const float* p, size_t i) { return p[i]; }
+__device__ __forceinline__ float load_elem(const bf16_t* p, size_t i) { return bf16_to_f32(p[i]); }
+__device__ __forceinline__ void store_elem(float* p, size_t i, float v) { p[i] = v; }
+__device__ __forceinline__ void store_elem(bf16_t* p, size_t i, float v) { p[i] = f32_to_bf16(v); }
+
+// log2(e) and ln(2) in float32.
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+// ----------------------------------------------------------- problem shape
+struct Shape {
+  int B, Hq, Hkv, T, M, d;
+  int G() const { return Hq / Hkv; }
+  int R() const { return G() * T; }      // packed query rows per KV head
+  int Nk() const { return M + T; }       // key columns per KV head
+  int BH() const { return B * Hkv; }
+};
+
+// Packed row r of a KV head is (chunk position i = r / G, group member g = r % G).
+// The keys a chunk position i may see are columns [0, M + i + 1).
+// A partial-sum slot that covers packed rows [r0, r1) therefore sees key
+// columns [0, kv_end) with kv_end = M + min(T-1, (r1-1)/G) + 1.
+__host__ __device__ __forceinline__ int kv_end_for_rows(int r1, int G, int T, int M) {
+  int i_max = (r1 - 1) / G;
+  if (i_max > T - 1) i_max = T - 1;
+  return M + i_max + 1;
+}
+
+// ---------------------------------------------------------- workspace plan
+// Layout of the scratch buffer used by h2o_sdpa_chunk. All offsets are byte
+// offsets, 256-byte aligned.
+struct Plan {
+  int path;            // 0 = generic (float/bf16 VALU), 1 = bf16 MFMA, 2 = bf16 decode
+  int rows_per_part;   // packed rows per colsum partial
+  int nparts;          // partials per KV head
+  int nsplit;          // key-range splits per row tile (MFMA path)
+  size_t off_stats;    // float2 (m, l) per (split, bh, row)  or lse per (bh,row)
+  size_t off_parts;    // float colsum partials [nparts][BH][Nk]
+  size_t off_opart;    // float O partials [nsplit][BH][R][d] (nsplit > 1)
+  size_t off_logits;   // decode: float logits [BH][G][Nk]
+  size_t bytes;
+};
+Plan make_plan(const Shape& s, int dtype);
+int mfma_rows_per_block();   // packed rows per workgroup of the MFMA kernels
+int mfma_rows_per_part();    // packed rows per colsum partial of the MFMA kernels
+int decode_nsplit(int M);    // split blocks of the decode kernels for M cache slots
+bool decode_supports(int d, int G);   // (d, G) pairs the decode kernels handle
+
+// ------------------------------------------------------------- launchers
+// Each returns hipSuccess or the launch error. They assume validated inputs.
+hipError_t launch_sdpa_generic(const Shape& s, const Plan& p, int dtype, const void* q,
+                               const void* kc, const void* vc, const void* kn,
+                               const void* vn, void* out, float* lse, float* wsum,
+                               char* ws, float scale, hipStream_t st);
+hipError_t launch_sdpa_mfma(const Shape& s, const Plan& p, const void* q, const void* kc,
+                            const void* vc, const void* kn, const void* vn, void* out,
+                            float* lse, float* wsum, char* ws, float scale, hipStream_t st);
+hipError_t launch_sdpa_decode(const Shape& s, const Plan& p, const void* q, const void* kc,
+                              const void* vc, const void* kn, const void* vn, void* out,
+                              float* lse, float* wsum, char* ws, float scale,
+                              hipStream_t st);
+hipError_t launch_colsum_reduce(const Shape& s, const Plan& p, const float* parts,
+                                float* wsum, hipStream_t st);
+hipError_t launch_accumulate(float* scores, const float* wsum, int rows, int M, int T,
+                             hipStream_t st);
+hipError_t launch_bottomk(const float* scores, int rows, int M, int k, int32_t* idx,
+                          hipStream_t st);
+hipError_t launch_insert(void* kc, void* vc, float* scores, int32_t* token_pos,
+                         const void* kn, const void* vn, const float* wsum,
+                         const int32_t* idx, int rows, int M, int T, int d, int k,
+                         int32_t pos0, int elem_bytes, hipStream_t st);
+
+}  // namespace h2o

@@ -1,0 +1,222 @@
+// Column-sum reduce, H2O score accumulation, bottom-k selection and insert.
+#include "internal.h"
+
+namespace h2o {
+namespace {
+
+// ------------------------------------------------------------ colsum reduce
+// wsum[bh][j] = sum over the partial slots p (in increasing p, so the result
+// is bitwise reproducible) whose rows can see column j.
+__global__ __launch_bounds__(256) void colsum_reduce_kernel(const float* __restrict__ parts,
+                                                            float* __restrict__ wsum, int nparts,
+                                                            int rows_per_part, int BH, int Nk,
+                                                            int G, int T, int M) {
+  const int j = blockIdx.x * blockDim.x + threadIdx.x;
+  const int bh = blockIdx.y;
+  if (j >= Nk) return;
+  const int R = G * T;
+  float s = 0.f;
+  for (int p = 0; p < nparts; ++p) {
+    const int r1 = min((p + 1) * rows_per_part, R);
+    if (j < kv_end_for_rows(r1, G, T, M)) s += parts[((size_t)p * BH + bh) * Nk + j];
+  }
+  wsum[(size_t)bh * Nk + j] = s;
+}
+
+// ---------------------------------------------------------------- accumulate
+__global__ __launch_bounds__(256) void accumulate_kernel(float* __restrict__ scores,
+                                                         const float* __restrict__ wsum, int M,
+                                                         int T) {
+  const int row = blockIdx.y;
+  const float* w = wsum + (size_t)row * (M + T);
+  float* s = scores + (size_t)row * M;
+  for (int j = blockIdx.x * blockDim.x + threadIdx.x; j < M; j += gridDim.x * blockDim.x)
+    s[j] = s[j] + w[j];
+}
+
+// ------------------------------------------------------------------ bottom-k
+// Order-preserving map of a float32 score to uint32 (a < b  <=>  key(a) <
+// key(b)); both zeros map to the same key.
+__device__ __forceinline__ uint32_t order_key(float x) {
+  uint32_t u = __float_as_uint(x);
+  if ((u << 1) == 0u) u = 0u;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+constexpr int kSelThreads = 1024;
+constexpr int kSelWaves = kSelThreads / 64;
+
+// Exclusive prefix sum over the block (thread order); also returns the total.
+__device__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* tmp, uint32_t* total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  uint32_t x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    uint32_t y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) tmp[wave] = x;
+  __syncthreads();
+  if (wave == 0) {
+    uint32_t w = lane < kSelWaves ? tmp[lane] : 0u;
+    uint32_t z = w;
+#pragma unroll
+    for (int o = 1; o < kSelWaves; o <<= 1) {
+      uint32_t y = __shfl_up(z, o, 64);
+      if (lane >= o) z += y;
+    }
+    if (lane < kSelWaves) tmp[kSelWaves + lane] = z - w;   // exclusive wave offsets
+    if (lane == kSelWaves - 1) tmp[2 * kSelWaves] = z;
+  }
+  __syncthreads();
+  const uint32_t res = tmp[kSelWaves + wave] + x - v;
+  *total = tmp[2 * kSelWaves];
+  __syncthreads();
+  return res;
+}
+
+// One block per row. Radix-select the k-th smallest key tau (8 bits per pass,
+// most significant first), then emit, in ascending slot order, every slot with
+// key < tau and the lowest-index (k - #less) slots with key == tau.
+__global__ __launch_bounds__(kSelThreads) void bottomk_kernel(const float* __restrict__ scores,
+                                                              int M, int k,
+                                                              int32_t* __restrict__ idx) {
+  __shared__ uint32_t hist[256];
+  __shared__ uint32_t tmp[2 * kSelWaves + 1];
+  __shared__ uint32_t sh_prefix, sh_krem;
+  const float* s = scores + (size_t)blockIdx.x * M;
+  int32_t* out = idx + (size_t)blockIdx.x * k;
+  if (k <= 0) return;
+  uint32_t prefix = 0, mask = 0, krem = (uint32_t)k;
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    for (int b = threadIdx.x; b < 256; b += kSelThreads) hist[b] = 0u;
+    __syncthreads();
+    for (int j = threadIdx.x; j < M; j += kSelThreads) {
+      const uint32_t key = order_key(s[j]);
+      if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    if (threadIdx.x < 64) {
+      const int lane = threadIdx.x;
+      const uint32_t c0 = hist[4 * lane], c1 = hist[4 * lane + 1], c2 = hist[4 * lane + 2],
+                     c3 = hist[4 * lane + 3];
+      const uint32_t c = c0 + c1 + c2 + c3;
+      uint32_t inc = c;
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        uint32_t y = __shfl_up(inc, o, 64);
+        if (lane >= o) inc += y;
+      }
+      const uint32_t exc = inc - c;
+      // the lane whose range holds the krem-th element
+      const unsigned long long hit = __ballot(inc >= krem && exc < krem);
+      const int src = __ffsll(hit) - 1;
+      if (lane == src) {
+        uint32_t before = exc, bin = 4u * lane;
+        if (before + c0 < krem) { before += c0; ++bin;
+          if (before + c1 < krem) { before += c1; ++bin;
+            if (before + c2 < krem) { before += c2; ++bin; } } }
+        sh_prefix = prefix | (bin << shift);
+        sh_krem = krem - before;
+      }
+    }
+    __syncthreads();
+    prefix = sh_prefix;
+    krem = sh_krem;
+    mask |= 255u << shift;
+    __syncthreads();
+  }
+  const uint32_t tau = prefix, need_eq = krem;
+  // Compaction in slot order: thread t owns the contiguous chunk [t*C, (t+1)*C).
+  const int C = (M + kSelThreads - 1) / kSelThreads;
+  const int j0 = min(M, (int)threadIdx.x * C), j1 = min(M, j0 + C);
+  uint32_t n_less = 0, n_eq = 0;
+  for (int j = j0; j < j1; ++j) {
+    const uint32_t key = order_key(s[j]);
+    n_less += key < tau;
+    n_eq += key == tau;
+  }
+  uint32_t tot;
+  const uint32_t eq_before = block_exclusive_scan(n_eq, tmp, &tot);
+  uint32_t take_eq = 0;
+  if (eq_before < need_eq) take_eq = min(n_eq, need_eq - eq_before);
+  const uint32_t pos = block_exclusive_scan(n_less + take_eq, tmp, &tot);
+  uint32_t w = pos, eq_seen = 0;
+  for (int j = j0; j < j1; ++j) {
+    const uint32_t key = order_key(s[j]);
+    bool sel = key < tau;
+    if (key == tau) { sel = eq_seen < take_eq; ++eq_seen; }
+    if (sel && w < (uint32_t)k) out[w++] = j;
+  }
+}
+
+// -------------------------------------------------------------------- insert
+// Block (x, row) copies chunk keys/values i in [x*kPer, x*kPer + kPer) into
+// their evicted slots, 16 bytes per thread per step.
+constexpr int kInsThreads = 256;
+
+__global__ __launch_bounds__(kInsThreads) void insert_kernel(
+    uint4* __restrict__ kc, uint4* __restrict__ vc, float* __restrict__ scores,
+    int32_t* __restrict__ token_pos, const uint4* __restrict__ kn, const uint4* __restrict__ vn,
+    const float* __restrict__ wsum, const int32_t* __restrict__ idx, int M, int T, int vecs,
+    int k, int kPer, int32_t pos0) {
+  const size_t row = blockIdx.y;
+  const int i0 = blockIdx.x * kPer;
+  const int n = min(kPer, k - i0);
+  for (int e = threadIdx.x; e < n * vecs; e += kInsThreads) {
+    const int i = i0 + e / vecs, c = e % vecs;
+    const int slot = idx[row * k + i];
+    if ((unsigned)slot >= (unsigned)M) continue;
+    kc[(row * M + slot) * vecs + c] = kn[(row * T + i) * vecs + c];
+    vc[(row * M + slot) * vecs + c] = vn[(row * T + i) * vecs + c];
+  }
+  for (int e = threadIdx.x; e < n; e += kInsThreads) {
+    const int i = i0 + e;
+    const int slot = idx[row * k + i];
+    if ((unsigned)slot >= (unsigned)M) continue;
+    scores[row * M + slot] = wsum[row * (size_t)(M + T) + M + i];
+    if (token_pos) token_pos[row * M + slot] = pos0 + i;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_colsum_reduce(const Shape& s, const Plan& p, const float* parts, float* wsum,
+                                hipStream_t st) {
+  dim3 grid((s.Nk() + 255) / 256, s.BH());
+  colsum_reduce_kernel<<<grid, 256, 0, st>>>(parts, wsum, p.nparts, p.rows_per_part, s.BH(),
+                                             s.Nk(), s.G(), s.T, s.M);
+  return hipGetLastError();
+}
+
+hipError_t launch_accumulate(float* scores, const float* wsum, int rows, int M, int T,
+                             hipStream_t st) {
+  if (rows == 0 || M == 0) return hipSuccess;
+  int bx = (M + 256 * 4 - 1) / (256 * 4);
+  dim3 grid(bx < 1 ? 1 : bx, rows);
+  accumulate_kernel<<<grid, 256, 0, st>>>(scores, wsum, M, T);
+  return hipGetLastError();
+}
+
+hipError_t launch_bottomk(const float* scores, int rows, int M, int k, int32_t* idx,
+                          hipStream_t st) {
+  if (rows == 0 || k == 0) return hipSuccess;
+  bottomk_kernel<<<rows, kSelThreads, 0, st>>>(scores, M, k, idx);
+  return hipGetLastError();
+}
+
+hipError_t launch_insert(void* kc, void* vc, float* scores, int32_t* token_pos, const void* kn,
+                         const void* vn, const float* wsum, const int32_t* idx, int rows, int M,
+                         int T, int d, int k, int32_t pos0, int elem_bytes, hipStream_t st) {
+  if (rows == 0 || k == 0) return hipSuccess;
+  const int vecs = d * elem_bytes / 16;
+  int kPer = kInsThreads / vecs;
+  if (kPer < 1) kPer = 1;
+  dim3 grid((k + kPer - 1) / kPer, rows);
+  insert_kernel<<<grid, kInsThreads, 0, st>>>((uint4*)kc, (uint4*)vc, scores, token_pos,
+                                              (const uint4*)kn, (const uint4*)vn, wsum, idx, M, T,
+                                              vecs, k, kPer, pos0);
+  return hipGetLastError();
+}
+
+}  // namespace h2o

@@ -1,0 +1,220 @@
+"""ctypes binding of libh2o.so (the C ABI in include/h2o.h).
+
+Argument marshalling only: shapes and dtypes are read off torch tensors,
+pointers and the current HIP stream are passed through, and a non-OK status
+raises ``H2OError``. Every step of the computation runs in the library's HIP
+kernels; there is no fallback. If the library is not built, the first call
+raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libh2o.so")
+
+H2O_OK, H2O_EINVAL, H2O_ESHAPE, H2O_EDTYPE, H2O_EALIGN, H2O_EWORKSPACE, \
+    H2O_ENODEVICE, H2O_ELAUNCH = range(8)
+H2O_F32, H2O_BF16 = 0, 1
+STATUS_NAMES = ["H2O_OK", "H2O_EINVAL", "H2O_ESHAPE", "H2O_EDTYPE", "H2O_EALIGN",
+                "H2O_EWORKSPACE", "H2O_ENODEVICE", "H2O_ELAUNCH"]
+EXPORTED = ["h2o_workspace_bytes", "h2o_sdpa_chunk", "h2o_accumulate_scores",
+            "h2o_evict_insert", "h2o_bottomk", "h2o_last_error", "h2o_debug_force_path",
+            "h2o_version"]
+
+
+class H2OError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        self.status = status
+        name = STATUS_NAMES[status] if 0 <= status < len(STATUS_NAMES) else str(status)
+        super().__init__(f"{name}: {msg}")
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library with argument types set (loads on first use)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built: run `python -m "
+                           "paper_2608_19920_amd.build` (no fallback exists)")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i, f, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+    L.h2o_workspace_bytes.argtypes = [i] * 7
+    L.h2o_workspace_bytes.restype = sz
+    L.h2o_sdpa_chunk.argtypes = [vp] * 9 + [sz] + [i] * 6 + [f, i, vp]
+    L.h2o_sdpa_chunk.restype = i
+    L.h2o_accumulate_scores.argtypes = [vp, vp, i, i, i, i, vp]
+    L.h2o_accumulate_scores.restype = i
+    L.h2o_evict_insert.argtypes = [vp] * 8 + [i] * 6 + [ctypes.c_int32, i, vp]
+    L.h2o_evict_insert.restype = i
+    L.h2o_bottomk.argtypes = [vp, i, i, i, vp, vp]
+    L.h2o_bottomk.restype = i
+    L.h2o_last_error.argtypes = []
+    L.h2o_last_error.restype = ctypes.c_char_p
+    L.h2o_debug_force_path.argtypes = [i]
+    L.h2o_debug_force_path.restype = i
+    L.h2o_version.argtypes = []
+    L.h2o_version.restype = ctypes.c_char_p
+    _lib = L
+    return L
+
+
+def _check(status: int) -> None:
+    if status != H2O_OK:
+        raise H2OError(status, lib().h2o_last_error().decode())
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return H2O_F32
+    if t.dtype == torch.bfloat16:
+        return H2O_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _dev(t: Optional[torch.Tensor], name: str):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def h2o_version() -> str:
+    return lib().h2o_version().decode()
+
+
+def h2o_debug_force_path(path: int) -> None:
+    _check(lib().h2o_debug_force_path(int(path)))
+
+
+def h2o_workspace_bytes(B, Hq, Hkv, T, M, d, dtype) -> int:
+    code = dtype if isinstance(dtype, int) else _dtype_code(torch.empty(0, dtype=dtype))
+    return int(lib().h2o_workspace_bytes(B, Hq, Hkv, T, M, d, code))
+
+
+def h2o_sdpa_chunk(q, k_cache, v_cache, k_new, v_new, out, lse, wsum, workspace,
+                   scale: Optional[float] = None, stream=None) -> None:
+    """q [B,Hq,T,d]; caches [B,Hkv,M,d]; new [B,Hkv,T,d]; out like q;
+    lse [B,Hq,T] f32; wsum [B,Hkv,M+T] f32; workspace uint8 of
+    h2o_workspace_bytes(...) bytes."""
+    B, Hq, T, d = q.shape
+    Hkv, M = k_cache.shape[1], k_cache.shape[2]
+    dt = _dtype_code(q)
+    for name, t in (("k_cache", k_cache), ("v_cache", v_cache), ("k_new", k_new),
+                    ("v_new", v_new), ("out", out)):
+        if t.dtype != q.dtype:
+            raise TypeError(f"{name} dtype {t.dtype} != q dtype {q.dtype}")
+    if tuple(k_cache.shape) != (B, Hkv, M, d) or tuple(v_cache.shape) != (B, Hkv, M, d):
+        raise ValueError("cache shape mismatch")
+    if tuple(k_new.shape) != (B, Hkv, T, d) or tuple(v_new.shape) != (B, Hkv, T, d):
+        raise ValueError("k_new/v_new shape mismatch")
+    if tuple(out.shape) != (B, Hq, T, d):
+        raise ValueError("out shape mismatch")
+    if tuple(lse.shape) != (B, Hq, T) or lse.dtype != torch.float32:
+        raise ValueError("lse must be float32 [B,Hq,T]")
+    if tuple(wsum.shape) != (B, Hkv, M + T) or wsum.dtype != torch.float32:
+        raise ValueError("wsum must be float32 [B,Hkv,M+T]")
+    if scale is None:
+        scale = d ** -0.5
+    nbytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(lib().h2o_sdpa_chunk(
+        _dev(q, "q"), _dev(k_cache, "k_cache"), _dev(v_cache, "v_cache"),
+        _dev(k_new, "k_new"), _dev(v_new, "v_new"), _dev(out, "out"), _dev(lse, "lse"),
+        _dev(wsum, "wsum"), _dev(workspace, "workspace"), nbytes,
+        B, Hq, Hkv, T, M, d, float(scale), dt, _stream(stream)))
+
+
+def h2o_accumulate_scores(scores, wsum, stream=None) -> None:
+    """scores [B,Hkv,M] f32 (in-out) += wsum[..., :M]; wsum [B,Hkv,M+T]."""
+    B, Hkv, M = scores.shape
+    T = wsum.shape[2] - M
+    if scores.dtype != torch.float32 or wsum.dtype != torch.float32:
+        raise TypeError("scores and wsum must be float32")
+    if tuple(wsum.shape[:2]) != (B, Hkv) or T < 0:
+        raise ValueError("wsum shape mismatch")
+    _check(lib().h2o_accumulate_scores(_dev(scores, "scores"), _dev(wsum, "wsum"),
+                                       B, Hkv, M, T, _stream(stream)))
+
+
+def h2o_evict_insert(k_cache, v_cache, scores, token_pos, k_new, v_new, wsum, evict_idx,
+                     pos0: int, stream=None) -> None:
+    """Bottom-k eviction of the accumulated scores and insert of the chunk."""
+    B, Hkv, M, d = k_cache.shape
+    T = k_new.shape[2]
+    k = evict_idx.shape[2]
+    dt = _dtype_code(k_cache)
+    if v_cache.dtype != k_cache.dtype or k_new.dtype != k_cache.dtype or \
+            v_new.dtype != k_cache.dtype:
+        raise TypeError("cache and chunk tensors must share one dtype")
+    if tuple(v_cache.shape) != (B, Hkv, M, d) or tuple(k_new.shape) != (B, Hkv, T, d) or \
+            tuple(v_new.shape) != (B, Hkv, T, d):
+        raise ValueError("shape mismatch")
+    if tuple(scores.shape) != (B, Hkv, M) or scores.dtype != torch.float32:
+        raise ValueError("scores must be float32 [B,Hkv,M]")
+    if tuple(wsum.shape) != (B, Hkv, M + T) or wsum.dtype != torch.float32:
+        raise ValueError("wsum must be float32 [B,Hkv,M+T]")
+    if evict_idx.dtype != torch.int32 or tuple(evict_idx.shape[:2]) != (B, Hkv):
+        raise ValueError("evict_idx must be int32 [B,Hkv,k]")
+    if token_pos is not None and (token_pos.dtype != torch.int32 or
+                                  tuple(token_pos.shape) != (B, Hkv, M)):
+        raise ValueError("token_pos must be int32 [B,Hkv,M]")
+    _check(lib().h2o_evict_insert(
+        _dev(k_cache, "k_cache"), _dev(v_cache, "v_cache"), _dev(scores, "scores"),
+        _dev(token_pos, "token_pos"), _dev(k_new, "k_new"), _dev(v_new, "v_new"),
+        _dev(wsum, "wsum"), _dev(evict_idx, "evict_idx"), B, Hkv, M, T, d, k, int(pos0), dt,
+        _stream(stream)))
+
+
+def h2o_bottomk(scores, k: int, idx_out, stream=None) -> None:
+    """scores [..., M] f32; idx_out [..., k] int32 (ascending indices)."""
+    M = scores.shape[-1]
+    rows = scores.numel() // max(M, 1)
+    if scores.dtype != torch.float32 or idx_out.dtype != torch.int32:
+        raise TypeError("scores must be float32, idx_out int32")
+    if idx_out.numel() != rows * k:
+        raise ValueError("idx_out size mismatch")
+    _check(lib().h2o_bottomk(_dev(scores, "scores"), rows, M, int(k), _dev(idx_out, "idx_out"),
+                             _stream(stream)))
+
+
+# ------------------------------------------------------------ conveniences
+def alloc_step(B, Hq, Hkv, T, M, d, dtype, device="cuda"):
+    """Output and scratch tensors for one h2o_sdpa_chunk call."""
+    code = _dtype_code(torch.empty(0, dtype=dtype))
+    ws = h2o_workspace_bytes(B, Hq, Hkv, T, M, d, code)
+    return dict(
+        out=torch.empty(B, Hq, T, d, dtype=dtype, device=device),
+        lse=torch.empty(B, Hq, T, dtype=torch.float32, device=device),
+        wsum=torch.empty(B, Hkv, M + T, dtype=torch.float32, device=device),
+        workspace=torch.empty(max(ws, 16), dtype=torch.uint8, device=device),
+        evict_idx=torch.empty(B, Hkv, T, dtype=torch.int32, device=device),
+    )
+
+
+def step(state, q, k_new, v_new, bufs, pos0: int, scale=None, stream=None) -> None:
+    """One chunk step in place: attend, accumulate, evict + insert.
+
+    ``state`` holds k_cache, v_cache, scores, token_pos (token_pos may be None).
+    """
+    h2o_sdpa_chunk(q, state["k_cache"], state["v_cache"], k_new, v_new, bufs["out"],
+                   bufs["lse"], bufs["wsum"], bufs["workspace"], scale, stream)
+    h2o_accumulate_scores(state["scores"], bufs["wsum"], stream)
+    h2o_evict_insert(state["k_cache"], state["v_cache"], state["scores"], state.get("token_pos"),
+                     k_new, v_new, bufs["wsum"], bufs["evict_idx"], pos0, stream)

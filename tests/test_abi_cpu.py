@@ -1,0 +1,154 @@
+"""Host-side checks of libh2o.so: it loads, exports every function the header
+declares, and rejects bad arguments before touching the device.
+
+Fake (aligned, never dereferenced) pointers are used only for calls that must
+fail host validation; the one call that passes validation runs only where no
+device is visible and must report H2O_ENODEVICE.
+"""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+import torch
+
+from paper_2608_19920_amd import h2o as H
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "h2o.h")
+P = 0x10000          # an aligned fake address; validation fails before any use
+MIS = 0x10004        # misaligned
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(h2o_[a-z_0-9]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(H.LIB_PATH):
+        pytest.skip("libh2o.so not built")
+    return H.lib()
+
+
+def test_header_and_exports_agree(L):
+    fns = header_functions()
+    assert set(fns) == set(H.EXPORTED)
+    out = subprocess.run(["nm", "-D", "--defined-only", H.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r" T (h2o_\w+)", out))
+    for f in fns:
+        assert f in exported, f
+        assert hasattr(L, f)
+
+
+def test_version(L):
+    assert "gfx950" in H.h2o_version()
+
+
+def _sdpa(L, **kw):
+    a = dict(q=P, kc=P, vc=P, kn=P, vn=P, out=P, lse=P, wsum=P, ws=P, wsb=1 << 40, B=1, Hq=4,
+             Hkv=2, T=8, M=16, d=64, scale=0.125, dt=1, st=None)
+    a.update(kw)
+    return L.h2o_sdpa_chunk(a["q"], a["kc"], a["vc"], a["kn"], a["vn"], a["out"], a["lse"],
+                            a["wsum"], a["ws"], a["wsb"], a["B"], a["Hq"], a["Hkv"], a["T"],
+                            a["M"], a["d"], a["scale"], a["dt"], a["st"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dt=7), H.H2O_EDTYPE),
+    (dict(Hq=3, Hkv=2), H.H2O_ESHAPE),
+    (dict(d=96), H.H2O_ESHAPE),
+    (dict(B=0), H.H2O_ESHAPE),
+    (dict(T=0), H.H2O_EINVAL),
+    (dict(M=-1), H.H2O_EINVAL),
+    (dict(q=None), H.H2O_EINVAL),
+    (dict(wsum=None), H.H2O_EINVAL),
+    (dict(kc=None), H.H2O_EINVAL),
+    (dict(scale=float("nan")), H.H2O_EINVAL),
+    (dict(scale=-1.0), H.H2O_EINVAL),
+    (dict(out=MIS), H.H2O_EALIGN),
+    (dict(vc=MIS), H.H2O_EALIGN),
+    (dict(wsb=16), H.H2O_EWORKSPACE),
+    (dict(M=1 << 30, d=128), H.H2O_ESHAPE),
+])
+def test_sdpa_rejects(L, kw, code):
+    assert _sdpa(L, **kw) == code
+    assert len(L.h2o_last_error()) > 0
+
+
+def test_workspace_bytes(L):
+    assert L.h2o_workspace_bytes(1, 4, 2, 64, 256, 64, 0) > 0
+    assert L.h2o_workspace_bytes(1, 4, 2, 64, 256, 65, 0) == 0
+    assert L.h2o_workspace_bytes(1, 4, 3, 64, 256, 64, 1) == 0
+    assert L.h2o_workspace_bytes(1, 4, 2, 64, 256, 64, 5) == 0
+
+
+def _evict(L, **kw):
+    a = dict(kc=P, vc=P, sc=P, tp=P, kn=P, vn=P, w=P, idx=P, B=1, Hkv=2, M=16, T=4, d=64, k=4,
+             pos0=16, dt=1, st=None)
+    a.update(kw)
+    return L.h2o_evict_insert(a["kc"], a["vc"], a["sc"], a["tp"], a["kn"], a["vn"], a["w"],
+                              a["idx"], a["B"], a["Hkv"], a["M"], a["T"], a["d"], a["k"],
+                              a["pos0"], a["dt"], a["st"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(k=3), H.H2O_EINVAL),
+    (dict(M=3), H.H2O_EINVAL),
+    (dict(dt=2), H.H2O_EDTYPE),
+    (dict(d=32), H.H2O_ESHAPE),
+    (dict(Hkv=0), H.H2O_ESHAPE),
+    (dict(sc=None), H.H2O_EINVAL),
+    (dict(idx=None), H.H2O_EINVAL),
+    (dict(tp=MIS), H.H2O_EALIGN),
+    (dict(T=0, k=0), H.H2O_EINVAL),
+])
+def test_evict_rejects(L, kw, code):
+    assert _evict(L, **kw) == code
+
+
+@pytest.mark.parametrize("args,code", [
+    ((P, 4, 10, 11, P, None), H.H2O_EINVAL),
+    ((P, 4, 10, -1, P, None), H.H2O_EINVAL),
+    ((None, 4, 10, 3, P, None), H.H2O_EINVAL),
+    ((MIS, 4, 10, 3, P, None), H.H2O_EALIGN),
+])
+def test_bottomk_rejects(L, args, code):
+    assert L.h2o_bottomk(*args) == code
+
+
+def test_accumulate_rejects(L):
+    assert L.h2o_accumulate_scores(None, P, 1, 2, 8, 1, None) == H.H2O_EINVAL
+    assert L.h2o_accumulate_scores(P, P, 0, 2, 8, 1, None) == H.H2O_ESHAPE
+    assert L.h2o_accumulate_scores(P, MIS, 1, 2, 8, 1, None) == H.H2O_EALIGN
+
+
+def test_debug_path_hook(L):
+    assert L.h2o_debug_force_path(5) == H.H2O_EINVAL
+    assert L.h2o_debug_force_path(-1) == H.H2O_OK
+
+
+@pytest.mark.skipif(torch.cuda.device_count() > 0, reason="a device is visible")
+def test_no_device_is_reported(L):
+    assert _sdpa(L) == H.H2O_ENODEVICE
+    assert _evict(L) == H.H2O_ENODEVICE
+    assert L.h2o_bottomk(P, 4, 10, 3, P, None) == H.H2O_ENODEVICE
+    assert L.h2o_accumulate_scores(P, P, 1, 2, 8, 1, None) == H.H2O_ENODEVICE
+
+
+def test_binding_raises_typed_errors(L):
+    with pytest.raises(H.H2OError) as e:
+        H._check(L.h2o_debug_force_path(9))
+    assert e.value.status == H.H2O_EINVAL and "H2O_EINVAL" in str(e.value)
+
+
+def test_binding_refuses_host_tensors():
+    q = torch.zeros(1, 2, 4, 64)
+    kc = torch.zeros(1, 1, 8, 64)
+    with pytest.raises(ValueError):
+        H.h2o_sdpa_chunk(q, kc, kc, q[:, :1], q[:, :1], q, torch.zeros(1, 2, 4),
+                         torch.zeros(1, 1, 12), torch.zeros(16, dtype=torch.uint8))

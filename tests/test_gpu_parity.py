@@ -1,0 +1,252 @@
+"""GPU parity: the HIP path through the C ABI against the float64 oracle.
+
+Tolerances: normwise relative error per (b, head) slice <= 1e-5 for float32
+and <= 2e-2 for bf16, for out, lse, wsum and the accumulated scores.
+Selection is bit-exact when run on the oracle's float32 score vector; the
+insert is bitwise.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import rel_err
+from paper_2608_19920_amd import h2o as H
+from paper_2608_19920_amd import workloads as W
+import _gpu as U
+from _gpu import say
+
+pytestmark = pytest.mark.gpu
+
+BF16_PATHS = [-1, 0, 1]       # automatic, generic VALU, MFMA
+
+
+@pytest.fixture
+def path(request):
+    p = request.param
+    H.h2o_debug_force_path(p)
+    yield p
+    H.h2o_debug_force_path(-1)
+
+
+def _check_attention(x, dtype, res, heads=None, extra=""):
+    q, kc, vc, kn, vn = x["q"], x["k_cache"], x["v_cache"], x["k_new"], x["v_new"]
+    o_full = oracle.sdpa_chunk(q, kc, vc, kn, vn, x["scale"], heads=heads)
+    o, l, w = o_full
+    go, gl, gw = res
+    if heads is not None:
+        G = q.shape[1] // kc.shape[1]
+        hq = [(b, h * G + g) for b, h in heads for g in range(G)]
+        sel = lambda a, hs: np.stack([a[b, h] for b, h in hs])
+        o, go, l, gl = sel(o, hq), sel(go, hq), sel(l, hq), sel(gl, hq)
+        w, gw = sel(w, heads), sel(gw, heads)
+    tol = U.TOL[dtype]
+    e_o = rel_err(go, o, axes=(-2, -1))
+    e_l = rel_err(gl, l, axes=(-1,))
+    e_w = rel_err(gw, w, axes=(-1,))
+    say(f"  {extra} err out {e_o:.2e} lse {e_l:.2e} wsum {e_w:.2e} (tol {tol})")
+    assert np.isfinite(go).all() and np.isfinite(gl).all() and np.isfinite(gw).all()
+    assert e_o <= tol and e_l <= tol and e_w <= tol
+    return o_full
+
+
+SHAPES = [  # B, Hq, Hkv, d, M, T
+    (1, 4, 2, 64, 256, 64),
+    (1, 1, 1, 64, 17, 5),
+    (2, 8, 2, 128, 100, 33),
+    (1, 7, 1, 128, 300, 70),
+    (1, 8, 1, 64, 64, 16),
+    (2, 4, 4, 128, 129, 1),
+    (1, 28, 4, 128, 257, 40),
+    (1, 4, 1, 128, 0, 20),
+    (2, 16, 4, 64, 1000, 3),
+    (1, 32, 8, 64, 513, 1),
+]
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "B%dHq%dHkv%dd%dM%dT%d" % s)
+def test_sdpa_f32(shape):
+    say(f"sdpa f32 {shape}")
+    w = W.custom(**dict(zip("B Hq Hkv d M T".split(), shape)), dtype="f32", heavy_frac=0.02)
+    x = W.make_inputs(w, seed=1)
+    res = U.run_sdpa(x["q"], x["k_cache"], x["v_cache"], x["k_new"], x["v_new"], x["scale"], "f32")
+    _check_attention(x, "f32", res)
+
+
+@pytest.mark.parametrize("path", BF16_PATHS, indirect=True)
+@pytest.mark.parametrize("shape", SHAPES, ids=lambda s: "B%dHq%dHkv%dd%dM%dT%d" % s)
+def test_sdpa_bf16(shape, path):
+    say(f"sdpa bf16 {shape} path {path}")
+    w = W.custom(**dict(zip("B Hq Hkv d M T".split(), shape)), dtype="bf16", heavy_frac=0.02)
+    x = W.make_inputs(w, seed=2)
+    res = U.run_sdpa(x["q"], x["k_cache"], x["v_cache"], x["k_new"], x["v_new"], x["scale"],
+                     "bf16")
+    _check_attention(x, "bf16", res, extra=f"path {path}")
+
+
+def test_tiny_f32_full_step():
+    """The 1x4x2, d64, M256, T64 float32 step: attention, accumulate, evict, insert."""
+    wl = W.WORKLOADS["tiny_f32"]
+    say(f"full step {wl.describe()}")
+    x = W.make_inputs(wl, seed=0)
+    st = U.device_state(x, "f32")
+    tdt = torch.float32
+    q, kn, vn = (U.to_dev(x[n], tdt) for n in ("q", "k_new", "v_new"))
+    bufs = H.alloc_step(wl.B, wl.Hq, wl.Hkv, wl.T, wl.M, wl.d, tdt)
+    H.h2o_sdpa_chunk(q, st["k_cache"], st["v_cache"], kn, vn, bufs["out"], bufs["lse"],
+                     bufs["wsum"], bufs["workspace"], float(x["scale"]))
+    torch.cuda.synchronize()
+    res = tuple(U.to_np(bufs[n]) for n in ("out", "lse", "wsum"))
+    o, l, w = _check_attention(x, "f32", res)
+    H.h2o_accumulate_scores(st["scores"], bufs["wsum"])
+    torch.cuda.synchronize()
+    g_acc = st["scores"].cpu().numpy()
+    # bitwise: the kernel adds exactly the float32 values it was given
+    np.testing.assert_array_equal(g_acc, oracle.accumulate_scores(x["scores"], res[2]))
+    o_acc = oracle.accumulate_scores(x["scores"], w)
+    assert rel_err(g_acc, o_acc, axes=(-1,)) <= 1e-5
+    # selection on the oracle's own float32 scores is bit-exact
+    np.testing.assert_array_equal(U.gpu_bottomk(o_acc, wl.T), oracle.bottomk(o_acc, wl.T))
+    # end-to-end eviction from the GPU's own scores + bitwise insert
+    H.h2o_evict_insert(st["k_cache"], st["v_cache"], st["scores"], st["token_pos"], kn, vn,
+                       bufs["wsum"], bufs["evict_idx"], int(x["pos0"]))
+    torch.cuda.synchronize()
+    g_idx = bufs["evict_idx"].cpu().numpy()
+    np.testing.assert_array_equal(g_idx, oracle.bottomk(g_acc, wl.T))
+    kc2, vc2, sc2, tp2, _ = oracle.evict_insert(x["k_cache"], x["v_cache"], g_acc, x["token_pos"],
+                                                x["k_new"], x["v_new"], res[2], wl.T,
+                                                int(x["pos0"]))
+    np.testing.assert_array_equal(st["k_cache"].cpu().numpy(), kc2)
+    np.testing.assert_array_equal(st["v_cache"].cpu().numpy(), vc2)
+    np.testing.assert_array_equal(st["scores"].cpu().numpy(), sc2)
+    np.testing.assert_array_equal(st["token_pos"].cpu().numpy(), tp2)
+
+
+@pytest.mark.parametrize("rows,M,k,quant", [
+    (1, 1, 1, None), (3, 10, 10, None), (4, 300, 64, None), (4, 300, 64, 2),
+    (8, 8192, 1024, None), (8, 8192, 1024, 3), (2, 16384, 2048, 0), (64, 4096, 1, None),
+    (64, 4096, 1, 0), (5, 33, 32, 1), (2, 32768, 512, None), (3, 4097, 4096, 5)])
+def test_bottomk_exact(rows, M, k, quant):
+    say(f"bottomk rows {rows} M {M} k {k} quant {quant}")
+    rng = np.random.default_rng(rows * M + k)
+    s = rng.standard_exponential((rows, M)).astype(np.float32)
+    if quant is not None:
+        s = (np.floor(s * 2 ** quant) / 2 ** quant).astype(np.float32)
+    if M > 3:
+        s[0, :3] = -0.0
+    np.testing.assert_array_equal(U.gpu_bottomk(s, k), oracle.bottomk(s, k))
+
+
+def test_bottomk_negative_and_huge_values():
+    s = np.array([[3.0, -1.0, np.inf, -np.inf, 0.0, -0.0, 1e-45, -1e-45, 3.4e38, 2.0]],
+                 np.float32)
+    for k in range(0, 11):
+        if k == 0:
+            continue
+        np.testing.assert_array_equal(U.gpu_bottomk(s, k), oracle.bottomk(s, k))
+
+
+@pytest.mark.parametrize("path", BF16_PATHS, indirect=True)
+def test_bitwise_repeatable(path):
+    say(f"repeatability path {path}")
+    w = W.custom(B=1, Hq=8, Hkv=2, d=128, M=777, T=100, dtype="bf16", heavy_frac=0.02)
+    x = W.make_inputs(w, seed=5)
+    a = U.run_sdpa(x["q"], x["k_cache"], x["v_cache"], x["k_new"], x["v_new"], x["scale"], "bf16")
+    b = U.run_sdpa(x["q"], x["k_cache"], x["v_cache"], x["k_new"], x["v_new"], x["scale"], "bf16")
+    for u, v in zip(a, b):
+        np.testing.assert_array_equal(u, v)
+
+
+def _state_to_np(st):
+    return {k: (v.float() if v.dtype == torch.bfloat16 else v).cpu().numpy()
+            for k, v in st.items()}
+
+
+@pytest.mark.parametrize("name,nheads", [("prefill_bf16", 2), ("longcache_bf16", 2),
+                                         ("gqa7_bf16", 1)])
+def test_full_size_step_sampled_heads(name, nheads):
+    """Full-size chunk step; the oracle recomputes a sample of (b, kv-head)
+    pairs (all their query heads, all keys) and the eviction is checked on
+    the sampled heads' oracle scores (bit-exact) and for validity on all."""
+    wl = W.WORKLOADS[name]
+    say(f"full-size {wl.describe()}")
+    x = W.make_inputs(wl, seed=0)
+    st = U.device_state(x, "bf16")
+    tdt = torch.bfloat16
+    q, kn, vn = (U.to_dev(x[n], tdt) for n in ("q", "k_new", "v_new"))
+    bufs = H.alloc_step(wl.B, wl.Hq, wl.Hkv, wl.T, wl.M, wl.d, tdt)
+    H.h2o_sdpa_chunk(q, st["k_cache"], st["v_cache"], kn, vn, bufs["out"], bufs["lse"],
+                     bufs["wsum"], bufs["workspace"], float(x["scale"]))
+    H.h2o_accumulate_scores(st["scores"], bufs["wsum"])
+    torch.cuda.synchronize()
+    res = tuple(U.to_np(bufs[n]) for n in ("out", "lse", "wsum"))
+    g_acc = st["scores"].cpu().numpy()
+    rng = np.random.default_rng(0)
+    pairs = [(b, h) for b in range(wl.B) for h in range(wl.Hkv)]
+    heads = [pairs[i] for i in rng.choice(len(pairs), size=nheads, replace=False)]
+    o, l, w = _check_attention(x, "bf16", res, heads=heads, extra=f"heads {heads}")
+    # every query row's weights sum to one: per KV head, sum_j wsum = T*G
+    np.testing.assert_allclose(res[2].sum(-1), wl.T * wl.G, rtol=2e-3)
+    M, k = wl.M, wl.T
+    for (b, h) in heads:
+        o_acc = oracle.accumulate_scores(x["scores"][b, h], w[b, h])
+        assert rel_err(g_acc[b, h], o_acc, axes=(-1,)) <= 2e-2
+        np.testing.assert_array_equal(U.gpu_bottomk(o_acc[None], k)[0],
+                                      oracle.bottomk(o_acc[None], k)[0])
+    H.h2o_evict_insert(st["k_cache"], st["v_cache"], st["scores"], st["token_pos"], kn, vn,
+                       bufs["wsum"], bufs["evict_idx"], int(x["pos0"]))
+    torch.cuda.synchronize()
+    g_idx = bufs["evict_idx"].cpu().numpy()
+    np.testing.assert_array_equal(g_idx, oracle.bottomk(g_acc, k))     # on the GPU's scores
+    for (b, h) in heads:       # validity against the oracle's scores (near-ties only differ)
+        o_acc = oracle.accumulate_scores(x["scores"][b, h], w[b, h]).astype(np.float64)
+        tau = np.sort(o_acc)[k - 1]
+        delta = 4 * 2e-2 * o_acc.max()
+        ev = g_idx[b, h]
+        kept = np.setdiff1d(np.arange(M), ev)
+        assert (o_acc[ev] <= tau + delta).all() and (o_acc[kept] >= tau - delta).all()
+    kc = st["k_cache"].float().cpu().numpy()
+    for (b, h) in heads:
+        np.testing.assert_array_equal(kc[b, h][g_idx[b, h]], x["k_new"][b, h])
+        untouched = np.setdiff1d(np.arange(M), g_idx[b, h])
+        np.testing.assert_array_equal(kc[b, h][untouched], x["k_cache"][b, h][untouched])
+    assert (st["token_pos"].cpu().numpy()[0, 0][g_idx[0, 0]] ==
+            int(x["pos0"]) + np.arange(k)).all()
+
+
+def test_decode_trajectory_teacher_forced():
+    """16 decode steps (T=1, k=1); before each step the oracle takes the GPU's
+    state, so every step is checked on its own."""
+    wl = W.WORKLOADS["decode_bf16"]
+    say(f"decode {wl.describe()}")
+    x = W.make_inputs(wl, seed=0)
+    st = U.device_state(x, "bf16")
+    tdt = torch.bfloat16
+    bufs = H.alloc_step(wl.B, wl.Hq, wl.Hkv, 1, wl.M, wl.d, tdt)
+    n_mismatch = 0
+    for s in range(wl.steps):
+        pre = _state_to_np(st)
+        q, kn, vn = (U.to_dev(x[n][s], tdt) for n in ("q_steps", "k_new_steps", "v_new_steps"))
+        pos = int(x["pos0"]) + s
+        H.step(st, q, kn, vn, bufs, pos, float(x["scale"]))
+        torch.cuda.synchronize()
+        pre_k = pre["k_cache"].astype(np.float32)
+        pre_v = pre["v_cache"].astype(np.float32)
+        ref = oracle.h2o_step(pre_k, pre_v, pre["scores"], pre["token_pos"], x["q_steps"][s],
+                              x["k_new_steps"][s], x["v_new_steps"][s], pos, x["scale"])
+        go, gw = U.to_np(bufs["out"]), U.to_np(bufs["wsum"])
+        assert rel_err(go, ref["out"], axes=(-2, -1)) <= 2e-2
+        assert rel_err(gw, ref["wsum"], axes=(-1,)) <= 2e-2
+        g_idx = bufs["evict_idx"].cpu().numpy()
+        n_mismatch += int((g_idx != ref["evict_idx"]).sum())
+        # the GPU's choice is the argmin of the GPU's own accumulated scores
+        g_acc = oracle.accumulate_scores(pre["scores"], gw)
+        np.testing.assert_array_equal(g_idx, oracle.bottomk(g_acc, 1))
+        # and the inserted key is where the GPU says
+        kc = st["k_cache"].float().cpu().numpy()
+        for b in range(wl.B):
+            for h in range(wl.Hkv):
+                np.testing.assert_array_equal(kc[b, h, g_idx[b, h, 0]], x["k_new_steps"][s, b, h, 0])
+    say(f"  eviction choices differing from the oracle over 16 steps: {n_mismatch} / "
+        f"{16 * wl.B * wl.Hkv}")
+    assert n_mismatch <= 2

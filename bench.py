@@ -1,0 +1,286 @@
+#!/usr/bin/env python3
+"""Benchmark of the H2O chunk step on one MI355X.
+
+Default workload: token generation, B=8, Hq=32, Hkv=8, d=64, M=4096, T=1,
+bf16. One bench step is one token step (h2o_sdpa_chunk + h2o_accumulate_scores
++ h2o_evict_insert) for each of 8 independent layer states, so the 8 x 69 MB
+working set exceeds the 256 MB Infinity Cache and the step streams from HBM.
+The steps are captured in one HIP graph and replayed; ``value`` is algorithmic
+bytes per second (GB/s) over the timed steps.
+
+The chunked-prefill shapes (d=128: B1 Hq32 Hkv8 M8192 T1024; B4 Hq32 Hkv8
+M32768 T512; B2 Hq28 Hkv4 M16384 T2048) are timed too and reported under
+"prefill" as TFLOP/s of algorithmic attention work W = 4 d P B Hq,
+P = T*M + T(T+1)/2.
+
+Prints one JSON line. ``--gpus N`` with N > 1 exits: this build runs on one GPU.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "H2O SDPA TFLOP/s (% bf16 MFMA peak) prefill; decode HBM GB/s (% peak)"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+LAYERS = 8
+PREFILL = ["prefill_bf16", "longcache_bf16", "gqa7_bf16"]
+
+
+def decode_step_bytes(w) -> int:
+    """Algorithmic HBM bytes of one token step of one layer state."""
+    kv = 2 * w.B * w.Hkv * w.M * w.d * 2           # K and V cache read once
+    q_out = 2 * w.B * w.Hq * w.T * w.d * 2         # q read, out written
+    new = 4 * w.B * w.Hkv * w.T * w.d * 2          # k_new/v_new read and written to the cache
+    scores = 2 * w.B * w.Hkv * w.M * 4             # scores read and written once
+    return kv + q_out + new + scores
+
+
+def decode_split_bytes(w) -> int:
+    """Algorithmic bytes of one launch of the decode split kernel: the cache
+    rows it streams plus the queries."""
+    return 2 * w.B * w.Hkv * w.M * w.d * 2 + w.B * w.Hq * w.d * 2
+
+
+def attention_flops(w) -> float:
+    P = w.T * w.M + w.T * (w.T + 1) / 2
+    return 4.0 * w.d * P * w.B * w.Hq
+
+
+def _src_hash(names):
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(ROOT, "paper_2608_19920_amd", "csrc", n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_for(kernel: str, src_files):
+    """HBM bytes per launch from the committed rocprofv3 counter summary, or
+    None if there is none or the kernel sources changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f).get(kernel)
+    if not rec or rec.get("src_hash") != _src_hash(src_files):
+        return None
+    return rec.get("bytes_per_launch")
+
+
+# ----------------------------------------------------------------- device side
+def _dev_state(x, torch):
+    bf = torch.bfloat16
+    to = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).to("cuda").to(dt)
+    return dict(k_cache=to(x["k_cache"], bf), v_cache=to(x["v_cache"], bf),
+                scores=to(x["scores"], torch.float32),
+                token_pos=to(x["token_pos"], torch.int32))
+
+
+def bench_decode(args, torch, H, W):
+    w = W.WORKLOADS["decode_bf16"]
+    bf = torch.bfloat16
+    layers = []
+    for layer in range(LAYERS):
+        x = W.make_inputs(w, seed=layer)
+        st = _dev_state(x, torch)
+        to = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to("cuda").to(bf)
+        inp = dict(q=to(x["q_steps"][0]), k_new=to(x["k_new_steps"][0]),
+                   v_new=to(x["v_new_steps"][0]), pos0=int(x["pos0"]), scale=float(x["scale"]))
+        bufs = H.alloc_step(w.B, w.Hq, w.Hkv, w.T, w.M, w.d, bf)
+        layers.append((st, inp, bufs))
+    del x
+
+    def step():
+        for st, inp, bufs in layers:
+            H.step(st, inp["q"], inp["k_new"], inp["v_new"], bufs, inp["pos0"], inp["scale"])
+
+    stream = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    with torch.cuda.stream(stream):
+        step()                                   # eager warm-up on the capture stream
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=stream):
+        step()
+    torch.cuda.synchronize()
+    for _ in range(args.warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t_wall = time.perf_counter()
+    e0.record()
+    for _ in range(args.steps):
+        graph.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall
+    ms_step = e0.elapsed_time(e1) / args.steps
+
+    # Per-kernel durations: the same steps once more, eager, with the library
+    # bracketing each of its launches by events on the launch stream.
+    H.h2o_debug_timing(True)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    ktimes = {k: H.h2o_debug_kernel_time(k) for k in
+              ("decode_split", "decode_combine", "accumulate", "argmin_insert")}
+    H.h2o_debug_timing(False)
+    step_bytes = decode_step_bytes(w) * LAYERS
+    gbs = step_bytes / (ms_step * 1e-3) / 1e9
+    ms_split, n_split = ktimes["decode_split"]
+    avg_split_ms = ms_split / max(n_split, 1)
+    ach = decode_split_bytes(w) / (avg_split_ms * 1e-3) / 1e9
+    roof = {"kernel": "decode_split", "bound": "hbm", "achieved": round(ach, 1),
+            "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
+            "traffic": traffic_for("decode_split", ["decode.hip"]),
+            "algorithmic_bytes_per_launch": decode_split_bytes(w),
+            "avg_launch_us": round(avg_split_ms * 1e3, 2),
+            "kernel_us": {k: round(v[0] / max(v[1], 1) * 1e3, 2) for k, v in ktimes.items()},
+            "timing": "HIP events recorded by the library around each launch, on its stream, "
+                      "over an eager pass of the timed steps"}
+    return dict(w=w, ms_step=ms_step, value=gbs, roofline=roof, wall_s=t_wall,
+                step_bytes=step_bytes)
+
+
+def bench_prefill(name, args, torch, H, W):
+    w = W.WORKLOADS[name]
+    x = W.make_inputs(w, seed=0)
+    bf = torch.bfloat16
+    to = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to("cuda").to(bf)
+    st = _dev_state(x, torch)
+    q, kn, vn = to(x["q"]), to(x["k_new"]), to(x["v_new"])
+    pos0, scale = int(x["pos0"]), float(x["scale"])
+    del x
+    bufs = H.alloc_step(w.B, w.Hq, w.Hkv, w.T, w.M, w.d, bf)
+    sdpa = lambda: H.h2o_sdpa_chunk(q, st["k_cache"], st["v_cache"], kn, vn, bufs["out"],
+                                    bufs["lse"], bufs["wsum"], bufs["workspace"], scale)
+    reps = max(3, args.steps // 5)
+    for _ in range(max(2, args.warmup)):
+        sdpa()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        sdpa()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    H.h2o_debug_timing(True)
+    for _ in range(reps):
+        sdpa()
+    torch.cuda.synchronize()
+    kt = {k: H.h2o_debug_kernel_time(k) for k in
+          ("mfma_lse", "mfma_main", "split_reduce", "colsum_reduce")}
+    H.h2o_debug_timing(False)
+    # whole step: attention + accumulate + evict/insert
+    e0.record()
+    for _ in range(reps):
+        H.step(st, q, kn, vn, bufs, pos0, scale)
+    e1.record()
+    torch.cuda.synchronize()
+    ms_step = e0.elapsed_time(e1) / reps
+    Wf = attention_flops(w)
+    tf = Wf / (ms * 1e-3) / 1e12
+    main_ms = kt["mfma_main"][0] / max(kt["mfma_main"][1], 1)
+    ach_main = Wf / (main_ms * 1e-3) / 1e12
+    return {"workload": w.describe(), "tflops": round(tf, 1),
+            "frac_of_bf16_peak": round(tf / BF16_PEAK_TFLOPS, 4),
+            "ms_sdpa": round(ms, 4), "ms_full_step": round(ms_step, 4),
+            "kernel_us": {k: round(v[0] / max(v[1], 1) * 1e3, 1) for k, v in kt.items()},
+            "roofline_main": {"kernel": "mfma_main", "bound": "mfma",
+                              "achieved": round(ach_main, 1), "peak": BF16_PEAK_TFLOPS,
+                              "unit": "TFLOP/s", "frac": round(ach_main / BF16_PEAK_TFLOPS, 4),
+                              "traffic": traffic_for("mfma_main", ["sdpa_mfma.hip"])}}
+
+
+# -------------------------------------------------------------- CPU baseline
+def cpu_baseline(w, budget_s, W):
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count()
+    x = W.make_inputs(w, seed=0)
+    state = (x["k_cache"], x["v_cache"], x["scores"], x["token_pos"])
+    n, t0 = 0, time.perf_counter()
+    while True:
+        s = n % w.steps
+        r = oracle.h2o_step(*state, x["q_steps"][s], x["k_new_steps"][s], x["v_new_steps"][s],
+                            int(x["pos0"]) + n, x["scale"])
+        state = (r["k_cache"], r["v_cache"], r["scores"], r["token_pos"])
+        n += 1
+        if time.perf_counter() - t0 > budget_s or n >= 64:
+            break
+    dt = (time.perf_counter() - t0) / n
+    return {"value": round(decode_step_bytes(w) / dt / 1e9, 4), "unit": "GB/s",
+            "cores": int(threads), "kind": "oracle",
+            "sample": f"{n} token steps of one layer state ({w.describe()}), float64 numpy",
+            "s_per_step": round(dt, 3)}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--cpu-budget", type=float, default=15.0,
+                    help="seconds of oracle work for the CPU baseline (0 = skip)")
+    ap.add_argument("--no-prefill", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py: this build runs on one GPU only; use --gpus 1", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2608_19920_amd import h2o as H
+    from paper_2608_19920_amd import workloads as W
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    H.lib()
+    print(f"# bench: decode {LAYERS} layer states, steps {args.steps}", file=sys.stderr, flush=True)
+    dec = bench_decode(args, torch, H, W)
+    print(f"# decode: {dec['ms_step']*1e3:.1f} us/step, {dec['value']:.0f} GB/s", file=sys.stderr,
+          flush=True)
+    prefill = []
+    if not args.no_prefill:
+        for name in PREFILL:
+            r = bench_prefill(name, args, torch, H, W)
+            print(f"# {name}: {r['tflops']} TFLOP/s", file=sys.stderr, flush=True)
+            prefill.append(r)
+            torch.cuda.empty_cache()
+    w = dec["w"]
+    cpu = None
+    if args.cpu_budget > 0:
+        cpu = cpu_baseline(w, args.cpu_budget, W)
+        print(f"# cpu oracle: {cpu['value']} GB/s on {cpu['cores']} threads", file=sys.stderr,
+              flush=True)
+    rec = {
+        "metric": METRIC, "value": round(dec["value"], 1), "unit": "GB/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(dec["ms_step"], 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"decode_bf16 token step over {LAYERS} layer states "
+                               f"(hipGraph replay)", "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv,
+                   "d": w.d, "M": w.M, "T": w.T, "layers": LAYERS,
+                   "bytes_per_step": dec["step_bytes"],
+                   "frac_of_hbm_peak": round(dec["value"] / HBM_PEAK_GBS, 4)},
+        "roofline": dec["roofline"],
+        "cpu_baseline": cpu,
+        "prefill": prefill,
+    }
+    print(json.dumps(rec))
+
+
+if __name__ == "__main__":
+    main()

@@ -137,6 +137,19 @@ const char* h2o_last_error(void);
  * H2O_EINVAL for other values. */
 int h2o_debug_force_path(int path);
 
+/* Benchmark hook, not needed in normal use. h2o_debug_timing(1) makes every
+ * kernel launch of the library record a start and a stop event on the launch
+ * stream (do not use it under stream capture); h2o_debug_timing(0) stops it.
+ * Either call clears the totals. h2o_debug_kernel_time(id, &ms, &n) waits for
+ * the recorded events and returns the summed duration (milliseconds) and the
+ * launch count of kernel `id` since the last h2o_debug_timing call. Ids:
+ *   0 generic lse pass   1 generic main pass   2 MFMA lse pass
+ *   3 MFMA main pass     4 split reduce        5 column-sum reduce
+ *   6 accumulate         7 bottom-k            8 insert
+ *   9 decode split      10 decode combine     11 argmin + insert (k == 1) */
+int h2o_debug_timing(int on);
+int h2o_debug_kernel_time(int kernel_id, double* total_ms, long* count);
+
 /* Library version string. */
 const char* h2o_version(void);
 

@@ -8,6 +8,7 @@
 #include <cstring>
 #include <mutex>
 #include <string>
+#include <vector>
 
 #include "../../include/h2o.h"
 #include "internal.h"
@@ -17,6 +18,28 @@ namespace {
 
 thread_local std::string g_last_error;
 std::atomic<int> g_forced_path{-1};
+
+// Timing hook state: pending (kernel id, start, stop) event triples and the
+// per-kernel totals folded in by h2o_debug_kernel_time.
+std::atomic<bool> g_timing{false};
+std::mutex g_timing_mu;
+struct Pending { int id; hipEvent_t a, b; };
+std::vector<Pending> g_pending;
+double g_total_ms[K_COUNT];
+long g_count[K_COUNT];
+
+void fold_pending() {
+  for (auto& p : g_pending) {
+    float ms = 0.f;
+    if (hipEventSynchronize(p.b) == hipSuccess && hipEventElapsedTime(&ms, p.a, p.b) == hipSuccess) {
+      g_total_ms[p.id] += ms;
+      g_count[p.id] += 1;
+    }
+    (void)hipEventDestroy(p.a);
+    (void)hipEventDestroy(p.b);
+  }
+  g_pending.clear();
+}
 
 int fail(int code, const char* fmt, ...) {
   char buf[512];
@@ -74,6 +97,25 @@ int check_shape(int B, int Hq, int Hkv, int T, int M, int d) {
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 }  // namespace
+
+LaunchTimer::LaunchTimer(int kid, hipStream_t s) : id(kid), st(s), ev0(nullptr) {
+  if (!g_timing.load()) return;
+  hipEvent_t a;
+  if (hipEventCreate(&a) != hipSuccess) return;
+  if (hipEventRecord(a, st) != hipSuccess) { (void)hipEventDestroy(a); return; }
+  ev0 = a;
+}
+
+LaunchTimer::~LaunchTimer() {
+  if (!ev0) return;
+  hipEvent_t a = static_cast<hipEvent_t>(ev0), b;
+  if (hipEventCreate(&b) != hipSuccess || hipEventRecord(b, st) != hipSuccess) {
+    (void)hipEventDestroy(a);
+    return;
+  }
+  std::lock_guard<std::mutex> lk(g_timing_mu);
+  g_pending.push_back({id, a, b});
+}
 
 Plan make_plan(const Shape& s, int dtype) {
   Plan p{};
@@ -146,6 +188,26 @@ const char* h2o_last_error(void) { return g_last_error.c_str(); }
 int h2o_debug_force_path(int path) {
   if (path < -1 || path > 2) return fail(H2O_EINVAL, "path must be -1..2");
   g_forced_path.store(path);
+  return ok();
+}
+
+// Timing hook for benchmarks: while on, every kernel launch is bracketed by
+// events on its stream. Switching it (on or off) clears the totals.
+int h2o_debug_timing(int on) {
+  std::lock_guard<std::mutex> lk(g_timing_mu);
+  fold_pending();
+  for (int i = 0; i < K_COUNT; ++i) { g_total_ms[i] = 0.0; g_count[i] = 0; }
+  g_timing.store(on != 0);
+  return ok();
+}
+
+int h2o_debug_kernel_time(int kernel_id, double* total_ms, long* count) {
+  if (kernel_id < 0 || kernel_id >= K_COUNT || !total_ms || !count)
+    return fail(H2O_EINVAL, "kernel id out of range or null output");
+  std::lock_guard<std::mutex> lk(g_timing_mu);
+  fold_pending();
+  *total_ms = g_total_ms[kernel_id];
+  *count = g_count[kernel_id];
   return ok();
 }
 
@@ -245,10 +307,17 @@ int h2o_evict_insert(void* k_cache, void* v_cache, float* scores, int32_t* token
   int rc = check_device();
   if (rc) return rc;
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  hipError_t e = launch_bottomk(scores, B * Hkv, M, k, evict_idx, st);
-  if (e == hipSuccess)
-    e = launch_insert(k_cache, v_cache, scores, token_pos, k_new, v_new, wsum, evict_idx,
-                      B * Hkv, M, T, d, k, pos0, dtype == H2O_F32 ? 4 : 2, st);
+  const int eb = dtype == H2O_F32 ? 4 : 2;
+  hipError_t e;
+  if (k == 1) {
+    e = launch_argmin_insert(k_cache, v_cache, scores, token_pos, k_new, v_new, wsum, evict_idx,
+                             B * Hkv, M, T, d, pos0, eb, st);
+  } else {
+    e = launch_bottomk(scores, B * Hkv, M, k, evict_idx, st);
+    if (e == hipSuccess)
+      e = launch_insert(k_cache, v_cache, scores, token_pos, k_new, v_new, wsum, evict_idx,
+                        B * Hkv, M, T, d, k, pos0, eb, st);
+  }
   if (e != hipSuccess) return fail(H2O_ELAUNCH, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
 }

@@ -61,18 +61,18 @@ __global__ __launch_bounds__(kThreads) void decode_split(
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int kg = tid / kLanesPerKey, slice = tid % kLanesPerKey;
 
+  // Rows past the block's last slot re-read that slot (always in bounds) and
+  // are masked below, so every load is unconditional and issued up front.
   uint4 kr[kRounds][VPL], vr[kRounds][VPL];
   const bf16_t* kbase = kc + (bh * M + j0) * (size_t)D + slice * EPL;
   const bf16_t* vbase = vc + (bh * M + j0) * (size_t)D + slice * EPL;
 #pragma unroll
   for (int rd = 0; rd < kRounds; ++rd) {
-    const int kk = rd * kKeysPerRound + kg;
+    const int kk = min(rd * kKeysPerRound + kg, n - 1);
 #pragma unroll
     for (int v = 0; v < VPL; ++v) {
-      kr[rd][v] = kk < n ? *reinterpret_cast<const uint4*>(kbase + (size_t)kk * D + 8 * v)
-                         : make_uint4(0, 0, 0, 0);
-      vr[rd][v] = kk < n ? *reinterpret_cast<const uint4*>(vbase + (size_t)kk * D + 8 * v)
-                         : make_uint4(0, 0, 0, 0);
+      kr[rd][v] = *reinterpret_cast<const uint4*>(kbase + (size_t)kk * D + 8 * v);
+      vr[rd][v] = *reinterpret_cast<const uint4*>(vbase + (size_t)kk * D + 8 * v);
     }
   }
   float qs[G][EPL];
@@ -172,6 +172,11 @@ __global__ __launch_bounds__(kThreads) void decode_split(
   }
 }
 
+// Block (x, bh): merges the splits of head bh (every block recomputes the
+// few per-head statistics), then writes wsum for columns [x*kCols, +kCols);
+// block x == 0 also writes out and lse.
+constexpr int kCols = 1024;
+
 template <int D>
 __global__ __launch_bounds__(kThreads) void decode_combine(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ kn, const bf16_t* __restrict__ vn,
@@ -181,7 +186,7 @@ __global__ __launch_bounds__(kThreads) void decode_combine(
   constexpr int kMaxG = kMaxGD / 64;
   __shared__ float lnew[kMaxG], lam[kMaxG], mfin[kMaxG], linv[kMaxG];
   const int G = Hq / Hkv;
-  const size_t bh = blockIdx.x;
+  const size_t bh = blockIdx.y;
   const int b = (int)(bh / Hkv), h = (int)(bh % Hkv);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   // logit of the chunk's own key for each query head (one wave per head)
@@ -207,25 +212,28 @@ __global__ __launch_bounds__(kThreads) void decode_combine(
     lam[g] = lm;
     mfin[g] = mx;
     linv[g] = 1.f / L;
-    lse[(size_t)(b * Hq + h * G + g)] = lm * kLn2;
+    if (blockIdx.x == 0) lse[(size_t)(b * Hq + h * G + g)] = lm * kLn2;
   }
   __syncthreads();
-  for (int c = tid; c < G * D; c += kThreads) {
-    const int g = c / D, dd = c % D;
-    float a = __builtin_amdgcn_exp2f(lnew[g] - mfin[g]) * bf16_to_f32(vn[bh * D + dd]);
-    for (int s = 0; s < nsplit; ++s)
-      a = fmaf(dO[(bh * nsplit + s) * (size_t)(G * D) + c],
-               __builtin_amdgcn_exp2f(dstat[(bh * nsplit + s) * G + g].x - mfin[g]), a);
-    out[(size_t)(b * Hq + h * G + g) * D + dd] = f32_to_bf16(a * linv[g]);
+  if (blockIdx.x == 0) {
+    for (int c = tid; c < G * D; c += kThreads) {
+      const int g = c / D, dd = c % D;
+      float a = __builtin_amdgcn_exp2f(lnew[g] - mfin[g]) * bf16_to_f32(vn[bh * D + dd]);
+      for (int s = 0; s < nsplit; ++s)
+        a = fmaf(dO[(bh * nsplit + s) * (size_t)(G * D) + c],
+                 __builtin_amdgcn_exp2f(dstat[(bh * nsplit + s) * G + g].x - mfin[g]), a);
+      out[(size_t)(b * Hq + h * G + g) * D + dd] = f32_to_bf16(a * linv[g]);
+    }
   }
   float* w = wsum + bh * (size_t)(M + 1);
-  for (int j = tid; j < M; j += kThreads) {
+  const int c0 = blockIdx.x * kCols, c1 = min(M, c0 + kCols);
+  for (int j = c0 + tid; j < c1; j += kThreads) {
     float a = 0.f;
     for (int g = 0; g < G; ++g)
       a += __builtin_amdgcn_exp2f(logits[(bh * G + g) * (size_t)M + j] - lam[g]);
     w[j] = a;
   }
-  if (tid == 0) {
+  if (blockIdx.x == 0 && tid == 0) {
     float a = 0.f;
     for (int g = 0; g < G; ++g) a += __builtin_amdgcn_exp2f(lnew[g] - lam[g]);
     w[M] = a;
@@ -260,6 +268,7 @@ hipError_t launch_sdpa_decode(const Shape& s, const Plan& p, const void* q, cons
   if (s.M > 0) {
     dim3 grid(ns, s.BH());
     const int G = s.G();
+    LaunchTimer lt(K_DECODE_SPLIT, st);
 #define H2O_SPLIT(DD, GG) \
   launch_split<DD, GG>(grid, st, q, kc, vc, s.Hq, s.Hkv, s.M, c, logits, dstat, dO)
     if (s.d == 64) {
@@ -278,12 +287,14 @@ hipError_t launch_sdpa_decode(const Shape& s, const Plan& p, const void* q, cons
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
+  LaunchTimer lt(K_DECODE_COMBINE, st);
+  const dim3 cgrid(s.M > 0 ? (s.M + kCols - 1) / kCols : 1, s.BH());
   if (s.d == 64)
-    decode_combine<64><<<s.BH(), kThreads, 0, st>>>(
+    decode_combine<64><<<cgrid, kThreads, 0, st>>>(
         (const bf16_t*)q, (const bf16_t*)kn, (const bf16_t*)vn, s.Hq, s.Hkv, s.M, ns, c, logits,
         dstat, dO, (bf16_t*)out, lse, wsum);
   else
-    decode_combine<128><<<s.BH(), kThreads, 0, st>>>(
+    decode_combine<128><<<cgrid, kThreads, 0, st>>>(
         (const bf16_t*)q, (const bf16_t*)kn, (const bf16_t*)vn, s.Hq, s.Hkv, s.M, ns, c, logits,
         dstat, dO, (bf16_t*)out, lse, wsum);
   return hipGetLastError();

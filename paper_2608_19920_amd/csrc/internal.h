@@ -67,6 +67,22 @@ int mfma_rows_per_part();    // packed rows per colsum partial of the MFMA kerne
 int decode_nsplit(int M);    // split blocks of the decode kernels for M cache slots
 bool decode_supports(int d, int G);   // (d, G) pairs the decode kernels handle
 
+// ------------------------------------------------------------ kernel timing
+// Identifiers of every kernel the library launches (for the timing hook).
+enum KernelId {
+  K_GENERIC_LSE = 0, K_GENERIC_MAIN, K_MFMA_LSE, K_MFMA_MAIN, K_SPLIT_REDUCE, K_COLSUM_REDUCE,
+  K_ACCUMULATE, K_BOTTOMK, K_INSERT, K_DECODE_SPLIT, K_DECODE_COMBINE, K_ARGMIN_INSERT, K_COUNT
+};
+// While timing is switched on (h2o_debug_timing), a LaunchTimer brackets one
+// kernel launch with two events recorded on the launch stream.
+struct LaunchTimer {
+  LaunchTimer(int id, hipStream_t st);
+  ~LaunchTimer();
+  int id;
+  hipStream_t st;
+  void* ev0;
+};
+
 // ------------------------------------------------------------- launchers
 // Each returns hipSuccess or the launch error. They assume validated inputs.
 hipError_t launch_sdpa_generic(const Shape& s, const Plan& p, int dtype, const void* q,
@@ -86,6 +102,10 @@ hipError_t launch_accumulate(float* scores, const float* wsum, int rows, int M, 
                              hipStream_t st);
 hipError_t launch_bottomk(const float* scores, int rows, int M, int k, int32_t* idx,
                           hipStream_t st);
+hipError_t launch_argmin_insert(void* kc, void* vc, float* scores, int32_t* token_pos,
+                                const void* kn, const void* vn, const float* wsum, int32_t* idx,
+                                int rows, int M, int T, int d, int32_t pos0, int elem_bytes,
+                                hipStream_t st);
 hipError_t launch_insert(void* kc, void* vc, float* scores, int32_t* token_pos,
                          const void* kn, const void* vn, const float* wsum,
                          const int32_t* idx, int rows, int M, int T, int d, int k,

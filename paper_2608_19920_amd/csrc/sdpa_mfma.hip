@@ -31,6 +31,7 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));   // 16 bytes, register type
 
 constexpr int BN = 32;   // keys per tile
 
@@ -63,12 +64,32 @@ __device__ __forceinline__ float colsum16(float a0, float a1, float a2, float a3
 }
 
 __host__ __device__ constexpr int kstride(int D) { return D + 8; }   // bf16 per K row in LDS
-constexpr int VSTR = BN + 8;                                        // bf16 per V^T row in LDS
 
-// Position of key kk (0..31) of a tile inside a V^T row: lane group g reads
-// 8 consecutive entries that hold keys {4g..4g+3, 16+4g..16+4g+3}.
-__device__ __forceinline__ int vt_pos(int kk) {
-  return 8 * ((kk & 15) >> 2) + 4 * (kk >> 4) + (kk & 3);
+
+// V operand of O^T = V^T P^T. The V tile sits in LDS like the K tile
+// ([key][d]) and the transposing LDS read ds_read_b64_tr_b16 builds the
+// operand: within each 16-lane group, lane i receives element
+// i%4 of the 8-byte chunks addressed by lanes 4k + i/4, k = 0..3. Lane
+// 4k + c of group g therefore addresses row (key) 4g + k, columns
+// 16*db + 4c..+3, and lane i ends up with V[4g + k][16*db + i] - the keys of
+// k-index (g, k) in the P^T operand.
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+
+__device__ __forceinline__ s16x4 lds_read_tr16(const bf16_t* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (lds_s16x4*)((__attribute__((address_space(3))) bf16_t*)(p)));
+}
+
+template <int D>
+__device__ __forceinline__ bf16x8 v_operand(const bf16_t* Vs, int db, int lane) {
+  const int g = lane >> 4, i = lane & 15;
+  const bf16_t* base = Vs + (4 * g + (i >> 2)) * kstride(D) + 16 * db + 4 * (i & 3);
+  const s16x4 lo = lds_read_tr16(base);                       // keys 4g + k
+  const s16x4 hi = lds_read_tr16(base + 16 * kstride(D));     // keys 16 + 4g + k
+  typedef short s16x8 __attribute__((ext_vector_type(8)));
+  const s16x8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  return __builtin_bit_cast(bf16x8, v);
 }
 
 struct Geo {
@@ -82,34 +103,36 @@ __device__ __forceinline__ const bf16_t* kv_row(const bf16_t* cache, const bf16_
   return j < M ? cache + (bh * M + j) * (size_t)D : fresh + (bh * T + (j - M)) * (size_t)D;
 }
 
-// Stage the 32-key K tile starting at column j0 into Ks[key][d].
+// K/V tiles travel global -> registers -> LDS. The loads for tile t+1 are
+// issued before tile t is computed and stored to the other LDS buffer after
+// it, so one barrier per tile suffices. Key rows past the last column re-read
+// that column (always in bounds); they are masked as invisible chunk keys.
+// Thread chunk e covers row (tid + e*NT) / (D/8), 16-byte part (tid + e*NT) % (D/8).
 template <int D, int NT>
-__device__ __forceinline__ void stage_k(bf16_t* Ks, const Geo& g, size_t bh, int j0) {
-  constexpr int CH = D / 8;
-  for (int c = threadIdx.x; c < BN * CH; c += NT) {
-    const int kk = c / CH, part = c % CH, j = j0 + kk;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (j < g.Nk) v = *reinterpret_cast<const uint4*>(kv_row(g.kc, g.kn, bh, j, g.M, g.T, D) + part * 8);
-    *reinterpret_cast<uint4*>(Ks + kk * kstride(D) + part * 8) = v;
+struct Tile {
+  static constexpr int CH = D / 8;          // 16-byte chunks per row
+  static constexpr int N = BN * CH / NT;    // chunks per thread per tile
+};
+
+template <int D, int NT, int N>
+__device__ __forceinline__ void load_rows(u32x4 (&r)[N], const bf16_t* cache,
+                                          const bf16_t* fresh, const Geo& g, size_t bh, int j0) {
+  constexpr int CH = Tile<D, NT>::CH;
+#pragma unroll
+  for (int e = 0; e < N; ++e) {
+    const int c = threadIdx.x + e * NT, kk = c / CH, part = c % CH;
+    const int j = min(j0 + kk, g.Nk - 1);
+    r[e] = *reinterpret_cast<const u32x4*>(kv_row(cache, fresh, bh, j, g.M, g.T, D) + part * 8);
   }
 }
 
-// Stage the V tile transposed: Vt[d][vt_pos(key)].
-template <int D, int NT>
-__device__ __forceinline__ void stage_vt(bf16_t* Vt, const Geo& g, size_t bh, int j0) {
-  constexpr int CH = D / 8;
-  for (int c = threadIdx.x; c < (BN / 2) * CH; c += NT) {
-    const int pair = c / CH, part = c % CH, kk = 2 * pair, j = j0 + kk;
-    uint4 a = make_uint4(0, 0, 0, 0), b = make_uint4(0, 0, 0, 0);
-    if (j < g.Nk) a = *reinterpret_cast<const uint4*>(kv_row(g.vc, g.vn, bh, j, g.M, g.T, D) + part * 8);
-    if (j + 1 < g.Nk) b = *reinterpret_cast<const uint4*>(kv_row(g.vc, g.vn, bh, j + 1, g.M, g.T, D) + part * 8);
-    const uint32_t av[4] = {a.x, a.y, a.z, a.w}, bv[4] = {b.x, b.y, b.z, b.w};
-    uint32_t* dst = reinterpret_cast<uint32_t*>(Vt + (part * 8) * VSTR + vt_pos(kk));
+template <int D, int NT, int N>
+__device__ __forceinline__ void store_rows(bf16_t* lds, const u32x4 (&r)[N]) {
+  constexpr int CH = Tile<D, NT>::CH;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      dst[(2 * e) * (VSTR / 2)] = (av[e] & 0xFFFFu) | (bv[e] << 16);
-      dst[(2 * e + 1) * (VSTR / 2)] = (av[e] >> 16) | (bv[e] & 0xFFFF0000u);
-    }
+  for (int e = 0; e < N; ++e) {
+    const int c = threadIdx.x + e * NT, kk = c / CH, part = c % CH;
+    *reinterpret_cast<u32x4*>(lds + kk * kstride(D) + part * 8) = r[e];
   }
 }
 
@@ -125,7 +148,7 @@ __device__ __forceinline__ void load_q(bf16x8 (&qf)[NQB][D / 32], const Geo& g, 
     const bf16_t* src = g.q + ((size_t)(b * Hq + h * g.G + gg) * g.T + i) * D + 8 * (lane >> 4);
 #pragma unroll
     for (int s = 0; s < D / 32; ++s) {
-      uint4 v = ok ? *reinterpret_cast<const uint4*>(src + 32 * s) : make_uint4(0, 0, 0, 0);
+      const u32x4 v = ok ? *reinterpret_cast<const u32x4*>(src + 32 * s) : u32x4{0u, 0u, 0u, 0u};
       qf[qb][s] = __builtin_bit_cast(bf16x8, v);
     }
   }
@@ -161,7 +184,7 @@ template <int D, int NW, int NQB>
 __global__ __launch_bounds__(NW * 64) void lse_pass(Geo g, int Hq, int Hkv, int nsplit,
                                                     float c_log2, float2* __restrict__ stats) {
   constexpr int NT = NW * 64, ROWS = NW * NQB * 16;
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[BN * kstride(D)];
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[2][BN * kstride(D)];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int rt = blockIdx.x / nsplit, sp = blockIdx.x % nsplit;
   const size_t bh = blockIdx.y;
@@ -182,13 +205,15 @@ __global__ __launch_bounds__(NW * 64) void lse_pass(Geo g, int Hq, int Hkv, int 
 #pragma unroll
   for (int qb = 0; qb < NQB; ++qb) { m[qb] = -INFINITY; l[qb] = 0.f; }
 
+  u32x4 pk[Tile<D, NT>::N];
+  load_rows<D, NT>(pk, g.kc, g.kn, g, bh, t0 * BN);
+  store_rows<D, NT>(Ks[0], pk);
+  __syncthreads();
   for (int t = t0; t < t1; ++t) {
-    const int j0 = t * BN;
-    __syncthreads();
-    stage_k<D, NT>(Ks, g, bh, j0);
-    __syncthreads();
+    const int j0 = t * BN, cur = (t - t0) & 1;
+    load_rows<D, NT>(pk, g.kc, g.kn, g, bh, min(t + 1, t1 - 1) * BN);
     f32x4 sacc[2][NQB];
-    scores_tile<D, NQB>(sacc, Ks, qf, lane);
+    scores_tile<D, NQB>(sacc, Ks[cur], qf, lane);
     const bool full = j0 + BN - 1 - g.M <= i_min;
 #pragma unroll
     for (int qb = 0; qb < NQB; ++qb) {
@@ -214,6 +239,8 @@ __global__ __launch_bounds__(NW * 64) void lse_pass(Geo g, int Hq, int Hkv, int 
       l[qb] = acc;
       m[qb] = mn;
     }
+    store_rows<D, NT>(Ks[cur ^ 1], pk);
+    __syncthreads();
   }
   // merge the four lane groups (disjoint key subsets of the same query)
 #pragma unroll
@@ -240,8 +267,8 @@ __global__ __launch_bounds__(NW * 64) void main_pass(Geo g, int Hq, int Hkv, int
                                                      float* __restrict__ opart,
                                                      float* __restrict__ lse_out) {
   constexpr int NT = NW * 64, ROWS = NW * NQB * 16;
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[BN * kstride(D)];
-  __shared__ __attribute__((aligned(16))) bf16_t Vt[D * VSTR];
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[2][BN * kstride(D)];
+  __shared__ __attribute__((aligned(16))) bf16_t Vs[2][BN * kstride(D)];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int rt = blockIdx.x / nsplit, sp = blockIdx.x % nsplit;
   const size_t bh = blockIdx.y;
@@ -287,14 +314,19 @@ __global__ __launch_bounds__(NW * 64) void main_pass(Geo g, int Hq, int Hkv, int
 
   float* prow = parts + ((size_t)(rt * NW + wave) * BH + bh) * g.Nk;
 
+  u32x4 pk[Tile<D, NT>::N], pv[Tile<D, NT>::N];
+  load_rows<D, NT>(pk, g.kc, g.kn, g, bh, t0 * BN);
+  load_rows<D, NT>(pv, g.vc, g.vn, g, bh, t0 * BN);
+  store_rows<D, NT>(Ks[0], pk);
+  store_rows<D, NT>(Vs[0], pv);
+  __syncthreads();
   for (int t = t0; t < t1; ++t) {
-    const int j0 = t * BN;
-    __syncthreads();
-    stage_k<D, NT>(Ks, g, bh, j0);
-    stage_vt<D, NT>(Vt, g, bh, j0);
-    __syncthreads();
+    const int j0 = t * BN, cur = (t - t0) & 1;
+    const int jn = min(t + 1, t1 - 1) * BN;
+    load_rows<D, NT>(pk, g.kc, g.kn, g, bh, jn);
+    load_rows<D, NT>(pv, g.vc, g.vn, g, bh, jn);
     f32x4 sacc[2][NQB];
-    scores_tile<D, NQB>(sacc, Ks, qf, lane);
+    scores_tile<D, NQB>(sacc, Ks[cur], qf, lane);
     const bool full = j0 + BN - 1 - g.M <= i_min;
     bf16x8 pb[NQB];
     float cs[2][4];
@@ -327,11 +359,13 @@ __global__ __launch_bounds__(NW * 64) void main_pass(Geo g, int Hq, int Hkv, int
     // O^T += V^T P^T
 #pragma unroll
     for (int db = 0; db < D / 16; ++db) {
-      const bf16x8 a = *reinterpret_cast<const bf16x8*>(Vt + (db * 16 + (lane & 15)) * VSTR +
-                                                        8 * (lane >> 4));
+      const bf16x8 a = v_operand<D>(Vs[cur], db, lane);
 #pragma unroll
       for (int qb = 0; qb < NQB; ++qb) oacc[db][qb] = mfma(a, pb[qb], oacc[db][qb]);
     }
+    store_rows<D, NT>(Ks[cur ^ 1], pk);
+    store_rows<D, NT>(Vs[cur ^ 1], pv);
+    __syncthreads();
   }
   // write O (lane: query qb*16 + l%16, d = db*16 + 4*(l/16) + r)
 #pragma unroll
@@ -396,15 +430,22 @@ hipError_t run(const Shape& s, const Plan& p, const void* q, const void* kc, con
   float2* stats = reinterpret_cast<float2*>(ws + p.off_stats);
   float* parts = reinterpret_cast<float*>(ws + p.off_parts);
   float* opart = reinterpret_cast<float*>(ws + p.off_opart);
-  lse_pass<D, NW, NQB><<<grid, NW * 64, 0, st>>>(g, s.Hq, s.Hkv, p.nsplit, c, stats);
+  {
+    LaunchTimer lt(K_MFMA_LSE, st);
+    lse_pass<D, NW, NQB><<<grid, NW * 64, 0, st>>>(g, s.Hq, s.Hkv, p.nsplit, c, stats);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  main_pass<D, NW, NQB><<<grid, NW * 64, 0, st>>>(g, s.Hq, s.Hkv, p.nsplit, c, stats, parts,
-                                                  (bf16_t*)out, opart, lse);
+  {
+    LaunchTimer lt(K_MFMA_MAIN, st);
+    main_pass<D, NW, NQB><<<grid, NW * 64, 0, st>>>(g, s.Hq, s.Hkv, p.nsplit, c, stats, parts,
+                                                    (bf16_t*)out, opart, lse);
+  }
   e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (p.nsplit > 1) {
     const size_t n4 = (size_t)s.BH() * s.R() * s.d / 4;
+    LaunchTimer lt(K_SPLIT_REDUCE, st);
     split_reduce<D><<<(unsigned)((n4 + 255) / 256), 256, 0, st>>>(
         opart, (bf16_t*)out, s.Hq, s.Hkv, s.G(), s.T, s.R(), s.BH(), p.nsplit);
     e = hipGetLastError();

@@ -179,11 +179,70 @@ __global__ __launch_bounds__(kInsThreads) void insert_kernel(
   }
 }
 
+// k == 1 (token generation): the (score, slot)-smallest slot of each row and
+// the insert into it, one block per row.
+constexpr int kArgThreads = 256;
+
+__global__ __launch_bounds__(kArgThreads) void argmin_insert_kernel(
+    uint4* __restrict__ kc, uint4* __restrict__ vc, float* __restrict__ scores,
+    int32_t* __restrict__ token_pos, const uint4* __restrict__ kn, const uint4* __restrict__ vn,
+    const float* __restrict__ wsum, int32_t* __restrict__ idx, int M, int T, int vecs,
+    int32_t pos0) {
+  __shared__ uint32_t red_hi[kArgThreads / 64], red_lo[kArgThreads / 64];
+  __shared__ int sh_slot;
+  const size_t row = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const float* s = scores + row * M;
+  uint32_t bk = 0xFFFFFFFFu, bj = 0xFFFFFFFFu;     // (key, slot), lexicographic
+  for (int j = tid; j < M; j += kArgThreads) {
+    const uint32_t key = order_key(s[j]);
+    if (key < bk || (key == bk && (uint32_t)j < bj)) { bk = key; bj = (uint32_t)j; }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint32_t ok = __shfl_xor(bk, o, 64), oj = __shfl_xor(bj, o, 64);
+    if (ok < bk || (ok == bk && oj < bj)) { bk = ok; bj = oj; }
+  }
+  if (lane == 0) { red_hi[wave] = bk; red_lo[wave] = bj; }
+  __syncthreads();
+  if (tid == 0) {
+    for (int w = 1; w < kArgThreads / 64; ++w)
+      if (red_hi[w] < bk || (red_hi[w] == bk && red_lo[w] < bj)) { bk = red_hi[w]; bj = red_lo[w]; }
+    const int slot = (int)bj;
+    sh_slot = slot;
+    idx[row] = slot;
+    if ((unsigned)slot < (unsigned)M) {
+      scores[row * M + slot] = wsum[row * (size_t)(M + T) + M];
+      if (token_pos) token_pos[row * M + slot] = pos0;
+    }
+  }
+  __syncthreads();
+  const int slot = sh_slot;
+  if ((unsigned)slot >= (unsigned)M) return;
+  for (int c = tid; c < vecs; c += kArgThreads) {
+    kc[(row * M + slot) * vecs + c] = kn[(row * T) * vecs + c];
+    vc[(row * M + slot) * vecs + c] = vn[(row * T) * vecs + c];
+  }
+}
+
 }  // namespace
+
+hipError_t launch_argmin_insert(void* kc, void* vc, float* scores, int32_t* token_pos,
+                                const void* kn, const void* vn, const float* wsum, int32_t* idx,
+                                int rows, int M, int T, int d, int32_t pos0, int elem_bytes,
+                                hipStream_t st) {
+  if (rows == 0) return hipSuccess;
+  LaunchTimer lt(K_ARGMIN_INSERT, st);
+  argmin_insert_kernel<<<rows, kArgThreads, 0, st>>>(
+      (uint4*)kc, (uint4*)vc, scores, token_pos, (const uint4*)kn, (const uint4*)vn, wsum, idx, M,
+      T, d * elem_bytes / 16, pos0);
+  return hipGetLastError();
+}
 
 hipError_t launch_colsum_reduce(const Shape& s, const Plan& p, const float* parts, float* wsum,
                                 hipStream_t st) {
   dim3 grid((s.Nk() + 255) / 256, s.BH());
+  LaunchTimer lt(K_COLSUM_REDUCE, st);
   colsum_reduce_kernel<<<grid, 256, 0, st>>>(parts, wsum, p.nparts, p.rows_per_part, s.BH(),
                                              s.Nk(), s.G(), s.T, s.M);
   return hipGetLastError();
@@ -194,6 +253,7 @@ hipError_t launch_accumulate(float* scores, const float* wsum, int rows, int M, 
   if (rows == 0 || M == 0) return hipSuccess;
   int bx = (M + 256 * 4 - 1) / (256 * 4);
   dim3 grid(bx < 1 ? 1 : bx, rows);
+  LaunchTimer lt(K_ACCUMULATE, st);
   accumulate_kernel<<<grid, 256, 0, st>>>(scores, wsum, M, T);
   return hipGetLastError();
 }
@@ -201,6 +261,7 @@ hipError_t launch_accumulate(float* scores, const float* wsum, int rows, int M, 
 hipError_t launch_bottomk(const float* scores, int rows, int M, int k, int32_t* idx,
                           hipStream_t st) {
   if (rows == 0 || k == 0) return hipSuccess;
+  LaunchTimer lt(K_BOTTOMK, st);
   bottomk_kernel<<<rows, kSelThreads, 0, st>>>(scores, M, k, idx);
   return hipGetLastError();
 }
@@ -213,6 +274,7 @@ hipError_t launch_insert(void* kc, void* vc, float* scores, int32_t* token_pos, 
   int kPer = kInsThreads / vecs;
   if (kPer < 1) kPer = 1;
   dim3 grid((k + kPer - 1) / kPer, rows);
+  LaunchTimer lt(K_INSERT, st);
   insert_kernel<<<grid, kInsThreads, 0, st>>>((uint4*)kc, (uint4*)vc, scores, token_pos,
                                               (const uint4*)kn, (const uint4*)vn, wsum, idx, M, T,
                                               vecs, k, kPer, pos0);

@@ -24,7 +24,11 @@ STATUS_NAMES = ["H2O_OK", "H2O_EINVAL", "H2O_ESHAPE", "H2O_EDTYPE", "H2O_EALIGN"
                 "H2O_EWORKSPACE", "H2O_ENODEVICE", "H2O_ELAUNCH"]
 EXPORTED = ["h2o_workspace_bytes", "h2o_sdpa_chunk", "h2o_accumulate_scores",
             "h2o_evict_insert", "h2o_bottomk", "h2o_last_error", "h2o_debug_force_path",
-            "h2o_version"]
+            "h2o_debug_timing", "h2o_debug_kernel_time", "h2o_version"]
+KERNEL_IDS = {"generic_lse": 0, "generic_main": 1, "mfma_lse": 2, "mfma_main": 3,
+              "split_reduce": 4, "colsum_reduce": 5, "accumulate": 6, "bottomk": 7,
+              "insert": 8, "decode_split": 9, "decode_combine": 10,
+              "argmin_insert": 11}
 
 
 class H2OError(RuntimeError):
@@ -61,6 +65,11 @@ def lib() -> ctypes.CDLL:
     L.h2o_last_error.restype = ctypes.c_char_p
     L.h2o_debug_force_path.argtypes = [i]
     L.h2o_debug_force_path.restype = i
+    L.h2o_debug_timing.argtypes = [i]
+    L.h2o_debug_timing.restype = i
+    L.h2o_debug_kernel_time.argtypes = [i, ctypes.POINTER(ctypes.c_double),
+                                        ctypes.POINTER(ctypes.c_long)]
+    L.h2o_debug_kernel_time.restype = i
     L.h2o_version.argtypes = []
     L.h2o_version.restype = ctypes.c_char_p
     _lib = L
@@ -102,6 +111,18 @@ def h2o_version() -> str:
 
 def h2o_debug_force_path(path: int) -> None:
     _check(lib().h2o_debug_force_path(int(path)))
+
+
+def h2o_debug_timing(on: bool) -> None:
+    _check(lib().h2o_debug_timing(1 if on else 0))
+
+
+def h2o_debug_kernel_time(kernel) -> tuple:
+    """(total milliseconds, launch count) of a kernel since h2o_debug_timing."""
+    kid = KERNEL_IDS[kernel] if isinstance(kernel, str) else int(kernel)
+    ms, n = ctypes.c_double(0.0), ctypes.c_long(0)
+    _check(lib().h2o_debug_kernel_time(kid, ctypes.byref(ms), ctypes.byref(n)))
+    return ms.value, n.value
 
 
 def h2o_workspace_bytes(B, Hq, Hkv, T, M, d, dtype) -> int:

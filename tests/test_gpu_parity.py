@@ -146,10 +146,31 @@ def test_bottomk_negative_and_huge_values():
         np.testing.assert_array_equal(U.gpu_bottomk(s, k), oracle.bottomk(s, k))
 
 
-@pytest.mark.parametrize("path", BF16_PATHS, indirect=True)
+DECODE_SHAPES = [(2, 4, 4, 128, 129, 1), (1, 32, 8, 64, 513, 1), (8, 32, 8, 64, 4096, 1),
+                 (3, 16, 2, 64, 1000, 1), (1, 2, 1, 64, 256, 1), (2, 8, 2, 128, 300, 1),
+                 (1, 8, 8, 64, 1, 1), (1, 4, 2, 64, 0, 1)]
+
+
+@pytest.mark.parametrize("shape", DECODE_SHAPES, ids=lambda s: "B%dHq%dHkv%dd%dM%dT%d" % s)
+def test_sdpa_decode_path(shape):
+    H.h2o_debug_force_path(2)
+    try:
+        say(f"decode path {shape}")
+        w = W.custom(**dict(zip("B Hq Hkv d M T".split(), shape)), dtype="bf16",
+                     heavy_frac=0.02)
+        x = W.make_inputs(w, seed=3)
+        res = U.run_sdpa(x["q"], x["k_cache"], x["v_cache"], x["k_new"], x["v_new"],
+                         x["scale"], "bf16")
+        _check_attention(x, "bf16", res, extra="decode path")
+    finally:
+        H.h2o_debug_force_path(-1)
+
+
+@pytest.mark.parametrize("path", BF16_PATHS + [2], indirect=True)
 def test_bitwise_repeatable(path):
     say(f"repeatability path {path}")
-    w = W.custom(B=1, Hq=8, Hkv=2, d=128, M=777, T=100, dtype="bf16", heavy_frac=0.02)
+    w = W.custom(B=1, Hq=8, Hkv=2, d=128, M=777, T=1 if path == 2 else 100, dtype="bf16",
+                 heavy_frac=0.02)
     x = W.make_inputs(w, seed=5)
     a = U.run_sdpa(x["q"], x["k_cache"], x["v_cache"], x["k_new"], x["v_new"], x["scale"], "bf16")
     b = U.run_sdpa(x["q"], x["k_cache"], x["v_cache"], x["k_new"], x["v_new"], x["scale"], "bf16")

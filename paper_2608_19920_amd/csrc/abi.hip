@@ -128,21 +128,27 @@ Plan make_plan(const Shape& s, int dtype) {
   if (path == 2 && (s.T != 1 || !decode_supports(s.d, s.G()))) path = 1;
   p.path = path;
   p.nsplit = 1;
+  p.nsplit_lse = 1;
+  p.parts_ld = (int)Nk;
   if (path == 1) {
     // Split the key range of each row tile when there are too few blocks to
-    // give every CU two workgroups; keep at least 8 key tiles per split.
+    // fill the CUs: the main pass runs one wave per SIMD (two 2-wave blocks per
+    // CU), the lse pass two. Keep at least 8 key tiles per split.
     const int rows_blk = mfma_rows_per_block();
     const long long nrt = (R + rows_blk - 1) / rows_blk;
     const long long blocks = nrt * (long long)BH;
     const long long ntiles = (Nk + 31) / 32;
-    long long ns = (512 + blocks - 1) / blocks;
-    long long cap = ntiles / 8;
-    if (ns > cap) ns = cap;
-    if (ns > 8) ns = 8;
-    if (ns < 1) ns = 1;
-    p.nsplit = (int)ns;
+    auto pick = [&](long long target, long long maxs) {
+      long long ns = (target + blocks - 1) / blocks;
+      if (ns > ntiles / 8) ns = ntiles / 8;
+      if (ns > maxs) ns = maxs;
+      return (int)(ns < 1 ? 1 : ns);
+    };
+    p.nsplit = pick(512, 8);
+    p.nsplit_lse = pick(1024, 16);
     p.rows_per_part = mfma_rows_per_part();
     p.nparts = (int)(nrt * (rows_blk / p.rows_per_part));
+    p.parts_ld = (int)((Nk + 31) / 32 * 32);
   } else if (path == 2) {
     p.nsplit = decode_nsplit(s.M);
     p.rows_per_part = 0;
@@ -163,9 +169,10 @@ Plan make_plan(const Shape& s, int dtype) {
   }
   size_t off = 0;
   p.off_stats = off;
-  off = align256(off + (size_t)p.nsplit * BH * R * sizeof(float) * 2);
+  off = align256(off + (size_t)(p.nsplit_lse > p.nsplit ? p.nsplit_lse : p.nsplit) * BH * R *
+                           sizeof(float) * 2);
   p.off_parts = off;
-  off = align256(off + (size_t)p.nparts * BH * Nk * sizeof(float));
+  off = align256(off + (size_t)p.nparts * BH * p.parts_ld * sizeof(float));
   p.off_opart = off;
   if (p.nsplit > 1) off = align256(off + (size_t)p.nsplit * BH * R * s.d * sizeof(float));
   p.off_logits = off;

@@ -54,7 +54,9 @@ struct Plan {
   int path;            // 0 = generic (float/bf16 VALU), 1 = bf16 MFMA, 2 = bf16 decode
   int rows_per_part;   // packed rows per colsum partial
   int nparts;          // partials per KV head
-  int nsplit;          // key-range splits per row tile (MFMA path)
+  int nsplit;          // key-range splits per row tile of the main pass (MFMA path)
+  int nsplit_lse;      // key-range splits per row tile of the lse pass (MFMA path)
+  int parts_ld;        // floats per colsum partial row (>= Nk)
   size_t off_stats;    // float2 (m, l) per (split, bh, row)  or lse per (bh,row)
   size_t off_parts;    // float colsum partials [nparts][BH][Nk]
   size_t off_opart;    // float O partials [nsplit][BH][R][d] (nsplit > 1)

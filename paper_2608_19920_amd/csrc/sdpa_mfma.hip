@@ -16,14 +16,14 @@
 // orientation. For a 16(key) x 16(query) block the accumulator lane l holds
 // keys 4*(l/16)+r (r = 0..3) of query l%16, which is exactly the layout of a
 // B operand of the next product O^T = V^T P^T (32 keys per MFMA), so P never
-// leaves registers. V^T is staged in LDS with the keys of each 32-key tile
-// permuted to match that layout. Row statistics reduce inside a lane; the
-// column sums reduce across the 16 lanes of a DPP row.
+// leaves registers. Row statistics reduce inside a lane; the column sums
+// reduce across the 16 lanes of a DPP row.
 //
 // Workgroup: NW waves, each owning NQB*16 consecutive packed rows
 // (r = i*G + g: chunk position i, query head h*G+g); all waves share one
 // 32-key K/V tile in LDS, so the K/V of a KV head is staged once for the G
-// query heads of its group.
+// query heads of its group. Tiles are double buffered: the global loads of
+// tile t+1 are in flight while tile t is computed.
 #include "internal.h"
 
 namespace h2o {
@@ -32,6 +32,9 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));   // 16 bytes, register type
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
 constexpr int BN = 32;   // keys per tile
 
@@ -50,6 +53,8 @@ constexpr int kQuadXor2 = 0x4E;   // quad_perm [2,3,0,1]
 
 // Sum of a[r] (key 4*(l/16)+r, this lane's query) over the 16 lanes of the
 // DPP row. Returns, in every lane, the total for key 4*(l/16) + (l%16)/4.
+// Each step hands half of the remaining values to the partner lane and keeps
+// the other half, so 4 values need 6 + 3 + 2 operations.
 __device__ __forceinline__ float colsum16(float a0, float a1, float a2, float a3, int lane) {
   const bool b3 = lane & 8, b2 = lane & 4;
   const float t0 = b3 ? a2 : a0, t1 = b3 ? a3 : a1;   // kept pair
@@ -63,19 +68,23 @@ __device__ __forceinline__ float colsum16(float a0, float a1, float a2, float a3
   return y;
 }
 
-__host__ __device__ constexpr int kstride(int D) { return D + 8; }   // bf16 per K row in LDS
-
+#ifndef H2O_KPAD
+#define H2O_KPAD 8
+#endif
+#ifndef H2O_VPAD
+#define H2O_VPAD 16
+#endif
+// bf16 per LDS row of the K and V tiles (row pitch 272 / 288 bytes at d=128)
+__host__ __device__ constexpr int kstride(int D) { return D + H2O_KPAD; }
+__host__ __device__ constexpr int vstride(int D) { return D + H2O_VPAD; }
 
 // V operand of O^T = V^T P^T. The V tile sits in LDS like the K tile
 // ([key][d]) and the transposing LDS read ds_read_b64_tr_b16 builds the
-// operand: within each 16-lane group, lane i receives element
-// i%4 of the 8-byte chunks addressed by lanes 4k + i/4, k = 0..3. Lane
-// 4k + c of group g therefore addresses row (key) 4g + k, columns
-// 16*db + 4c..+3, and lane i ends up with V[4g + k][16*db + i] - the keys of
-// k-index (g, k) in the P^T operand.
-typedef short s16x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
-
+// operand: within each 16-lane group, lane i receives element i%4 of the
+// 8-byte chunks addressed by lanes 4k + i/4, k = 0..3. Lane 4k + c of group
+// g therefore addresses row (key) 4g + k, columns 16*db + 4c..+3, and lane i
+// ends up with V[4g + k][16*db + i] - the keys of k-index (g, k) in the P^T
+// operand; a second read covers keys 16 + 4g + k.
 __device__ __forceinline__ s16x4 lds_read_tr16(const bf16_t* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
       (lds_s16x4*)((__attribute__((address_space(3))) bf16_t*)(p)));
@@ -84,10 +93,9 @@ __device__ __forceinline__ s16x4 lds_read_tr16(const bf16_t* p) {
 template <int D>
 __device__ __forceinline__ bf16x8 v_operand(const bf16_t* Vs, int db, int lane) {
   const int g = lane >> 4, i = lane & 15;
-  const bf16_t* base = Vs + (4 * g + (i >> 2)) * kstride(D) + 16 * db + 4 * (i & 3);
-  const s16x4 lo = lds_read_tr16(base);                       // keys 4g + k
-  const s16x4 hi = lds_read_tr16(base + 16 * kstride(D));     // keys 16 + 4g + k
-  typedef short s16x8 __attribute__((ext_vector_type(8)));
+  const bf16_t* base = Vs + (4 * g + (i >> 2)) * vstride(D) + 16 * db + 4 * (i & 3);
+  const s16x4 lo = lds_read_tr16(base);
+  const s16x4 hi = lds_read_tr16(base + 16 * vstride(D));
   const s16x8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
   return __builtin_bit_cast(bf16x8, v);
 }
@@ -98,42 +106,60 @@ struct Geo {
   const bf16_t *kc, *vc, *kn, *vn;
 };
 
-__device__ __forceinline__ const bf16_t* kv_row(const bf16_t* cache, const bf16_t* fresh,
-                                                size_t bh, int j, int M, int T, int D) {
-  return j < M ? cache + (bh * M + j) * (size_t)D : fresh + (bh * T + (j - M)) * (size_t)D;
-}
-
-// K/V tiles travel global -> registers -> LDS. The loads for tile t+1 are
-// issued before tile t is computed and stored to the other LDS buffer after
-// it, so one barrier per tile suffices. Key rows past the last column re-read
-// that column (always in bounds); they are masked as invisible chunk keys.
-// Thread chunk e covers row (tid + e*NT) / (D/8), 16-byte part (tid + e*NT) % (D/8).
+// ------------------------------------------------------------ tile staging
+// Thread chunk e of a tile is row (tid + e*NT) / (D/8), 16-byte part
+// (tid + e*NT) % (D/8); its byte offset inside a tile of global rows and
+// inside an LDS tile is fixed per thread, so a tile load is a uniform base
+// plus constant offsets. Rows past the last key column re-read that column
+// (always in bounds); they are masked as invisible chunk keys.
 template <int D, int NT>
 struct Tile {
-  static constexpr int CH = D / 8;          // 16-byte chunks per row
-  static constexpr int N = BN * CH / NT;    // chunks per thread per tile
+  static constexpr int CH = D / 8;
+  static constexpr int N = BN * CH / NT;
+  uint32_t goff[N];   // bytes from the tile's first global row
+  uint32_t loff[N];   // bytes from the LDS tile base (K tiles)
+  uint32_t vloff[N];  // bytes from the LDS tile base (V tiles)
+  int row[N], part[N];
+  __device__ __forceinline__ Tile() {
+#pragma unroll
+    for (int e = 0; e < N; ++e) {
+      const int c = threadIdx.x + e * NT;
+      row[e] = c / CH;
+      part[e] = c % CH;
+      goff[e] = (uint32_t)(row[e] * D + part[e] * 8) * 2u;
+      loff[e] = (uint32_t)(row[e] * kstride(D) + part[e] * 8) * 2u;
+      vloff[e] = (uint32_t)(row[e] * vstride(D) + part[e] * 8) * 2u;
+    }
+  }
 };
 
 template <int D, int NT, int N>
-__device__ __forceinline__ void load_rows(u32x4 (&r)[N], const bf16_t* cache,
-                                          const bf16_t* fresh, const Geo& g, size_t bh, int j0) {
-  constexpr int CH = Tile<D, NT>::CH;
+__device__ __forceinline__ void load_tile(u32x4 (&r)[N], const Tile<D, NT>& tl,
+                                          const bf16_t* cache_bh, const bf16_t* fresh_bh, int j0,
+                                          int M, int Nk) {
+  // Tiles wholly inside the cache or wholly inside the chunk have one base row.
+  const bool in_cache = j0 + BN <= M, in_chunk = j0 >= M && j0 + BN <= Nk;
+  if (in_cache || in_chunk) {
+    const char* base = reinterpret_cast<const char*>(
+        in_cache ? cache_bh + (size_t)j0 * D : fresh_bh + (size_t)(j0 - M) * D);
 #pragma unroll
-  for (int e = 0; e < N; ++e) {
-    const int c = threadIdx.x + e * NT, kk = c / CH, part = c % CH;
-    const int j = min(j0 + kk, g.Nk - 1);
-    r[e] = *reinterpret_cast<const u32x4*>(kv_row(cache, fresh, bh, j, g.M, g.T, D) + part * 8);
+    for (int e = 0; e < N; ++e) r[e] = *reinterpret_cast<const u32x4*>(base + tl.goff[e]);
+  } else {
+#pragma unroll
+    for (int e = 0; e < N; ++e) {
+      const int j = min(j0 + tl.row[e], Nk - 1);
+      const bf16_t* p = j < M ? cache_bh + (size_t)j * D : fresh_bh + (size_t)(j - M) * D;
+      r[e] = *reinterpret_cast<const u32x4*>(p + tl.part[e] * 8);
+    }
   }
 }
 
 template <int D, int NT, int N>
-__device__ __forceinline__ void store_rows(bf16_t* lds, const u32x4 (&r)[N]) {
-  constexpr int CH = Tile<D, NT>::CH;
+__device__ __forceinline__ void store_tile(bf16_t* lds, const uint32_t (&off)[N],
+                                           const u32x4 (&r)[N]) {
+  char* base = reinterpret_cast<char*>(lds);
 #pragma unroll
-  for (int e = 0; e < N; ++e) {
-    const int c = threadIdx.x + e * NT, kk = c / CH, part = c % CH;
-    *reinterpret_cast<u32x4*>(lds + kk * kstride(D) + part * 8) = r[e];
-  }
+  for (int e = 0; e < N; ++e) *reinterpret_cast<u32x4*>(base + off[e]) = r[e];
 }
 
 // Query fragments (B operand of S^T = K Q^T) for this wave's rows.
@@ -172,6 +198,9 @@ __device__ __forceinline__ void scores_tile(f32x4 (&sacc)[2][NQB], const bf16_t*
   }
 }
 
+// Key column j of a chunk is visible to chunk position i iff j < M or j-M <= i.
+__device__ __forceinline__ bool visible(int j, int M, int i) { return j < M || j - M <= i; }
+
 // Tiles [t0, t1) of a row tile's key range [0, ntiles*BN) for split sp.
 __device__ __forceinline__ void split_range(int ntiles, int nsplit, int sp, int& t0, int& t1) {
   const int per = (ntiles + nsplit - 1) / nsplit;
@@ -179,12 +208,106 @@ __device__ __forceinline__ void split_range(int ntiles, int nsplit, int sp, int&
   t1 = min(ntiles, t0 + per);
 }
 
+// Tiles are software pipelined over three LDS buffers: while the softmax
+// arithmetic of tile t runs, the MFMAs of S(t+1) are issued from the buffer
+// already holding tile t+1, and the global loads of tile t+2 are in flight;
+// tile t+2 then goes to the buffer tile t-1 used. One barrier per tile orders
+// the buffer reuse. Tiles whose columns some row of the block cannot see run
+// in a second loop with the causal mask applied; each loop body is straight
+// line so the compiler can interleave MFMA and VALU work.
+constexpr int NBUF = 3;
+
+// Instruction interleaving hints for the straight-line tile bodies:
+// sched_group_barrier(mask, n, id) asks the scheduler for n instructions of a
+// class (0x2 VALU, 0x8 MFMA) in order. The MFMAs of S(t+1) do not depend on
+// the softmax arithmetic of tile t, so they alternate with it.
+#ifndef H2O_INTERLEAVE
+#define H2O_INTERLEAVE 0
+#endif
+template <int NMFMA, int NVALU>
+__device__ __forceinline__ void interleave() {
+  if (!H2O_INTERLEAVE) return;
+#pragma unroll
+  for (int i = 0; i < NMFMA; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    __builtin_amdgcn_sched_group_barrier(0x002, NVALU, 0);
+  }
+}
+
+// First tile index at which some row of the block may see an invisible
+// column: tile t needs the mask iff t*BN + BN-1 - M > i_min.
+__device__ __forceinline__ int first_masked_tile(int M, int i_min) {
+  const int x = M + i_min - (BN - 1);          // mask needed iff t*BN > x
+  return x < 0 ? 0 : x / BN + 1;
+}
+
 // ------------------------------------------------------------------ pass A
+// Online (max, sum) update of one tile for every query of the wave. The
+// running maximum m is kept in raw score units (c > 0 keeps the order);
+// l sums exp2(c*(s - m)). Unmasked tiles have finite scores, so only masked
+// tiles need the guard for a maximum that is still -inf.
+template <bool MASKED, int NQB>
+__device__ __forceinline__ void lse_update(const f32x4 (&sacc)[2][NQB], float (&m)[NQB],
+                                           float (&l)[NQB], const int (&qi)[NQB], int j0, int M,
+                                           int lane, float c) {
+#pragma unroll
+  for (int qb = 0; qb < NQB; ++qb) {
+    float x[8];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float v = sacc[kb][qb][r];
+        if (MASKED && !visible(j0 + kb * 16 + 4 * (lane >> 4) + r, M, qi[qb])) v = -INFINITY;
+        x[kb * 4 + r] = v;
+      }
+    const float mn = __builtin_fmaxf(__builtin_fmaxf(__builtin_fmaxf(x[0], x[1]), x[2]),
+                     __builtin_fmaxf(__builtin_fmaxf(__builtin_fmaxf(x[3], x[4]), x[5]),
+                                     __builtin_fmaxf(__builtin_fmaxf(x[6], x[7]), m[qb])));
+    const float ms = (MASKED && mn == -INFINITY) ? 0.f : mn * c;
+    float acc = l[qb] * __builtin_amdgcn_exp2f(fmaf(m[qb], c, -ms));
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc += __builtin_amdgcn_exp2f(fmaf(x[e], c, -ms));
+    l[qb] = acc;
+    m[qb] = mn;
+  }
+}
+
+template <int D, int NT, int NQB>
+struct LseState {
+  f32x4 s_cur[2][NQB], s_nxt[2][NQB];
+  u32x4 pk[Tile<D, NT>::N];
+};
+
+template <bool MASKED, int D, int NT, int NQB>
+__device__ __forceinline__ void lse_loop(int ta, int tb, int t0, int t1, LseState<D, NT, NQB>& S,
+                                         const Tile<D, NT>& tl,
+                                         bf16_t (*Ks)[BN * kstride(D)],
+                                         const bf16x8 (&qf)[NQB][D / 32], float (&m)[NQB],
+                                         float (&l)[NQB], const int (&qi)[NQB],
+                                         const bf16_t* kc_bh, const bf16_t* kn_bh, const Geo& g,
+                                         int lane, float c) {
+  for (int t = ta; t < tb; ++t) {
+    const int j0 = t * BN;
+    const int b1 = (t + 1 - t0) % NBUF, b2 = (t + 2 - t0) % NBUF;
+    load_tile<D, NT>(S.pk, tl, kc_bh, kn_bh, min(t + 2, t1 - 1) * BN, g.M, g.Nk);
+    scores_tile<D, NQB>(S.s_nxt, Ks[b1], qf, lane);
+    lse_update<MASKED, NQB>(S.s_cur, m, l, qi, j0, g.M, lane, c);
+    interleave<2 * NQB * (D / 32), MASKED ? 8 : 5>();
+    store_tile<D, NT>(Ks[b2], tl.loff, S.pk);
+    __syncthreads();
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int qb = 0; qb < NQB; ++qb) S.s_cur[kb][qb] = S.s_nxt[kb][qb];
+  }
+}
+
 template <int D, int NW, int NQB>
 __global__ __launch_bounds__(NW * 64) void lse_pass(Geo g, int Hq, int Hkv, int nsplit,
                                                     float c_log2, float2* __restrict__ stats) {
   constexpr int NT = NW * 64, ROWS = NW * NQB * 16;
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[2][BN * kstride(D)];
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[NBUF][BN * kstride(D)];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int rt = blockIdx.x / nsplit, sp = blockIdx.x % nsplit;
   const size_t bh = blockIdx.y;
@@ -193,58 +316,39 @@ __global__ __launch_bounds__(NW * 64) void lse_pass(Geo g, int Hq, int Hkv, int 
   const int kv_end = kv_end_for_rows(min(row0 + ROWS, g.R), g.G, g.T, g.M);
   int t0, t1;
   split_range((kv_end + BN - 1) / BN, nsplit, sp, t0, t1);
-  const int i_min = min(wrow0, g.R - 1) / g.G;   // smallest chunk position of this wave
+  const int t_mask = min(t1, max(t0, first_masked_tile(g.M, min(row0, g.R - 1) / g.G)));
+  const bf16_t* kc_bh = g.kc + bh * (size_t)g.M * D;
+  const bf16_t* kn_bh = g.kn + bh * (size_t)g.T * D;
 
   bf16x8 qf[NQB][D / 32];
   load_q<D, NQB>(qf, g, b, h, Hq, wrow0, lane);
   int qi[NQB];
-#pragma unroll
-  for (int qb = 0; qb < NQB; ++qb) qi[qb] = (wrow0 + qb * 16 + (lane & 15)) / g.G;
-
   float m[NQB], l[NQB];
 #pragma unroll
-  for (int qb = 0; qb < NQB; ++qb) { m[qb] = -INFINITY; l[qb] = 0.f; }
+  for (int qb = 0; qb < NQB; ++qb) {
+    qi[qb] = (wrow0 + qb * 16 + (lane & 15)) / g.G;
+    m[qb] = -INFINITY;
+    l[qb] = 0.f;
+  }
 
-  u32x4 pk[Tile<D, NT>::N];
-  load_rows<D, NT>(pk, g.kc, g.kn, g, bh, t0 * BN);
-  store_rows<D, NT>(Ks[0], pk);
-  __syncthreads();
-  for (int t = t0; t < t1; ++t) {
-    const int j0 = t * BN, cur = (t - t0) & 1;
-    load_rows<D, NT>(pk, g.kc, g.kn, g, bh, min(t + 1, t1 - 1) * BN);
-    f32x4 sacc[2][NQB];
-    scores_tile<D, NQB>(sacc, Ks[cur], qf, lane);
-    const bool full = j0 + BN - 1 - g.M <= i_min;
-#pragma unroll
-    for (int qb = 0; qb < NQB; ++qb) {
-      float x[8];
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          float v = sacc[kb][qb][r] * c_log2;
-          if (!full) {
-            const int j = j0 + kb * 16 + 4 * (lane >> 4) + r;
-            if (j >= g.M && j - g.M > qi[qb]) v = -INFINITY;
-          }
-          x[kb * 4 + r] = v;
-        }
-      float tmax = fmaxf(fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3])),
-                         fmaxf(fmaxf(x[4], x[5]), fmaxf(x[6], x[7])));
-      const float mn = fmaxf(m[qb], tmax);
-      const float ms = mn == -INFINITY ? 0.f : mn;
-      float acc = l[qb] * __builtin_amdgcn_exp2f(m[qb] - ms);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc += __builtin_amdgcn_exp2f(x[e] - ms);
-      l[qb] = acc;
-      m[qb] = mn;
-    }
-    store_rows<D, NT>(Ks[cur ^ 1], pk);
+  LseState<D, NT, NQB> S;
+  const Tile<D, NT> tl;
+  if (t0 < t1) {
+    load_tile<D, NT>(S.pk, tl, kc_bh, kn_bh, t0 * BN, g.M, g.Nk);
+    store_tile<D, NT>(Ks[0], tl.loff, S.pk);
+    load_tile<D, NT>(S.pk, tl, kc_bh, kn_bh, min(t0 + 1, t1 - 1) * BN, g.M, g.Nk);
+    store_tile<D, NT>(Ks[1], tl.loff, S.pk);
     __syncthreads();
+    scores_tile<D, NQB>(S.s_cur, Ks[0], qf, lane);
+    lse_loop<false, D, NT, NQB>(t0, t_mask, t0, t1, S, tl, Ks, qf, m, l, qi, kc_bh, kn_bh, g, lane,
+                                c_log2);
+    lse_loop<true, D, NT, NQB>(t_mask, t1, t0, t1, S, tl, Ks, qf, m, l, qi, kc_bh, kn_bh, g, lane,
+                               c_log2);
   }
   // merge the four lane groups (disjoint key subsets of the same query)
 #pragma unroll
   for (int qb = 0; qb < NQB; ++qb) {
+    m[qb] *= c_log2;                    // raw score units -> log2 units
 #pragma unroll
     for (int o = 16; o <= 32; o <<= 1) {
       const float m2 = __shfl_xor(m[qb], o, 64), l2 = __shfl_xor(l[qb], o, 64);
@@ -259,16 +363,99 @@ __global__ __launch_bounds__(NW * 64) void lse_pass(Geo g, int Hq, int Hkv, int 
 }
 
 // ------------------------------------------------------------------ pass B
+// Probabilities of one tile (bf16 B operands of the PV product) and their
+// column partials over this wave's rows. The partial row is padded to whole
+// tiles, and the four lanes holding one column's total all store it.
+template <bool MASKED, int NQB>
+__device__ __forceinline__ void probs_tile(const f32x4 (&sacc)[2][NQB], bf16x8 (&pb)[NQB],
+                                           const float (&lam)[NQB], const int (&qi)[NQB],
+                                           float* prow, int j0, int M, int lane, float c) {
+  float cs[2][4];
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) cs[kb][r] = 0.f;
+#pragma unroll
+  for (int qb = 0; qb < NQB; ++qb) {
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float p = __builtin_amdgcn_exp2f(fmaf(sacc[kb][qb][r], c, -lam[qb]));
+        if (MASKED && !visible(j0 + kb * 16 + 4 * (lane >> 4) + r, M, qi[qb])) p = 0.f;
+        cs[kb][r] += p;
+        pb[qb][kb * 4 + r] = (__bf16)p;
+      }
+  }
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+    const float v = colsum16(cs[kb][0], cs[kb][1], cs[kb][2], cs[kb][3], lane);
+    prow[j0 + kb * 16 + 4 * (lane >> 4) + ((lane & 15) >> 2)] = v;
+  }
+}
+
+// O^T += V^T P^T for one tile.
+template <int D, int NQB>
+__device__ __forceinline__ void pv_tile(f32x4 (&oacc)[D / 16][NQB], const bf16x8 (&pb)[NQB],
+                                        const bf16_t* Vs, int lane) {
+#pragma unroll
+  for (int db = 0; db < D / 16; ++db) {
+    const bf16x8 a = v_operand<D>(Vs, db, lane);
+#pragma unroll
+    for (int qb = 0; qb < NQB; ++qb) oacc[db][qb] = mfma(a, pb[qb], oacc[db][qb]);
+  }
+}
+
+template <int D, int NT, int NQB>
+struct MainState {
+  f32x4 s_cur[2][NQB], s_nxt[2][NQB];
+  f32x4 oacc[D / 16][NQB];
+  u32x4 pk[Tile<D, NT>::N], pv[Tile<D, NT>::N];
+};
+
+template <bool MASKED, int D, int NT, int NQB>
+__device__ __forceinline__ void main_loop(int ta, int tb, int t0, int t1, MainState<D, NT, NQB>& S,
+                                          const Tile<D, NT>& tl,
+                                          bf16_t (*Ks)[BN * kstride(D)],
+                                          bf16_t (*Vs)[BN * vstride(D)],
+                                          const bf16x8 (&qf)[NQB][D / 32],
+                                          const float (&lam)[NQB], const int (&qi)[NQB],
+                                          float* prow, const bf16_t* kc_bh, const bf16_t* kn_bh,
+                                          const bf16_t* vc_bh, const bf16_t* vn_bh, const Geo& g,
+                                          int lane, float c) {
+  for (int t = ta; t < tb; ++t) {
+    const int j0 = t * BN;
+    const int b0 = (t - t0) % NBUF, b1 = (t + 1 - t0) % NBUF, b2 = (t + 2 - t0) % NBUF;
+    const int jn = min(t + 2, t1 - 1) * BN;
+    load_tile<D, NT>(S.pk, tl, kc_bh, kn_bh, jn, g.M, g.Nk);
+    load_tile<D, NT>(S.pv, tl, vc_bh, vn_bh, jn, g.M, g.Nk);
+    bf16x8 pb[NQB];
+    scores_tile<D, NQB>(S.s_nxt, Ks[b1], qf, lane);
+    probs_tile<MASKED, NQB>(S.s_cur, pb, lam, qi, prow, j0, g.M, lane, c);
+    pv_tile<D, NQB>(S.oacc, pb, Vs[b0], lane);
+    interleave<2 * NQB * (D / 32), MASKED ? 5 : 4>();
+    interleave<NQB * (D / 16), 1>();
+    store_tile<D, NT>(Ks[b2], tl.loff, S.pk);
+    store_tile<D, NT>(Vs[b2], tl.vloff, S.pv);
+    __syncthreads();
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int qb = 0; qb < NQB; ++qb) S.s_cur[kb][qb] = S.s_nxt[kb][qb];
+  }
+}
+
 template <int D, int NW, int NQB>
 __global__ __launch_bounds__(NW * 64) void main_pass(Geo g, int Hq, int Hkv, int nsplit,
-                                                     float c_log2, const float2* __restrict__ stats,
-                                                     float* __restrict__ parts,
+                                                     int nsplit_lse, float c_log2,
+                                                     const float2* __restrict__ stats,
+                                                     float* __restrict__ parts, int parts_ld,
                                                      bf16_t* __restrict__ out,
                                                      float* __restrict__ opart,
                                                      float* __restrict__ lse_out) {
   constexpr int NT = NW * 64, ROWS = NW * NQB * 16;
-  __shared__ __attribute__((aligned(16))) bf16_t Ks[2][BN * kstride(D)];
-  __shared__ __attribute__((aligned(16))) bf16_t Vs[2][BN * kstride(D)];
+  __shared__ __attribute__((aligned(16))) bf16_t Ks[NBUF][BN * kstride(D)];
+  __shared__ __attribute__((aligned(16))) bf16_t Vs[NBUF][BN * vstride(D)];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int rt = blockIdx.x / nsplit, sp = blockIdx.x % nsplit;
   const size_t bh = blockIdx.y;
@@ -278,7 +465,11 @@ __global__ __launch_bounds__(NW * 64) void main_pass(Geo g, int Hq, int Hkv, int
   const int kv_end = kv_end_for_rows(min(row0 + ROWS, g.R), g.G, g.T, g.M);
   int t0, t1;
   split_range((kv_end + BN - 1) / BN, nsplit, sp, t0, t1);
-  const int i_min = min(wrow0, g.R - 1) / g.G;
+  const int t_mask = min(t1, max(t0, first_masked_tile(g.M, min(row0, g.R - 1) / g.G)));
+  const bf16_t* kc_bh = g.kc + bh * (size_t)g.M * D;
+  const bf16_t* kn_bh = g.kn + bh * (size_t)g.T * D;
+  const bf16_t* vc_bh = g.vc + bh * (size_t)g.M * D;
+  const bf16_t* vn_bh = g.vn + bh * (size_t)g.T * D;
 
   bf16x8 qf[NQB][D / 32];
   load_q<D, NQB>(qf, g, b, h, Hq, wrow0, lane);
@@ -290,11 +481,12 @@ __global__ __launch_bounds__(NW * 64) void main_pass(Geo g, int Hq, int Hkv, int
     qi[qb] = r / g.G;
     if (r < g.R) {
       float mx = -INFINITY;
-      for (int s = 0; s < nsplit; ++s) mx = fmaxf(mx, stats[((size_t)s * BH + bh) * g.R + r].x);
+      for (int s = 0; s < nsplit_lse; ++s)
+        mx = fmaxf(mx, stats[((size_t)s * BH + bh) * g.R + r].x);
       float L = 0.f;
-      for (int s = 0; s < nsplit; ++s) {
+      for (int s = 0; s < nsplit_lse; ++s) {
         const float2 st = stats[((size_t)s * BH + bh) * g.R + r];
-        L += st.y * __builtin_amdgcn_exp2f(st.x - mx);
+        if (st.y > 0.f) L += st.y * __builtin_amdgcn_exp2f(st.x - mx);
       }
       lam[qb] = mx + __log2f(L);
     } else {
@@ -306,66 +498,31 @@ __global__ __launch_bounds__(NW * 64) void main_pass(Geo g, int Hq, int Hkv, int
     }
   }
 
-  f32x4 oacc[D / 16][NQB];
+  MainState<D, NT, NQB> S;
 #pragma unroll
   for (int db = 0; db < D / 16; ++db)
 #pragma unroll
-    for (int qb = 0; qb < NQB; ++qb) oacc[db][qb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int qb = 0; qb < NQB; ++qb) S.oacc[db][qb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  float* prow = parts + ((size_t)(rt * NW + wave) * BH + bh) * g.Nk;
+  float* prow = parts + ((size_t)(rt * NW + wave) * BH + bh) * parts_ld;
+  const Tile<D, NT> tl;
 
-  u32x4 pk[Tile<D, NT>::N], pv[Tile<D, NT>::N];
-  load_rows<D, NT>(pk, g.kc, g.kn, g, bh, t0 * BN);
-  load_rows<D, NT>(pv, g.vc, g.vn, g, bh, t0 * BN);
-  store_rows<D, NT>(Ks[0], pk);
-  store_rows<D, NT>(Vs[0], pv);
-  __syncthreads();
-  for (int t = t0; t < t1; ++t) {
-    const int j0 = t * BN, cur = (t - t0) & 1;
-    const int jn = min(t + 1, t1 - 1) * BN;
-    load_rows<D, NT>(pk, g.kc, g.kn, g, bh, jn);
-    load_rows<D, NT>(pv, g.vc, g.vn, g, bh, jn);
-    f32x4 sacc[2][NQB];
-    scores_tile<D, NQB>(sacc, Ks[cur], qf, lane);
-    const bool full = j0 + BN - 1 - g.M <= i_min;
-    bf16x8 pb[NQB];
-    float cs[2][4];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) cs[kb][r] = 0.f;
-#pragma unroll
-    for (int qb = 0; qb < NQB; ++qb) {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          float p = __builtin_amdgcn_exp2f(fmaf(sacc[kb][qb][r], c_log2, -lam[qb]));
-          if (!full) {
-            const int j = j0 + kb * 16 + 4 * (lane >> 4) + r;
-            if (j >= g.M && j - g.M > qi[qb]) p = 0.f;
-          }
-          cs[kb][r] += p;
-          pb[qb][kb * 4 + r] = (__bf16)p;
-        }
-    }
-    // column partials over this wave's rows
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      const float v = colsum16(cs[kb][0], cs[kb][1], cs[kb][2], cs[kb][3], lane);
-      const int j = j0 + kb * 16 + 4 * (lane >> 4) + ((lane & 15) >> 2);
-      if ((lane & 3) == 0 && j < g.Nk) prow[j] = v;
-    }
-    // O^T += V^T P^T
-#pragma unroll
-    for (int db = 0; db < D / 16; ++db) {
-      const bf16x8 a = v_operand<D>(Vs[cur], db, lane);
-#pragma unroll
-      for (int qb = 0; qb < NQB; ++qb) oacc[db][qb] = mfma(a, pb[qb], oacc[db][qb]);
-    }
-    store_rows<D, NT>(Ks[cur ^ 1], pk);
-    store_rows<D, NT>(Vs[cur ^ 1], pv);
+  if (t0 < t1) {
+    load_tile<D, NT>(S.pk, tl, kc_bh, kn_bh, t0 * BN, g.M, g.Nk);
+    load_tile<D, NT>(S.pv, tl, vc_bh, vn_bh, t0 * BN, g.M, g.Nk);
+    store_tile<D, NT>(Ks[0], tl.loff, S.pk);
+    store_tile<D, NT>(Vs[0], tl.vloff, S.pv);
+    const int j1 = min(t0 + 1, t1 - 1) * BN;
+    load_tile<D, NT>(S.pk, tl, kc_bh, kn_bh, j1, g.M, g.Nk);
+    load_tile<D, NT>(S.pv, tl, vc_bh, vn_bh, j1, g.M, g.Nk);
+    store_tile<D, NT>(Ks[1], tl.loff, S.pk);
+    store_tile<D, NT>(Vs[1], tl.vloff, S.pv);
     __syncthreads();
+    scores_tile<D, NQB>(S.s_cur, Ks[0], qf, lane);
+    main_loop<false, D, NT, NQB>(t0, t_mask, t0, t1, S, tl, Ks, Vs, qf, lam, qi, prow, kc_bh, kn_bh,
+                                 vc_bh, vn_bh, g, lane, c_log2);
+    main_loop<true, D, NT, NQB>(t_mask, t1, t0, t1, S, tl, Ks, Vs, qf, lam, qi, prow, kc_bh, kn_bh,
+                                vc_bh, vn_bh, g, lane, c_log2);
   }
   // write O (lane: query qb*16 + l%16, d = db*16 + 4*(l/16) + r)
 #pragma unroll
@@ -377,15 +534,15 @@ __global__ __launch_bounds__(NW * 64) void main_pass(Geo g, int Hq, int Hkv, int
 #pragma unroll
     for (int db = 0; db < D / 16; ++db) {
       const int dd = db * 16 + 4 * (lane >> 4);
+      const f32x4 o = S.oacc[db][qb];
       if (nsplit == 1) {
         uint2 v;
-        v.x = (uint32_t)f32_to_bf16(oacc[db][qb][0]) | ((uint32_t)f32_to_bf16(oacc[db][qb][1]) << 16);
-        v.y = (uint32_t)f32_to_bf16(oacc[db][qb][2]) | ((uint32_t)f32_to_bf16(oacc[db][qb][3]) << 16);
+        v.x = (uint32_t)f32_to_bf16(o[0]) | ((uint32_t)f32_to_bf16(o[1]) << 16);
+        v.y = (uint32_t)f32_to_bf16(o[2]) | ((uint32_t)f32_to_bf16(o[3]) << 16);
         *reinterpret_cast<uint2*>(out + orow + dd) = v;
       } else {
         float* dst = opart + (((size_t)sp * BH + bh) * g.R + r) * D + dd;
-        *reinterpret_cast<float4*>(dst) =
-            make_float4(oacc[db][qb][0], oacc[db][qb][1], oacc[db][qb][2], oacc[db][qb][3]);
+        *reinterpret_cast<float4*>(dst) = make_float4(o[0], o[1], o[2], o[3]);
       }
     }
   }
@@ -425,21 +582,22 @@ hipError_t run(const Shape& s, const Plan& p, const void* q, const void* kc, con
   Geo g{s.G(), s.T, s.M, s.R(), s.Nk(), (const bf16_t*)q, (const bf16_t*)kc,
         (const bf16_t*)vc, (const bf16_t*)kn, (const bf16_t*)vn};
   const int nrt = (s.R() + ROWS - 1) / ROWS;
-  dim3 grid(nrt * p.nsplit, s.BH());
+  dim3 grid(nrt * p.nsplit, s.BH()), grid_lse(nrt * p.nsplit_lse, s.BH());
   const float c = scale * kLog2e;
   float2* stats = reinterpret_cast<float2*>(ws + p.off_stats);
   float* parts = reinterpret_cast<float*>(ws + p.off_parts);
   float* opart = reinterpret_cast<float*>(ws + p.off_opart);
   {
     LaunchTimer lt(K_MFMA_LSE, st);
-    lse_pass<D, NW, NQB><<<grid, NW * 64, 0, st>>>(g, s.Hq, s.Hkv, p.nsplit, c, stats);
+    lse_pass<D, NW, NQB><<<grid_lse, NW * 64, 0, st>>>(g, s.Hq, s.Hkv, p.nsplit_lse, c, stats);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   {
     LaunchTimer lt(K_MFMA_MAIN, st);
-    main_pass<D, NW, NQB><<<grid, NW * 64, 0, st>>>(g, s.Hq, s.Hkv, p.nsplit, c, stats, parts,
-                                                    (bf16_t*)out, opart, lse);
+    main_pass<D, NW, NQB><<<grid, NW * 64, 0, st>>>(g, s.Hq, s.Hkv, p.nsplit, p.nsplit_lse, c,
+                                                    stats, parts, p.parts_ld, (bf16_t*)out, opart,
+                                                    lse);
   }
   e = hipGetLastError();
   if (e != hipSuccess) return e;

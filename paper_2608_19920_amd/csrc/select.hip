@@ -10,7 +10,7 @@ namespace {
 __global__ __launch_bounds__(256) void colsum_reduce_kernel(const float* __restrict__ parts,
                                                             float* __restrict__ wsum, int nparts,
                                                             int rows_per_part, int BH, int Nk,
-                                                            int G, int T, int M) {
+                                                            int ld, int G, int T, int M) {
   const int j = blockIdx.x * blockDim.x + threadIdx.x;
   const int bh = blockIdx.y;
   if (j >= Nk) return;
@@ -18,7 +18,7 @@ __global__ __launch_bounds__(256) void colsum_reduce_kernel(const float* __restr
   float s = 0.f;
   for (int p = 0; p < nparts; ++p) {
     const int r1 = min((p + 1) * rows_per_part, R);
-    if (j < kv_end_for_rows(r1, G, T, M)) s += parts[((size_t)p * BH + bh) * Nk + j];
+    if (j < kv_end_for_rows(r1, G, T, M)) s += parts[((size_t)p * BH + bh) * ld + j];
   }
   wsum[(size_t)bh * Nk + j] = s;
 }
@@ -244,7 +244,7 @@ hipError_t launch_colsum_reduce(const Shape& s, const Plan& p, const float* part
   dim3 grid((s.Nk() + 255) / 256, s.BH());
   LaunchTimer lt(K_COLSUM_REDUCE, st);
   colsum_reduce_kernel<<<grid, 256, 0, st>>>(parts, wsum, p.nparts, p.rows_per_part, s.BH(),
-                                             s.Nk(), s.G(), s.T, s.M);
+                                             s.Nk(), p.parts_ld, s.G(), s.T, s.M);
   return hipGetLastError();
 }
 

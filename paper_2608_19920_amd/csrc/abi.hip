@@ -150,7 +150,7 @@ Plan make_plan(const Shape& s, int dtype) {
     p.nparts = (int)(nrt * (rows_blk / p.rows_per_part));
     p.parts_ld = (int)((Nk + 31) / 32 * 32);
   } else if (path == 2) {
-    p.nsplit = decode_nsplit(s.M);
+    p.nsplit = s.M > 0 ? decode_max_split() : 0;   // capacity; the launch picks the count
     p.rows_per_part = 0;
     p.nparts = 0;
     size_t off = 0;

@@ -2,13 +2,12 @@
 // step streams the whole KV cache once and is bound by HBM bandwidth
 // (Sec. "Sparse Attention. Key-Value Caching": N_q = 1, N_k = N_C).
 //
-//   split    block (split s, head bh) covers cache slots [s*kChunk, +kChunk).
-//            Eight lanes share one key row: lane `slice` holds D/8 elements of
-//            it, so each wave load reads eight consecutive rows (contiguous
-//            bytes). All K and V loads of the block are issued before any
-//            arithmetic. Logits (log2 domain) reduce over the 8 lanes with
-//            DPP; the split's softmax partial (m, l, O-partial) per query head
-//            is written out, and so are the logits for the column sums.
+//   split    block (split s, head bh) streams rounds s, s+ns, ... of head bh.
+//            Sixteen lanes share one key row: lane `slice` holds D/16 elements
+//            of it, so each wave load reads four consecutive rows (contiguous
+//            bytes). Logits (log2 domain) reduce over the 16 lanes with DPP;
+//            the split's softmax partial (m, l, O-partial) per query head is
+//            written out, and so are the logits for the column sums.
 //   combine  block bh merges the splits with the chunk's own key (column M),
 //            writes out and lse, and wsum[j] = sum_g exp2(logit_gj - lambda_g)
 //            from the stored logits.
@@ -18,163 +17,181 @@ namespace h2o {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kLanesPerKey = 8;
-constexpr int kKeysPerRound = kThreads / kLanesPerKey;   // 32
-constexpr int kRounds = 8;
-constexpr int kChunk = kKeysPerRound * kRounds;          // 256 cache slots per block
+constexpr int kLanesPerKey = 16;                         // lanes sharing one key row
+constexpr int kKeysPerRound = kThreads / kLanesPerKey;   // 16
 constexpr int kMaxGD = 512;                              // G * D handled by these kernels
+constexpr int kMaxSplit = 64;                            // split blocks per head, at most
 
 template <int CTRL>
 __device__ __forceinline__ float dpp(float x) {
   return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, true));
 }
-// Sum over the 8 lanes of an aligned lane octet; every lane gets the total.
-__device__ __forceinline__ float sum8(float v) {
+// Sum over the 16 lanes of a DPP row; every lane gets the total.
+__device__ __forceinline__ float sum16(float v) {
   v += dpp<0xB1>(v);    // quad_perm [1,0,3,2]
   v += dpp<0x4E>(v);    // quad_perm [2,3,0,1]
-  v += dpp<0x141>(v);   // row_half_mirror: lane l <-> 7-l within each octet
+  v += dpp<0x141>(v);   // row_half_mirror: lane l <-> 7-l within each half row
+  v += dpp<0x140>(v);   // row_mirror: lane l <-> 15-l
   return v;
 }
 
-__device__ __forceinline__ void unpack8(const uint4 w, float* f) {
-  const uint32_t v[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    f[2 * e] = __uint_as_float(v[e] << 16);
-    f[2 * e + 1] = __uint_as_float(v[e] & 0xFFFF0000u);
+// EPL consecutive bf16 elements of a row, as float.
+template <int EPL>
+struct RowPiece {
+  typedef uint32_t raw_t __attribute__((ext_vector_type(EPL / 2)));
+  static __device__ __forceinline__ raw_t load(const bf16_t* p) {
+    return *reinterpret_cast<const raw_t*>(p);
   }
-}
+  static __device__ __forceinline__ void unpack(const raw_t w, float* f) {
+#pragma unroll
+    for (int e = 0; e < EPL / 2; ++e) {
+      f[2 * e] = __uint_as_float(w[e] << 16);
+      f[2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
+    }
+  }
+};
 
-template <int D, int G>
+// Streaming split kernel. The cache slots of head bh are walked in rounds of
+// 16 slots (one slot per 16-lane DPP row; lane `slice` holds D/16 elements
+// of the row); block (s, bh) takes rounds s, s + ns, s + 2 ns, ... so that
+// the ns blocks of a head sweep its K and V rows together. The K and V rows
+// of the next PF rounds of a block are in flight while a round is computed.
+// Each lane row keeps, per query head, a reference maximum m (the first
+// logit it saw, raised only when a later logit exceeds it by more than 64 in
+// log2 units, which keeps every exp2 term below 2^64), the sum l of
+// exp2(logit - m) and the weighted V accumulator; the block merges them at
+// the end.
+template <int D, int G, int PF>
 __global__ __launch_bounds__(kThreads) void decode_split(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
-    int Hq, int Hkv, int M, float c_log2, float* __restrict__ logits, float2* __restrict__ dstat,
-    float* __restrict__ dO) {
-  constexpr int EPL = D / kLanesPerKey;   // elements per lane (8 or 16)
-  constexpr int VPL = EPL / 8;            // 16-byte vectors per lane
-  __shared__ float red[kThreads / 64][G][2];
+    int Hq, int Hkv, int M, float c_log2, float* __restrict__ logits,
+    float2* __restrict__ dstat, float* __restrict__ dO) {
+  constexpr int EPL = D / kLanesPerKey;   // elements per lane (4 or 8)
+  typedef RowPiece<EPL> RP;
+  __shared__ float red[kThreads / 64][G];
   __shared__ float acc_s[kKeysPerRound][G * D + 4];
   const int s = blockIdx.x, nsplit = gridDim.x;
   const size_t bh = blockIdx.y;
   const int b = (int)(bh / Hkv), h = (int)(bh % Hkv);
-  const int j0 = s * kChunk, n = min(kChunk, M - j0);
+  const int head_rounds = (M + kKeysPerRound - 1) / kKeysPerRound;
+  const int nrounds = (head_rounds - s + nsplit - 1) / nsplit;   // rounds s, s+ns, ...
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int kg = tid / kLanesPerKey, slice = tid % kLanesPerKey;
+  const bf16_t* kbase = kc + bh * (size_t)M * D + slice * EPL;
+  const bf16_t* vbase = vc + bh * (size_t)M * D + slice * EPL;
+  auto slot_of = [&](int rd) { return (s + rd * nsplit) * kKeysPerRound + kg; };
 
-  // Rows past the block's last slot re-read that slot (always in bounds) and
-  // are masked below, so every load is unconditional and issued up front.
-  uint4 kr[kRounds][VPL], vr[kRounds][VPL];
-  const bf16_t* kbase = kc + (bh * M + j0) * (size_t)D + slice * EPL;
-  const bf16_t* vbase = vc + (bh * M + j0) * (size_t)D + slice * EPL;
+  // ring of PF rounds; slots past the cache re-read the last slot
+  typename RP::raw_t kr[PF], vr[PF];
+  auto issue = [&](int rd, int slot_) {
+    const int kk = min(slot_of(rd), M - 1);
+    kr[slot_] = RP::load(kbase + (size_t)kk * D);
+    vr[slot_] = RP::load(vbase + (size_t)kk * D);
+  };
 #pragma unroll
-  for (int rd = 0; rd < kRounds; ++rd) {
-    const int kk = min(rd * kKeysPerRound + kg, n - 1);
-#pragma unroll
-    for (int v = 0; v < VPL; ++v) {
-      kr[rd][v] = *reinterpret_cast<const uint4*>(kbase + (size_t)kk * D + 8 * v);
-      vr[rd][v] = *reinterpret_cast<const uint4*>(vbase + (size_t)kk * D + 8 * v);
-    }
-  }
+  for (int u = 0; u < PF; ++u) issue(u, u);
   float qs[G][EPL];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
-    const bf16_t* qp = q + (size_t)(b * Hq + h * G + g) * D + slice * EPL;
+    float f[EPL];
+    RP::unpack(RP::load(q + (size_t)(b * Hq + h * G + g) * D + slice * EPL), f);
 #pragma unroll
-    for (int v = 0; v < VPL; ++v) {
-      float f[8];
-      unpack8(*reinterpret_cast<const uint4*>(qp + 8 * v), f);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) qs[g][8 * v + e] = f[e] * c_log2;
-    }
+    for (int e = 0; e < EPL; ++e) qs[g][e] = f[e] * c_log2;
   }
-  // logits of this lane octet's keys, every lane of the octet holds them
-  float lg[kRounds][G];
-#pragma unroll
-  for (int rd = 0; rd < kRounds; ++rd) {
-    float kf[EPL];
-#pragma unroll
-    for (int v = 0; v < VPL; ++v) unpack8(kr[rd][v], kf + 8 * v);
-#pragma unroll
-    for (int g = 0; g < G; ++g) {
-      float a = 0.f;
-#pragma unroll
-      for (int e = 0; e < EPL; ++e) a = fmaf(qs[g][e], kf[e], a);
-      lg[rd][g] = sum8(a);
-    }
-  }
-  // block max per query head
+  float m[G], l[G], acc[G][EPL];
 #pragma unroll
   for (int g = 0; g < G; ++g) {
-    float m = -INFINITY;
-#pragma unroll
-    for (int rd = 0; rd < kRounds; ++rd)
-      if (rd * kKeysPerRound + kg < n) m = fmaxf(m, lg[rd][g]);
-    for (int o = 8; o < 64; o <<= 1) m = fmaxf(m, __shfl_xor(m, o, 64));
-    if (lane == 0) red[wave][g][0] = m;
-  }
-  __syncthreads();
-  float mg[G];
-#pragma unroll
-  for (int g = 0; g < G; ++g) {
-    float m = red[0][g][0];
-#pragma unroll
-    for (int w = 1; w < kThreads / 64; ++w) m = fmaxf(m, red[w][g][0]);
-    mg[g] = m;
-  }
-  // probabilities, row sums, stored logits, O partial over this lane's keys
-  float acc[G][EPL];
-#pragma unroll
-  for (int g = 0; g < G; ++g)
+    m[g] = -INFINITY;
+    l[g] = 0.f;
 #pragma unroll
     for (int e = 0; e < EPL; ++e) acc[g][e] = 0.f;
-  float lsum[G];
+  }
+  for (int rd0 = 0; rd0 < nrounds; rd0 += PF) {
 #pragma unroll
-  for (int g = 0; g < G; ++g) lsum[g] = 0.f;
+    for (int u = 0; u < PF; ++u) {
+      const int rd = rd0 + u;
+      if (rd < nrounds) {
+        const int kk = slot_of(rd);
+        const bool ok = kk < M;
+        float kf[EPL], vf[EPL];
+        RP::unpack(kr[u], kf);
+        RP::unpack(vr[u], vf);
+        issue(rd + PF, u);                       // refill the slot just consumed
+        float lgs[G];
 #pragma unroll
-  for (int rd = 0; rd < kRounds; ++rd) {
-    const int kk = rd * kKeysPerRound + kg;
-    const bool ok = kk < n;
-    float vf[EPL];
+        for (int g = 0; g < G; ++g) {
+          float a = 0.f;
 #pragma unroll
-    for (int v = 0; v < VPL; ++v) unpack8(vr[rd][v], vf + 8 * v);
+          for (int e = 0; e < EPL; ++e) a = fmaf(qs[g][e], kf[e], a);
+          lgs[g] = sum16(a);
+        }
+        if (ok && slice == 0) {                    // logits stored key-major: [bh][slot][g]
+          float* dst = logits + ((bh * M) + kk) * (size_t)G;
 #pragma unroll
-    for (int g = 0; g < G; ++g) {
-      const float p = ok ? __builtin_amdgcn_exp2f(lg[rd][g] - mg[g]) : 0.f;
-      lsum[g] += p;
-      if (ok && slice == (g % kLanesPerKey))
-        logits[(bh * G + g) * (size_t)M + j0 + kk] = lg[rd][g];
+          for (int g = 0; g < G; ++g) dst[g] = lgs[g];
+        }
 #pragma unroll
-      for (int e = 0; e < EPL; ++e) acc[g][e] = fmaf(p, vf[e], acc[g][e]);
+        for (int g = 0; g < G; ++g) {
+          const float lg = lgs[g];
+          if (ok && lg > m[g] + 64.f) {            // first slot, or a much larger logit
+            const float sc = __builtin_amdgcn_exp2f(m[g] - lg);
+            l[g] *= sc;
+#pragma unroll
+            for (int e = 0; e < EPL; ++e) acc[g][e] *= sc;
+            m[g] = lg;
+          }
+          const float p = ok ? __builtin_amdgcn_exp2f(lg - m[g]) : 0.f;
+          l[g] += p;
+#pragma unroll
+          for (int e = 0; e < EPL; ++e) acc[g][e] = fmaf(p, vf[e], acc[g][e]);
+        }
+      }
     }
   }
+  // block merge: common maximum per query head, rescale, sum through LDS
 #pragma unroll
   for (int g = 0; g < G; ++g) {
-    float l = lsum[g];      // identical in the 8 lanes of an octet: reduce over octets
-    for (int o = 8; o < 64; o <<= 1) l += __shfl_xor(l, o, 64);
-    if (lane == 0) red[wave][g][1] = l;
+    float mx = m[g];
+    for (int o = 16; o < 64; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+    if (lane == 0) red[wave][g] = mx;
   }
-  // O partial: sum the per-octet accumulators through LDS
+  __syncthreads();
+  float mb[G];
 #pragma unroll
-  for (int g = 0; g < G; ++g)
+  for (int g = 0; g < G; ++g) {
+    float mx = red[0][g];
 #pragma unroll
-    for (int e = 0; e < EPL; ++e) acc_s[kg][g * D + slice * EPL + e] = acc[g][e];
+    for (int w = 1; w < kThreads / 64; ++w) mx = fmaxf(mx, red[w][g]);
+    mb[g] = mx;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int g = 0; g < G; ++g) {
+    const float sc = m[g] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m[g] - mb[g]);
+    float lv = slice == 0 ? l[g] * sc : 0.f;   // l is identical in the 16 lanes of a row
+    for (int o = 16; o < 64; o <<= 1) lv += __shfl_xor(lv, o, 64);
+    if (lane == 0) red[wave][g] = lv;
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) acc_s[kg][g * D + slice * EPL + e] = acc[g][e] * sc;
+  }
   __syncthreads();
   if (tid < G) {
-    float l = 0.f;
-    for (int w = 0; w < kThreads / 64; ++w) l += red[w][tid][1];
-    dstat[(bh * nsplit + s) * G + tid] = make_float2(mg[tid], l);
+    float lt = 0.f;
+    for (int w = 0; w < kThreads / 64; ++w) lt += red[w][tid];
+    dstat[(bh * nsplit + s) * G + tid] = make_float2(mb[tid], lt);
   }
   for (int c = tid; c < G * D; c += kThreads) {
     float a = 0.f;
-#pragma unroll 8
+#pragma unroll
     for (int k2 = 0; k2 < kKeysPerRound; ++k2) a += acc_s[k2][c];
     dO[(bh * nsplit + s) * (size_t)(G * D) + c] = a;
   }
 }
 
 // Block (x, bh): merges the splits of head bh (every block recomputes the
-// few per-head statistics), then writes wsum for columns [x*kCols, +kCols);
-// block x == 0 also writes out and lse.
+// few per-head statistics from the split partials staged in LDS), then
+// writes wsum for columns [x*kCols, +kCols); block x == 0 also writes out
+// and lse.
 constexpr int kCols = 1024;
 
 template <int D>
@@ -185,10 +202,12 @@ __global__ __launch_bounds__(kThreads) void decode_combine(
     float* __restrict__ lse, float* __restrict__ wsum) {
   constexpr int kMaxG = kMaxGD / 64;
   __shared__ float lnew[kMaxG], lam[kMaxG], mfin[kMaxG], linv[kMaxG];
+  __shared__ float2 st_s[kMaxSplit * kMaxG];
   const int G = Hq / Hkv;
   const size_t bh = blockIdx.y;
   const int b = (int)(bh / Hkv), h = (int)(bh % Hkv);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  for (int i = tid; i < nsplit * G; i += kThreads) st_s[i] = dstat[bh * nsplit * G + i];
   // logit of the chunk's own key for each query head (one wave per head)
   for (int g = wave; g < G; g += kThreads / 64) {
     float a = 0.f;
@@ -202,11 +221,11 @@ __global__ __launch_bounds__(kThreads) void decode_combine(
   if (tid < G) {
     const int g = tid;
     float mx = lnew[g];
-    for (int s = 0; s < nsplit; ++s) mx = fmaxf(mx, dstat[(bh * nsplit + s) * G + g].x);
+    for (int s = 0; s < nsplit; ++s) mx = fmaxf(mx, st_s[s * G + g].x);
     float L = __builtin_amdgcn_exp2f(lnew[g] - mx);
     for (int s = 0; s < nsplit; ++s) {
-      const float2 st = dstat[(bh * nsplit + s) * G + g];
-      L += st.y * __builtin_amdgcn_exp2f(st.x - mx);
+      const float2 st = st_s[s * G + g];
+      if (st.y > 0.f) L += st.y * __builtin_amdgcn_exp2f(st.x - mx);
     }
     const float lm = mx + __log2f(L);
     lam[g] = lm;
@@ -219,18 +238,21 @@ __global__ __launch_bounds__(kThreads) void decode_combine(
     for (int c = tid; c < G * D; c += kThreads) {
       const int g = c / D, dd = c % D;
       float a = __builtin_amdgcn_exp2f(lnew[g] - mfin[g]) * bf16_to_f32(vn[bh * D + dd]);
-      for (int s = 0; s < nsplit; ++s)
-        a = fmaf(dO[(bh * nsplit + s) * (size_t)(G * D) + c],
-                 __builtin_amdgcn_exp2f(dstat[(bh * nsplit + s) * G + g].x - mfin[g]), a);
+#pragma unroll 8
+      for (int s = 0; s < nsplit; ++s) {
+        const float2 st = st_s[s * G + g];
+        const float w = st.y > 0.f ? __builtin_amdgcn_exp2f(st.x - mfin[g]) : 0.f;
+        a = fmaf(dO[(bh * nsplit + s) * (size_t)(G * D) + c], w, a);
+      }
       out[(size_t)(b * Hq + h * G + g) * D + dd] = f32_to_bf16(a * linv[g]);
     }
   }
   float* w = wsum + bh * (size_t)(M + 1);
+  const float* lgb = logits + bh * (size_t)M * G;
   const int c0 = blockIdx.x * kCols, c1 = min(M, c0 + kCols);
   for (int j = c0 + tid; j < c1; j += kThreads) {
     float a = 0.f;
-    for (int g = 0; g < G; ++g)
-      a += __builtin_amdgcn_exp2f(logits[(bh * G + g) * (size_t)M + j] - lam[g]);
+    for (int g = 0; g < G; ++g) a += __builtin_amdgcn_exp2f(lgb[(size_t)j * G + g] - lam[g]);
     w[j] = a;
   }
   if (blockIdx.x == 0 && tid == 0) {
@@ -240,17 +262,45 @@ __global__ __launch_bounds__(kThreads) void decode_combine(
   }
 }
 
+// Split blocks per head such that all blocks of the grid are resident at
+// once (blocks per CU of this kernel instance x CUs), at most kMaxSplit and
+// at most one per round of slots.
 template <int D, int G>
-void launch_split(dim3 grid, hipStream_t st, const void* q, const void* kc, const void* vc,
-                  int Hq, int Hkv, int M, float c, float* logits, float2* dstat, float* dO) {
-  decode_split<D, G><<<grid, kThreads, 0, st>>>((const bf16_t*)q, (const bf16_t*)kc,
-                                                (const bf16_t*)vc, Hq, Hkv, M, c, logits, dstat,
-                                                dO);
+int split_count(int M, int BH) {
+  static int resident = 0;
+  if (!resident) {
+    int per_cu = 0, dev = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, decode_split<D, G, 8>, kThreads,
+                                                     0) != hipSuccess || per_cu < 1)
+      per_cu = 2;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        cus < 1)
+      cus = 256;
+    (void)hipGetLastError();
+    resident = per_cu * cus;
+  }
+  int ns = resident / BH;
+  const int rounds = (M + kKeysPerRound - 1) / kKeysPerRound;
+  if (ns > rounds) ns = rounds;
+  if (ns > kMaxSplit) ns = kMaxSplit;
+  return ns < 1 ? 1 : ns;
+}
+
+template <int D, int G>
+int launch_split(hipStream_t st, int BH, const void* q, const void* kc, const void* vc, int Hq,
+                 int Hkv, int M, float c, float* logits, float2* dstat, float* dO) {
+  const int ns = split_count<D, G>(M, BH);
+  decode_split<D, G, 8><<<dim3(ns, BH), kThreads, 0, st>>>((const bf16_t*)q, (const bf16_t*)kc,
+                                                           (const bf16_t*)vc, Hq, Hkv, M, c,
+                                                           logits, dstat, dO);
+  return ns;
 }
 
 }  // namespace
 
-int decode_nsplit(int M) { return (M + kChunk - 1) / kChunk; }
+int decode_max_split() { return kMaxSplit; }
+
 // The decode kernels are instantiated for these (d, G) pairs.
 bool decode_supports(int d, int G) {
   return (d == 64 && (G == 1 || G == 2 || G == 4 || G == 8)) ||
@@ -264,13 +314,12 @@ hipError_t launch_sdpa_decode(const Shape& s, const Plan& p, const void* q, cons
   float* logits = reinterpret_cast<float*>(ws + p.off_logits);
   float2* dstat = reinterpret_cast<float2*>(ws + p.off_stats);
   float* dO = reinterpret_cast<float*>(ws + p.off_opart);
-  const int ns = p.nsplit;
+  int ns = 0;
   if (s.M > 0) {
-    dim3 grid(ns, s.BH());
     const int G = s.G();
     LaunchTimer lt(K_DECODE_SPLIT, st);
 #define H2O_SPLIT(DD, GG) \
-  launch_split<DD, GG>(grid, st, q, kc, vc, s.Hq, s.Hkv, s.M, c, logits, dstat, dO)
+  ns = launch_split<DD, GG>(st, s.BH(), q, kc, vc, s.Hq, s.Hkv, s.M, c, logits, dstat, dO)
     if (s.d == 64) {
       if (G == 1) H2O_SPLIT(64, 1);
       else if (G == 2) H2O_SPLIT(64, 2);

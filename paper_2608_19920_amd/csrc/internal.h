@@ -66,7 +66,7 @@ struct Plan {
 Plan make_plan(const Shape& s, int dtype);
 int mfma_rows_per_block();   // packed rows per workgroup of the MFMA kernels
 int mfma_rows_per_part();    // packed rows per colsum partial of the MFMA kernels
-int decode_nsplit(int M);    // split blocks of the decode kernels for M cache slots
+int decode_max_split();      // largest split-block count per head of the decode kernels
 bool decode_supports(int d, int G);   // (d, G) pairs the decode kernels handle
 
 // ------------------------------------------------------------ kernel timing

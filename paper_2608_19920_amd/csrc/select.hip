@@ -194,9 +194,22 @@ __global__ __launch_bounds__(kArgThreads) void argmin_insert_kernel(
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const float* s = scores + row * M;
   uint32_t bk = 0xFFFFFFFFu, bj = 0xFFFFFFFFu;     // (key, slot), lexicographic
-  for (int j = tid; j < M; j += kArgThreads) {
+  // four independent loads per step; slots are visited in increasing order
+  // per thread, so a strict < keeps the lowest slot among equal keys
+  int j = tid;
+  for (; j + 3 * kArgThreads < M; j += 4 * kArgThreads) {
+    float v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) v[u] = s[j + u * kArgThreads];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const uint32_t key = order_key(v[u]);
+      if (key < bk) { bk = key; bj = (uint32_t)(j + u * kArgThreads); }
+    }
+  }
+  for (; j < M; j += kArgThreads) {
     const uint32_t key = order_key(s[j]);
-    if (key < bk || (key == bk && (uint32_t)j < bj)) { bk = key; bj = (uint32_t)j; }
+    if (key < bk) { bk = key; bj = (uint32_t)j; }
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) {

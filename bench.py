@@ -18,7 +18,6 @@ Prints one JSON line. ``--gpus N`` with N > 1 exits: this build runs on one GPU.
 from __future__ import annotations
 
 import argparse
-import hashlib
 import json
 import os
 import sys
@@ -56,23 +55,17 @@ def attention_flops(w) -> float:
     return 4.0 * w.d * P * w.B * w.Hq
 
 
-def _src_hash(names):
-    h = hashlib.sha256()
-    for n in names:
-        with open(os.path.join(ROOT, "paper_2608_19920_amd", "csrc", n), "rb") as f:
-            h.update(f.read())
-    return h.hexdigest()[:16]
-
-
-def traffic_for(kernel: str, src_files):
-    """HBM bytes per launch from the committed rocprofv3 counter summary, or
-    None if there is none or the kernel sources changed since it was taken."""
+def traffic_for(kernel: str, workload: str):
+    """HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated) from the
+    committed rocprofv3 counter summary, or None if there is none or the
+    kernel's sources changed since the counters were taken."""
+    from paper_2608_19920_amd.counters import KERNELS, src_hash
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
-        rec = json.load(f).get(kernel)
-    if not rec or rec.get("src_hash") != _src_hash(src_files):
+        rec = json.load(f).get(f"{kernel}@{workload}")
+    if not rec or rec.get("src_hash") != src_hash(KERNELS[kernel][1]):
         return None
     return rec.get("bytes_per_launch")
 
@@ -142,12 +135,13 @@ def bench_decode(args, torch, H, W):
     ach = decode_split_bytes(w) / (avg_split_ms * 1e-3) / 1e9
     roof = {"kernel": "decode_split", "bound": "hbm", "achieved": round(ach, 1),
             "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(ach / HBM_PEAK_GBS, 4),
-            "traffic": traffic_for("decode_split", ["decode.hip"]),
+            "traffic": traffic_for("decode_split", w.name),
             "algorithmic_bytes_per_launch": decode_split_bytes(w),
             "avg_launch_us": round(avg_split_ms * 1e3, 2),
             "kernel_us": {k: round(v[0] / max(v[1], 1) * 1e3, 2) for k, v in ktimes.items()},
-            "timing": "HIP events recorded by the library around each launch, on its stream, "
-                      "over an eager pass of the timed steps"}
+            "timing": "start/stop HIP events of hipExtLaunchKernel (stamped at the kernel's "
+                      "own begin and end) on the launch stream, over an eager pass of the "
+                      "timed steps"}
     return dict(w=w, ms_step=ms_step, value=gbs, roofline=roof, wall_s=t_wall,
                 step_bytes=step_bytes)
 
@@ -200,7 +194,7 @@ def bench_prefill(name, args, torch, H, W):
             "roofline_main": {"kernel": "mfma_main", "bound": "mfma",
                               "achieved": round(ach_main, 1), "peak": BF16_PEAK_TFLOPS,
                               "unit": "TFLOP/s", "frac": round(ach_main / BF16_PEAK_TFLOPS, 4),
-                              "traffic": traffic_for("mfma_main", ["sdpa_mfma.hip"])}}
+                              "traffic": traffic_for("mfma_main", w.name)}}
 
 
 # -------------------------------------------------------------- CPU baseline

@@ -98,23 +98,19 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 }  // namespace
 
-LaunchTimer::LaunchTimer(int kid, hipStream_t s) : id(kid), st(s), ev0(nullptr) {
-  if (!g_timing.load()) return;
-  hipEvent_t a;
-  if (hipEventCreate(&a) != hipSuccess) return;
-  if (hipEventRecord(a, st) != hipSuccess) { (void)hipEventDestroy(a); return; }
-  ev0 = a;
+bool timing_begin(hipEvent_t* a, hipEvent_t* b) {
+  if (!g_timing.load()) return false;
+  if (hipEventCreate(a) != hipSuccess) return false;
+  if (hipEventCreate(b) != hipSuccess) {
+    (void)hipEventDestroy(*a);
+    return false;
+  }
+  return true;
 }
 
-LaunchTimer::~LaunchTimer() {
-  if (!ev0) return;
-  hipEvent_t a = static_cast<hipEvent_t>(ev0), b;
-  if (hipEventCreate(&b) != hipSuccess || hipEventRecord(b, st) != hipSuccess) {
-    (void)hipEventDestroy(a);
-    return;
-  }
+void timing_end(int kid, hipEvent_t a, hipEvent_t b) {
   std::lock_guard<std::mutex> lk(g_timing_mu);
-  g_pending.push_back({id, a, b});
+  g_pending.push_back({kid, a, b});
 }
 
 Plan make_plan(const Shape& s, int dtype) {

@@ -288,13 +288,13 @@ int split_count(int M, int BH) {
 }
 
 template <int D, int G>
-int launch_split(hipStream_t st, int BH, const void* q, const void* kc, const void* vc, int Hq,
-                 int Hkv, int M, float c, float* logits, float2* dstat, float* dO) {
-  const int ns = split_count<D, G>(M, BH);
-  decode_split<D, G, 8><<<dim3(ns, BH), kThreads, 0, st>>>((const bf16_t*)q, (const bf16_t*)kc,
-                                                           (const bf16_t*)vc, Hq, Hkv, M, c,
-                                                           logits, dstat, dO);
-  return ns;
+hipError_t launch_split(hipStream_t st, int BH, const void* q, const void* kc, const void* vc,
+                        int Hq, int Hkv, int M, float c, float* logits, float2* dstat, float* dO,
+                        int* ns) {
+  *ns = split_count<D, G>(M, BH);
+  return launch_kernel(K_DECODE_SPLIT, decode_split<D, G, 8>, dim3(*ns, BH), dim3(kThreads), st,
+                       (const bf16_t*)q, (const bf16_t*)kc, (const bf16_t*)vc, Hq, Hkv, M, c,
+                       logits, dstat, dO);
 }
 
 }  // namespace
@@ -317,9 +317,9 @@ hipError_t launch_sdpa_decode(const Shape& s, const Plan& p, const void* q, cons
   int ns = 0;
   if (s.M > 0) {
     const int G = s.G();
-    LaunchTimer lt(K_DECODE_SPLIT, st);
+    hipError_t e = hipErrorInvalidValue;
 #define H2O_SPLIT(DD, GG) \
-  ns = launch_split<DD, GG>(st, s.BH(), q, kc, vc, s.Hq, s.Hkv, s.M, c, logits, dstat, dO)
+  e = launch_split<DD, GG>(st, s.BH(), q, kc, vc, s.Hq, s.Hkv, s.M, c, logits, dstat, dO, &ns)
     if (s.d == 64) {
       if (G == 1) H2O_SPLIT(64, 1);
       else if (G == 2) H2O_SPLIT(64, 2);
@@ -333,20 +333,14 @@ hipError_t launch_sdpa_decode(const Shape& s, const Plan& p, const void* q, cons
       else return hipErrorInvalidValue;
     }
 #undef H2O_SPLIT
-    hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
-  LaunchTimer lt(K_DECODE_COMBINE, st);
   const dim3 cgrid(s.M > 0 ? (s.M + kCols - 1) / kCols : 1, s.BH());
-  if (s.d == 64)
-    decode_combine<64><<<cgrid, kThreads, 0, st>>>(
-        (const bf16_t*)q, (const bf16_t*)kn, (const bf16_t*)vn, s.Hq, s.Hkv, s.M, ns, c, logits,
-        dstat, dO, (bf16_t*)out, lse, wsum);
-  else
-    decode_combine<128><<<cgrid, kThreads, 0, st>>>(
-        (const bf16_t*)q, (const bf16_t*)kn, (const bf16_t*)vn, s.Hq, s.Hkv, s.M, ns, c, logits,
-        dstat, dO, (bf16_t*)out, lse, wsum);
-  return hipGetLastError();
+  auto combine = s.d == 64 ? decode_combine<64> : decode_combine<128>;
+  return launch_kernel(K_DECODE_COMBINE, combine, cgrid, dim3(kThreads), st, (const bf16_t*)q,
+                       (const bf16_t*)kn, (const bf16_t*)vn, s.Hq, s.Hkv, s.M, ns, c,
+                       (const float*)logits, (const float2*)dstat, (const float*)dO,
+                       (bf16_t*)out, lse, wsum);
 }
 
 }  // namespace h2o

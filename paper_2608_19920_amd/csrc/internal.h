@@ -2,6 +2,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 #include <stddef.h>
 #include <stdint.h>
 
@@ -75,15 +76,27 @@ enum KernelId {
   K_GENERIC_LSE = 0, K_GENERIC_MAIN, K_MFMA_LSE, K_MFMA_MAIN, K_SPLIT_REDUCE, K_COLSUM_REDUCE,
   K_ACCUMULATE, K_BOTTOMK, K_INSERT, K_DECODE_SPLIT, K_DECODE_COMBINE, K_ARGMIN_INSERT, K_COUNT
 };
-// While timing is switched on (h2o_debug_timing), a LaunchTimer brackets one
-// kernel launch with two events recorded on the launch stream.
-struct LaunchTimer {
-  LaunchTimer(int id, hipStream_t st);
-  ~LaunchTimer();
-  int id;
-  hipStream_t st;
-  void* ev0;
-};
+// While timing is switched on (h2o_debug_timing), kernels go out through
+// hipExtLaunchKernel with a start and a stop event: the runtime stamps them
+// with the kernel's own begin and end, so the pair measures the kernel and
+// not the dispatch around it. timing_begin creates the pair (false when timing
+// is off); timing_end queues it for h2o_debug_kernel_time.
+bool timing_begin(hipEvent_t* a, hipEvent_t* b);
+void timing_end(int kernel_id, hipEvent_t a, hipEvent_t b);
+
+template <typename F, typename... Args>
+hipError_t launch_kernel(int kernel_id, F kern, dim3 grid, dim3 block, hipStream_t st,
+                         Args... args) {
+  hipEvent_t a = nullptr, b = nullptr;
+  if (timing_begin(&a, &b)) {
+    hipExtLaunchKernelGGL(kern, grid, block, 0, st, a, b, 0, args...);
+    const hipError_t e = hipGetLastError();
+    timing_end(kernel_id, a, b);
+    return e;
+  }
+  hipLaunchKernelGGL(kern, grid, block, 0, st, args...);
+  return hipGetLastError();
+}
 
 // ------------------------------------------------------------- launchers
 // Each returns hipSuccess or the launch error. They assume validated inputs.

@@ -151,16 +151,13 @@ hipError_t run(const Shape& s, const Plan& p, const void* q, const void* kc, con
   dim3 grid((s.R() + kRows - 1) / kRows, s.BH());
   float* lse_ws = reinterpret_cast<float*>(ws + p.off_stats);
   float* parts = reinterpret_cast<float*>(ws + p.off_parts);
-  { LaunchTimer lt(K_GENERIC_LSE, st);
-  pass_a<E, D><<<grid, kRows, 0, st>>>((const E*)q, (const E*)kc, (const E*)kn, lse, lse_ws,
-                                       s.Hq, s.Hkv, s.T, s.M, scale); }
-  hipError_t e = hipGetLastError();
+  hipError_t e = launch_kernel(K_GENERIC_LSE, pass_a<E, D>, grid, dim3(kRows), st, (const E*)q,
+                               (const E*)kc, (const E*)kn, lse, lse_ws, s.Hq, s.Hkv, s.T, s.M,
+                               scale);
   if (e != hipSuccess) return e;
-  { LaunchTimer lt(K_GENERIC_MAIN, st);
-  pass_b<E, D><<<grid, kRows, 0, st>>>((const E*)q, (const E*)kc, (const E*)vc, (const E*)kn,
-                                       (const E*)vn, (E*)out, lse_ws, parts, s.Hq, s.Hkv, s.T,
-                                       s.M, scale); }
-  e = hipGetLastError();
+  e = launch_kernel(K_GENERIC_MAIN, pass_b<E, D>, grid, dim3(kRows), st, (const E*)q,
+                    (const E*)kc, (const E*)vc, (const E*)kn, (const E*)vn, (E*)out,
+                    (const float*)lse_ws, parts, s.Hq, s.Hkv, s.T, s.M, scale);
   if (e != hipSuccess) return e;
   return launch_colsum_reduce(s, p, parts, wsum, st);
 }

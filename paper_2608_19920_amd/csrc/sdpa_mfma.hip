@@ -587,26 +587,18 @@ hipError_t run(const Shape& s, const Plan& p, const void* q, const void* kc, con
   float2* stats = reinterpret_cast<float2*>(ws + p.off_stats);
   float* parts = reinterpret_cast<float*>(ws + p.off_parts);
   float* opart = reinterpret_cast<float*>(ws + p.off_opart);
-  {
-    LaunchTimer lt(K_MFMA_LSE, st);
-    lse_pass<D, NW, NQB><<<grid_lse, NW * 64, 0, st>>>(g, s.Hq, s.Hkv, p.nsplit_lse, c, stats);
-  }
-  hipError_t e = hipGetLastError();
+  hipError_t e = launch_kernel(K_MFMA_LSE, lse_pass<D, NW, NQB>, grid_lse, dim3(NW * 64), st,
+                               g, s.Hq, s.Hkv, p.nsplit_lse, c, stats);
   if (e != hipSuccess) return e;
-  {
-    LaunchTimer lt(K_MFMA_MAIN, st);
-    main_pass<D, NW, NQB><<<grid, NW * 64, 0, st>>>(g, s.Hq, s.Hkv, p.nsplit, p.nsplit_lse, c,
-                                                    stats, parts, p.parts_ld, (bf16_t*)out, opart,
-                                                    lse);
-  }
-  e = hipGetLastError();
+  e = launch_kernel(K_MFMA_MAIN, main_pass<D, NW, NQB>, grid, dim3(NW * 64), st, g, s.Hq, s.Hkv,
+                    p.nsplit, p.nsplit_lse, c, (const float2*)stats, parts, p.parts_ld,
+                    (bf16_t*)out, opart, lse);
   if (e != hipSuccess) return e;
   if (p.nsplit > 1) {
     const size_t n4 = (size_t)s.BH() * s.R() * s.d / 4;
-    LaunchTimer lt(K_SPLIT_REDUCE, st);
-    split_reduce<D><<<(unsigned)((n4 + 255) / 256), 256, 0, st>>>(
-        opart, (bf16_t*)out, s.Hq, s.Hkv, s.G(), s.T, s.R(), s.BH(), p.nsplit);
-    e = hipGetLastError();
+    e = launch_kernel(K_SPLIT_REDUCE, split_reduce<D>, dim3((unsigned)((n4 + 255) / 256)),
+                      dim3(256), st, (const float*)opart, (bf16_t*)out, s.Hq, s.Hkv, s.G(), s.T,
+                      s.R(), s.BH(), p.nsplit);
     if (e != hipSuccess) return e;
   }
   return launch_colsum_reduce(s, p, parts, wsum, st);

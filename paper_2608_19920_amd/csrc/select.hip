@@ -245,20 +245,16 @@ hipError_t launch_argmin_insert(void* kc, void* vc, float* scores, int32_t* toke
                                 int rows, int M, int T, int d, int32_t pos0, int elem_bytes,
                                 hipStream_t st) {
   if (rows == 0) return hipSuccess;
-  LaunchTimer lt(K_ARGMIN_INSERT, st);
-  argmin_insert_kernel<<<rows, kArgThreads, 0, st>>>(
-      (uint4*)kc, (uint4*)vc, scores, token_pos, (const uint4*)kn, (const uint4*)vn, wsum, idx, M,
-      T, d * elem_bytes / 16, pos0);
-  return hipGetLastError();
+  return launch_kernel(K_ARGMIN_INSERT, argmin_insert_kernel, dim3(rows), dim3(kArgThreads), st,
+                       (uint4*)kc, (uint4*)vc, scores, token_pos, (const uint4*)kn,
+                       (const uint4*)vn, wsum, idx, M, T, d * elem_bytes / 16, pos0);
 }
 
 hipError_t launch_colsum_reduce(const Shape& s, const Plan& p, const float* parts, float* wsum,
                                 hipStream_t st) {
   dim3 grid((s.Nk() + 255) / 256, s.BH());
-  LaunchTimer lt(K_COLSUM_REDUCE, st);
-  colsum_reduce_kernel<<<grid, 256, 0, st>>>(parts, wsum, p.nparts, p.rows_per_part, s.BH(),
-                                             s.Nk(), p.parts_ld, s.G(), s.T, s.M);
-  return hipGetLastError();
+  return launch_kernel(K_COLSUM_REDUCE, colsum_reduce_kernel, grid, dim3(256), st, parts, wsum,
+                       p.nparts, p.rows_per_part, s.BH(), s.Nk(), p.parts_ld, s.G(), s.T, s.M);
 }
 
 hipError_t launch_accumulate(float* scores, const float* wsum, int rows, int M, int T,
@@ -266,17 +262,14 @@ hipError_t launch_accumulate(float* scores, const float* wsum, int rows, int M, 
   if (rows == 0 || M == 0) return hipSuccess;
   int bx = (M + 256 * 4 - 1) / (256 * 4);
   dim3 grid(bx < 1 ? 1 : bx, rows);
-  LaunchTimer lt(K_ACCUMULATE, st);
-  accumulate_kernel<<<grid, 256, 0, st>>>(scores, wsum, M, T);
-  return hipGetLastError();
+  return launch_kernel(K_ACCUMULATE, accumulate_kernel, grid, dim3(256), st, scores, wsum, M, T);
 }
 
 hipError_t launch_bottomk(const float* scores, int rows, int M, int k, int32_t* idx,
                           hipStream_t st) {
   if (rows == 0 || k == 0) return hipSuccess;
-  LaunchTimer lt(K_BOTTOMK, st);
-  bottomk_kernel<<<rows, kSelThreads, 0, st>>>(scores, M, k, idx);
-  return hipGetLastError();
+  return launch_kernel(K_BOTTOMK, bottomk_kernel, dim3(rows), dim3(kSelThreads), st, scores, M, k,
+                       idx);
 }
 
 hipError_t launch_insert(void* kc, void* vc, float* scores, int32_t* token_pos, const void* kn,
@@ -287,11 +280,9 @@ hipError_t launch_insert(void* kc, void* vc, float* scores, int32_t* token_pos, 
   int kPer = kInsThreads / vecs;
   if (kPer < 1) kPer = 1;
   dim3 grid((k + kPer - 1) / kPer, rows);
-  LaunchTimer lt(K_INSERT, st);
-  insert_kernel<<<grid, kInsThreads, 0, st>>>((uint4*)kc, (uint4*)vc, scores, token_pos,
-                                              (const uint4*)kn, (const uint4*)vn, wsum, idx, M, T,
-                                              vecs, k, kPer, pos0);
-  return hipGetLastError();
+  return launch_kernel(K_INSERT, insert_kernel, grid, dim3(kInsThreads), st, (uint4*)kc,
+                       (uint4*)vc, scores, token_pos, (const uint4*)kn, (const uint4*)vn, wsum,
+                       idx, M, T, vecs, k, kPer, pos0);
 }
 
 }  // namespace h2o

@@ -138,8 +138,9 @@ const char* h2o_last_error(void);
 int h2o_debug_force_path(int path);
 
 /* Benchmark hook, not needed in normal use. h2o_debug_timing(1) makes every
- * kernel launch of the library record a start and a stop event on the launch
- * stream (do not use it under stream capture); h2o_debug_timing(0) stops it.
+ * kernel launch of the library go through hipExtLaunchKernel with a start and
+ * a stop event, which the runtime stamps at the kernel's own begin and end
+ * (do not use it under stream capture); h2o_debug_timing(0) stops it.
  * Either call clears the totals. h2o_debug_kernel_time(id, &ms, &n) waits for
  * the recorded events and returns the summed duration (milliseconds) and the
  * launch count of kernel `id` since the last h2o_debug_timing call. Ids:

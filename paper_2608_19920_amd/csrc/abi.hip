@@ -194,8 +194,9 @@ int h2o_debug_force_path(int path) {
   return ok();
 }
 
-// Timing hook for benchmarks: while on, every kernel launch is bracketed by
-// events on its stream. Switching it (on or off) clears the totals.
+// Timing hook for benchmarks: while on, every kernel launch carries a start
+// and a stop event stamped at the kernel's begin and end. Switching it (on or
+// off) clears the totals.
 int h2o_debug_timing(int on) {
   std::lock_guard<std::mutex> lk(g_timing_mu);
   fold_pending();

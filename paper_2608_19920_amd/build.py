@@ -27,6 +27,16 @@ FLAGS = [
     # packed FP32 VALU ops are left out of the device code on purpose
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
 ]
+# Per-source additions. The decode kernels keep their MFMA accumulators in
+# VGPRs: they are rescaled by VALU code, and AGPR accumulators would be copied
+# back and forth every step.
+FILE_FLAGS = {
+    "decode.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+}
+
+
+def flags_for(src: str):
+    return FLAGS + FILE_FLAGS.get(os.path.basename(src), [])
 
 
 def _quiet(text: str) -> str:
@@ -37,7 +47,7 @@ def _quiet(text: str) -> str:
 
 def _compile(src: str) -> str:
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *FLAGS, "-x", "hip", "-c", src, "-o", obj]
+    cmd = [HIPCC, *flags_for(src), "-x", "hip", "-c", src, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     msg = _quiet(r.stdout + r.stderr).strip()
     if r.returncode != 0:

@@ -155,8 +155,9 @@ Plan make_plan(const Shape& s, int dtype) {
     p.off_opart = off;
     off = align256(off + (size_t)p.nsplit * BH * s.G() * s.d * sizeof(float));
     p.off_logits = off;
-    off = align256(off + BH * s.G() * (size_t)s.M * sizeof(float));
-    p.off_parts = off;
+    off = align256(off + BH * s.G() * (size_t)((s.M + 3) & ~3) * sizeof(float));
+    p.off_parts = off;   // sink for the logit stores of masked slots (64 lanes x 16 B)
+    off = align256(off + 64 * 16);
     p.bytes = off;
     return p;
   } else {

@@ -2,12 +2,13 @@
 // step streams the whole KV cache once and is bound by HBM bandwidth
 // (Sec. "Sparse Attention. Key-Value Caching": N_q = 1, N_k = N_C).
 //
-//   split    block (split s, head bh) streams rounds s, s+ns, ... of head bh.
-//            Sixteen lanes share one key row: lane `slice` holds D/16 elements
-//            of it, so each wave load reads four consecutive rows (contiguous
-//            bytes). Logits (log2 domain) reduce over the 16 lanes with DPP;
-//            the split's softmax partial (m, l, O-partial) per query head is
-//            written out, and so are the logits for the column sums.
+//   split    block (split s, head bh): each of its 4 waves streams steps of 32
+//            cache slots (steps s*4 + w, + 4 ns, ...). The G queries of the
+//            group are the columns of bf16 MFMA products: S^T = K Q^T straight
+//            from the loaded K rows, O^T += V^T P with V passed through LDS
+//            and read back transposed. The split's softmax partial (m, l,
+//            O-partial) per query head is written out, and so are the float32
+//            logits for the column sums ([bh][g][slot]).
 //   combine  block bh merges the splits with the chunk's own key (column M),
 //            writes out and lse, and wsum[j] = sum_g exp2(logit_gj - lambda_g)
 //            from the stored logits.
@@ -17,173 +18,227 @@ namespace h2o {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kLanesPerKey = 16;                         // lanes sharing one key row
-constexpr int kKeysPerRound = kThreads / kLanesPerKey;   // 16
+constexpr int kWaves = kThreads / 64;
+constexpr int kStep = 32;                                // cache slots per wave step
 constexpr int kMaxGD = 512;                              // G * D handled by these kernels
 constexpr int kMaxSplit = 64;                            // split blocks per head, at most
+constexpr int kBufferFlags = 0x00020000;                 // buffer descriptor word 3 (32-bit data)
 
-template <int CTRL>
-__device__ __forceinline__ float dpp(float x) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, true));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef short s16x8 __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+
+__device__ __forceinline__ f32x4 mfma(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
-// Sum over the 16 lanes of a DPP row; every lane gets the total.
-__device__ __forceinline__ float sum16(float v) {
-  v += dpp<0xB1>(v);    // quad_perm [1,0,3,2]
-  v += dpp<0x4E>(v);    // quad_perm [2,3,0,1]
-  v += dpp<0x141>(v);   // row_half_mirror: lane l <-> 7-l within each half row
-  v += dpp<0x140>(v);   // row_mirror: lane l <-> 15-l
-  return v;
+__device__ __forceinline__ u32x4 load16(const bf16_t* p) {
+  return *reinterpret_cast<const u32x4*>(p);
 }
 
-// EPL consecutive bf16 elements of a row, as float.
-template <int EPL>
-struct RowPiece {
-  typedef uint32_t raw_t __attribute__((ext_vector_type(EPL / 2)));
-  static __device__ __forceinline__ raw_t load(const bf16_t* p) {
-    return *reinterpret_cast<const raw_t*>(p);
-  }
-  static __device__ __forceinline__ void unpack(const raw_t w, float* f) {
-#pragma unroll
-    for (int e = 0; e < EPL / 2; ++e) {
-      f[2 * e] = __uint_as_float(w[e] << 16);
-      f[2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
-    }
-  }
-};
+// floats per row of the stored logits ([bh][g][slot]; 16-byte aligned rows)
+__host__ __device__ constexpr int logit_pitch(int M) { return (M + 3) & ~3; }
 
-// Streaming split kernel. The cache slots of head bh are walked in rounds of
-// 16 slots (one slot per 16-lane DPP row; lane `slice` holds D/16 elements
-// of the row); block (s, bh) takes rounds s, s + ns, s + 2 ns, ... so that
-// the ns blocks of a head sweep its K and V rows together. The K and V rows
-// of the next PF rounds of a block are in flight while a round is computed.
-// Each lane row keeps, per query head, a reference maximum m (the first
-// logit it saw, raised only when a later logit exceeds it by more than 64 in
-// log2 units, which keeps every exp2 term below 2^64), the sum l of
-// exp2(logit - m) and the weighted V accumulator; the block merges them at
-// the end.
-template <int D, int G, int PF>
+// bf16 per LDS row of a staged V step (32 rows x D)
+template <int D>
+__host__ __device__ constexpr int vpitch() { return D + 16; }
+
+// A operand of O^T = V^T P for rows d = 16*db .. 16*db+15 of V^T. Within each
+// 16-lane group, ds_read_b64_tr_b16 hands lane i element i%4 of the 8-byte
+// chunks addressed by lanes 4k + i/4 (k = 0..3). Lane 4k + c of group j
+// addresses slot 4j + k, columns 16*db + 4c..+3, so lane i of group j ends up
+// with V[4j + k][16*db + i], k = 0..3; a second read covers slots 16 + 4j + k.
+// These are the slots of the P operand built from the S^T accumulators.
+template <int D>
+__device__ __forceinline__ bf16x8 v_operand(const bf16_t* vs, int db, int lane) {
+  const int j = lane >> 4, i = lane & 15;
+  const bf16_t* p = vs + (4 * j + (i >> 2)) * vpitch<D>() + 16 * db + 4 * (i & 3);
+  typedef __attribute__((address_space(3))) bf16_t lds_bf16;
+  const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)((lds_bf16*)p));
+  const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (lds_s16x4*)((lds_bf16*)(p + 16 * vpitch<D>())));
+  const s16x8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+// Streaming split kernel.
+//
+// Operand layouts of v_mfma_f32_16x16x32_bf16 (A: lane l holds row l%16,
+// k = 8*(l/16)..+7; B: lane l holds column l%16, the same k; C: lane l holds
+// rows 4*(l/16)..+3 of column l%16):
+//   S^T[slot, col] = sum_d K[slot, d] Q[col, d]: A = 16 K rows as loaded from
+//     global memory (lane l: slot 16*kb + l%16, d = 32*dh + 8*(l/16)..+7),
+//     B = the queries, column c holding query head c % G (columns repeat the
+//     G heads, so every lane has a real logit and duplicate stores write
+//     equal values).
+//   O^T[d, col] += sum_slot V[slot, d] P[slot, col]: the S^T accumulators of
+//     the step's two 16-slot blocks, converted to bf16, are the B operand
+//     (lane l: slots 16*kb + 4*(l/16) + r); A comes from v_operand.
+// Each column keeps a reference maximum m, common to the 4 lanes holding the
+// column; it is raised (a wave-uniform, rare branch) when a logit exceeds it
+// by more than 64 in log2 units, which keeps every exp2 term below 2^64. K
+// and V come in through buffer loads whose range is the head, so slots past
+// the cache read as zero; they are masked, and their logit stores go to a
+// sink.
+template <int D, int G>
 __global__ __launch_bounds__(kThreads) void decode_split(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
     int Hq, int Hkv, int M, float c_log2, float* __restrict__ logits,
-    float2* __restrict__ dstat, float* __restrict__ dO) {
-  constexpr int EPL = D / kLanesPerKey;   // elements per lane (4 or 8)
-  typedef RowPiece<EPL> RP;
-  __shared__ float red[kThreads / 64][G];
-  __shared__ float acc_s[kKeysPerRound][G * D + 4];
+    float2* __restrict__ dstat, float* __restrict__ dO, float* __restrict__ sink) {
+  constexpr int DH = D / 32;                 // MFMA k-chunks of a row
+  constexpr int NK = 2 * DH;                 // K loads per step (two 16-slot blocks)
+  constexpr int RPL = 512 / D;               // V rows per wave load
+  constexpr int NV = kStep / RPL;            // V loads per step
+  constexpr int VP = vpitch<D>();
+  static_assert(G <= 16 && (D == 64 || D == 128), "decode shape");
+  __shared__ __attribute__((aligned(16))) bf16_t vs_all[kWaves][kStep * VP];
+  __shared__ float red_m[kWaves][16], red_l[kWaves][16];
+  __shared__ float ored[kWaves][G][D];
   const int s = blockIdx.x, nsplit = gridDim.x;
   const size_t bh = blockIdx.y;
   const int b = (int)(bh / Hkv), h = (int)(bh % Hkv);
-  const int head_rounds = (M + kKeysPerRound - 1) / kKeysPerRound;
-  const int nrounds = (head_rounds - s + nsplit - 1) / nsplit;   // rounds s, s+ns, ...
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int kg = tid / kLanesPerKey, slice = tid % kLanesPerKey;
-  const bf16_t* kbase = kc + bh * (size_t)M * D + slice * EPL;
-  const bf16_t* vbase = vc + bh * (size_t)M * D + slice * EPL;
-  auto slot_of = [&](int rd) { return (s + rd * nsplit) * kKeysPerRound + kg; };
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int col = lane & 15, grp = lane >> 4;
+  const int head_steps = (M + kStep - 1) / kStep;
+  const int stream = s * kWaves + wave, nstreams = nsplit * kWaves;
+  const int nst = stream < head_steps ? (head_steps - stream + nstreams - 1) / nstreams : 0;
+  // K and V of head bh as buffer resources: rows past the cache read as zero
+  const int head_bytes = (int)((uint32_t)M * (uint32_t)(D * 2));
+  const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(kc + bh * (size_t)M * D), (short)0, head_bytes, kBufferFlags);
+  const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc(
+      (void*)(vc + bh * (size_t)M * D), (short)0, head_bytes, kBufferFlags);
+  bf16_t* vs = vs_all[wave];
+  const int vrow = lane / (D / 8), vcol = 8 * (lane % (D / 8));
+  const uint32_t koff = (uint32_t)(col * D + 8 * grp) * 2u;   // + block / chunk offsets
+  const uint32_t voff = (uint32_t)(vrow * D + vcol) * 2u;
+  // logits are stored head-major, [bh][g][slot] with the row padded to a multiple of 4
+  float* lg_out = logits + (bh * G + col % G) * (size_t)logit_pitch(M);
 
-  // ring of PF rounds; slots past the cache re-read the last slot
-  typename RP::raw_t kr[PF], vr[PF];
-  auto issue = [&](int rd, int slot_) {
-    const int kk = min(slot_of(rd), M - 1);
-    kr[slot_] = RP::load(kbase + (size_t)kk * D);
-    vr[slot_] = RP::load(vbase + (size_t)kk * D);
+  // Two ring slots: a step's loads are issued before the previous step is
+  // consumed, so every wait leaves the other slot's loads in flight. Steps
+  // past the head read as zero (buffer range) and are masked.
+  u32x4 kr[2][NK], vr[2][NV];
+  auto issue = [&](int k, int u) {
+    const uint32_t base = (uint32_t)((stream + k * nstreams) * kStep) * (uint32_t)(D * 2);
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int dh = 0; dh < DH; ++dh)
+        kr[u][kb * DH + dh] = __builtin_bit_cast(
+            u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                       krs, (int)(base + koff + (uint32_t)((16 * kb * D + 32 * dh) * 2)), 0, 0));
+#pragma unroll
+    for (int t = 0; t < NV; ++t)
+      vr[u][t] = __builtin_bit_cast(
+          u32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                     vrs, (int)(base + voff + (uint32_t)(t * RPL * D * 2)), 0, 0));
   };
+
+  bf16x8 qb[DH];
+  {
+    const bf16_t* qrow = q + (size_t)(b * Hq + h * G + col % G) * D + 8 * grp;
 #pragma unroll
-  for (int u = 0; u < PF; ++u) issue(u, u);
-  float qs[G][EPL];
-#pragma unroll
-  for (int g = 0; g < G; ++g) {
-    float f[EPL];
-    RP::unpack(RP::load(q + (size_t)(b * Hq + h * G + g) * D + slice * EPL), f);
-#pragma unroll
-    for (int e = 0; e < EPL; ++e) qs[g][e] = f[e] * c_log2;
+    for (int dh = 0; dh < DH; ++dh) qb[dh] = __builtin_bit_cast(bf16x8, load16(qrow + 32 * dh));
   }
-  float m[G], l[G], acc[G][EPL];
+  float m = -INFINITY, l = 0.f;
+  f32x4 oacc[D / 16];
 #pragma unroll
-  for (int g = 0; g < G; ++g) {
-    m[g] = -INFINITY;
-    l[g] = 0.f;
+  for (int db = 0; db < D / 16; ++db) oacc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  auto consume = [&](int k, int u) {
+    const int key0 = (stream + k * nstreams) * kStep;
 #pragma unroll
-    for (int e = 0; e < EPL; ++e) acc[g][e] = 0.f;
-  }
-  for (int rd0 = 0; rd0 < nrounds; rd0 += PF) {
+    for (int t = 0; t < NV; ++t)
+      *reinterpret_cast<u32x4*>(vs + (t * RPL + vrow) * VP + vcol) = vr[u][t];
+    f32x4 sacc[2];
 #pragma unroll
-    for (int u = 0; u < PF; ++u) {
-      const int rd = rd0 + u;
-      if (rd < nrounds) {
-        const int kk = slot_of(rd);
-        const bool ok = kk < M;
-        float kf[EPL], vf[EPL];
-        RP::unpack(kr[u], kf);
-        RP::unpack(vr[u], vf);
-        issue(rd + PF, u);                       // refill the slot just consumed
-        float lgs[G];
+    for (int kb = 0; kb < 2; ++kb) {
+      sacc[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int g = 0; g < G; ++g) {
-          float a = 0.f;
-#pragma unroll
-          for (int e = 0; e < EPL; ++e) a = fmaf(qs[g][e], kf[e], a);
-          lgs[g] = sum16(a);
-        }
-        if (ok && slice == 0) {                    // logits stored key-major: [bh][slot][g]
-          float* dst = logits + ((bh * M) + kk) * (size_t)G;
-#pragma unroll
-          for (int g = 0; g < G; ++g) dst[g] = lgs[g];
-        }
-#pragma unroll
-        for (int g = 0; g < G; ++g) {
-          const float lg = lgs[g];
-          if (ok && lg > m[g] + 64.f) {            // first slot, or a much larger logit
-            const float sc = __builtin_amdgcn_exp2f(m[g] - lg);
-            l[g] *= sc;
-#pragma unroll
-            for (int e = 0; e < EPL; ++e) acc[g][e] *= sc;
-            m[g] = lg;
-          }
-          const float p = ok ? __builtin_amdgcn_exp2f(lg - m[g]) : 0.f;
-          l[g] += p;
-#pragma unroll
-          for (int e = 0; e < EPL; ++e) acc[g][e] = fmaf(p, vf[e], acc[g][e]);
-        }
-      }
+      for (int dh = 0; dh < DH; ++dh)
+        sacc[kb] = mfma(__builtin_bit_cast(bf16x8, kr[u][kb * DH + dh]), qb[dh], sacc[kb]);
     }
-  }
-  // block merge: common maximum per query head, rescale, sum through LDS
+    float lg[8];
+    float mx = -INFINITY;
 #pragma unroll
-  for (int g = 0; g < G; ++g) {
-    float mx = m[g];
-    for (int o = 16; o < 64; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
-    if (lane == 0) red[wave][g] = mx;
+    for (int i = 0; i < 8; ++i) {
+      lg[i] = sacc[i >> 2][i & 3] * c_log2;
+      mx = fmaxf(mx, lg[i]);
+    }
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {   // 4 consecutive slots of one head per lane
+      // stores of masked slots go to the sink, so that no store is conditional
+      const int k4 = key0 + 16 * kb + 4 * grp;
+      float* dst = k4 < M ? lg_out + k4 : sink + 4 * lane;
+      *reinterpret_cast<f32x4*>(dst) =
+          f32x4{lg[4 * kb], lg[4 * kb + 1], lg[4 * kb + 2], lg[4 * kb + 3]};
+    }
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    if (__builtin_amdgcn_ballot_w64(mx > m + 64.f)) {    // wave-uniform, rare after the start
+      const bool up = mx > m + 64.f;
+      const float sc = up ? __builtin_amdgcn_exp2f(m - mx) : 1.f;
+      l *= sc;
+#pragma unroll
+      for (int db = 0; db < D / 16; ++db) oacc[db] *= sc;
+      m = up ? mx : m;
+    }
+    bf16x8 pb;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int key = key0 + 16 * (i >> 2) + 4 * grp + (i & 3);
+      const float p = key < M ? __builtin_amdgcn_exp2f(lg[i] - m) : 0.f;
+      l += p;
+      pb[i] = (__bf16)p;
+    }
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int db = 0; db < D / 16; ++db) oacc[db] = mfma(v_operand<D>(vs, db, lane), pb, oacc[db]);
+  };
+
+  issue(0, 0);
+  for (int k = 0; k < nst; k += 2) {
+    issue(k + 1, 1);
+    consume(k, 0);
+    if (k + 1 >= nst) break;
+    issue(k + 2, 0);
+    consume(k + 1, 1);
+  }
+  // block merge: per column, the common maximum over the waves
+  l += __shfl_xor(l, 16, 64);
+  l += __shfl_xor(l, 32, 64);
+  if (grp == 0) {
+    red_m[wave][col] = m;
+    red_l[wave][col] = l;
   }
   __syncthreads();
-  float mb[G];
+  float mb = red_m[0][col];
 #pragma unroll
-  for (int g = 0; g < G; ++g) {
-    float mx = red[0][g];
+  for (int w = 1; w < kWaves; ++w) mb = fmaxf(mb, red_m[w][col]);
+  const float sc = m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - mb);
+  if (col < G) {
 #pragma unroll
-    for (int w = 1; w < kThreads / 64; ++w) mx = fmaxf(mx, red[w][g]);
-    mb[g] = mx;
-  }
-  __syncthreads();
+    for (int db = 0; db < D / 16; ++db)
 #pragma unroll
-  for (int g = 0; g < G; ++g) {
-    const float sc = m[g] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m[g] - mb[g]);
-    float lv = slice == 0 ? l[g] * sc : 0.f;   // l is identical in the 16 lanes of a row
-    for (int o = 16; o < 64; o <<= 1) lv += __shfl_xor(lv, o, 64);
-    if (lane == 0) red[wave][g] = lv;
-#pragma unroll
-    for (int e = 0; e < EPL; ++e) acc_s[kg][g * D + slice * EPL + e] = acc[g][e] * sc;
+      for (int r = 0; r < 4; ++r) ored[wave][col][16 * db + 4 * grp + r] = oacc[db][r] * sc;
   }
   __syncthreads();
   if (tid < G) {
+    float mg = red_m[0][tid];
+    for (int w = 1; w < kWaves; ++w) mg = fmaxf(mg, red_m[w][tid]);
     float lt = 0.f;
-    for (int w = 0; w < kThreads / 64; ++w) lt += red[w][tid];
-    dstat[(bh * nsplit + s) * G + tid] = make_float2(mb[tid], lt);
+    for (int w = 0; w < kWaves; ++w)
+      if (red_m[w][tid] != -INFINITY) lt += red_l[w][tid] * __builtin_amdgcn_exp2f(red_m[w][tid] - mg);
+    dstat[(bh * nsplit + s) * G + tid] = make_float2(mg, lt);
   }
   for (int c = tid; c < G * D; c += kThreads) {
     float a = 0.f;
 #pragma unroll
-    for (int k2 = 0; k2 < kKeysPerRound; ++k2) a += acc_s[k2][c];
+    for (int w = 0; w < kWaves; ++w) a += ored[w][c / D][c % D];
     dO[(bh * nsplit + s) * (size_t)(G * D) + c] = a;
   }
 }
@@ -248,11 +303,12 @@ __global__ __launch_bounds__(kThreads) void decode_combine(
     }
   }
   float* w = wsum + bh * (size_t)(M + 1);
-  const float* lgb = logits + bh * (size_t)M * G;
+  const float* lgb = logits + bh * (size_t)G * logit_pitch(M);
   const int c0 = blockIdx.x * kCols, c1 = min(M, c0 + kCols);
   for (int j = c0 + tid; j < c1; j += kThreads) {
     float a = 0.f;
-    for (int g = 0; g < G; ++g) a += __builtin_amdgcn_exp2f(lgb[(size_t)j * G + g] - lam[g]);
+    for (int g = 0; g < G; ++g)
+      a += __builtin_amdgcn_exp2f(lgb[(size_t)g * logit_pitch(M) + j] - lam[g]);
     w[j] = a;
   }
   if (blockIdx.x == 0 && tid == 0) {
@@ -264,13 +320,13 @@ __global__ __launch_bounds__(kThreads) void decode_combine(
 
 // Split blocks per head such that all blocks of the grid are resident at
 // once (blocks per CU of this kernel instance x CUs), at most kMaxSplit and
-// at most one per round of slots.
+// at most one wave per step of slots.
 template <int D, int G>
 int split_count(int M, int BH) {
   static int resident = 0;
   if (!resident) {
     int per_cu = 0, dev = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, decode_split<D, G, 8>, kThreads,
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, decode_split<D, G>, kThreads,
                                                      0) != hipSuccess || per_cu < 1)
       per_cu = 2;
     if (hipGetDevice(&dev) != hipSuccess ||
@@ -281,8 +337,9 @@ int split_count(int M, int BH) {
     resident = per_cu * cus;
   }
   int ns = resident / BH;
-  const int rounds = (M + kKeysPerRound - 1) / kKeysPerRound;
-  if (ns > rounds) ns = rounds;
+  const int steps = (M + kStep - 1) / kStep;
+  const int max_ns = (steps + kWaves - 1) / kWaves;
+  if (ns > max_ns) ns = max_ns;
   if (ns > kMaxSplit) ns = kMaxSplit;
   return ns < 1 ? 1 : ns;
 }
@@ -290,11 +347,11 @@ int split_count(int M, int BH) {
 template <int D, int G>
 hipError_t launch_split(hipStream_t st, int BH, const void* q, const void* kc, const void* vc,
                         int Hq, int Hkv, int M, float c, float* logits, float2* dstat, float* dO,
-                        int* ns) {
+                        float* sink, int* ns) {
   *ns = split_count<D, G>(M, BH);
-  return launch_kernel(K_DECODE_SPLIT, decode_split<D, G, 8>, dim3(*ns, BH), dim3(kThreads), st,
+  return launch_kernel(K_DECODE_SPLIT, decode_split<D, G>, dim3(*ns, BH), dim3(kThreads), st,
                        (const bf16_t*)q, (const bf16_t*)kc, (const bf16_t*)vc, Hq, Hkv, M, c,
-                       logits, dstat, dO);
+                       logits, dstat, dO, sink);
 }
 
 }  // namespace
@@ -314,12 +371,14 @@ hipError_t launch_sdpa_decode(const Shape& s, const Plan& p, const void* q, cons
   float* logits = reinterpret_cast<float*>(ws + p.off_logits);
   float2* dstat = reinterpret_cast<float2*>(ws + p.off_stats);
   float* dO = reinterpret_cast<float*>(ws + p.off_opart);
+  float* sink = reinterpret_cast<float*>(ws + p.off_parts);
   int ns = 0;
   if (s.M > 0) {
     const int G = s.G();
     hipError_t e = hipErrorInvalidValue;
 #define H2O_SPLIT(DD, GG) \
-  e = launch_split<DD, GG>(st, s.BH(), q, kc, vc, s.Hq, s.Hkv, s.M, c, logits, dstat, dO, &ns)
+  e = launch_split<DD, GG>(st, s.BH(), q, kc, vc, s.Hq, s.Hkv, s.M, c, logits, dstat, dO, sink, \
+                           &ns)
     if (s.d == 64) {
       if (G == 1) H2O_SPLIT(64, 1);
       else if (G == 2) H2O_SPLIT(64, 2);

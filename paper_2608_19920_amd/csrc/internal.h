@@ -59,7 +59,7 @@ struct Plan {
   int nsplit_lse;      // key-range splits per row tile of the lse pass (MFMA path)
   int parts_ld;        // floats per colsum partial row (>= Nk)
   size_t off_stats;    // float2 (m, l) per (split, bh, row)  or lse per (bh,row)
-  size_t off_parts;    // float colsum partials [nparts][BH][Nk]
+  size_t off_parts;    // float colsum partials [nparts][BH][Nk]; decode: 1 KiB store sink
   size_t off_opart;    // float O partials [nsplit][BH][R][d] (nsplit > 1)
   size_t off_logits;   // decode: float logits [BH][G][Nk]
   size_t bytes;

@@ -2,8 +2,8 @@
 """Benchmark of the H2O chunk step on one MI355X.
 
 Default workload: token generation, B=8, Hq=32, Hkv=8, d=64, M=4096, T=1,
-bf16. One bench step is one token step (h2o_sdpa_chunk + h2o_accumulate_scores
-+ h2o_evict_insert) for each of 8 independent layer states, so the 8 x 69 MB
+bf16. One bench step is one token step (h2o_chunk_step: attention, score
+accumulation, eviction and insert) for each of 8 independent layer states, so the 8 x 69 MB
 working set exceeds the 256 MB Infinity Cache and the step streams from HBM.
 The steps are captured in one HIP graph and replayed; ``value`` is algorithmic
 bytes per second (GB/s) over the timed steps.
@@ -125,8 +125,7 @@ def bench_decode(args, torch, H, W):
     for _ in range(args.steps):
         step()
     torch.cuda.synchronize()
-    ktimes = {k: H.h2o_debug_kernel_time(k) for k in
-              ("decode_split", "decode_combine", "accumulate", "argmin_insert")}
+    ktimes = {k: H.h2o_debug_kernel_time(k) for k in ("decode_split", "decode_finish")}
     H.h2o_debug_timing(False)
     step_bytes = decode_step_bytes(w) * LAYERS
     gbs = step_bytes / (ms_step * 1e-3) / 1e9

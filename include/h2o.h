@@ -120,6 +120,23 @@ int h2o_evict_insert(void* k_cache, void* v_cache, float* scores,
                      int M, int T, int d, int k, int32_t pos0, int dtype,
                      void* stream);
 
+/* The three calls above in one: h2o_sdpa_chunk, then h2o_accumulate_scores,
+ * then h2o_evict_insert with k = T (the step of Sec. "Fine-Tuning for Sparse
+ * Attention": attend over cache and chunk, add the summed weights to the H2O
+ * scores of Eq. h2o-score, overwrite the T lowest-scored slots with the
+ * chunk). Arguments and results are those of the three calls (same bits);
+ * every buffer they read or write is an argument here, the workspace is the
+ * one h2o_workspace_bytes() sizes, and M >= T. For T == 1 in bf16 the step
+ * is two kernel launches: the split attention kernel, then one block per KV
+ * head that merges the splits, accumulates the scores, picks the slot and
+ * inserts; other shapes run the kernels of the three calls in order. */
+int h2o_chunk_step(const void* q, void* k_cache, void* v_cache, float* scores,
+                   int32_t* token_pos, const void* k_new, const void* v_new,
+                   void* out, float* lse, float* wsum, int32_t* evict_idx,
+                   void* workspace, size_t workspace_bytes, int B, int Hq,
+                   int Hkv, int T, int M, int d, float scale, int32_t pos0,
+                   int dtype, void* stream);
+
 /* The selection of h2o_evict_insert alone: for each of `rows` rows of M
  * float32 scores, the k smallest by (score, index), ascending indices, into
  * idx_out [rows, k]. 0 <= k <= M. */
@@ -147,7 +164,8 @@ int h2o_debug_force_path(int path);
  *   0 generic lse pass   1 generic main pass   2 MFMA lse pass
  *   3 MFMA main pass     4 split reduce        5 column-sum reduce
  *   6 accumulate         7 bottom-k            8 insert
- *   9 decode split      10 decode combine     11 argmin + insert (k == 1) */
+ *   9 decode split      10 decode combine     11 argmin + insert (k == 1)
+ *  12 decode finish (h2o_chunk_step, T == 1) */
 int h2o_debug_timing(int on);
 int h2o_debug_kernel_time(int kernel_id, double* total_ms, long* count);
 

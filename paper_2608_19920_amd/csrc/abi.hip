@@ -177,6 +177,52 @@ Plan make_plan(const Shape& s, int dtype) {
   return p;
 }
 
+namespace {
+
+// Validation shared by the entry points that run the attention; fills *plan.
+int check_sdpa(const void* q, const void* k_cache, const void* v_cache, const void* k_new,
+               const void* v_new, const void* out, const float* lse, const float* wsum,
+               const void* workspace, size_t workspace_bytes, int B, int Hq, int Hkv, int T,
+               int M, int d, float scale, int dtype, Plan* plan) {
+  if (dtype != H2O_F32 && dtype != H2O_BF16) return fail(H2O_EDTYPE, "dtype %d unknown", dtype);
+  int rc = check_shape(B, Hq, Hkv, T, M, d);
+  if (rc) return rc;
+  if (!q || !k_new || !v_new || !out || !lse || !wsum || (M > 0 && (!k_cache || !v_cache)))
+    return fail(H2O_EINVAL, "null tensor pointer");
+  if (!(std::isfinite(scale) && scale > 0.f)) return fail(H2O_EINVAL, "scale must be finite > 0");
+  const void* ptrs[] = {q, k_new, v_new, out, lse, wsum, workspace};
+  for (const void* p : ptrs)
+    if (p && !aligned16(p)) return fail(H2O_EALIGN, "tensor pointer not 16-byte aligned");
+  if (M > 0 && (!aligned16(k_cache) || !aligned16(v_cache)))
+    return fail(H2O_EALIGN, "cache pointer not 16-byte aligned");
+  const Shape s{B, Hq, Hkv, T, M, d};
+  *plan = make_plan(s, dtype);
+  if (workspace_bytes < plan->bytes || (plan->bytes > 0 && !workspace))
+    return fail(H2O_EWORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes,
+                plan->bytes);
+  return H2O_OK;
+}
+
+hipError_t launch_sdpa(const Shape& s, const Plan& p, int dtype, const void* q,
+                       const void* k_cache, const void* v_cache, const void* k_new,
+                       const void* v_new, void* out, float* lse, float* wsum, void* workspace,
+                       float scale, hipStream_t st) {
+  char* ws = reinterpret_cast<char*>(workspace);
+  switch (p.path) {
+    case 1:
+      return launch_sdpa_mfma(s, p, q, k_cache, v_cache, k_new, v_new, out, lse, wsum, ws,
+                              scale, st);
+    case 2:
+      return launch_sdpa_decode(s, p, q, k_cache, v_cache, k_new, v_new, out, lse, wsum, ws,
+                                scale, st);
+    default:
+      return launch_sdpa_generic(s, p, dtype, q, k_cache, v_cache, k_new, v_new, out, lse,
+                                 wsum, ws, scale, st);
+  }
+}
+
+}  // namespace
+
 }  // namespace h2o
 
 using namespace h2o;
@@ -227,38 +273,54 @@ int h2o_sdpa_chunk(const void* q, const void* k_cache, const void* v_cache, cons
                    const void* v_new, void* out, float* lse, float* wsum, void* workspace,
                    size_t workspace_bytes, int B, int Hq, int Hkv, int T, int M, int d,
                    float scale, int dtype, void* stream) {
-  if (dtype != H2O_F32 && dtype != H2O_BF16) return fail(H2O_EDTYPE, "dtype %d unknown", dtype);
-  int rc = check_shape(B, Hq, Hkv, T, M, d);
+  Plan p;
+  int rc = check_sdpa(q, k_cache, v_cache, k_new, v_new, out, lse, wsum, workspace,
+                      workspace_bytes, B, Hq, Hkv, T, M, d, scale, dtype, &p);
+  if (!rc) rc = check_device();
   if (rc) return rc;
-  if (!q || !k_new || !v_new || !out || !lse || !wsum || (M > 0 && (!k_cache || !v_cache)))
-    return fail(H2O_EINVAL, "null tensor pointer");
-  if (!(std::isfinite(scale) && scale > 0.f)) return fail(H2O_EINVAL, "scale must be finite > 0");
-  const void* ptrs[] = {q, k_new, v_new, out, lse, wsum, workspace};
-  for (const void* p : ptrs)
-    if (p && !aligned16(p)) return fail(H2O_EALIGN, "tensor pointer not 16-byte aligned");
-  if (M > 0 && (!aligned16(k_cache) || !aligned16(v_cache)))
-    return fail(H2O_EALIGN, "cache pointer not 16-byte aligned");
-  Shape s{B, Hq, Hkv, T, M, d};
-  Plan p = make_plan(s, dtype);
-  if (workspace_bytes < p.bytes || (p.bytes > 0 && !workspace))
-    return fail(H2O_EWORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, p.bytes);
+  const Shape s{B, Hq, Hkv, T, M, d};
+  hipError_t e = launch_sdpa(s, p, dtype, q, k_cache, v_cache, k_new, v_new, out, lse, wsum,
+                             workspace, scale, reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(H2O_ELAUNCH, "kernel launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int h2o_chunk_step(const void* q, void* k_cache, void* v_cache, float* scores,
+                   int32_t* token_pos, const void* k_new, const void* v_new, void* out,
+                   float* lse, float* wsum, int32_t* evict_idx, void* workspace,
+                   size_t workspace_bytes, int B, int Hq, int Hkv, int T, int M, int d,
+                   float scale, int32_t pos0, int dtype, void* stream) {
+  Plan p;
+  int rc = check_sdpa(q, k_cache, v_cache, k_new, v_new, out, lse, wsum, workspace,
+                      workspace_bytes, B, Hq, Hkv, T, M, d, scale, dtype, &p);
+  if (rc) return rc;
+  if (M < T) return fail(H2O_EINVAL, "cache length M (%d) must be >= T (%d)", M, T);
+  if (!scores || !evict_idx) return fail(H2O_EINVAL, "null tensor pointer");
+  if (!aligned16(scores) || !aligned16(evict_idx) || (token_pos && !aligned16(token_pos)))
+    return fail(H2O_EALIGN, "tensor pointer not 16-byte aligned");
   rc = check_device();
   if (rc) return rc;
+  const Shape s{B, Hq, Hkv, T, M, d};
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   char* ws = reinterpret_cast<char*>(workspace);
   hipError_t e;
-  switch (p.path) {
-    case 1:
-      e = launch_sdpa_mfma(s, p, q, k_cache, v_cache, k_new, v_new, out, lse, wsum, ws, scale,
-                           st);
-      break;
-    case 2:
-      e = launch_sdpa_decode(s, p, q, k_cache, v_cache, k_new, v_new, out, lse, wsum, ws,
-                             scale, st);
-      break;
-    default:
-      e = launch_sdpa_generic(s, p, dtype, q, k_cache, v_cache, k_new, v_new, out, lse, wsum,
-                              ws, scale, st);
+  if (p.path == 2) {
+    e = launch_decode_step(s, p, q, k_cache, v_cache, k_new, v_new, out, lse, wsum, scores,
+                           token_pos, evict_idx, pos0, ws, scale, st);
+  } else {
+    const int rows = B * Hkv, eb = dtype == H2O_F32 ? 4 : 2;
+    e = launch_sdpa(s, p, dtype, q, k_cache, v_cache, k_new, v_new, out, lse, wsum, workspace,
+                    scale, st);
+    if (e == hipSuccess) e = launch_accumulate(scores, wsum, rows, M, T, st);
+    if (e == hipSuccess && T == 1) {
+      e = launch_argmin_insert(k_cache, v_cache, scores, token_pos, k_new, v_new, wsum,
+                               evict_idx, rows, M, T, d, pos0, eb, st);
+    } else if (e == hipSuccess) {
+      e = launch_bottomk(scores, rows, M, T, evict_idx, st);
+      if (e == hipSuccess)
+        e = launch_insert(k_cache, v_cache, scores, token_pos, k_new, v_new, wsum, evict_idx,
+                          rows, M, T, d, T, pos0, eb, st);
+    }
   }
   if (e != hipSuccess) return fail(H2O_ELAUNCH, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();

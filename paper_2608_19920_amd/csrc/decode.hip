@@ -243,10 +243,99 @@ __global__ __launch_bounds__(kThreads) void decode_split(
   }
 }
 
-// Block (x, bh): merges the splits of head bh (every block recomputes the
-// few per-head statistics from the split partials staged in LDS), then
-// writes wsum for columns [x*kCols, +kCols); block x == 0 also writes out
-// and lse.
+// ------------------------------------------------------------------ combine
+// Per-head merge of the split partials with the chunk's own key (column M),
+// shared by the combine kernel and the fused finish kernel so that both give
+// the same bits.
+constexpr int kMaxG = kMaxGD / 64;
+struct HeadStats {
+  float lnew[kMaxG], lam[kMaxG], mfin[kMaxG], linv[kMaxG];
+  float wt[kMaxSplit * kMaxG];   // weight of split s, head g: exp2(m_sg - mfin_g) or 0
+};
+
+// One wave per query head g: the chunk key's logit (log2 units), the common
+// maximum mfin over it and the splits' maxima, lam = log2 of the softmax
+// normaliser, 1 / normaliser and each split's weight, with wave reductions
+// (lane s holds split s; at most 64 splits). Writes lse when asked. Ends
+// synced.
+template <int D, int NT>
+__device__ __forceinline__ void head_stats(HeadStats& hs, const bf16_t* q, const bf16_t* kn,
+                                           const float2* dstat, int Hq, int Hkv, int G,
+                                           int nsplit, float c_log2, size_t bh, float* lse) {
+  const int b = (int)(bh / Hkv), h = (int)(bh % Hkv);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  for (int g = wave; g < G; g += NT / 64) {
+    const float2 st = lane < nsplit ? dstat[(bh * nsplit + lane) * G + g]
+                                    : make_float2(-INFINITY, 0.f);
+    float a = 0.f;
+    for (int dd = lane; dd < D; dd += 64)
+      a = fmaf(bf16_to_f32(q[(size_t)(b * Hq + h * G + g) * D + dd]),
+               bf16_to_f32(kn[bh * D + dd]), a);
+    for (int o = 32; o > 0; o >>= 1) a += __shfl_xor(a, o, 64);
+    const float lnew = a * c_log2;
+    float mx = fmaxf(lnew, st.x);
+    for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+    const float wt = st.y > 0.f ? __builtin_amdgcn_exp2f(st.x - mx) : 0.f;
+    float L = st.y * wt;
+    for (int o = 32; o > 0; o >>= 1) L += __shfl_xor(L, o, 64);
+    L += __builtin_amdgcn_exp2f(lnew - mx);
+    if (lane < nsplit) hs.wt[lane * G + g] = wt;
+    if (lane == 0) {
+      const float lm = mx + __log2f(L);
+      hs.lnew[g] = lnew;
+      hs.lam[g] = lm;
+      hs.mfin[g] = mx;
+      hs.linv[g] = 1.f / L;
+      if (lse) lse[(size_t)(b * Hq + h * G + g)] = lm * kLn2;
+    }
+  }
+  __syncthreads();
+}
+
+// Output element c = g*D + dd of head bh: the chunk key's term plus the
+// weighted split O-partials in split order, normalised. The first PRE
+// partials come from pre[] (registers), the rest from dO.
+template <int D, int PRE>
+__device__ __forceinline__ float out_elem(const HeadStats& hs, const bf16_t* vn,
+                                          const float* dO, const float* pre, int G,
+                                          int nsplit, size_t bh, int c) {
+  const int g = c / D, dd = c % D;
+  float a = __builtin_amdgcn_exp2f(hs.lnew[g] - hs.mfin[g]) * bf16_to_f32(vn[bh * D + dd]);
+#pragma unroll
+  for (int s = 0; s < PRE; ++s)
+    if (s < nsplit) a = fmaf(pre[s], hs.wt[s * G + g], a);
+  for (int s = PRE; s < nsplit; ++s)
+    a = fmaf(dO[(bh * nsplit + s) * (size_t)(G * D) + c], hs.wt[s * G + g], a);
+  return a * hs.linv[g];
+}
+
+// out rows of the G query heads of head bh from the split O-partials.
+template <int D, int NT>
+__device__ __forceinline__ void head_out(const HeadStats& hs, const bf16_t* vn, const float* dO,
+                                         bf16_t* out, int Hq, int Hkv, int G, int nsplit,
+                                         size_t bh) {
+  const int b = (int)(bh / Hkv), h = (int)(bh % Hkv);
+  for (int c = threadIdx.x; c < G * D; c += NT) {
+    const float v = out_elem<D, 0>(hs, vn, dO, nullptr, G, nsplit, bh, c);
+    out[(size_t)(b * Hq + h * G) * D + c] = f32_to_bf16(v);
+  }
+}
+
+// Summed weight of cache slot j: sum_g exp2(logit_gj - lam_g), g in order.
+__device__ __forceinline__ float slot_weight(const HeadStats& hs, const float* lgb, int pitch,
+                                             int G, int j) {
+  float a = 0.f;
+  for (int g = 0; g < G; ++g) a += __builtin_amdgcn_exp2f(lgb[(size_t)g * pitch + j] - hs.lam[g]);
+  return a;
+}
+__device__ __forceinline__ float chunk_weight(const HeadStats& hs, int G) {
+  float a = 0.f;
+  for (int g = 0; g < G; ++g) a += __builtin_amdgcn_exp2f(hs.lnew[g] - hs.lam[g]);
+  return a;
+}
+
+// Block (x, bh) writes wsum for columns [x*kCols, +kCols) of head bh; block
+// x == 0 also writes out, lse and the chunk key's column.
 constexpr int kCols = 1024;
 
 template <int D>
@@ -255,66 +344,125 @@ __global__ __launch_bounds__(kThreads) void decode_combine(
     int Hq, int Hkv, int M, int nsplit, float c_log2, const float* __restrict__ logits,
     const float2* __restrict__ dstat, const float* __restrict__ dO, bf16_t* __restrict__ out,
     float* __restrict__ lse, float* __restrict__ wsum) {
-  constexpr int kMaxG = kMaxGD / 64;
-  __shared__ float lnew[kMaxG], lam[kMaxG], mfin[kMaxG], linv[kMaxG];
-  __shared__ float2 st_s[kMaxSplit * kMaxG];
+  __shared__ HeadStats hs;
   const int G = Hq / Hkv;
   const size_t bh = blockIdx.y;
-  const int b = (int)(bh / Hkv), h = (int)(bh % Hkv);
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  for (int i = tid; i < nsplit * G; i += kThreads) st_s[i] = dstat[bh * nsplit * G + i];
-  // logit of the chunk's own key for each query head (one wave per head)
-  for (int g = wave; g < G; g += kThreads / 64) {
-    float a = 0.f;
-    for (int dd = lane; dd < D; dd += 64)
-      a = fmaf(bf16_to_f32(q[(size_t)(b * Hq + h * G + g) * D + dd]),
-               bf16_to_f32(kn[bh * D + dd]), a);
-    for (int o = 32; o > 0; o >>= 1) a += __shfl_xor(a, o, 64);
-    if (lane == 0) lnew[g] = a * c_log2;
-  }
-  __syncthreads();
-  if (tid < G) {
-    const int g = tid;
-    float mx = lnew[g];
-    for (int s = 0; s < nsplit; ++s) mx = fmaxf(mx, st_s[s * G + g].x);
-    float L = __builtin_amdgcn_exp2f(lnew[g] - mx);
-    for (int s = 0; s < nsplit; ++s) {
-      const float2 st = st_s[s * G + g];
-      if (st.y > 0.f) L += st.y * __builtin_amdgcn_exp2f(st.x - mx);
-    }
-    const float lm = mx + __log2f(L);
-    lam[g] = lm;
-    mfin[g] = mx;
-    linv[g] = 1.f / L;
-    if (blockIdx.x == 0) lse[(size_t)(b * Hq + h * G + g)] = lm * kLn2;
-  }
-  __syncthreads();
-  if (blockIdx.x == 0) {
-    for (int c = tid; c < G * D; c += kThreads) {
-      const int g = c / D, dd = c % D;
-      float a = __builtin_amdgcn_exp2f(lnew[g] - mfin[g]) * bf16_to_f32(vn[bh * D + dd]);
-#pragma unroll 8
-      for (int s = 0; s < nsplit; ++s) {
-        const float2 st = st_s[s * G + g];
-        const float w = st.y > 0.f ? __builtin_amdgcn_exp2f(st.x - mfin[g]) : 0.f;
-        a = fmaf(dO[(bh * nsplit + s) * (size_t)(G * D) + c], w, a);
-      }
-      out[(size_t)(b * Hq + h * G + g) * D + dd] = f32_to_bf16(a * linv[g]);
-    }
-  }
+  head_stats<D, kThreads>(hs, q, kn, dstat, Hq, Hkv, G, nsplit, c_log2, bh,
+                          blockIdx.x == 0 ? lse : nullptr);
+  if (blockIdx.x == 0) head_out<D, kThreads>(hs, vn, dO, out, Hq, Hkv, G, nsplit, bh);
   float* w = wsum + bh * (size_t)(M + 1);
   const float* lgb = logits + bh * (size_t)G * logit_pitch(M);
   const int c0 = blockIdx.x * kCols, c1 = min(M, c0 + kCols);
-  for (int j = c0 + tid; j < c1; j += kThreads) {
-    float a = 0.f;
-    for (int g = 0; g < G; ++g)
-      a += __builtin_amdgcn_exp2f(lgb[(size_t)g * logit_pitch(M) + j] - lam[g]);
-    w[j] = a;
+  for (int j = c0 + threadIdx.x; j < c1; j += kThreads)
+    w[j] = slot_weight(hs, lgb, logit_pitch(M), G, j);
+  if (blockIdx.x == 0 && threadIdx.x == 0) w[M] = chunk_weight(hs, G);
+}
+
+// Fused end of a token step, one block per head: the combine above, then
+// scores[j] += wsum[j] for every cache slot, the (score, slot)-smallest slot
+// (lower slot first among equal scores; -0 equals +0), and the insert of the
+// chunk's key, value, score wsum[M] and token position into that slot. Same
+// arithmetic as the combine, accumulate and argmin-insert kernels. The block
+// is latency-bound, so everything it reads (a pass of logits and scores, the
+// split statistics and O-partials, the chunk's key and value rows) is
+// requested before the first value is needed.
+constexpr int kFinThreads = 1024;
+constexpr int kFinCols = 8;   // slots per thread and pass
+
+template <int D, int G>
+__global__ __launch_bounds__(kFinThreads) void decode_finish(
+    const bf16_t* __restrict__ q, bf16_t* __restrict__ kc, bf16_t* __restrict__ vc,
+    const bf16_t* __restrict__ kn, const bf16_t* __restrict__ vn, int Hq, int Hkv, int M,
+    int nsplit, float c_log2, const float* __restrict__ logits, const float2* __restrict__ dstat,
+    const float* __restrict__ dO, bf16_t* __restrict__ out, float* __restrict__ lse,
+    float* __restrict__ wsum, float* __restrict__ scores, int32_t* __restrict__ token_pos,
+    int32_t* __restrict__ evict_idx, int32_t pos0) {
+  constexpr int NT = kFinThreads, PASS = NT * kFinCols;
+  __shared__ HeadStats hs;
+  __shared__ uint32_t red_k[NT / 64], red_j[NT / 64];
+  __shared__ int sh_slot;
+  const size_t bh = blockIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int pitch = logit_pitch(M);
+  float* w = wsum + bh * (size_t)(M + 1);
+  float* sc = scores + bh * (size_t)M;
+  const float* lgb = logits + bh * (size_t)G * pitch;
+  float lg[kFinCols][G], sv[kFinCols];
+  auto load_pass = [&](int base) {   // M >= 1: clamped slots are in bounds
+#pragma unroll
+    for (int u = 0; u < kFinCols; ++u) {
+      const int j = min(base + u * NT + tid, M - 1);
+#pragma unroll
+      for (int g = 0; g < G; ++g) lg[u][g] = lgb[(size_t)g * pitch + j];
+      sv[u] = sc[j];
+    }
+  };
+  typedef uint32_t u4 __attribute__((ext_vector_type(4)));
+  u4 krow = {0u, 0u, 0u, 0u}, vrow = {0u, 0u, 0u, 0u};
+  if (tid < D / 8) {
+    krow = reinterpret_cast<const u4*>(kn + bh * (size_t)D)[tid];
+    vrow = reinterpret_cast<const u4*>(vn + bh * (size_t)D)[tid];
   }
-  if (blockIdx.x == 0 && tid == 0) {
-    float a = 0.f;
-    for (int g = 0; g < G; ++g) a += __builtin_amdgcn_exp2f(lnew[g] - lam[g]);
-    w[M] = a;
+  // thread c < G*D owns output element c (G*D <= NT); its first kPre split
+  // partials come in with the other early loads
+  constexpr int kPre = 16;
+  float pre[kPre];
+  const bool has_c = tid < G * D;
+#pragma unroll
+  for (int s = 0; s < kPre; ++s)
+    pre[s] = has_c && s < nsplit ? dO[(bh * nsplit + s) * (size_t)(G * D) + tid] : 0.f;
+  load_pass(0);
+  head_stats<D, NT>(hs, q, kn, dstat, Hq, Hkv, G, nsplit, c_log2, bh, lse);
+  if (has_c) {
+    const float v = out_elem<D, kPre>(hs, vn, dO, pre, G, nsplit, bh, tid);
+    const int b = (int)(bh / Hkv), h = (int)(bh % Hkv);
+    out[(size_t)(b * Hq + h * G) * D + tid] = f32_to_bf16(v);
+  }
+  // slots visited in increasing order per thread: a strict < keeps the lowest
+  // slot among equal keys
+  uint32_t bk = 0xFFFFFFFFu, bj = 0xFFFFFFFFu;
+  for (int base = 0; base < M; base += PASS) {
+    if (base > 0) load_pass(base);
+#pragma unroll
+    for (int u = 0; u < kFinCols; ++u) {
+      const int j = base + u * NT + tid;
+      float wj = 0.f;
+#pragma unroll
+      for (int g = 0; g < G; ++g) wj += __builtin_amdgcn_exp2f(lg[u][g] - hs.lam[g]);
+      if (j < M) {
+        w[j] = wj;
+        const float s = sv[u] + wj;
+        sc[j] = s;
+        const uint32_t key = order_key(s);
+        if (key < bk) { bk = key; bj = (uint32_t)j; }
+      }
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const uint32_t ok = __shfl_xor(bk, o, 64), oj = __shfl_xor(bj, o, 64);
+    if (ok < bk || (ok == bk && oj < bj)) { bk = ok; bj = oj; }
+  }
+  if (lane == 0) { red_k[wave] = bk; red_j[wave] = bj; }
+  __syncthreads();
+  if (tid == 0) {
+    for (int v = 1; v < NT / 64; ++v)
+      if (red_k[v] < bk || (red_k[v] == bk && red_j[v] < bj)) { bk = red_k[v]; bj = red_j[v]; }
+    const int slot = (int)bj;
+    const float wnew = chunk_weight(hs, G);
+    w[M] = wnew;
+    sh_slot = slot;
+    evict_idx[bh] = slot;
+    if ((unsigned)slot < (unsigned)M) {
+      sc[slot] = wnew;
+      if (token_pos) token_pos[bh * M + slot] = pos0;
+    }
+  }
+  __syncthreads();
+  const int slot = sh_slot;
+  if ((unsigned)slot < (unsigned)M && tid < D / 8) {
+    reinterpret_cast<u4*>(kc + (bh * M + slot) * (size_t)D)[tid] = krow;
+    reinterpret_cast<u4*>(vc + (bh * M + slot) * (size_t)D)[tid] = vrow;
   }
 }
 
@@ -364,42 +512,80 @@ bool decode_supports(int d, int G) {
          (d == 128 && (G == 1 || G == 2 || G == 4));
 }
 
-hipError_t launch_sdpa_decode(const Shape& s, const Plan& p, const void* q, const void* kc,
-                              const void* vc, const void* kn, const void* vn, void* out,
-                              float* lse, float* wsum, char* ws, float scale, hipStream_t st) {
-  const float c = scale * kLog2e;
+namespace {
+
+// The split kernel over the cache (if any); returns the split count in *ns.
+hipError_t launch_decode_split(const Shape& s, const Plan& p, const void* q, const void* kc,
+                               const void* vc, char* ws, float c, hipStream_t st, int* ns) {
   float* logits = reinterpret_cast<float*>(ws + p.off_logits);
   float2* dstat = reinterpret_cast<float2*>(ws + p.off_stats);
   float* dO = reinterpret_cast<float*>(ws + p.off_opart);
   float* sink = reinterpret_cast<float*>(ws + p.off_parts);
-  int ns = 0;
-  if (s.M > 0) {
-    const int G = s.G();
-    hipError_t e = hipErrorInvalidValue;
+  *ns = 0;
+  if (s.M == 0) return hipSuccess;
+  const int G = s.G();
+  hipError_t e = hipErrorInvalidValue;
 #define H2O_SPLIT(DD, GG) \
-  e = launch_split<DD, GG>(st, s.BH(), q, kc, vc, s.Hq, s.Hkv, s.M, c, logits, dstat, dO, sink, \
-                           &ns)
-    if (s.d == 64) {
-      if (G == 1) H2O_SPLIT(64, 1);
-      else if (G == 2) H2O_SPLIT(64, 2);
-      else if (G == 4) H2O_SPLIT(64, 4);
-      else if (G == 8) H2O_SPLIT(64, 8);
-      else return hipErrorInvalidValue;
-    } else {
-      if (G == 1) H2O_SPLIT(128, 1);
-      else if (G == 2) H2O_SPLIT(128, 2);
-      else if (G == 4) H2O_SPLIT(128, 4);
-      else return hipErrorInvalidValue;
-    }
-#undef H2O_SPLIT
-    if (e != hipSuccess) return e;
+  e = launch_split<DD, GG>(st, s.BH(), q, kc, vc, s.Hq, s.Hkv, s.M, c, logits, dstat, dO, sink, ns)
+  if (s.d == 64) {
+    if (G == 1) H2O_SPLIT(64, 1);
+    else if (G == 2) H2O_SPLIT(64, 2);
+    else if (G == 4) H2O_SPLIT(64, 4);
+    else if (G == 8) H2O_SPLIT(64, 8);
+  } else {
+    if (G == 1) H2O_SPLIT(128, 1);
+    else if (G == 2) H2O_SPLIT(128, 2);
+    else if (G == 4) H2O_SPLIT(128, 4);
   }
+#undef H2O_SPLIT
+  return e;
+}
+
+}  // namespace
+
+hipError_t launch_sdpa_decode(const Shape& s, const Plan& p, const void* q, const void* kc,
+                              const void* vc, const void* kn, const void* vn, void* out,
+                              float* lse, float* wsum, char* ws, float scale, hipStream_t st) {
+  const float c = scale * kLog2e;
+  int ns = 0;
+  hipError_t e = launch_decode_split(s, p, q, kc, vc, ws, c, st, &ns);
+  if (e != hipSuccess) return e;
   const dim3 cgrid(s.M > 0 ? (s.M + kCols - 1) / kCols : 1, s.BH());
   auto combine = s.d == 64 ? decode_combine<64> : decode_combine<128>;
   return launch_kernel(K_DECODE_COMBINE, combine, cgrid, dim3(kThreads), st, (const bf16_t*)q,
                        (const bf16_t*)kn, (const bf16_t*)vn, s.Hq, s.Hkv, s.M, ns, c,
-                       (const float*)logits, (const float2*)dstat, (const float*)dO,
-                       (bf16_t*)out, lse, wsum);
+                       (const float*)(ws + p.off_logits), (const float2*)(ws + p.off_stats),
+                       (const float*)(ws + p.off_opart), (bf16_t*)out, lse, wsum);
+}
+
+hipError_t launch_decode_step(const Shape& s, const Plan& p, const void* q, void* kc, void* vc,
+                              const void* kn, const void* vn, void* out, float* lse,
+                              float* wsum, float* scores, int32_t* token_pos, int32_t* evict_idx,
+                              int32_t pos0, char* ws, float scale, hipStream_t st) {
+  const float c = scale * kLog2e;
+  int ns = 0;
+  hipError_t e = launch_decode_split(s, p, q, kc, vc, ws, c, st, &ns);
+  if (e != hipSuccess) return e;
+  const int G = s.G();
+  auto go = [&](auto kern) {
+    return launch_kernel(K_DECODE_FINISH, kern, dim3(s.BH()), dim3(kFinThreads), st,
+                         (const bf16_t*)q, (bf16_t*)kc, (bf16_t*)vc, (const bf16_t*)kn,
+                         (const bf16_t*)vn, s.Hq, s.Hkv, s.M, ns, c,
+                         (const float*)(ws + p.off_logits), (const float2*)(ws + p.off_stats),
+                         (const float*)(ws + p.off_opart), (bf16_t*)out, lse, wsum, scores,
+                         token_pos, evict_idx, pos0);
+  };
+  if (s.d == 64) {
+    if (G == 1) return go(decode_finish<64, 1>);
+    if (G == 2) return go(decode_finish<64, 2>);
+    if (G == 4) return go(decode_finish<64, 4>);
+    if (G == 8) return go(decode_finish<64, 8>);
+  } else {
+    if (G == 1) return go(decode_finish<128, 1>);
+    if (G == 2) return go(decode_finish<128, 2>);
+    if (G == 4) return go(decode_finish<128, 4>);
+  }
+  return hipErrorInvalidValue;
 }
 
 }  // namespace h2o

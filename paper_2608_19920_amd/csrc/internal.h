@@ -25,6 +25,14 @@ __device__ __forceinline__ float load_elem(const bf16_t* p, size_t i) { return b
 __device__ __forceinline__ void store_elem(float* p, size_t i, float v) { p[i] = v; }
 __device__ __forceinline__ void store_elem(bf16_t* p, size_t i, float v) { p[i] = f32_to_bf16(v); }
 
+// Order-preserving map of a float32 score to uint32 (a < b  <=>  key(a) <
+// key(b)); both zeros map to the same key.
+__device__ __forceinline__ uint32_t order_key(float x) {
+  uint32_t u = __float_as_uint(x);
+  if ((u << 1) == 0u) u = 0u;
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
 // log2(e) and ln(2) in float32.
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
@@ -74,7 +82,8 @@ bool decode_supports(int d, int G);   // (d, G) pairs the decode kernels handle
 // Identifiers of every kernel the library launches (for the timing hook).
 enum KernelId {
   K_GENERIC_LSE = 0, K_GENERIC_MAIN, K_MFMA_LSE, K_MFMA_MAIN, K_SPLIT_REDUCE, K_COLSUM_REDUCE,
-  K_ACCUMULATE, K_BOTTOMK, K_INSERT, K_DECODE_SPLIT, K_DECODE_COMBINE, K_ARGMIN_INSERT, K_COUNT
+  K_ACCUMULATE, K_BOTTOMK, K_INSERT, K_DECODE_SPLIT, K_DECODE_COMBINE, K_ARGMIN_INSERT,
+  K_DECODE_FINISH, K_COUNT
 };
 // While timing is switched on (h2o_debug_timing), kernels go out through
 // hipExtLaunchKernel with a start and a stop event: the runtime stamps them
@@ -111,6 +120,12 @@ hipError_t launch_sdpa_decode(const Shape& s, const Plan& p, const void* q, cons
                               const void* vc, const void* kn, const void* vn, void* out,
                               float* lse, float* wsum, char* ws, float scale,
                               hipStream_t st);
+// T == 1, one call for the whole step: split kernel, then one block per head
+// merges the splits, accumulates the scores, picks the slot and inserts.
+hipError_t launch_decode_step(const Shape& s, const Plan& p, const void* q, void* kc, void* vc,
+                              const void* kn, const void* vn, void* out, float* lse,
+                              float* wsum, float* scores, int32_t* token_pos, int32_t* evict_idx,
+                              int32_t pos0, char* ws, float scale, hipStream_t st);
 hipError_t launch_colsum_reduce(const Shape& s, const Plan& p, const float* parts,
                                 float* wsum, hipStream_t st);
 hipError_t launch_accumulate(float* scores, const float* wsum, int rows, int M, int T,

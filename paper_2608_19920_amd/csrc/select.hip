@@ -35,13 +35,6 @@ __global__ __launch_bounds__(256) void accumulate_kernel(float* __restrict__ sco
 }
 
 // ------------------------------------------------------------------ bottom-k
-// Order-preserving map of a float32 score to uint32 (a < b  <=>  key(a) <
-// key(b)); both zeros map to the same key.
-__device__ __forceinline__ uint32_t order_key(float x) {
-  uint32_t u = __float_as_uint(x);
-  if ((u << 1) == 0u) u = 0u;
-  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
 
 constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / 64;

@@ -23,12 +23,12 @@ H2O_F32, H2O_BF16 = 0, 1
 STATUS_NAMES = ["H2O_OK", "H2O_EINVAL", "H2O_ESHAPE", "H2O_EDTYPE", "H2O_EALIGN",
                 "H2O_EWORKSPACE", "H2O_ENODEVICE", "H2O_ELAUNCH"]
 EXPORTED = ["h2o_workspace_bytes", "h2o_sdpa_chunk", "h2o_accumulate_scores",
-            "h2o_evict_insert", "h2o_bottomk", "h2o_last_error", "h2o_debug_force_path",
+            "h2o_evict_insert", "h2o_chunk_step", "h2o_bottomk", "h2o_last_error", "h2o_debug_force_path",
             "h2o_debug_timing", "h2o_debug_kernel_time", "h2o_version"]
 KERNEL_IDS = {"generic_lse": 0, "generic_main": 1, "mfma_lse": 2, "mfma_main": 3,
               "split_reduce": 4, "colsum_reduce": 5, "accumulate": 6, "bottomk": 7,
               "insert": 8, "decode_split": 9, "decode_combine": 10,
-              "argmin_insert": 11}
+              "argmin_insert": 11, "decode_finish": 12}
 
 
 class H2OError(RuntimeError):
@@ -59,6 +59,8 @@ def lib() -> ctypes.CDLL:
     L.h2o_accumulate_scores.restype = i
     L.h2o_evict_insert.argtypes = [vp] * 8 + [i] * 6 + [ctypes.c_int32, i, vp]
     L.h2o_evict_insert.restype = i
+    L.h2o_chunk_step.argtypes = [vp] * 12 + [sz] + [i] * 6 + [f, ctypes.c_int32, i, vp]
+    L.h2o_chunk_step.restype = i
     L.h2o_bottomk.argtypes = [vp, i, i, i, vp, vp]
     L.h2o_bottomk.restype = i
     L.h2o_last_error.argtypes = []
@@ -203,6 +205,44 @@ def h2o_evict_insert(k_cache, v_cache, scores, token_pos, k_new, v_new, wsum, ev
         _stream(stream)))
 
 
+def h2o_chunk_step(q, k_cache, v_cache, scores, token_pos, k_new, v_new, out, lse, wsum,
+                   evict_idx, workspace, pos0: int, scale: Optional[float] = None,
+                   stream=None) -> None:
+    """h2o_sdpa_chunk + h2o_accumulate_scores + h2o_evict_insert (k = T) in one
+    call; shapes as there."""
+    B, Hq, T, d = q.shape
+    Hkv, M = k_cache.shape[1], k_cache.shape[2]
+    dt = _dtype_code(q)
+    for name, t in (("k_cache", k_cache), ("v_cache", v_cache), ("k_new", k_new),
+                    ("v_new", v_new), ("out", out)):
+        if t.dtype != q.dtype:
+            raise TypeError(f"{name} dtype {t.dtype} != q dtype {q.dtype}")
+    if tuple(k_cache.shape) != (B, Hkv, M, d) or tuple(v_cache.shape) != (B, Hkv, M, d) or \
+            tuple(k_new.shape) != (B, Hkv, T, d) or tuple(v_new.shape) != (B, Hkv, T, d) or \
+            tuple(out.shape) != (B, Hq, T, d):
+        raise ValueError("shape mismatch")
+    if tuple(lse.shape) != (B, Hq, T) or lse.dtype != torch.float32:
+        raise ValueError("lse must be float32 [B,Hq,T]")
+    if tuple(wsum.shape) != (B, Hkv, M + T) or wsum.dtype != torch.float32:
+        raise ValueError("wsum must be float32 [B,Hkv,M+T]")
+    if tuple(scores.shape) != (B, Hkv, M) or scores.dtype != torch.float32:
+        raise ValueError("scores must be float32 [B,Hkv,M]")
+    if tuple(evict_idx.shape) != (B, Hkv, T) or evict_idx.dtype != torch.int32:
+        raise ValueError("evict_idx must be int32 [B,Hkv,T]")
+    if token_pos is not None and (token_pos.dtype != torch.int32 or
+                                  tuple(token_pos.shape) != (B, Hkv, M)):
+        raise ValueError("token_pos must be int32 [B,Hkv,M]")
+    if scale is None:
+        scale = d ** -0.5
+    nbytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(lib().h2o_chunk_step(
+        _dev(q, "q"), _dev(k_cache, "k_cache"), _dev(v_cache, "v_cache"),
+        _dev(scores, "scores"), _dev(token_pos, "token_pos"), _dev(k_new, "k_new"),
+        _dev(v_new, "v_new"), _dev(out, "out"), _dev(lse, "lse"), _dev(wsum, "wsum"),
+        _dev(evict_idx, "evict_idx"), _dev(workspace, "workspace"), nbytes,
+        B, Hq, Hkv, T, M, d, float(scale), int(pos0), dt, _stream(stream)))
+
+
 def h2o_bottomk(scores, k: int, idx_out, stream=None) -> None:
     """scores [..., M] f32; idx_out [..., k] int32 (ascending indices)."""
     M = scores.shape[-1]
@@ -229,11 +269,18 @@ def alloc_step(B, Hq, Hkv, T, M, d, dtype, device="cuda"):
     )
 
 
-def step(state, q, k_new, v_new, bufs, pos0: int, scale=None, stream=None) -> None:
-    """One chunk step in place: attend, accumulate, evict + insert.
+def step(state, q, k_new, v_new, bufs, pos0: int, scale=None, stream=None,
+         fused: bool = True) -> None:
+    """One chunk step in place: attend, accumulate, evict + insert, through
+    h2o_chunk_step (``fused``) or the three separate calls.
 
     ``state`` holds k_cache, v_cache, scores, token_pos (token_pos may be None).
     """
+    if fused:
+        h2o_chunk_step(q, state["k_cache"], state["v_cache"], state["scores"],
+                       state.get("token_pos"), k_new, v_new, bufs["out"], bufs["lse"],
+                       bufs["wsum"], bufs["evict_idx"], bufs["workspace"], pos0, scale, stream)
+        return
     h2o_sdpa_chunk(q, state["k_cache"], state["v_cache"], k_new, v_new, bufs["out"],
                    bufs["lse"], bufs["wsum"], bufs["workspace"], scale, stream)
     h2o_accumulate_scores(state["scores"], bufs["wsum"], stream)

@@ -111,6 +111,34 @@ def test_evict_rejects(L, kw, code):
     assert _evict(L, **kw) == code
 
 
+def _step(L, **kw):
+    a = dict(q=P, kc=P, vc=P, sc=P, tp=P, kn=P, vn=P, out=P, lse=P, w=P, idx=P, ws=P,
+             wsb=1 << 40, B=1, Hq=4, Hkv=2, T=4, M=16, d=64, scale=0.125, pos0=16, dt=1, st=None)
+    a.update(kw)
+    return L.h2o_chunk_step(a["q"], a["kc"], a["vc"], a["sc"], a["tp"], a["kn"], a["vn"],
+                            a["out"], a["lse"], a["w"], a["idx"], a["ws"], a["wsb"], a["B"],
+                            a["Hq"], a["Hkv"], a["T"], a["M"], a["d"], a["scale"], a["pos0"],
+                            a["dt"], a["st"])
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dt=3), H.H2O_EDTYPE),
+    (dict(Hq=6, Hkv=4), H.H2O_ESHAPE),
+    (dict(M=3), H.H2O_EINVAL),
+    (dict(sc=None), H.H2O_EINVAL),
+    (dict(idx=None), H.H2O_EINVAL),
+    (dict(q=None), H.H2O_EINVAL),
+    (dict(scale=0.0), H.H2O_EINVAL),
+    (dict(tp=MIS), H.H2O_EALIGN),
+    (dict(sc=MIS), H.H2O_EALIGN),
+    (dict(lse=MIS), H.H2O_EALIGN),
+    (dict(wsb=8), H.H2O_EWORKSPACE),
+])
+def test_chunk_step_rejects(L, kw, code):
+    assert _step(L, **kw) == code
+    assert len(L.h2o_last_error()) > 0
+
+
 @pytest.mark.parametrize("args,code", [
     ((P, 4, 10, 11, P, None), H.H2O_EINVAL),
     ((P, 4, 10, -1, P, None), H.H2O_EINVAL),
@@ -138,6 +166,7 @@ def test_no_device_is_reported(L):
     assert _evict(L) == H.H2O_ENODEVICE
     assert L.h2o_bottomk(P, 4, 10, 3, P, None) == H.H2O_ENODEVICE
     assert L.h2o_accumulate_scores(P, P, 1, 2, 8, 1, None) == H.H2O_ENODEVICE
+    assert _step(L) == H.H2O_ENODEVICE
 
 
 def test_binding_raises_typed_errors(L):

@@ -271,3 +271,38 @@ def test_decode_trajectory_teacher_forced():
     say(f"  eviction choices differing from the oracle over 16 steps: {n_mismatch} / "
         f"{16 * wl.B * wl.Hkv}")
     assert n_mismatch <= 2
+
+
+STEP_SHAPES = [  # B, Hq, Hkv, d, M, T, dtype
+    (8, 32, 8, 64, 4096, 1, "bf16"),
+    (2, 8, 2, 64, 700, 1, "bf16"),
+    (1, 8, 1, 64, 37, 1, "bf16"),
+    (2, 8, 4, 128, 1025, 1, "bf16"),
+    (1, 2, 2, 128, 3, 1, "bf16"),
+    (1, 4, 2, 64, 256, 64, "f32"),
+    (1, 8, 2, 128, 300, 70, "bf16"),
+    (2, 4, 2, 64, 500, 1, "f32"),
+]
+
+
+@pytest.mark.parametrize("shape", STEP_SHAPES)
+def test_chunk_step_equals_three_calls(shape):
+    """h2o_chunk_step gives the same bits as h2o_sdpa_chunk + h2o_accumulate_scores
+    + h2o_evict_insert, and its attention matches the oracle."""
+    B, Hq, Hkv, d, M, T, dt = shape
+    wl = W.custom("step", B=B, Hq=Hq, Hkv=Hkv, d=d, M=M, T=T, dtype=dt, heavy_frac=0.02)
+    say(f"chunk step {wl.describe()}")
+    x = W.make_inputs(wl, seed=11)
+    tdt = torch.float32 if dt == "f32" else torch.bfloat16
+    q, kn, vn = (U.to_dev(x[n], tdt) for n in ("q", "k_new", "v_new"))
+    res = []
+    for fused in (False, True):
+        st = U.device_state(x, dt)
+        bufs = H.alloc_step(B, Hq, Hkv, T, M, d, tdt)
+        H.step(st, q, kn, vn, bufs, int(x["pos0"]), float(x["scale"]), fused=fused)
+        torch.cuda.synchronize()
+        res.append({**{n: U.to_np(bufs[n]) for n in ("out", "lse", "wsum", "evict_idx")},
+                    **{n: U.to_np(st[n]) for n in ("k_cache", "v_cache", "scores", "token_pos")}})
+    for n in res[0]:
+        np.testing.assert_array_equal(res[1][n], res[0][n], err_msg=n)
+    _check_attention(x, dt, (res[1]["out"], res[1]["lse"], res[1]["wsum"]), extra="fused")

@@ -61,8 +61,8 @@ extern "C" {
 typedef enum {
   H2O_OK = 0,
   H2O_EINVAL = 1,      /* null pointer, k != T, T < 1, M < k, bad scale     */
-  H2O_ESHAPE = 2,      /* Hq % Hkv != 0, d not in {64,128}, sizes <= 0 or
-                          too large for 32-bit element counts per head        */
+  H2O_ESHAPE = 2,      /* Hq % Hkv != 0, d not in {64,128}, sizes <= 0, or
+                          (M+T)*d or (Hq/Hkv)*T*d >= 2^30 elements per head   */
   H2O_EDTYPE = 3,      /* dtype not H2O_F32 / H2O_BF16                        */
   H2O_EALIGN = 4,      /* a tensor pointer is not 16-byte aligned             */
   H2O_EWORKSPACE = 5,  /* workspace smaller than h2o_workspace_bytes()        */

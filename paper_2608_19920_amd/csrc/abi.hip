@@ -89,7 +89,7 @@ int check_shape(int B, int Hq, int Hkv, int T, int M, int d) {
   if (M < 0) return fail(H2O_EINVAL, "cache length M must be >= 0");
   const long long nk = (long long)M + T;
   const long long rows = (long long)(Hq / Hkv) * T;
-  if (nk * d >= (1ll << 31) || rows * d >= (1ll << 31) || (long long)B * Hq >= (1 << 24))
+  if (nk * d >= (1ll << 30) || rows * d >= (1ll << 30) || (long long)B * Hq >= (1 << 24))
     return fail(H2O_ESHAPE, "shape too large for 32-bit per-head indexing");
   return H2O_OK;
 }

@@ -22,7 +22,6 @@ constexpr int kWaves = kThreads / 64;
 constexpr int kStep = 32;                                // cache slots per wave step
 constexpr int kMaxGD = 512;                              // G * D handled by these kernels
 constexpr int kMaxSplit = 64;                            // split blocks per head, at most
-constexpr int kBufferFlags = 0x00020000;                 // buffer descriptor word 3 (32-bit data)
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -106,11 +105,9 @@ __global__ __launch_bounds__(kThreads) void decode_split(
   const int stream = s * kWaves + wave, nstreams = nsplit * kWaves;
   const int nst = stream < head_steps ? (head_steps - stream + nstreams - 1) / nstreams : 0;
   // K and V of head bh as buffer resources: rows past the cache read as zero
-  const int head_bytes = (int)((uint32_t)M * (uint32_t)(D * 2));
-  const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(kc + bh * (size_t)M * D), (short)0, head_bytes, kBufferFlags);
-  const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc(
-      (void*)(vc + bh * (size_t)M * D), (short)0, head_bytes, kBufferFlags);
+  const uint32_t head_bytes = (uint32_t)M * (uint32_t)(D * 2);
+  const __amdgpu_buffer_rsrc_t krs = buffer_rsrc(kc + bh * (size_t)M * D, head_bytes);
+  const __amdgpu_buffer_rsrc_t vrs = buffer_rsrc(vc + bh * (size_t)M * D, head_bytes);
   bf16_t* vs = vs_all[wave];
   const int vrow = lane / (D / 8), vcol = 8 * (lane % (D / 8));
   const uint32_t koff = (uint32_t)(col * D + 8 * grp) * 2u;   // + block / chunk offsets

@@ -25,6 +25,14 @@ __device__ __forceinline__ float load_elem(const bf16_t* p, size_t i) { return b
 __device__ __forceinline__ void store_elem(float* p, size_t i, float v) { p[i] = v; }
 __device__ __forceinline__ void store_elem(bf16_t* p, size_t i, float v) { p[i] = f32_to_bf16(v); }
 
+// Buffer resource over [base, base + bytes): loads at offsets past the end
+// return zero. Word 3 selects 32-bit data for gfx9-family buffers.
+constexpr int kBufferFlags = 0x00020000;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
+                                           kBufferFlags);
+}
+
 // Order-preserving map of a float32 score to uint32 (a < b  <=>  key(a) <
 // key(b)); both zeros map to the same key.
 __device__ __forceinline__ uint32_t order_key(float x) {

@@ -22,8 +22,8 @@
 // Workgroup: NW waves, each owning NQB*16 consecutive packed rows
 // (r = i*G + g: chunk position i, query head h*G+g); all waves share one
 // 32-key K/V tile in LDS, so the K/V of a KV head is staged once for the G
-// query heads of its group. Tiles are double buffered: the global loads of
-// tile t+1 are in flight while tile t is computed.
+// query heads of its group. Tiles are triple buffered in LDS (see the
+// software pipeline below).
 #include "internal.h"
 
 namespace h2o {
@@ -241,6 +241,30 @@ __device__ __forceinline__ int first_masked_tile(int M, int i_min) {
   return x < 0 ? 0 : x / BN + 1;
 }
 
+// ------------------------------------------------------------ block order
+// Workgroups go to the 8 XCDs round-robin in dispatch order, and each XCD
+// has its own L2. The blocks that read the same K/V tiles - one (head, key
+// split) group, all its row tiles - are given consecutive dispatch slots of
+// one XCD, so they start together there and share that L2. Grid: (nrt *
+// nsplit, BH); falls back to the plain order when the groups do not divide
+// evenly over the XCDs.
+constexpr int kXcds = 8;
+struct BlockId { int rt, sp, bh; };
+__device__ __forceinline__ BlockId block_id(int nsplit) {
+  const int nrt = gridDim.x / nsplit, ngroups = nsplit * gridDim.y;
+  const int lin = blockIdx.x + blockIdx.y * gridDim.x;
+  int grp, rt;
+  if (ngroups % kXcds == 0) {
+    const int i = lin / kXcds;
+    grp = (i / nrt) * kXcds + lin % kXcds;
+    rt = i % nrt;
+  } else {
+    grp = lin / nrt;
+    rt = lin % nrt;
+  }
+  return BlockId{rt, grp % nsplit, grp / nsplit};
+}
+
 // ------------------------------------------------------------------ pass A
 // Online (max, sum) update of one tile for every query of the wave. The
 // running maximum m is kept in raw score units (c > 0 keeps the order);
@@ -309,8 +333,9 @@ __global__ __launch_bounds__(NW * 64) void lse_pass(Geo g, int Hq, int Hkv, int 
   constexpr int NT = NW * 64, ROWS = NW * NQB * 16;
   __shared__ __attribute__((aligned(16))) bf16_t Ks[NBUF][BN * kstride(D)];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int rt = blockIdx.x / nsplit, sp = blockIdx.x % nsplit;
-  const size_t bh = blockIdx.y;
+  const BlockId id = block_id(nsplit);
+  const int rt = id.rt, sp = id.sp;
+  const size_t bh = id.bh;
   const int b = (int)(bh / Hkv), h = (int)(bh % Hkv);
   const int row0 = rt * ROWS, wrow0 = row0 + wave * NQB * 16;
   const int kv_end = kv_end_for_rows(min(row0 + ROWS, g.R), g.G, g.T, g.M);
@@ -457,8 +482,9 @@ __global__ __launch_bounds__(NW * 64) void main_pass(Geo g, int Hq, int Hkv, int
   __shared__ __attribute__((aligned(16))) bf16_t Ks[NBUF][BN * kstride(D)];
   __shared__ __attribute__((aligned(16))) bf16_t Vs[NBUF][BN * vstride(D)];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int rt = blockIdx.x / nsplit, sp = blockIdx.x % nsplit;
-  const size_t bh = blockIdx.y;
+  const BlockId id = block_id(nsplit);
+  const int rt = id.rt, sp = id.sp;
+  const size_t bh = id.bh;
   const int BH = gridDim.y;
   const int b = (int)(bh / Hkv), h = (int)(bh % Hkv);
   const int row0 = rt * ROWS, wrow0 = row0 + wave * NQB * 16;

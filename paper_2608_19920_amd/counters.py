@@ -6,8 +6,9 @@ Two sub-commands:
 ``rocprofv3 --pmc FETCH_SIZE`` (or ``WRITE_SIZE``) pass records it per
 dispatch:
 
-    decode   one token step (B8 Hq32 Hkv8 d64 M4096, bf16) on each of 8 layer
-             states, 3 times over, so every launch streams its cache from HBM
+    decode   one token step (h2o_chunk_step, B8 Hq32 Hkv8 d64 M4096, bf16) on
+             each of 8 layer states, 3 times over, so every launch streams
+             its cache from HBM
     prefill  the chunked-prefill attention of one prefill workload (bf16)
     copy     a plain device-to-device copy of 1 GiB, the calibration: its
              algorithmic traffic is exactly 1 GiB read and 1 GiB written
@@ -34,7 +35,7 @@ COPY_BYTES = 1 << 30
 # kernel label -> (substring of the rocprofv3 kernel name, sources it is built from)
 KERNELS = {
     "decode_split": ("decode_split<", ["decode.hip"]),
-    "decode_combine": ("decode_combine<", ["decode.hip"]),
+    "decode_finish": ("decode_finish<", ["decode.hip"]),
     "mfma_lse": ("lse_pass<", ["sdpa_mfma.hip"]),
     "mfma_main": ("main_pass<", ["sdpa_mfma.hip"]),
 }

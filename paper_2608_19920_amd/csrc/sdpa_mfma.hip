@@ -389,12 +389,12 @@ __global__ __launch_bounds__(NW * 64) void lse_pass(Geo g, int Hq, int Hkv, int 
 
 // ------------------------------------------------------------------ pass B
 // Probabilities of one tile (bf16 B operands of the PV product) and their
-// column partials over this wave's rows. The partial row is padded to whole
-// tiles, and the four lanes holding one column's total all store it.
+// column partials over this wave's rows, into the wave's LDS row for the
+// tile (the four lanes holding one column's total all store it).
 template <bool MASKED, int NQB>
 __device__ __forceinline__ void probs_tile(const f32x4 (&sacc)[2][NQB], bf16x8 (&pb)[NQB],
                                            const float (&lam)[NQB], const int (&qi)[NQB],
-                                           float* prow, int j0, int M, int lane, float c) {
+                                           float* cs_row, int j0, int M, int lane, float c) {
   float cs[2][4];
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb)
@@ -415,7 +415,7 @@ __device__ __forceinline__ void probs_tile(const f32x4 (&sacc)[2][NQB], bf16x8 (
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb) {
     const float v = colsum16(cs[kb][0], cs[kb][1], cs[kb][2], cs[kb][3], lane);
-    prow[j0 + kb * 16 + 4 * (lane >> 4) + ((lane & 15) >> 2)] = v;
+    cs_row[kb * 16 + 4 * (lane >> 4) + ((lane & 15) >> 2)] = v;
   }
 }
 
@@ -438,6 +438,9 @@ struct MainState {
   u32x4 pk[Tile<D, NT>::N], pv[Tile<D, NT>::N];
 };
 
+// The waves' column partials of a tile meet in cs_lds[tile parity][wave];
+// after the tile's barrier, threads 0..BN-1 add them in wave order and store
+// the block's partial row (one partial per block and row tile).
 template <bool MASKED, int D, int NT, int NQB>
 __device__ __forceinline__ void main_loop(int ta, int tb, int t0, int t1, MainState<D, NT, NQB>& S,
                                           const Tile<D, NT>& tl,
@@ -445,9 +448,11 @@ __device__ __forceinline__ void main_loop(int ta, int tb, int t0, int t1, MainSt
                                           bf16_t (*Vs)[BN * vstride(D)],
                                           const bf16x8 (&qf)[NQB][D / 32],
                                           const float (&lam)[NQB], const int (&qi)[NQB],
-                                          float* prow, const bf16_t* kc_bh, const bf16_t* kn_bh,
+                                          float (*cs_lds)[NT / 64][BN], float* prow,
+                                          const bf16_t* kc_bh, const bf16_t* kn_bh,
                                           const bf16_t* vc_bh, const bf16_t* vn_bh, const Geo& g,
                                           int lane, float c) {
+  const int wave = threadIdx.x >> 6;
   for (int t = ta; t < tb; ++t) {
     const int j0 = t * BN;
     const int b0 = (t - t0) % NBUF, b1 = (t + 1 - t0) % NBUF, b2 = (t + 2 - t0) % NBUF;
@@ -456,13 +461,20 @@ __device__ __forceinline__ void main_loop(int ta, int tb, int t0, int t1, MainSt
     load_tile<D, NT>(S.pv, tl, vc_bh, vn_bh, jn, g.M, g.Nk);
     bf16x8 pb[NQB];
     scores_tile<D, NQB>(S.s_nxt, Ks[b1], qf, lane);
-    probs_tile<MASKED, NQB>(S.s_cur, pb, lam, qi, prow, j0, g.M, lane, c);
+    probs_tile<MASKED, NQB>(S.s_cur, pb, lam, qi, cs_lds[(t - t0) & 1][wave], j0, g.M, lane, c);
     pv_tile<D, NQB>(S.oacc, pb, Vs[b0], lane);
     interleave<2 * NQB * (D / 32), MASKED ? 5 : 4>();
     interleave<NQB * (D / 16), 1>();
     store_tile<D, NT>(Ks[b2], tl.loff, S.pk);
     store_tile<D, NT>(Vs[b2], tl.vloff, S.pv);
     __syncthreads();
+    if (threadIdx.x < BN) {
+      const float (*cs)[BN] = cs_lds[(t - t0) & 1];
+      float a = cs[0][threadIdx.x];
+#pragma unroll
+      for (int w = 1; w < NT / 64; ++w) a += cs[w][threadIdx.x];
+      prow[j0 + threadIdx.x] = a;
+    }
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -530,7 +542,8 @@ __global__ __launch_bounds__(NW * 64) void main_pass(Geo g, int Hq, int Hkv, int
 #pragma unroll
     for (int qb = 0; qb < NQB; ++qb) S.oacc[db][qb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  float* prow = parts + ((size_t)(rt * NW + wave) * BH + bh) * parts_ld;
+  __shared__ float cs_lds[2][NW][BN];
+  float* prow = parts + ((size_t)rt * BH + bh) * parts_ld;
   const Tile<D, NT> tl;
 
   if (t0 < t1) {
@@ -545,9 +558,11 @@ __global__ __launch_bounds__(NW * 64) void main_pass(Geo g, int Hq, int Hkv, int
     store_tile<D, NT>(Vs[1], tl.vloff, S.pv);
     __syncthreads();
     scores_tile<D, NQB>(S.s_cur, Ks[0], qf, lane);
-    main_loop<false, D, NT, NQB>(t0, t_mask, t0, t1, S, tl, Ks, Vs, qf, lam, qi, prow, kc_bh, kn_bh,
+    main_loop<false, D, NT, NQB>(t0, t_mask, t0, t1, S, tl, Ks, Vs, qf, lam, qi, cs_lds, prow,
+                                 kc_bh, kn_bh,
                                  vc_bh, vn_bh, g, lane, c_log2);
-    main_loop<true, D, NT, NQB>(t_mask, t1, t0, t1, S, tl, Ks, Vs, qf, lam, qi, prow, kc_bh, kn_bh,
+    main_loop<true, D, NT, NQB>(t_mask, t1, t0, t1, S, tl, Ks, Vs, qf, lam, qi, cs_lds, prow,
+                                kc_bh, kn_bh,
                                 vc_bh, vn_bh, g, lane, c_log2);
   }
   // write O (lane: query qb*16 + l%16, d = db*16 + 4*(l/16) + r)
@@ -600,11 +615,17 @@ __global__ __launch_bounds__(256) void split_reduce(const float* __restrict__ op
   *reinterpret_cast<uint2*>(out + ((size_t)(b * Hq + h * G + gg) * T + i) * D + dd) = o;
 }
 
-template <int D, int NW, int NQB>
+// Both passes use 128-row blocks: the lse pass as 2 waves x 64 rows, the
+// main pass as 4 waves x 32 rows (fewer registers per wave, so two waves
+// share each SIMD).
+constexpr int kLseWaves = 2, kLseQB = 4, kMainWaves = 4, kMainQB = 2;
+static_assert(kLseWaves * kLseQB == kMainWaves * kMainQB, "one row tiling");
+
+template <int D>
 hipError_t run(const Shape& s, const Plan& p, const void* q, const void* kc, const void* vc,
                const void* kn, const void* vn, void* out, float* lse, float* wsum, char* ws,
                float scale, hipStream_t st) {
-  constexpr int ROWS = NW * NQB * 16;
+  constexpr int ROWS = kMainWaves * kMainQB * 16;
   Geo g{s.G(), s.T, s.M, s.R(), s.Nk(), (const bf16_t*)q, (const bf16_t*)kc,
         (const bf16_t*)vc, (const bf16_t*)kn, (const bf16_t*)vn};
   const int nrt = (s.R() + ROWS - 1) / ROWS;
@@ -613,10 +634,11 @@ hipError_t run(const Shape& s, const Plan& p, const void* q, const void* kc, con
   float2* stats = reinterpret_cast<float2*>(ws + p.off_stats);
   float* parts = reinterpret_cast<float*>(ws + p.off_parts);
   float* opart = reinterpret_cast<float*>(ws + p.off_opart);
-  hipError_t e = launch_kernel(K_MFMA_LSE, lse_pass<D, NW, NQB>, grid_lse, dim3(NW * 64), st,
-                               g, s.Hq, s.Hkv, p.nsplit_lse, c, stats);
+  hipError_t e = launch_kernel(K_MFMA_LSE, lse_pass<D, kLseWaves, kLseQB>, grid_lse,
+                               dim3(kLseWaves * 64), st, g, s.Hq, s.Hkv, p.nsplit_lse, c, stats);
   if (e != hipSuccess) return e;
-  e = launch_kernel(K_MFMA_MAIN, main_pass<D, NW, NQB>, grid, dim3(NW * 64), st, g, s.Hq, s.Hkv,
+  e = launch_kernel(K_MFMA_MAIN, main_pass<D, kMainWaves, kMainQB>, grid, dim3(kMainWaves * 64),
+                    st, g, s.Hq, s.Hkv,
                     p.nsplit, p.nsplit_lse, c, (const float2*)stats, parts, p.parts_ld,
                     (bf16_t*)out, opart, lse);
   if (e != hipSuccess) return e;
@@ -633,15 +655,15 @@ hipError_t run(const Shape& s, const Plan& p, const void* q, const void* kc, con
 }  // namespace
 
 // Rows of packed queries per workgroup of the MFMA kernels, and per colsum
-// partial (one partial per wave).
-int mfma_rows_per_block() { return 2 * 4 * 16; }
-int mfma_rows_per_part() { return 4 * 16; }
+// partial (one partial per block).
+int mfma_rows_per_block() { return kMainWaves * kMainQB * 16; }
+int mfma_rows_per_part() { return kMainWaves * kMainQB * 16; }
 
 hipError_t launch_sdpa_mfma(const Shape& s, const Plan& p, const void* q, const void* kc,
                             const void* vc, const void* kn, const void* vn, void* out, float* lse,
                             float* wsum, char* ws, float scale, hipStream_t st) {
-  if (s.d == 64) return run<64, 2, 4>(s, p, q, kc, vc, kn, vn, out, lse, wsum, ws, scale, st);
-  return run<128, 2, 4>(s, p, q, kc, vc, kn, vn, out, lse, wsum, ws, scale, st);
+  if (s.d == 64) return run<64>(s, p, q, kc, vc, kn, vn, out, lse, wsum, ws, scale, st);
+  return run<128>(s, p, q, kc, vc, kn, vn, out, lse, wsum, ws, scale, st);
 }
 
 }  // namespace h2o

@@ -128,8 +128,9 @@ Plan make_plan(const Shape& s, int dtype) {
   p.parts_ld = (int)Nk;
   if (path == 1) {
     // Split the key range of each row tile when there are too few blocks to
-    // fill the CUs: two 4-wave main-pass blocks and four 2-wave lse-pass
-    // blocks fit one CU. Keep at least 8 key tiles per split.
+    // fill the CUs: two 4-wave blocks of the main pass fit one CU, and the
+    // lighter lse pass is given twice as many. Keep at least 8 key tiles per
+    // split.
     const int rows_blk = mfma_rows_per_block();
     const long long nrt = (R + rows_blk - 1) / rows_blk;
     const long long blocks = nrt * (long long)BH;

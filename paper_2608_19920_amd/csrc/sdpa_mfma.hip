@@ -615,10 +615,10 @@ __global__ __launch_bounds__(256) void split_reduce(const float* __restrict__ op
   *reinterpret_cast<uint2*>(out + ((size_t)(b * Hq + h * G + gg) * T + i) * D + dd) = o;
 }
 
-// Both passes use 128-row blocks: the lse pass as 2 waves x 64 rows, the
-// main pass as 4 waves x 32 rows (fewer registers per wave, so two waves
-// share each SIMD).
-constexpr int kLseWaves = 2, kLseQB = 4, kMainWaves = 4, kMainQB = 2;
+// Both passes use 128-row blocks of 4 waves x 32 rows: few enough registers
+// per wave that two or more waves share each SIMD and hide each other's
+// latencies.
+constexpr int kLseWaves = 4, kLseQB = 2, kMainWaves = 4, kMainQB = 2;
 static_assert(kLseWaves * kLseQB == kMainWaves * kMainQB, "one row tiling");
 
 template <int D>

@@ -306,3 +306,34 @@ def test_chunk_step_equals_three_calls(shape):
     for n in res[0]:
         np.testing.assert_array_equal(res[1][n], res[0][n], err_msg=n)
     _check_attention(x, dt, (res[1]["out"], res[1]["lse"], res[1]["wsum"]), extra="fused")
+
+
+@pytest.mark.parametrize("shape", [(8, 32, 8, 64, 4096, 1, "bf16"), (1, 8, 2, 128, 300, 70, "bf16")])
+def test_graph_replays_match_eager(shape):
+    """The chunk step captured in a HIP graph and replayed three times (the
+    state advancing each time, with eager work and synchronisation between
+    replays) gives the same bits as the same steps run eagerly."""
+    B, Hq, Hkv, d, M, T, dt = shape
+    wl = W.custom("graph", B=B, Hq=Hq, Hkv=Hkv, d=d, M=M, T=T, dtype=dt, heavy_frac=0.02)
+    say(f"graph replay {wl.describe()}")
+    x = W.make_inputs(wl, seed=5)
+    tdt = torch.bfloat16
+    q, kn, vn = (U.to_dev(x[n], tdt) for n in ("q", "k_new", "v_new"))
+    pos0, scale = int(x["pos0"]), float(x["scale"])
+    sg, se = U.device_state(x, dt), U.device_state(x, dt)
+    bg = H.alloc_step(B, Hq, Hkv, T, M, d, tdt)
+    be = H.alloc_step(B, Hq, Hkv, T, M, d, tdt)
+    stream = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=stream):
+        H.step(sg, q, kn, vn, bg, pos0, scale)
+    torch.cuda.synchronize()          # capture does not run the step
+    for r in range(3):
+        graph.replay()
+        H.step(se, q, kn, vn, be, pos0, scale)
+        torch.cuda.synchronize()
+        for n in ("out", "lse", "wsum", "evict_idx"):
+            np.testing.assert_array_equal(U.to_np(bg[n]), U.to_np(be[n]), err_msg=f"replay {r} {n}")
+        for n in ("k_cache", "v_cache", "scores", "token_pos"):
+            np.testing.assert_array_equal(U.to_np(sg[n]), U.to_np(se[n]), err_msg=f"replay {r} {n}")

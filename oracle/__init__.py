@@ -3,8 +3,8 @@
 TEST INFRASTRUCTURE ONLY: imported by ``tests/``, ``__graft_entry__.smoke()``
 and the ``cpu_baseline`` leg of ``bench.py``, never by the library.
 """
-from .h2o_oracle import (accumulate_scores, bottomk, decode, evict_insert,
-                         h2o_step, rel_err, sdpa_chunk, visible)
+from .h2o_oracle import (POLICIES, accumulate_scores, bottomk, decode, evict_insert,
+                         h2o_step, rel_err, sdpa_chunk, selection_keys, visible)
 
-__all__ = ["accumulate_scores", "bottomk", "decode", "evict_insert",
-           "h2o_step", "rel_err", "sdpa_chunk", "visible"]
+__all__ = ["POLICIES", "accumulate_scores", "bottomk", "decode", "evict_insert",
+           "h2o_step", "rel_err", "sdpa_chunk", "selection_keys", "visible"]

@@ -24,7 +24,9 @@ time, with numpy float64 matrix products as the only library primitive:
    sum over chunks), held in float32 storage: one IEEE float32 addition.
 5. Eviction: per (b, kv-head), the k slots with the smallest score
    (Sec. "Variants of Heavy-Hitter Oracle"), ties broken by the lower slot
-   index, returned in ascending slot order.
+   index, returned in ascending slot order; or the ranking of one of the
+   paper's two variants of the score, normalised by age (h2o_norm) or
+   summed over the batch (h2o_orig).
 6. Insert: scatter of the chunk's keys/values into the evicted slots along the
    slot axis (Sec. "Fine-Tuning for Sparse Attention", the linear recurrence;
    Sec. "Buffer Read/Write Access by torch.scatter, torch.gather"); new key i
@@ -143,18 +145,57 @@ def bottomk(scores, k: int) -> np.ndarray:
     return res.reshape(*lead, k)
 
 
+# ------------------------------------------------- the H2O score variants
+POLICIES = ("h2o", "h2o_norm", "h2o_orig")
+
+
+def selection_keys(scores, token_pos, policy: str, t: int) -> np.ndarray:
+    """The float32 vector the eviction ranks, from the accumulated float32
+    scores phi(b, h, j) (Sec. "Variants of Heavy-Hitter Oracle"):
+
+      h2o       phi itself, per (b, kv-head)                        [B, H, M]
+      h2o_norm  phi / (t - token_pos): the score divided by the slot's age,
+                t being the number of tokens processed, this chunk
+                included; one correctly rounded float32 division (the age
+                is exact in float32)                                 [B, H, M]
+      h2o_orig  the sum over the batch of phi, one slot set per kv-head;
+                float32 additions in increasing b                    [H, M]
+    """
+    s = np.asarray(scores, np.float32)
+    if policy == "h2o":
+        return s.copy()
+    if policy == "h2o_norm":
+        if token_pos is None:
+            raise ValueError("h2o_norm needs token positions")
+        age = t - np.asarray(token_pos, np.int64)
+        if (age < 1).any() or (age >= 1 << 24).any():
+            raise ValueError("slot ages must be in [1, 2^24)")
+        return (s / age.astype(np.float32)).astype(np.float32)
+    if policy == "h2o_orig":
+        acc = s[0].copy()
+        for b in range(1, s.shape[0]):
+            acc = (acc + s[b]).astype(np.float32)
+        return acc
+    raise ValueError(f"unknown policy {policy!r}")
+
+
 # ------------------------------------------------------------ step 6: insert
 def evict_insert(k_cache, v_cache, scores, token_pos, k_new, v_new, wsum,
-                 k: int, pos0: int):
-    """Evict the k lowest-score slots per (b, kv-head) and insert the chunk.
+                 k: int, pos0: int, policy: str = "h2o"):
+    """Evict the k lowest-ranked slots per (b, kv-head) and insert the chunk.
 
-    ``scores`` are the accumulated float32 scores. Returns new copies
-    (k_cache, v_cache, scores, token_pos, evict_idx); token_pos may be None.
+    ``scores`` are the accumulated float32 scores; the ranking is that of
+    ``selection_keys`` (h2o_orig: one slot set per kv-head, used for every b).
+    Returns new copies (k_cache, v_cache, scores, token_pos, evict_idx);
+    token_pos may be None except for h2o_norm.
     """
     T = k_new.shape[2]
     if k != T:
         raise ValueError("every chunk key is inserted: k must equal T")
-    idx = bottomk(scores, k)
+    keys = selection_keys(scores, token_pos, policy, pos0 + T)
+    idx = bottomk(keys, k)
+    if policy == "h2o_orig":
+        idx = np.broadcast_to(idx, (k_cache.shape[0],) + idx.shape).copy()
     kc, vc = k_cache.copy(), v_cache.copy()
     sc = np.asarray(scores, np.float32).copy()
     tp = None if token_pos is None else token_pos.copy()
@@ -174,8 +215,8 @@ def evict_insert(k_cache, v_cache, scores, token_pos, k_new, v_new, wsum,
 
 # --------------------------------------------------------------- whole step
 def h2o_step(k_cache, v_cache, scores, token_pos, q, k_new, v_new, pos0: int,
-             scale: Optional[float] = None):
-    """One chunk step: attend, accumulate, evict, insert.
+             scale: Optional[float] = None, policy: str = "h2o"):
+    """One chunk step: attend, accumulate, evict (ranking of ``policy``), insert.
 
     Returns dict with out, lse, wsum (float64), scores_acc (float32 scores after
     accumulation), evict_idx and the new cache state.
@@ -184,7 +225,7 @@ def h2o_step(k_cache, v_cache, scores, token_pos, q, k_new, v_new, pos0: int,
     acc = accumulate_scores(scores, wsum)
     T = q.shape[2]
     kc, vc, sc, tp, idx = evict_insert(k_cache, v_cache, acc, token_pos,
-                                       k_new, v_new, wsum, T, pos0)
+                                       k_new, v_new, wsum, T, pos0, policy)
     return dict(out=out, lse=lse, wsum=wsum, scores_acc=acc, evict_idx=idx,
                 k_cache=kc, v_cache=vc, scores=sc, token_pos=tp)
 

@@ -379,3 +379,115 @@ def test_planted_mistakes_are_caught(monkeypatch):
     with monkeypatch.context() as m:
         m.setattr(oracle, "sdpa_chunk", strided)
         assert _pin_failures(None), "strided head mapping not caught"
+
+
+# ------------------------------------------------------ score variants
+def _acc_state(B, H, M, seed, quant=None):
+    rng = np.random.default_rng(seed)
+    s = rng.standard_exponential((B, H, M)).astype(np.float32)
+    if quant is not None:
+        s = (np.floor(s * quant) / quant).astype(np.float32)
+    tp = rng.integers(0, 1000, size=(B, H, M)).astype(np.int32)
+    return s, tp
+
+
+def test_norm_keys_brute_force():
+    """h2o_norm ranks phi / (t - token_pos), one float32 division per slot:
+    each key equals the float32 rounding of the exact quotient."""
+    s, tp = _acc_state(2, 3, 40, 0)
+    t = 1500
+    keys = oracle.selection_keys(s, tp, "h2o_norm", t)
+    for idx in np.ndindex(s.shape):
+        exact = float(s[idx]) / float(t - int(tp[idx]))   # float64: the quotient rounds once more
+        assert keys[idx] == np.float32(exact)
+    k = 7
+    ref = np.sort(np.lexsort((np.arange(40), keys[1, 2].astype(np.float64)))[:k])
+    np.testing.assert_array_equal(oracle.bottomk(keys, k)[1, 2], ref)
+
+
+def test_norm_with_equal_ages_is_h2o():
+    """Dividing every score by the same power of two keeps the ranking."""
+    s, _ = _acc_state(2, 2, 64, 1, quant=8)
+    tp = np.full(s.shape, 100, np.int32)
+    a = oracle.bottomk(oracle.selection_keys(s, tp, "h2o_norm", 100 + 16), 9)
+    np.testing.assert_array_equal(a, oracle.bottomk(s, 9))
+
+
+def test_norm_prefers_evicting_old_slots():
+    """Two slots with equal scores: the older one (larger age) has the smaller
+    normalised score and is evicted first."""
+    s = np.ones((1, 1, 4), np.float32)
+    tp = np.array([[[50, 10, 60, 40]]], np.int32)
+    idx = oracle.bottomk(oracle.selection_keys(s, tp, "h2o_norm", 70), 1)
+    assert idx[0, 0, 0] == 1
+
+
+def test_orig_keys_are_exact_batch_sums():
+    """h2o_orig: with scores on a grid of 1/8 the float32 batch sums are exact,
+    so they equal integer arithmetic; one slot set serves every batch entry."""
+    s, tp = _acc_state(5, 3, 50, 2, quant=8)
+    keys = oracle.selection_keys(s, tp, "h2o_orig", 0)
+    exact = (np.round(s.astype(np.float64) * 8).astype(np.int64).sum(axis=0)) / 8.0
+    np.testing.assert_array_equal(keys.astype(np.float64), exact)
+    B, H, M = s.shape
+    T = 4
+    kc = np.zeros((B, H, M, 8), np.float32)
+    kn = np.ones((B, H, T, 8), np.float32)
+    w = np.zeros((B, H, M + T))
+    *_, idx = oracle.evict_insert(kc, kc, s, tp, kn, kn, w, T, 1000, "h2o_orig")
+    for b in range(B):
+        np.testing.assert_array_equal(idx[b], oracle.bottomk(keys, T))
+
+
+def test_orig_with_one_batch_entry_is_h2o():
+    s, tp = _acc_state(1, 4, 33, 3)
+    np.testing.assert_array_equal(oracle.bottomk(oracle.selection_keys(s, tp, "h2o_orig", 0), 5),
+                                  oracle.bottomk(s, 5)[0])
+
+
+def test_variants_insert_like_h2o():
+    """The variants change which slots are evicted, not what is written there:
+    new keys/values, the chunk key's own summed weight, token position pos0+i."""
+    rng = np.random.default_rng(4)
+    B, H, M, T, d = 2, 2, 20, 3, 8
+    kc = rng.standard_normal((B, H, M, d)).astype(np.float32)
+    vc = rng.standard_normal((B, H, M, d)).astype(np.float32)
+    kn = rng.standard_normal((B, H, T, d)).astype(np.float32)
+    vn = rng.standard_normal((B, H, T, d)).astype(np.float32)
+    s, tp = _acc_state(B, H, M, 5)
+    w = rng.random((B, H, M + T))
+    for pol in ("h2o_norm", "h2o_orig"):
+        kc2, vc2, sc2, tp2, idx = oracle.evict_insert(kc, vc, s, tp, kn, kn * 0 + vn, w, T, 2000, pol)
+        for b in range(B):
+            for h in range(H):
+                e = idx[b, h]
+                np.testing.assert_array_equal(kc2[b, h, e], kn[b, h])
+                np.testing.assert_array_equal(sc2[b, h, e], w[b, h, M:].astype(np.float32))
+                np.testing.assert_array_equal(tp2[b, h, e], 2000 + np.arange(T))
+                keep = np.setdiff1d(np.arange(M), e)
+                np.testing.assert_array_equal(kc2[b, h, keep], kc[b, h, keep])
+                np.testing.assert_array_equal(sc2[b, h, keep], s[b, h, keep])
+
+
+def test_variant_mistakes_are_caught(monkeypatch):
+    """Plausible slips in the variants fail the pins above."""
+    orig = O.selection_keys
+
+    def age_off_by_one(scores, token_pos, policy, t):
+        if policy == "h2o_norm":
+            return orig(scores, token_pos, policy, t + 1)
+        return orig(scores, token_pos, policy, t)
+
+    def sum_over_heads(scores, token_pos, policy, t):
+        if policy == "h2o_orig":
+            s = np.asarray(scores, np.float32)
+            return np.broadcast_to(s.sum(axis=1, dtype=np.float32)[:, None], s.shape)[0].copy()
+        return orig(scores, token_pos, policy, t)
+
+    for fn, test in ((age_off_by_one, test_norm_keys_brute_force),
+                     (sum_over_heads, test_orig_keys_are_exact_batch_sums)):
+        with monkeypatch.context() as m:
+            m.setattr(O, "selection_keys", fn)
+            m.setattr(oracle, "selection_keys", fn)
+            with pytest.raises(AssertionError):
+                test()

@@ -72,6 +72,22 @@ typedef enum {
 
 typedef enum { H2O_F32 = 0, H2O_BF16 = 1 } h2o_dtype;
 
+/* The ranking the eviction uses (Sec. "Variants of Heavy-Hitter Oracle"):
+ *   H2O_POLICY_H2O   the accumulated score phi itself, per (b, KV head)
+ *   H2O_POLICY_NORM  h2o_norm: phi divided by the slot's age t - token_pos,
+ *                    t = pos0 + T (the tokens processed, this chunk
+ *                    included); one correctly rounded float32 division per
+ *                    slot; every age must lie in [1, 2^24) (not checked:
+ *                    it is device data)
+ *   H2O_POLICY_ORIG  h2o_orig: phi summed over the batch (float32 additions
+ *                    in increasing b), one slot set per KV head shared by
+ *                    every batch entry */
+typedef enum {
+  H2O_POLICY_H2O = 0,
+  H2O_POLICY_NORM = 1,
+  H2O_POLICY_ORIG = 2
+} h2o_policy;
+
 /* Bytes of device scratch h2o_sdpa_chunk needs for this shape (0 on invalid
  * arguments). The workspace holds partial row statistics and per-row-tile
  * partial column sums; its contents on entry are ignored. */
@@ -120,6 +136,29 @@ int h2o_evict_insert(void* k_cache, void* v_cache, float* scores,
                      int M, int T, int d, int k, int32_t pos0, int dtype,
                      void* stream);
 
+/* Bytes of device scratch h2o_evict_insert_policy needs (0 for
+ * H2O_POLICY_H2O and on invalid arguments): the ranked keys (NORM: B*Hkv*M
+ * floats; ORIG: Hkv*M floats plus Hkv*k indices). */
+size_t h2o_evict_workspace_bytes(int B, int Hkv, int M, int k, int policy);
+
+/* h2o_evict_insert with the ranking of `policy` (an h2o_policy). E is the k
+ * slots with the smallest (key, slot) where key is the policy's value for
+ * the slot; for H2O_POLICY_ORIG the E of KV head h is the same for every b.
+ * The insert is that of h2o_evict_insert: the new slots take the new key's
+ * own summed weight wsum[b,h,M+i] as their (unnormalised) score and pos0 + i
+ * as their position. H2O_POLICY_NORM needs token_pos (the ages); the
+ * others accept NULL. workspace holds at least h2o_evict_workspace_bytes()
+ * (H2O_EWORKSPACE otherwise; NULL is fine when that is 0), its contents on
+ * entry are ignored. With H2O_POLICY_H2O the result is that of
+ * h2o_evict_insert, bit for bit. */
+int h2o_evict_insert_policy(void* k_cache, void* v_cache, float* scores,
+                            int32_t* token_pos, const void* k_new,
+                            const void* v_new, const float* wsum,
+                            int32_t* evict_idx, int B, int Hkv, int M, int T,
+                            int d, int k, int32_t pos0, int dtype, int policy,
+                            void* workspace, size_t workspace_bytes,
+                            void* stream);
+
 /* The three calls above in one: h2o_sdpa_chunk, then h2o_accumulate_scores,
  * then h2o_evict_insert with k = T (the step of Sec. "Fine-Tuning for Sparse
  * Attention": attend over cache and chunk, add the summed weights to the H2O
@@ -165,7 +204,8 @@ int h2o_debug_force_path(int path);
  *   3 MFMA main pass     4 split reduce        5 column-sum reduce
  *   6 accumulate         7 bottom-k            8 insert
  *   9 decode split      10 decode combine     11 argmin + insert (k == 1)
- *  12 decode finish (h2o_chunk_step, T == 1) */
+ *  12 decode finish (h2o_chunk_step, T == 1)
+ *  13 score-variant keys and index broadcast (h2o_evict_insert_policy) */
 int h2o_debug_timing(int on);
 int h2o_debug_kernel_time(int kernel_id, double* total_ms, long* count);
 

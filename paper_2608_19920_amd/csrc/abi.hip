@@ -96,6 +96,15 @@ int check_shape(int B, int Hq, int Hkv, int T, int M, int d) {
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// Workspace of the score-variant eviction: the ranked keys, and for h2o_orig
+// the per-head index rows before the broadcast over the batch.
+size_t evict_workspace(int B, int Hkv, int M, int k, int policy) {
+  if (policy == H2O_POLICY_NORM) return align256((size_t)B * Hkv * M * 4);
+  if (policy == H2O_POLICY_ORIG)
+    return align256((size_t)Hkv * M * 4) + align256((size_t)Hkv * k * 4);
+  return 0;
+}
+
 }  // namespace
 
 bool timing_begin(hipEvent_t* a, hipEvent_t* b) {
@@ -314,7 +323,7 @@ int h2o_chunk_step(const void* q, void* k_cache, void* v_cache, float* scores,
                     scale, st);
     if (e == hipSuccess) e = launch_accumulate(scores, wsum, rows, M, T, st);
     if (e == hipSuccess && T == 1) {
-      e = launch_argmin_insert(k_cache, v_cache, scores, token_pos, k_new, v_new, wsum,
+      e = launch_argmin_insert(k_cache, v_cache, scores, scores, 0, token_pos, k_new, v_new, wsum,
                                evict_idx, rows, M, T, d, pos0, eb, st);
     } else if (e == hipSuccess) {
       e = launch_bottomk(scores, rows, M, T, evict_idx, st);
@@ -355,10 +364,25 @@ int h2o_bottomk(const float* scores, int rows, int M, int k, int32_t* idx_out, v
   return ok();
 }
 
+size_t h2o_evict_workspace_bytes(int B, int Hkv, int M, int k, int policy) {
+  if (B < 1 || Hkv < 1 || M < 0 || k < 0) return 0;
+  return evict_workspace(B, Hkv, M, k, policy);
+}
+
 int h2o_evict_insert(void* k_cache, void* v_cache, float* scores, int32_t* token_pos,
                      const void* k_new, const void* v_new, const float* wsum, int32_t* evict_idx,
                      int B, int Hkv, int M, int T, int d, int k, int32_t pos0, int dtype,
                      void* stream) {
+  return h2o_evict_insert_policy(k_cache, v_cache, scores, token_pos, k_new, v_new, wsum,
+                                 evict_idx, B, Hkv, M, T, d, k, pos0, dtype, H2O_POLICY_H2O,
+                                 nullptr, 0, stream);
+}
+
+int h2o_evict_insert_policy(void* k_cache, void* v_cache, float* scores, int32_t* token_pos,
+                            const void* k_new, const void* v_new, const float* wsum,
+                            int32_t* evict_idx, int B, int Hkv, int M, int T, int d, int k,
+                            int32_t pos0, int dtype, int policy, void* workspace,
+                            size_t workspace_bytes, void* stream) {
   if (dtype != H2O_F32 && dtype != H2O_BF16) return fail(H2O_EDTYPE, "dtype %d unknown", dtype);
   if (B < 1 || Hkv < 1) return fail(H2O_ESHAPE, "B, Hkv must be >= 1");
   if (d != 64 && d != 128) return fail(H2O_ESHAPE, "head dim d=%d not supported (64 or 128)", d);
@@ -369,22 +393,52 @@ int h2o_evict_insert(void* k_cache, void* v_cache, float* scores, int32_t* token
     return fail(H2O_ESHAPE, "too large");
   if (!k_cache || !v_cache || !scores || !k_new || !v_new || !wsum || !evict_idx)
     return fail(H2O_EINVAL, "null tensor pointer");
-  const void* ptrs[] = {k_cache, v_cache, scores, token_pos, k_new, v_new, wsum, evict_idx};
+  if (policy != H2O_POLICY_H2O && policy != H2O_POLICY_NORM && policy != H2O_POLICY_ORIG)
+    return fail(H2O_EINVAL, "policy %d unknown", policy);
+  if (policy == H2O_POLICY_NORM && !token_pos)
+    return fail(H2O_EINVAL, "h2o_norm needs token_pos (the slot ages)");
+  const size_t need = evict_workspace(B, Hkv, M, k, policy);
+  if (workspace_bytes < need)
+    return fail(H2O_EWORKSPACE, "workspace %zu bytes, need %zu", workspace_bytes, need);
+  if (need > 0 && !workspace) return fail(H2O_EINVAL, "null workspace");
+  const void* ptrs[] = {k_cache, v_cache, scores, token_pos, k_new, v_new, wsum, evict_idx,
+                        workspace};
   for (const void* p : ptrs)
     if (p && !aligned16(p)) return fail(H2O_EALIGN, "tensor pointer not 16-byte aligned");
   int rc = check_device();
   if (rc) return rc;
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  const int eb = dtype == H2O_F32 ? 4 : 2;
-  hipError_t e;
-  if (k == 1) {
-    e = launch_argmin_insert(k_cache, v_cache, scores, token_pos, k_new, v_new, wsum, evict_idx,
-                             B * Hkv, M, T, d, pos0, eb, st);
-  } else {
-    e = launch_bottomk(scores, B * Hkv, M, k, evict_idx, st);
+  const int eb = dtype == H2O_F32 ? 4 : 2, rows = B * Hkv;
+  // The ranked keys: the scores themselves, or the policy's keys in the
+  // workspace (h2o_orig: one row per kv head, shared by the batch).
+  const float* keys = scores;
+  int key_rows = 0;
+  float* wk = reinterpret_cast<float*>(workspace);
+  hipError_t e = hipSuccess;
+  if (policy == H2O_POLICY_NORM) {
+    e = launch_norm_keys(scores, token_pos, wk, rows, M, pos0 + T, st);
+    keys = wk;
+  } else if (policy == H2O_POLICY_ORIG) {
+    e = launch_orig_keys(scores, wk, B, Hkv, M, st);
+    keys = wk;
+    key_rows = Hkv;
+  }
+  if (e == hipSuccess && k == 1) {
+    e = launch_argmin_insert(k_cache, v_cache, scores, keys, key_rows, token_pos, k_new, v_new,
+                             wsum, evict_idx, rows, M, T, d, pos0, eb, st);
+  } else if (e == hipSuccess && policy == H2O_POLICY_ORIG) {
+    int32_t* head_idx = reinterpret_cast<int32_t*>(
+        reinterpret_cast<char*>(workspace) + align256((size_t)Hkv * M * 4));
+    e = launch_bottomk(keys, Hkv, M, k, head_idx, st);
+    if (e == hipSuccess) e = launch_broadcast_rows(head_idx, evict_idx, B, Hkv * k, st);
     if (e == hipSuccess)
       e = launch_insert(k_cache, v_cache, scores, token_pos, k_new, v_new, wsum, evict_idx,
-                        B * Hkv, M, T, d, k, pos0, eb, st);
+                        rows, M, T, d, k, pos0, eb, st);
+  } else if (e == hipSuccess) {
+    e = launch_bottomk(keys, rows, M, k, evict_idx, st);
+    if (e == hipSuccess)
+      e = launch_insert(k_cache, v_cache, scores, token_pos, k_new, v_new, wsum, evict_idx,
+                        rows, M, T, d, k, pos0, eb, st);
   }
   if (e != hipSuccess) return fail(H2O_ELAUNCH, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();

@@ -91,7 +91,7 @@ bool decode_supports(int d, int G);   // (d, G) pairs the decode kernels handle
 enum KernelId {
   K_GENERIC_LSE = 0, K_GENERIC_MAIN, K_MFMA_LSE, K_MFMA_MAIN, K_SPLIT_REDUCE, K_COLSUM_REDUCE,
   K_ACCUMULATE, K_BOTTOMK, K_INSERT, K_DECODE_SPLIT, K_DECODE_COMBINE, K_ARGMIN_INSERT,
-  K_DECODE_FINISH, K_COUNT
+  K_DECODE_FINISH, K_KEYS, K_COUNT
 };
 // While timing is switched on (h2o_debug_timing), kernels go out through
 // hipExtLaunchKernel with a start and a stop event: the runtime stamps them
@@ -140,10 +140,18 @@ hipError_t launch_accumulate(float* scores, const float* wsum, int rows, int M, 
                              hipStream_t st);
 hipError_t launch_bottomk(const float* scores, int rows, int M, int k, int32_t* idx,
                           hipStream_t st);
-hipError_t launch_argmin_insert(void* kc, void* vc, float* scores, int32_t* token_pos,
-                                const void* kn, const void* vn, const float* wsum, int32_t* idx,
-                                int rows, int M, int T, int d, int32_t pos0, int elem_bytes,
-                                hipStream_t st);
+hipError_t launch_argmin_insert(void* kc, void* vc, float* scores, const float* keys,
+                                int key_rows, int32_t* token_pos, const void* kn, const void* vn,
+                                const float* wsum, int32_t* idx, int rows, int M, int T, int d,
+                                int32_t pos0, int elem_bytes, hipStream_t st);
+// Score variants: the ranked keys (h2o_norm per row, h2o_orig per kv head)
+// and the broadcast of one index row per kv head over the batch.
+hipError_t launch_norm_keys(const float* scores, const int32_t* token_pos, float* keys, int rows,
+                            int M, int32_t t, hipStream_t st);
+hipError_t launch_orig_keys(const float* scores, float* keys, int B, int Hkv, int M,
+                            hipStream_t st);
+hipError_t launch_broadcast_rows(const int32_t* src, int32_t* dst, int B, int n,
+                                 hipStream_t st);
 hipError_t launch_insert(void* kc, void* vc, float* scores, int32_t* token_pos,
                          const void* kn, const void* vn, const float* wsum,
                          const int32_t* idx, int rows, int M, int T, int d, int k,

@@ -176,16 +176,19 @@ __global__ __launch_bounds__(kInsThreads) void insert_kernel(
 // the insert into it, one block per row.
 constexpr int kArgThreads = 256;
 
+// The ranked values come from `keys` (the scores themselves, or a score
+// variant), row `row` or, with key_rows > 0, row `row % key_rows` (one key
+// row shared by the batch).
 __global__ __launch_bounds__(kArgThreads) void argmin_insert_kernel(
-    uint4* __restrict__ kc, uint4* __restrict__ vc, float* __restrict__ scores,
-    int32_t* __restrict__ token_pos, const uint4* __restrict__ kn, const uint4* __restrict__ vn,
-    const float* __restrict__ wsum, int32_t* __restrict__ idx, int M, int T, int vecs,
-    int32_t pos0) {
+    uint4* __restrict__ kc, uint4* __restrict__ vc, float* scores, const float* keys,
+    int key_rows, int32_t* __restrict__ token_pos, const uint4* __restrict__ kn,
+    const uint4* __restrict__ vn, const float* __restrict__ wsum, int32_t* __restrict__ idx,
+    int M, int T, int vecs, int32_t pos0) {
   __shared__ uint32_t red_hi[kArgThreads / 64], red_lo[kArgThreads / 64];
   __shared__ int sh_slot;
   const size_t row = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const float* s = scores + row * M;
+  const float* s = keys + (key_rows > 0 ? row % key_rows : row) * M;
   uint32_t bk = 0xFFFFFFFFu, bj = 0xFFFFFFFFu;     // (key, slot), lexicographic
   // four independent loads per step; slots are visited in increasing order
   // per thread, so a strict < keeps the lowest slot among equal keys
@@ -233,14 +236,83 @@ __global__ __launch_bounds__(kArgThreads) void argmin_insert_kernel(
 
 }  // namespace
 
-hipError_t launch_argmin_insert(void* kc, void* vc, float* scores, int32_t* token_pos,
-                                const void* kn, const void* vn, const float* wsum, int32_t* idx,
-                                int rows, int M, int T, int d, int32_t pos0, int elem_bytes,
-                                hipStream_t st) {
+hipError_t launch_argmin_insert(void* kc, void* vc, float* scores, const float* keys,
+                                int key_rows, int32_t* token_pos, const void* kn, const void* vn,
+                                const float* wsum, int32_t* idx, int rows, int M, int T, int d,
+                                int32_t pos0, int elem_bytes, hipStream_t st) {
   if (rows == 0) return hipSuccess;
   return launch_kernel(K_ARGMIN_INSERT, argmin_insert_kernel, dim3(rows), dim3(kArgThreads), st,
-                       (uint4*)kc, (uint4*)vc, scores, token_pos, (const uint4*)kn,
-                       (const uint4*)vn, wsum, idx, M, T, d * elem_bytes / 16, pos0);
+                       (uint4*)kc, (uint4*)vc, scores, keys, key_rows, token_pos,
+                       (const uint4*)kn, (const uint4*)vn, wsum, idx, M, T,
+                       d * elem_bytes / 16, pos0);
+}
+
+// ------------------------------------------------------- score variants
+// h2o_norm: keys = scores / (t - token_pos), one correctly rounded float32
+// division per slot (the age is exact in float32 below 2^24). n = rows * M.
+__global__ __launch_bounds__(256) void norm_keys_kernel(const float* __restrict__ scores,
+                                                        const int32_t* __restrict__ token_pos,
+                                                        float* __restrict__ keys, size_t n,
+                                                        int32_t t) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (size_t)gridDim.x * blockDim.x)
+    keys[i] = scores[i] / (float)(t - token_pos[i]);
+}
+
+// h2o_orig: keys[h, j] = sum over b of scores[b, h, j], float32 additions in
+// increasing b. n = Hkv * M, the size of one batch entry's scores.
+__global__ __launch_bounds__(256) void orig_keys_kernel(const float* __restrict__ scores,
+                                                        float* __restrict__ keys, int B,
+                                                        size_t n) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (size_t)gridDim.x * blockDim.x) {
+    float a = scores[i];
+    for (int b = 1; b < B; ++b) a += scores[(size_t)b * n + i];
+    keys[i] = a;
+  }
+}
+
+// dst[b, :] = src[:] for every b (n = Hkv * k indices per batch entry).
+__global__ __launch_bounds__(256) void broadcast_rows_kernel(const int32_t* __restrict__ src,
+                                                             int32_t* __restrict__ dst, int B,
+                                                             size_t n) {
+  const size_t total = (size_t)B * n;
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+       i += (size_t)gridDim.x * blockDim.x)
+    dst[i] = src[i % n];
+}
+
+namespace {
+// Grid of an elementwise pass over n items: 256 threads, at most 4096 blocks
+// (16 per CU), grid-stride beyond that.
+unsigned flat_blocks(size_t n) {
+  const size_t b = (n + 255) / 256;
+  return (unsigned)(b < 4096 ? b : 4096);
+}
+}  // namespace
+
+hipError_t launch_norm_keys(const float* scores, const int32_t* token_pos, float* keys, int rows,
+                            int M, int32_t t, hipStream_t st) {
+  const size_t n = (size_t)rows * M;
+  if (n == 0) return hipSuccess;
+  return launch_kernel(K_KEYS, norm_keys_kernel, dim3(flat_blocks(n)), dim3(256), st, scores,
+                       token_pos, keys, n, t);
+}
+
+hipError_t launch_orig_keys(const float* scores, float* keys, int B, int Hkv, int M,
+                            hipStream_t st) {
+  const size_t n = (size_t)Hkv * M;
+  if (n == 0) return hipSuccess;
+  return launch_kernel(K_KEYS, orig_keys_kernel, dim3(flat_blocks(n)), dim3(256), st, scores,
+                       keys, B, n);
+}
+
+hipError_t launch_broadcast_rows(const int32_t* src, int32_t* dst, int B, int n,
+                                 hipStream_t st) {
+  const size_t total = (size_t)B * n;
+  if (total == 0) return hipSuccess;
+  return launch_kernel(K_KEYS, broadcast_rows_kernel, dim3(flat_blocks(total)), dim3(256), st,
+                       src, dst, B, (size_t)n);
 }
 
 hipError_t launch_colsum_reduce(const Shape& s, const Plan& p, const float* parts, float* wsum,

@@ -23,12 +23,15 @@ H2O_F32, H2O_BF16 = 0, 1
 STATUS_NAMES = ["H2O_OK", "H2O_EINVAL", "H2O_ESHAPE", "H2O_EDTYPE", "H2O_EALIGN",
                 "H2O_EWORKSPACE", "H2O_ENODEVICE", "H2O_ELAUNCH"]
 EXPORTED = ["h2o_workspace_bytes", "h2o_sdpa_chunk", "h2o_accumulate_scores",
-            "h2o_evict_insert", "h2o_chunk_step", "h2o_bottomk", "h2o_last_error", "h2o_debug_force_path",
+            "h2o_evict_insert", "h2o_evict_workspace_bytes", "h2o_evict_insert_policy",
+            "h2o_chunk_step", "h2o_bottomk", "h2o_last_error", "h2o_debug_force_path",
             "h2o_debug_timing", "h2o_debug_kernel_time", "h2o_version"]
 KERNEL_IDS = {"generic_lse": 0, "generic_main": 1, "mfma_lse": 2, "mfma_main": 3,
               "split_reduce": 4, "colsum_reduce": 5, "accumulate": 6, "bottomk": 7,
               "insert": 8, "decode_split": 9, "decode_combine": 10,
-              "argmin_insert": 11, "decode_finish": 12}
+              "argmin_insert": 11, "decode_finish": 12, "variant_keys": 13}
+# eviction rankings (Sec. "Variants of Heavy-Hitter Oracle"), as h2o_policy
+POLICIES = {"h2o": 0, "h2o_norm": 1, "h2o_orig": 2}
 
 
 class H2OError(RuntimeError):
@@ -59,6 +62,11 @@ def lib() -> ctypes.CDLL:
     L.h2o_accumulate_scores.restype = i
     L.h2o_evict_insert.argtypes = [vp] * 8 + [i] * 6 + [ctypes.c_int32, i, vp]
     L.h2o_evict_insert.restype = i
+    L.h2o_evict_workspace_bytes.argtypes = [i] * 5
+    L.h2o_evict_workspace_bytes.restype = sz
+    L.h2o_evict_insert_policy.argtypes = [vp] * 8 + [i] * 6 + [ctypes.c_int32, i, i, vp, sz,
+                                                               vp]
+    L.h2o_evict_insert_policy.restype = i
     L.h2o_chunk_step.argtypes = [vp] * 12 + [sz] + [i] * 6 + [f, ctypes.c_int32, i, vp]
     L.h2o_chunk_step.restype = i
     L.h2o_bottomk.argtypes = [vp, i, i, i, vp, vp]
@@ -176,9 +184,7 @@ def h2o_accumulate_scores(scores, wsum, stream=None) -> None:
                                        B, Hkv, M, T, _stream(stream)))
 
 
-def h2o_evict_insert(k_cache, v_cache, scores, token_pos, k_new, v_new, wsum, evict_idx,
-                     pos0: int, stream=None) -> None:
-    """Bottom-k eviction of the accumulated scores and insert of the chunk."""
+def _evict_args(k_cache, v_cache, scores, token_pos, k_new, v_new, wsum, evict_idx):
     B, Hkv, M, d = k_cache.shape
     T = k_new.shape[2]
     k = evict_idx.shape[2]
@@ -198,11 +204,42 @@ def h2o_evict_insert(k_cache, v_cache, scores, token_pos, k_new, v_new, wsum, ev
     if token_pos is not None and (token_pos.dtype != torch.int32 or
                                   tuple(token_pos.shape) != (B, Hkv, M)):
         raise ValueError("token_pos must be int32 [B,Hkv,M]")
-    _check(lib().h2o_evict_insert(
-        _dev(k_cache, "k_cache"), _dev(v_cache, "v_cache"), _dev(scores, "scores"),
-        _dev(token_pos, "token_pos"), _dev(k_new, "k_new"), _dev(v_new, "v_new"),
-        _dev(wsum, "wsum"), _dev(evict_idx, "evict_idx"), B, Hkv, M, T, d, k, int(pos0), dt,
-        _stream(stream)))
+    ptrs = (_dev(k_cache, "k_cache"), _dev(v_cache, "v_cache"), _dev(scores, "scores"),
+            _dev(token_pos, "token_pos"), _dev(k_new, "k_new"), _dev(v_new, "v_new"),
+            _dev(wsum, "wsum"), _dev(evict_idx, "evict_idx"))
+    return ptrs, (B, Hkv, M, T, d, k), dt
+
+
+def h2o_evict_insert(k_cache, v_cache, scores, token_pos, k_new, v_new, wsum, evict_idx,
+                     pos0: int, stream=None) -> None:
+    """Bottom-k eviction of the accumulated scores and insert of the chunk."""
+    ptrs, sizes, dt = _evict_args(k_cache, v_cache, scores, token_pos, k_new, v_new, wsum,
+                                  evict_idx)
+    _check(lib().h2o_evict_insert(*ptrs, *sizes, int(pos0), dt, _stream(stream)))
+
+
+def _policy_code(policy) -> int:
+    if isinstance(policy, str):
+        if policy not in POLICIES:
+            raise ValueError(f"unknown policy {policy!r}")
+        return POLICIES[policy]
+    return int(policy)
+
+
+def h2o_evict_workspace_bytes(B, Hkv, M, k, policy) -> int:
+    return int(lib().h2o_evict_workspace_bytes(B, Hkv, M, k, _policy_code(policy)))
+
+
+def h2o_evict_insert_policy(k_cache, v_cache, scores, token_pos, k_new, v_new, wsum,
+                            evict_idx, pos0: int, policy, workspace=None, stream=None) -> None:
+    """h2o_evict_insert with the ranking of ``policy`` ("h2o", "h2o_norm",
+    "h2o_orig"); workspace is a uint8 tensor of h2o_evict_workspace_bytes()."""
+    ptrs, sizes, dt = _evict_args(k_cache, v_cache, scores, token_pos, k_new, v_new, wsum,
+                                  evict_idx)
+    nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().h2o_evict_insert_policy(*ptrs, *sizes, int(pos0), dt, _policy_code(policy),
+                                         _dev(workspace, "workspace"), nbytes,
+                                         _stream(stream)))
 
 
 def h2o_chunk_step(q, k_cache, v_cache, scores, token_pos, k_new, v_new, out, lse, wsum,
@@ -256,11 +293,14 @@ def h2o_bottomk(scores, k: int, idx_out, stream=None) -> None:
 
 
 # ------------------------------------------------------------ conveniences
-def alloc_step(B, Hq, Hkv, T, M, d, dtype, device="cuda"):
-    """Output and scratch tensors for one h2o_sdpa_chunk call."""
+def alloc_step(B, Hq, Hkv, T, M, d, dtype, device="cuda", policy="h2o"):
+    """Output and scratch tensors for one chunk step (``policy``'s eviction
+    workspace included)."""
     code = _dtype_code(torch.empty(0, dtype=dtype))
     ws = h2o_workspace_bytes(B, Hq, Hkv, T, M, d, code)
+    ews = h2o_evict_workspace_bytes(B, Hkv, M, T, policy)
     return dict(
+        evict_workspace=torch.empty(max(ews, 16), dtype=torch.uint8, device=device),
         out=torch.empty(B, Hq, T, d, dtype=dtype, device=device),
         lse=torch.empty(B, Hq, T, dtype=torch.float32, device=device),
         wsum=torch.empty(B, Hkv, M + T, dtype=torch.float32, device=device),
@@ -270,12 +310,23 @@ def alloc_step(B, Hq, Hkv, T, M, d, dtype, device="cuda"):
 
 
 def step(state, q, k_new, v_new, bufs, pos0: int, scale=None, stream=None,
-         fused: bool = True) -> None:
+         fused: bool = True, policy: str = "h2o") -> None:
     """One chunk step in place: attend, accumulate, evict + insert, through
-    h2o_chunk_step (``fused``) or the three separate calls.
+    h2o_chunk_step (``fused``, the h2o ranking) or the three separate calls
+    (the eviction ranks by ``policy``).
 
-    ``state`` holds k_cache, v_cache, scores, token_pos (token_pos may be None).
+    ``state`` holds k_cache, v_cache, scores, token_pos (token_pos may be None
+    except for h2o_norm).
     """
+    if policy != "h2o":
+        h2o_sdpa_chunk(q, state["k_cache"], state["v_cache"], k_new, v_new, bufs["out"],
+                       bufs["lse"], bufs["wsum"], bufs["workspace"], scale, stream)
+        h2o_accumulate_scores(state["scores"], bufs["wsum"], stream)
+        h2o_evict_insert_policy(state["k_cache"], state["v_cache"], state["scores"],
+                                state.get("token_pos"), k_new, v_new, bufs["wsum"],
+                                bufs["evict_idx"], pos0, policy, bufs["evict_workspace"],
+                                stream)
+        return
     if fused:
         h2o_chunk_step(q, state["k_cache"], state["v_cache"], state["scores"],
                        state.get("token_pos"), k_new, v_new, bufs["out"], bufs["lse"],

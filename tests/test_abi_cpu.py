@@ -111,6 +111,42 @@ def test_evict_rejects(L, kw, code):
     assert _evict(L, **kw) == code
 
 
+def _evict_policy(L, **kw):
+    a = dict(kc=P, vc=P, sc=P, tp=P, kn=P, vn=P, w=P, idx=P, B=2, Hkv=2, M=16, T=4, d=64, k=4,
+             pos0=16, dt=1, pol=1, ws=P, wsb=1 << 20, st=None)
+    a.update(kw)
+    return L.h2o_evict_insert_policy(a["kc"], a["vc"], a["sc"], a["tp"], a["kn"], a["vn"],
+                                     a["w"], a["idx"], a["B"], a["Hkv"], a["M"], a["T"], a["d"],
+                                     a["k"], a["pos0"], a["dt"], a["pol"], a["ws"], a["wsb"],
+                                     a["st"])
+
+
+def test_evict_workspace_bytes(L):
+    # h2o: none; norm: B*Hkv*M floats; orig: Hkv*M floats + Hkv*k indices (256-B sections)
+    assert L.h2o_evict_workspace_bytes(2, 2, 16, 4, 0) == 0
+    assert L.h2o_evict_workspace_bytes(2, 2, 1000, 4, 1) == 16128
+    assert L.h2o_evict_workspace_bytes(2, 2, 1000, 4, 2) == 8192 + 256
+    assert L.h2o_evict_workspace_bytes(2, 2, 16, 4, 7) == 0
+    assert L.h2o_evict_workspace_bytes(0, 2, 16, 4, 1) == 0
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(pol=3), H.H2O_EINVAL),
+    (dict(pol=-1), H.H2O_EINVAL),
+    (dict(pol=1, tp=None), H.H2O_EINVAL),
+    (dict(pol=1, wsb=64), H.H2O_EWORKSPACE),
+    (dict(pol=2, wsb=64), H.H2O_EWORKSPACE),
+    (dict(pol=2, ws=None), H.H2O_EINVAL),
+    (dict(pol=1, ws=MIS), H.H2O_EALIGN),
+    (dict(pol=2, k=3), H.H2O_EINVAL),
+    (dict(pol=1, dt=5), H.H2O_EDTYPE),
+    (dict(pol=2, sc=None), H.H2O_EINVAL),
+])
+def test_evict_policy_rejects(L, kw, code):
+    assert _evict_policy(L, **kw) == code
+    assert len(L.h2o_last_error()) > 0
+
+
 def _step(L, **kw):
     a = dict(q=P, kc=P, vc=P, sc=P, tp=P, kn=P, vn=P, out=P, lse=P, w=P, idx=P, ws=P,
              wsb=1 << 40, B=1, Hq=4, Hkv=2, T=4, M=16, d=64, scale=0.125, pos0=16, dt=1, st=None)
@@ -167,6 +203,10 @@ def test_no_device_is_reported(L):
     assert L.h2o_bottomk(P, 4, 10, 3, P, None) == H.H2O_ENODEVICE
     assert L.h2o_accumulate_scores(P, P, 1, 2, 8, 1, None) == H.H2O_ENODEVICE
     assert _step(L) == H.H2O_ENODEVICE
+    for pol in (0, 1, 2):
+        assert _evict_policy(L, pol=pol) == H.H2O_ENODEVICE
+    assert _evict_policy(L, pol=0, ws=None, wsb=0) == H.H2O_ENODEVICE
+    assert _evict_policy(L, pol=2, tp=None) == H.H2O_ENODEVICE
 
 
 def test_binding_raises_typed_errors(L):

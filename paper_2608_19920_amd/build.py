@@ -27,11 +27,13 @@ FLAGS = [
     # packed FP32 VALU ops are left out of the device code on purpose
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
 ]
-# Per-source additions. The decode kernels keep their MFMA accumulators in
-# VGPRs: they are rescaled by VALU code, and AGPR accumulators would be copied
-# back and forth every step.
+# Per-source additions. The MFMA kernels keep their accumulators in VGPRs:
+# the scores are read by VALU code every tile, and AGPR accumulators would be
+# copied back and forth. The prefill kernels never see a NaN (masked scores
+# are -inf), so max() needs no NaN quieting.
 FILE_FLAGS = {
     "decode.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+    "sdpa_mfma.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form", "-fno-honor-nans"],
 }
 
 

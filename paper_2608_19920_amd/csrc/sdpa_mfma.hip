@@ -210,9 +210,10 @@ __device__ __forceinline__ void split_range(int ntiles, int nsplit, int sp, int&
 
 // Tiles are software pipelined over three LDS buffers: while the softmax
 // arithmetic of tile t runs, the MFMAs of S(t+1) are issued from the buffer
-// already holding tile t+1, and the global loads of tile t+2 are in flight;
-// tile t+2 then goes to the buffer tile t-1 used. One barrier per tile orders
-// the buffer reuse. Tiles whose columns some row of the block cannot see run
+// already holding tile t+1, the rows of tile t+2 (loaded one tile earlier)
+// go from registers to the buffer tile t-1 used, and the global loads of
+// tile t+3 are issued into a second register set. One barrier per tile
+// orders the buffer reuse. Tiles whose columns some row of the block cannot see run
 // in a second loop with the causal mask applied; each loop body is straight
 // line so the compiler can interleave MFMA and VALU work.
 constexpr int NBUF = 3;
@@ -297,12 +298,39 @@ __device__ __forceinline__ void lse_update(const f32x4 (&sacc)[2][NQB], float (&
   }
 }
 
+// Loop state of pass A. At the start of tile t: sa holds S(t), and ka holds
+// the global rows of tile t+2, loaded but not yet written to LDS; kb is free.
 template <int D, int NT, int NQB>
 struct LseState {
-  f32x4 s_cur[2][NQB], s_nxt[2][NQB];
-  u32x4 pk[Tile<D, NT>::N];
+  f32x4 sa[2][NQB], sb[2][NQB];
+  u32x4 ka[Tile<D, NT>::N], kb[Tile<D, NT>::N];
 };
 
+// One tile of pass A: the loads of tile t+3 go to `fill` while the MFMAs of
+// S(t+1) and the update with S(t) run; then tile t+2 (in `put`) goes to the
+// LDS buffer tile t-1 used. The loads of tile t+3 are waited for only one
+// tile later.
+template <bool MASKED, int D, int NT, int NQB>
+__device__ __forceinline__ void lse_tile(int t, int t0, int t1, const f32x4 (&s_cur)[2][NQB],
+                                         f32x4 (&s_nxt)[2][NQB], u32x4 (&fill)[Tile<D, NT>::N],
+                                         const u32x4 (&put)[Tile<D, NT>::N],
+                                         const Tile<D, NT>& tl, bf16_t (*Ks)[BN * kstride(D)],
+                                         const bf16x8 (&qf)[NQB][D / 32], float (&m)[NQB],
+                                         float (&l)[NQB], const int (&qi)[NQB],
+                                         const bf16_t* kc_bh, const bf16_t* kn_bh, const Geo& g,
+                                         int lane, float c) {
+  const int b1 = (t + 1 - t0) % NBUF, b2 = (t + 2 - t0) % NBUF;
+  load_tile<D, NT>(fill, tl, kc_bh, kn_bh, min(t + 3, t1 - 1) * BN, g.M, g.Nk);
+  scores_tile<D, NQB>(s_nxt, Ks[b1], qf, lane);
+  lse_update<MASKED, NQB>(s_cur, m, l, qi, t * BN, g.M, lane, c);
+  interleave<2 * NQB * (D / 32), MASKED ? 8 : 5>();
+  store_tile<D, NT>(Ks[b2], tl.loff, put);
+  __syncthreads();
+}
+
+// Tiles [ta, tb): two tiles per trip with the roles of the register sets
+// swapped, so no accumulator or staging register is copied; an odd last
+// tile restores the state invariant with one copy.
 template <bool MASKED, int D, int NT, int NQB>
 __device__ __forceinline__ void lse_loop(int ta, int tb, int t0, int t1, LseState<D, NT, NQB>& S,
                                          const Tile<D, NT>& tl,
@@ -311,19 +339,22 @@ __device__ __forceinline__ void lse_loop(int ta, int tb, int t0, int t1, LseStat
                                          float (&l)[NQB], const int (&qi)[NQB],
                                          const bf16_t* kc_bh, const bf16_t* kn_bh, const Geo& g,
                                          int lane, float c) {
-  for (int t = ta; t < tb; ++t) {
-    const int j0 = t * BN;
-    const int b1 = (t + 1 - t0) % NBUF, b2 = (t + 2 - t0) % NBUF;
-    load_tile<D, NT>(S.pk, tl, kc_bh, kn_bh, min(t + 2, t1 - 1) * BN, g.M, g.Nk);
-    scores_tile<D, NQB>(S.s_nxt, Ks[b1], qf, lane);
-    lse_update<MASKED, NQB>(S.s_cur, m, l, qi, j0, g.M, lane, c);
-    interleave<2 * NQB * (D / 32), MASKED ? 8 : 5>();
-    store_tile<D, NT>(Ks[b2], tl.loff, S.pk);
-    __syncthreads();
+  int t = ta;
+  for (; t + 1 < tb; t += 2) {
+    lse_tile<MASKED, D, NT, NQB>(t, t0, t1, S.sa, S.sb, S.kb, S.ka, tl, Ks, qf, m, l, qi, kc_bh,
+                                 kn_bh, g, lane, c);
+    lse_tile<MASKED, D, NT, NQB>(t + 1, t0, t1, S.sb, S.sa, S.ka, S.kb, tl, Ks, qf, m, l, qi,
+                                 kc_bh, kn_bh, g, lane, c);
+  }
+  if (t < tb) {
+    lse_tile<MASKED, D, NT, NQB>(t, t0, t1, S.sa, S.sb, S.kb, S.ka, tl, Ks, qf, m, l, qi, kc_bh,
+                                 kn_bh, g, lane, c);
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int qb = 0; qb < NQB; ++qb) S.s_cur[kb][qb] = S.s_nxt[kb][qb];
+      for (int qb = 0; qb < NQB; ++qb) S.sa[kb][qb] = S.sb[kb][qb];
+#pragma unroll
+    for (int e = 0; e < Tile<D, NT>::N; ++e) S.ka[e] = S.kb[e];
   }
 }
 
@@ -359,12 +390,13 @@ __global__ __launch_bounds__(NW * 64) void lse_pass(Geo g, int Hq, int Hkv, int 
   LseState<D, NT, NQB> S;
   const Tile<D, NT> tl;
   if (t0 < t1) {
-    load_tile<D, NT>(S.pk, tl, kc_bh, kn_bh, t0 * BN, g.M, g.Nk);
-    store_tile<D, NT>(Ks[0], tl.loff, S.pk);
-    load_tile<D, NT>(S.pk, tl, kc_bh, kn_bh, min(t0 + 1, t1 - 1) * BN, g.M, g.Nk);
-    store_tile<D, NT>(Ks[1], tl.loff, S.pk);
+    load_tile<D, NT>(S.ka, tl, kc_bh, kn_bh, t0 * BN, g.M, g.Nk);
+    load_tile<D, NT>(S.kb, tl, kc_bh, kn_bh, min(t0 + 1, t1 - 1) * BN, g.M, g.Nk);
+    store_tile<D, NT>(Ks[0], tl.loff, S.ka);
+    store_tile<D, NT>(Ks[1], tl.loff, S.kb);
+    load_tile<D, NT>(S.ka, tl, kc_bh, kn_bh, min(t0 + 2, t1 - 1) * BN, g.M, g.Nk);
     __syncthreads();
-    scores_tile<D, NQB>(S.s_cur, Ks[0], qf, lane);
+    scores_tile<D, NQB>(S.sa, Ks[0], qf, lane);
     lse_loop<false, D, NT, NQB>(t0, t_mask, t0, t1, S, tl, Ks, qf, m, l, qi, kc_bh, kn_bh, g, lane,
                                 c_log2);
     lse_loop<true, D, NT, NQB>(t_mask, t1, t0, t1, S, tl, Ks, qf, m, l, qi, kc_bh, kn_bh, g, lane,
@@ -431,16 +463,53 @@ __device__ __forceinline__ void pv_tile(f32x4 (&oacc)[D / 16][NQB], const bf16x8
   }
 }
 
+// Loop state of pass B, with the invariant of pass A: at the start of tile t,
+// sa holds S(t) and (ka, va) the rows of tile t+2 not yet in LDS.
 template <int D, int NT, int NQB>
 struct MainState {
-  f32x4 s_cur[2][NQB], s_nxt[2][NQB];
+  f32x4 sa[2][NQB], sb[2][NQB];
   f32x4 oacc[D / 16][NQB];
-  u32x4 pk[Tile<D, NT>::N], pv[Tile<D, NT>::N];
+  u32x4 ka[Tile<D, NT>::N], va[Tile<D, NT>::N], kb[Tile<D, NT>::N], vb[Tile<D, NT>::N];
 };
 
-// The waves' column partials of a tile meet in cs_lds[tile parity][wave];
-// after the tile's barrier, threads 0..BN-1 add them in wave order and store
-// the block's partial row (one partial per block and row tile).
+// One tile of pass B. The waves' column partials of the tile meet in
+// cs_lds[tile parity][wave]; after the tile's barrier, threads 0..BN-1 add
+// them in wave order and store the block's partial row (one partial per
+// block and row tile).
+template <bool MASKED, int D, int NT, int NQB>
+__device__ __forceinline__ void main_tile(
+    int t, int t0, int t1, const f32x4 (&s_cur)[2][NQB], f32x4 (&s_nxt)[2][NQB],
+    f32x4 (&oacc)[D / 16][NQB], u32x4 (&kfill)[Tile<D, NT>::N],
+    u32x4 (&vfill)[Tile<D, NT>::N], const u32x4 (&kput)[Tile<D, NT>::N],
+    const u32x4 (&vput)[Tile<D, NT>::N], const Tile<D, NT>& tl, bf16_t (*Ks)[BN * kstride(D)],
+    bf16_t (*Vs)[BN * vstride(D)], const bf16x8 (&qf)[NQB][D / 32], const float (&lam)[NQB],
+    const int (&qi)[NQB], float (*cs_lds)[NT / 64][BN], float* prow, const bf16_t* kc_bh,
+    const bf16_t* kn_bh, const bf16_t* vc_bh, const bf16_t* vn_bh, const Geo& g, int lane,
+    float c) {
+  const int wave = threadIdx.x >> 6;
+  const int j0 = t * BN;
+  const int b0 = (t - t0) % NBUF, b1 = (t + 1 - t0) % NBUF, b2 = (t + 2 - t0) % NBUF;
+  const int jn = min(t + 3, t1 - 1) * BN;
+  load_tile<D, NT>(kfill, tl, kc_bh, kn_bh, jn, g.M, g.Nk);
+  load_tile<D, NT>(vfill, tl, vc_bh, vn_bh, jn, g.M, g.Nk);
+  bf16x8 pb[NQB];
+  scores_tile<D, NQB>(s_nxt, Ks[b1], qf, lane);
+  probs_tile<MASKED, NQB>(s_cur, pb, lam, qi, cs_lds[(t - t0) & 1][wave], j0, g.M, lane, c);
+  pv_tile<D, NQB>(oacc, pb, Vs[b0], lane);
+  interleave<2 * NQB * (D / 32), MASKED ? 5 : 4>();
+  interleave<NQB * (D / 16), 1>();
+  store_tile<D, NT>(Ks[b2], tl.loff, kput);
+  store_tile<D, NT>(Vs[b2], tl.vloff, vput);
+  __syncthreads();
+  if (threadIdx.x < BN) {
+    const float (*cs)[BN] = cs_lds[(t - t0) & 1];
+    float a = cs[0][threadIdx.x];
+#pragma unroll
+    for (int w = 1; w < NT / 64; ++w) a += cs[w][threadIdx.x];
+    prow[j0 + threadIdx.x] = a;
+  }
+}
+
 template <bool MASKED, int D, int NT, int NQB>
 __device__ __forceinline__ void main_loop(int ta, int tb, int t0, int t1, MainState<D, NT, NQB>& S,
                                           const Tile<D, NT>& tl,
@@ -452,33 +521,28 @@ __device__ __forceinline__ void main_loop(int ta, int tb, int t0, int t1, MainSt
                                           const bf16_t* kc_bh, const bf16_t* kn_bh,
                                           const bf16_t* vc_bh, const bf16_t* vn_bh, const Geo& g,
                                           int lane, float c) {
-  const int wave = threadIdx.x >> 6;
-  for (int t = ta; t < tb; ++t) {
-    const int j0 = t * BN;
-    const int b0 = (t - t0) % NBUF, b1 = (t + 1 - t0) % NBUF, b2 = (t + 2 - t0) % NBUF;
-    const int jn = min(t + 2, t1 - 1) * BN;
-    load_tile<D, NT>(S.pk, tl, kc_bh, kn_bh, jn, g.M, g.Nk);
-    load_tile<D, NT>(S.pv, tl, vc_bh, vn_bh, jn, g.M, g.Nk);
-    bf16x8 pb[NQB];
-    scores_tile<D, NQB>(S.s_nxt, Ks[b1], qf, lane);
-    probs_tile<MASKED, NQB>(S.s_cur, pb, lam, qi, cs_lds[(t - t0) & 1][wave], j0, g.M, lane, c);
-    pv_tile<D, NQB>(S.oacc, pb, Vs[b0], lane);
-    interleave<2 * NQB * (D / 32), MASKED ? 5 : 4>();
-    interleave<NQB * (D / 16), 1>();
-    store_tile<D, NT>(Ks[b2], tl.loff, S.pk);
-    store_tile<D, NT>(Vs[b2], tl.vloff, S.pv);
-    __syncthreads();
-    if (threadIdx.x < BN) {
-      const float (*cs)[BN] = cs_lds[(t - t0) & 1];
-      float a = cs[0][threadIdx.x];
-#pragma unroll
-      for (int w = 1; w < NT / 64; ++w) a += cs[w][threadIdx.x];
-      prow[j0 + threadIdx.x] = a;
-    }
+  int t = ta;
+  for (; t + 1 < tb; t += 2) {
+    main_tile<MASKED, D, NT, NQB>(t, t0, t1, S.sa, S.sb, S.oacc, S.kb, S.vb, S.ka, S.va, tl, Ks,
+                                  Vs, qf, lam, qi, cs_lds, prow, kc_bh, kn_bh, vc_bh, vn_bh, g,
+                                  lane, c);
+    main_tile<MASKED, D, NT, NQB>(t + 1, t0, t1, S.sb, S.sa, S.oacc, S.ka, S.va, S.kb, S.vb, tl,
+                                  Ks, Vs, qf, lam, qi, cs_lds, prow, kc_bh, kn_bh, vc_bh, vn_bh,
+                                  g, lane, c);
+  }
+  if (t < tb) {
+    main_tile<MASKED, D, NT, NQB>(t, t0, t1, S.sa, S.sb, S.oacc, S.kb, S.vb, S.ka, S.va, tl, Ks,
+                                  Vs, qf, lam, qi, cs_lds, prow, kc_bh, kn_bh, vc_bh, vn_bh, g,
+                                  lane, c);
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int qb = 0; qb < NQB; ++qb) S.s_cur[kb][qb] = S.s_nxt[kb][qb];
+      for (int qb = 0; qb < NQB; ++qb) S.sa[kb][qb] = S.sb[kb][qb];
+#pragma unroll
+    for (int e = 0; e < Tile<D, NT>::N; ++e) {
+      S.ka[e] = S.kb[e];
+      S.va[e] = S.vb[e];
+    }
   }
 }
 
@@ -547,17 +611,19 @@ __global__ __launch_bounds__(NW * 64) void main_pass(Geo g, int Hq, int Hkv, int
   const Tile<D, NT> tl;
 
   if (t0 < t1) {
-    load_tile<D, NT>(S.pk, tl, kc_bh, kn_bh, t0 * BN, g.M, g.Nk);
-    load_tile<D, NT>(S.pv, tl, vc_bh, vn_bh, t0 * BN, g.M, g.Nk);
-    store_tile<D, NT>(Ks[0], tl.loff, S.pk);
-    store_tile<D, NT>(Vs[0], tl.vloff, S.pv);
-    const int j1 = min(t0 + 1, t1 - 1) * BN;
-    load_tile<D, NT>(S.pk, tl, kc_bh, kn_bh, j1, g.M, g.Nk);
-    load_tile<D, NT>(S.pv, tl, vc_bh, vn_bh, j1, g.M, g.Nk);
-    store_tile<D, NT>(Ks[1], tl.loff, S.pk);
-    store_tile<D, NT>(Vs[1], tl.vloff, S.pv);
+    const int j1 = min(t0 + 1, t1 - 1) * BN, j2 = min(t0 + 2, t1 - 1) * BN;
+    load_tile<D, NT>(S.ka, tl, kc_bh, kn_bh, t0 * BN, g.M, g.Nk);
+    load_tile<D, NT>(S.va, tl, vc_bh, vn_bh, t0 * BN, g.M, g.Nk);
+    load_tile<D, NT>(S.kb, tl, kc_bh, kn_bh, j1, g.M, g.Nk);
+    load_tile<D, NT>(S.vb, tl, vc_bh, vn_bh, j1, g.M, g.Nk);
+    store_tile<D, NT>(Ks[0], tl.loff, S.ka);
+    store_tile<D, NT>(Vs[0], tl.vloff, S.va);
+    store_tile<D, NT>(Ks[1], tl.loff, S.kb);
+    store_tile<D, NT>(Vs[1], tl.vloff, S.vb);
+    load_tile<D, NT>(S.ka, tl, kc_bh, kn_bh, j2, g.M, g.Nk);
+    load_tile<D, NT>(S.va, tl, vc_bh, vn_bh, j2, g.M, g.Nk);
     __syncthreads();
-    scores_tile<D, NQB>(S.s_cur, Ks[0], qf, lane);
+    scores_tile<D, NQB>(S.sa, Ks[0], qf, lane);
     main_loop<false, D, NT, NQB>(t0, t_mask, t0, t1, S, tl, Ks, Vs, qf, lam, qi, cs_lds, prow,
                                  kc_bh, kn_bh,
                                  vc_bh, vn_bh, g, lane, c_log2);

@@ -69,12 +69,13 @@ __device__ __forceinline__ float colsum16(float a0, float a1, float a2, float a3
 }
 
 #ifndef H2O_KPAD
-#define H2O_KPAD 8
+#define H2O_KPAD 16
 #endif
 #ifndef H2O_VPAD
 #define H2O_VPAD 16
 #endif
-// bf16 per LDS row of the K and V tiles (row pitch 272 / 288 bytes at d=128)
+// bf16 per LDS row of the K and V tiles (row pitch 288 bytes at d=128; both
+// pitches make the operand reads and the tile stores free of bank conflicts)
 __host__ __device__ constexpr int kstride(int D) { return D + H2O_KPAD; }
 __host__ __device__ constexpr int vstride(int D) { return D + H2O_VPAD; }
 
@@ -429,10 +430,6 @@ __device__ __forceinline__ void probs_tile(const f32x4 (&sacc)[2][NQB], bf16x8 (
                                            float* cs_row, int j0, int M, int lane, float c) {
   float cs[2][4];
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) cs[kb][r] = 0.f;
-#pragma unroll
   for (int qb = 0; qb < NQB; ++qb) {
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -440,7 +437,7 @@ __device__ __forceinline__ void probs_tile(const f32x4 (&sacc)[2][NQB], bf16x8 (
       for (int r = 0; r < 4; ++r) {
         float p = __builtin_amdgcn_exp2f(fmaf(sacc[kb][qb][r], c, -lam[qb]));
         if (MASKED && !visible(j0 + kb * 16 + 4 * (lane >> 4) + r, M, qi[qb])) p = 0.f;
-        cs[kb][r] += p;
+        cs[kb][r] = qb == 0 ? p : cs[kb][r] + p;
         pb[qb][kb * 4 + r] = (__bf16)p;
       }
   }

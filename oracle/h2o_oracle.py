@@ -33,6 +33,11 @@ time, with numpy float64 matrix products as the only library primitive:
    goes to the i-th smallest evicted slot, its score starts at its own summed
    weight from this chunk, its token position is pos0 + i.
 
+The paper's own ordering of a chunk step (Sec. "Discussion: SDPA Kernels for
+Sparse Attention") writes the chunk into the cache first and masks by token
+position: ``sdpa_cache`` and ``h2o_step_insert_first`` below compute that
+variant by the same plain definitions.
+
 Readings of points the paper leaves open are listed in the repository's design
 notes; the ones that change results are repeated at the functions below.
 """
@@ -228,6 +233,109 @@ def h2o_step(k_cache, v_cache, scores, token_pos, q, k_new, v_new, pos0: int,
                                        k_new, v_new, wsum, T, pos0, policy)
     return dict(out=out, lse=lse, wsum=wsum, scores_acc=acc, evict_idx=idx,
                 k_cache=kc, v_cache=vc, scores=sc, token_pos=tp)
+
+
+# ------------------------------------- the paper's order: insert, then attend
+def visible_by_position(token_pos_bh, pos0: int, T: int) -> np.ndarray:
+    """Boolean [T, M]: may query i (token position pos0 + i) attend slot j?
+
+    The causal mask of sparse attention (Sec. "Discussion: SDPA Kernels for
+    Sparse Attention"): -inf * 1{P + i < t(b,h,j)} with P = pos0 and
+    t(b,h,j) the token position stored for the slot, so the slot is visible
+    iff t(b,h,j) <= pos0 + i.
+    """
+    tp = np.asarray(token_pos_bh, np.int64)
+    return tp[None, :] <= pos0 + np.arange(T)[:, None]
+
+
+def _head_masked(Qh: np.ndarray, K: np.ndarray, V: np.ndarray, allowed: np.ndarray,
+                 scale: float) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """``_head`` for an arbitrary mask. A row that sees no key has no softmax:
+    its output is 0, its lambda is -inf and it adds nothing to the column
+    sums."""
+    A = scale * (Qh @ K.T)
+    A = np.where(allowed, A, -np.inf)
+    some = allowed.any(axis=1)
+    amax = np.where(some, A.max(axis=1), 0.0)[:, None]
+    with np.errstate(divide="ignore"):
+        lam = amax[:, 0] + np.log(np.exp(A - amax).sum(axis=1))
+    Mw = np.where(some[:, None], np.exp(A - np.where(some, lam, 0.0)[:, None]), 0.0)
+    return Mw @ V, lam, Mw.sum(axis=0)
+
+
+def sdpa_cache(q, k_cache, v_cache, token_pos, pos0: int, scale: Optional[float] = None,
+               heads: Optional[Iterable[Tuple[int, int]]] = None):
+    """Attention of T queries (positions pos0 .. pos0+T-1) over the M cache
+    slots alone, masked by the slots' token positions (``visible_by_position``);
+    the chunk's own keys are expected in the cache already.
+
+    Shapes: q [B,Hq,T,d]; k_cache, v_cache [B,Hkv,M,d]; token_pos [B,Hkv,M].
+    Returns float64 (out [B,Hq,T,d], lse [B,Hq,T], wsum [B,Hkv,M]), wsum summed
+    over the group's query heads as in ``sdpa_chunk``; ``heads`` as there.
+    """
+    q = np.asarray(q)
+    B, Hq, T, d = q.shape
+    Hkv, M = k_cache.shape[1], k_cache.shape[2]
+    if Hq % Hkv:
+        raise ValueError("Hq must be a multiple of Hkv")
+    G = Hq // Hkv
+    if scale is None:
+        scale = 1.0 / np.sqrt(d)
+    scale = float(scale)
+    out = np.full((B, Hq, T, d), np.nan, F64)
+    lse = np.full((B, Hq, T), np.nan, F64)
+    wsum = np.full((B, Hkv, M), np.nan, F64)
+    if heads is None:
+        heads = [(b, h) for b in range(B) for h in range(Hkv)]
+    for b, h in heads:
+        allowed = visible_by_position(token_pos[b, h], pos0, T)
+        K = np.asarray(k_cache[b, h], F64)
+        V = np.asarray(v_cache[b, h], F64)
+        acc = np.zeros(M, F64)
+        for g in range(G):
+            hq = h * G + g
+            Y, lam, col = _head_masked(q[b, hq].astype(F64), K, V, allowed, scale)
+            out[b, hq] = Y
+            lse[b, hq] = lam
+            acc += col
+        wsum[b, h] = acc
+    return out, lse, wsum
+
+
+def h2o_step_insert_first(k_cache, v_cache, scores, token_pos, q, k_new, v_new,
+                          pos0: int, scale: Optional[float] = None, policy: str = "h2o"):
+    """One chunk step in the paper's order (Sec. "Sparse Attention. Key-Value
+    Caching" with the mask of Sec. "Discussion: SDPA Kernels for Sparse
+    Attention"):
+
+    1. rank the slots by the scores after ``pos0`` tokens (t = pos0 for
+       h2o_norm) and pick the T lowest (``bottomk``; h2o_orig: one set per
+       kv-head);
+    2. write chunk key/value i into the i-th picked slot, with token position
+       pos0 + i and score 0 (Eq. h2o-score sums from the slot's own position);
+    3. attend over the M slots with the token-position mask (``sdpa_cache``);
+    4. add the summed weights to the scores of all M slots (one float32
+       addition each).
+    """
+    T = q.shape[2]
+    keys = selection_keys(scores, token_pos, policy, pos0)
+    idx = bottomk(keys, T)
+    if policy == "h2o_orig":
+        idx = np.broadcast_to(idx, (k_cache.shape[0],) + idx.shape).copy()
+    kc, vc = k_cache.copy(), v_cache.copy()
+    sc = np.asarray(scores, np.float32).copy()
+    tp = np.asarray(token_pos, np.int32).copy()
+    B, H = sc.shape[0], sc.shape[1]
+    for b in range(B):
+        for h in range(H):
+            e = idx[b, h]
+            kc[b, h, e] = k_new[b, h]
+            vc[b, h, e] = v_new[b, h]
+            sc[b, h, e] = 0.0
+            tp[b, h, e] = pos0 + np.arange(T, dtype=np.int32)
+    out, lse, wsum = sdpa_cache(q, kc, vc, tp, pos0, scale)
+    return dict(out=out, lse=lse, wsum=wsum, evict_idx=idx, scores_inserted=sc,
+                k_cache=kc, v_cache=vc, scores=accumulate_scores(sc, wsum), token_pos=tp)
 
 
 def decode(k_cache, v_cache, scores, token_pos, q_steps, k_new_steps,

@@ -192,3 +192,62 @@ def brute_bottomk(scores, k):
         keyed = sorted((float(row[j]) + 0.0, j) for j in range(M))
         res.append(sorted(j for _, j in keyed[:k]))
     return np.array(res, np.int32).reshape(*s.shape[:-1], k)
+
+
+def brute_sdpa_positions(q, kc, vc, tp, pos0, scale):
+    """Attention over the cache slots masked by token position, by loops:
+    query i (position pos0 + i) sees slot j iff tp[b,h,j] <= pos0 + i. A
+    query that sees nothing gets out 0 and lse -inf. Returns float64
+    (out, lse, wsum [B,Hkv,M]); tiny shapes only."""
+    B, Hq, T, d = q.shape
+    Hkv, M = kc.shape[1], kc.shape[2]
+    G = Hq // Hkv
+    out = np.zeros((B, Hq, T, d))
+    lse = np.zeros((B, Hq, T))
+    wsum = np.zeros((B, Hkv, M))
+    for b in range(B):
+        for h in range(Hkv):
+            col_terms = [[] for _ in range(M)]
+            for g in range(G):
+                hq = h * G + g
+                for i in range(T):
+                    cols = [j for j in range(M) if int(tp[b, h, j]) <= pos0 + i]
+                    if not cols:
+                        lse[b, hq, i] = -math.inf
+                        continue
+                    qi = [float(x) for x in q[b, hq, i]]
+                    a = {j: float(scale) * math.fsum(qi[c] * float(kc[b, h, j, c])
+                                                     for c in range(d)) for j in cols}
+                    Z = math.fsum(math.exp(a[j]) for j in cols)
+                    lse[b, hq, i] = math.log(Z)
+                    for c in range(d):
+                        out[b, hq, i, c] = math.fsum(math.exp(a[j]) / Z * float(vc[b, h, j, c])
+                                                     for j in cols)
+                    for j in cols:
+                        col_terms[j].append(math.exp(a[j]) / Z)
+            for j in range(M):
+                wsum[b, h, j] = math.fsum(col_terms[j])
+    return out, lse, wsum
+
+
+def torch_sdpa_positions(q, kc, vc, tp, pos0, scale):
+    """Output and lse via torch's SDPA (float64, CPU) with the boolean mask
+    built from token positions; every row must see at least one slot."""
+    F = torch.nn.functional
+    B, Hq, T, d = q.shape
+    Hkv = kc.shape[1]
+    G = Hq // Hkv
+    out = np.zeros((B, Hq, T, d))
+    lse = np.zeros((B, Hq, T))
+    pos = torch.arange(T, dtype=torch.int64)[:, None] + int(pos0)
+    for b in range(B):
+        for h in range(Hkv):
+            mask = torch.from_numpy(np.asarray(tp[b, h], np.int64))[None, :] <= pos
+            K = torch.from_numpy(np.asarray(kc[b, h], np.float64))
+            V = torch.from_numpy(np.asarray(vc[b, h], np.float64))
+            for g in range(G):
+                Q = torch.from_numpy(np.asarray(q[b, h * G + g], np.float64))
+                out[b, h * G + g] = F.scaled_dot_product_attention(
+                    Q[None], K[None], V[None], attn_mask=mask[None], scale=float(scale))[0].numpy()
+                lse[b, h * G + g] = _lse_torch(Q, K, mask, float(scale)).numpy()
+    return out, lse

@@ -491,3 +491,157 @@ def test_variant_mistakes_are_caught(monkeypatch):
             m.setattr(oracle, "selection_keys", fn)
             with pytest.raises(AssertionError):
                 test()
+
+
+# ------------------------------------------- the paper's order: insert first
+def _position_state(B, Hq, Hkv, d, M, T, seed, pos0=500, dtype="f32"):
+    """A cache whose slots hold tokens before pos0, except T slots (scattered)
+    that hold the chunk at positions pos0 .. pos0+T-1, in slot order."""
+    rng = np.random.default_rng(seed)
+    x = _inputs(B, Hq, Hkv, d, M, T, seed=seed, dtype=dtype)
+    tp = rng.integers(0, pos0, size=(B, Hkv, M)).astype(np.int32)
+    ev = np.stack([np.stack([np.sort(rng.choice(M, T, replace=False)) for _ in range(Hkv)])
+                   for _ in range(B)])
+    kc, vc = x["k_cache"].copy(), x["v_cache"].copy()
+    for b in range(B):
+        for h in range(Hkv):
+            kc[b, h, ev[b, h]] = x["k_new"][b, h]
+            vc[b, h, ev[b, h]] = x["v_new"][b, h]
+            tp[b, h, ev[b, h]] = pos0 + np.arange(T)
+    return x, kc, vc, tp, ev, pos0
+
+
+@pytest.mark.parametrize("shape", [(1, 2, 1, 4, 6, 2), (2, 4, 2, 5, 9, 3), (1, 3, 3, 8, 5, 5)])
+def test_sdpa_cache_brute_force(shape):
+    """Brute force with arbitrary (non-monotone, repeated, future) positions,
+    including query rows that see no slot at all."""
+    B, Hq, Hkv, d, M, T = shape
+    rng = np.random.default_rng(sum(shape))
+    x = _inputs(*shape, seed=1)
+    pos0 = 10
+    tp = rng.integers(pos0 - 3, pos0 + T + 2, size=(B, Hkv, M)).astype(np.int32)
+    tp[0, 0, :] = pos0 + 1                 # head (0, 0): query 0 sees nothing
+    o, l, w = oracle.sdpa_cache(x["q"], x["k_cache"], x["v_cache"], tp, pos0, x["scale"])
+    bo, bl, bw = P.brute_sdpa_positions(x["q"], x["k_cache"], x["v_cache"], tp, pos0, x["scale"])
+    np.testing.assert_allclose(o, bo, rtol=1e-12, atol=1e-13)
+    np.testing.assert_array_equal(np.isneginf(l), np.isneginf(bl))
+    fin = np.isfinite(bl)
+    np.testing.assert_allclose(l[fin], bl[fin], rtol=1e-13, atol=1e-13)
+    np.testing.assert_allclose(w, bw, rtol=1e-12, atol=1e-13)
+    assert np.isneginf(l[0, 0, 0]) and not np.any(o[0, 0, 0])
+
+
+@pytest.mark.parametrize("shape", [(2, 6, 2, 16, 40, 9), (1, 8, 2, 32, 130, 17)])
+def test_sdpa_cache_torch(shape):
+    x, kc, vc, tp, _, pos0 = _position_state(*shape, seed=5, dtype="bf16")
+    o, l, _ = oracle.sdpa_cache(x["q"], kc, vc, tp, pos0, x["scale"])
+    to, tl = P.torch_sdpa_positions(x["q"], kc, vc, tp, pos0, x["scale"])
+    np.testing.assert_allclose(o, to, rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(l, tl, rtol=1e-13)
+
+
+@pytest.mark.parametrize("shape", [(1, 2, 1, 8, 12, 3), (2, 8, 2, 16, 50, 7)])
+def test_sdpa_cache_is_attention_over_cache_minus_chunk_slots_then_chunk(shape):
+    """With the chunk written into slots E and every other slot older than the
+    chunk, the position mask is the attend-over-[cache || chunk] rule of
+    ``sdpa_chunk`` applied to the slots outside E followed by the chunk: same
+    outputs, and the summed weights map slot for slot."""
+    B, Hq, Hkv, d, M, T = shape
+    x, kc, vc, tp, ev, pos0 = _position_state(*shape, seed=9)
+    o, l, w = oracle.sdpa_cache(x["q"], kc, vc, tp, pos0, x["scale"])
+    for b in range(B):
+        for h in range(Hkv):
+            keep = np.setdiff1d(np.arange(M), ev[b, h])
+            sub = lambda a: a[b:b + 1, h:h + 1]
+            G = Hq // Hkv
+            qs = x["q"][b:b + 1, h * G:(h + 1) * G]
+            co, cl, cw = oracle.sdpa_chunk(qs, sub(kc)[:, :, keep], sub(vc)[:, :, keep],
+                                           sub(x["k_new"]), sub(x["v_new"]), x["scale"])
+            np.testing.assert_allclose(o[b, h * G:(h + 1) * G], co[0], rtol=1e-12, atol=1e-13)
+            np.testing.assert_allclose(l[b, h * G:(h + 1) * G], cl[0], rtol=1e-13)
+            np.testing.assert_allclose(w[b, h, keep], cw[0, 0, :len(keep)], rtol=1e-12,
+                                       atol=1e-14)
+            np.testing.assert_allclose(w[b, h, ev[b, h]], cw[0, 0, len(keep):], rtol=1e-12,
+                                       atol=1e-14)
+
+
+def test_sdpa_cache_slot_permutation():
+    x, kc, vc, tp, _, pos0 = _position_state(2, 4, 2, 8, 20, 4, seed=2)
+    perm = np.random.default_rng(0).permutation(20)
+    o, l, w = oracle.sdpa_cache(x["q"], kc, vc, tp, pos0, x["scale"])
+    po, pl, pw = oracle.sdpa_cache(x["q"], kc[:, :, perm], vc[:, :, perm], tp[:, :, perm], pos0,
+                                   x["scale"])
+    np.testing.assert_allclose(po, o, rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(pl, l, rtol=1e-13)
+    np.testing.assert_allclose(pw, w[:, :, perm], rtol=1e-12, atol=1e-14)
+
+
+@pytest.mark.parametrize("policy", ["h2o", "h2o_norm", "h2o_orig"])
+def test_insert_first_step_bookkeeping(policy):
+    """The evicted slots are the bottom T of the ranking before the chunk
+    (t = pos0); they hold the chunk with positions pos0+i and score 0 + their
+    own summed weight; all other slots add their summed weight; every query
+    sees its own key, so the weights sum to T*G."""
+    B, Hq, Hkv, d, M, T = 2, 4, 2, 8, 30, 5
+    x = _inputs(B, Hq, Hkv, d, M, T, seed=4)
+    rng = np.random.default_rng(4)
+    tp = rng.integers(0, 400, size=(B, Hkv, M)).astype(np.int32)
+    pos0 = 400
+    r = oracle.h2o_step_insert_first(x["k_cache"], x["v_cache"], x["scores"], tp, x["q"],
+                                     x["k_new"], x["v_new"], pos0, x["scale"], policy)
+    s0 = np.asarray(x["scores"], np.float32)
+    if policy == "h2o":
+        keys = s0
+    elif policy == "h2o_norm":
+        keys = (s0 / (pos0 - tp).astype(np.float32)).astype(np.float32)
+    else:
+        keys = s0.sum(axis=0, dtype=np.float32)[None].repeat(B, 0)
+    w32 = r["wsum"].astype(np.float32)
+    G = Hq // Hkv
+    for b in range(B):
+        for h in range(Hkv):
+            ref = np.sort(np.lexsort((np.arange(M), keys[b, h].astype(np.float64)))[:T])
+            e = r["evict_idx"][b, h]
+            np.testing.assert_array_equal(e, ref)
+            np.testing.assert_array_equal(r["token_pos"][b, h, e], pos0 + np.arange(T))
+            np.testing.assert_array_equal(r["k_cache"][b, h, e], x["k_new"][b, h])
+            np.testing.assert_array_equal(r["scores"][b, h, e], w32[b, h, e])
+            keep = np.setdiff1d(np.arange(M), e)
+            np.testing.assert_array_equal(r["scores"][b, h, keep], s0[b, h, keep] + w32[b, h, keep])
+            assert abs(r["wsum"][b, h].sum() - T * G) < 1e-11
+            # query i sees exactly the slots older than the chunk and chunk keys <= i
+            assert np.all(r["wsum"][b, h, e[1:]] <= G * (T - np.arange(1, T)) + 1e-12)
+
+
+def test_insert_first_mistakes_are_caught(monkeypatch):
+    """A strict inequality in the position mask, a shifted P, or scores that are
+    not reset when a slot is overwritten, each fail a pin above."""
+    orig_vis, orig_step = O.visible_by_position, O.h2o_step_insert_first
+
+    def strict(tp, pos0, T):
+        return np.asarray(tp, np.int64)[None, :] < pos0 + np.arange(T)[:, None]
+
+    def shifted(tp, pos0, T):
+        return orig_vis(tp, pos0 + 1, T)
+
+    def no_reset(k_cache, v_cache, scores, token_pos, q, k_new, v_new, pos0, scale=None,
+                 policy="h2o"):
+        r = orig_step(k_cache, v_cache, scores, token_pos, q, k_new, v_new, pos0, scale, policy)
+        s = np.asarray(scores, np.float32)
+        for b in range(s.shape[0]):
+            for h in range(s.shape[1]):
+                e = r["evict_idx"][b, h]
+                r["scores"][b, h, e] = s[b, h, e] + r["wsum"][b, h, e].astype(np.float32)
+        return r
+
+    cases = [("visible_by_position", strict, lambda: test_sdpa_cache_brute_force((1, 2, 1, 4, 6, 2))),
+             ("visible_by_position", shifted,
+              lambda: test_sdpa_cache_is_attention_over_cache_minus_chunk_slots_then_chunk(
+                  (1, 2, 1, 8, 12, 3))),
+             ("h2o_step_insert_first", no_reset, lambda: test_insert_first_step_bookkeeping("h2o"))]
+    for name, fn, test in cases:
+        with monkeypatch.context() as m:
+            m.setattr(O, name, fn)
+            m.setattr(oracle, name, fn)
+            with pytest.raises(AssertionError):
+                test()

@@ -176,6 +176,53 @@ int h2o_chunk_step(const void* q, void* k_cache, void* v_cache, float* scores,
                    int Hkv, int T, int M, int d, float scale, int32_t pos0,
                    int dtype, void* stream);
 
+/* ---- The paper's order of a chunk step: insert, then attend (Sec.
+ * "Discussion: SDPA Kernels for Sparse Attention"). The chunk is written into
+ * the cache first and the attention masks each slot by its token position:
+ * slot j is visible to chunk query i iff token_pos[b,h,j] <= pos0 + i (the
+ * causal mask of sparse attention, -inf * 1{P + i < t(b,h,j)} with P = pos0),
+ * for any int32 positions, monotone or not. */
+
+/* Bytes of device scratch for h2o_sdpa_cache (policy H2O_POLICY_H2O) or for
+ * h2o_chunk_step_insert_first with `policy` (0 on invalid arguments). */
+size_t h2o_cache_workspace_bytes(int B, int Hq, int Hkv, int T, int M, int d,
+                                 int dtype, int policy);
+
+/* Attention of T queries (token positions pos0 .. pos0+T-1) over the M >= 1
+ * cache slots alone, masked by token_pos [B,Hkv,M] (int32, read only):
+ *   out[b,hq,i,:] = sum_j m_{i,j} v_cache[b,h,j,:] over visible slots j,
+ *   lse[b,hq,i]   = log sum_{visible j} exp(s_{i,j}),
+ *   wsum[b,h,j]   = sum_{hq in group h} sum_i m_{i,j}   ([B,Hkv,M], written)
+ * with s_{i,j} as in h2o_sdpa_chunk. A query that sees no slot gets out 0
+ * and lse -inf and adds nothing to wsum. Other arguments, precision and
+ * errors as for h2o_sdpa_chunk; workspace of h2o_cache_workspace_bytes(...,
+ * H2O_POLICY_H2O). */
+int h2o_sdpa_cache(const void* q, const void* k_cache, const void* v_cache,
+                   const int32_t* token_pos, void* out, float* lse, float* wsum,
+                   void* workspace, size_t workspace_bytes, int B, int Hq, int Hkv,
+                   int T, int M, int d, float scale, int32_t pos0, int dtype,
+                   void* stream);
+
+/* One chunk step in the paper's order (Sec. "Sparse Attention. Key-Value
+ * Caching", the mask of Sec. "Discussion: SDPA Kernels for Sparse
+ * Attention"), M >= T:
+ *   1. E = the T slots ranked lowest by `policy` (an h2o_policy) on the
+ *      scores after pos0 tokens (h2o_norm: ages pos0 - token_pos, which must
+ *      lie in [1, 2^24)), in ascending slot order, into evict_idx [B,Hkv,T];
+ *   2. chunk key/value i goes to slot E[i], with token_pos pos0 + i and
+ *      score 0 (Eq. h2o-score sums from the slot's own position);
+ *   3. h2o_sdpa_cache over the updated cache (out, lse, wsum [B,Hkv,M]);
+ *   4. scores[b,h,j] += wsum[b,h,j] for all M slots (one float32 addition).
+ * token_pos is required. Workspace of h2o_cache_workspace_bytes(..., policy);
+ * its contents on entry are ignored. */
+int h2o_chunk_step_insert_first(const void* q, void* k_cache, void* v_cache,
+                                float* scores, int32_t* token_pos,
+                                const void* k_new, const void* v_new, void* out,
+                                float* lse, float* wsum, int32_t* evict_idx,
+                                void* workspace, size_t workspace_bytes, int B,
+                                int Hq, int Hkv, int T, int M, int d, float scale,
+                                int32_t pos0, int dtype, int policy, void* stream);
+
 /* The selection of h2o_evict_insert alone: for each of `rows` rows of M
  * float32 scores, the k smallest by (score, index), ascending indices, into
  * idx_out [rows, k]. 0 <= k <= M. */

@@ -190,45 +190,98 @@ Plan make_plan(const Shape& s, int dtype) {
 namespace {
 
 // Validation shared by the entry points that run the attention; fills *plan.
+// In cache mode (token_pos non-null) the chunk's keys are in the cache:
+// k_new and v_new are not read, and M >= 1.
 int check_sdpa(const void* q, const void* k_cache, const void* v_cache, const void* k_new,
                const void* v_new, const void* out, const float* lse, const float* wsum,
                const void* workspace, size_t workspace_bytes, int B, int Hq, int Hkv, int T,
-               int M, int d, float scale, int dtype, Plan* plan) {
+               int M, int d, float scale, int dtype, Plan* plan,
+               const int32_t* token_pos = nullptr, size_t extra_bytes = 0) {
+  const bool cache = token_pos != nullptr;
   if (dtype != H2O_F32 && dtype != H2O_BF16) return fail(H2O_EDTYPE, "dtype %d unknown", dtype);
   int rc = check_shape(B, Hq, Hkv, T, M, d);
   if (rc) return rc;
-  if (!q || !k_new || !v_new || !out || !lse || !wsum || (M > 0 && (!k_cache || !v_cache)))
+  if (cache && M < 1) return fail(H2O_EINVAL, "cache length M must be >= 1");
+  if (!q || !out || !lse || !wsum || (!cache && (!k_new || !v_new)) ||
+      (M > 0 && (!k_cache || !v_cache)))
     return fail(H2O_EINVAL, "null tensor pointer");
   if (!(std::isfinite(scale) && scale > 0.f)) return fail(H2O_EINVAL, "scale must be finite > 0");
-  const void* ptrs[] = {q, k_new, v_new, out, lse, wsum, workspace};
+  const void* ptrs[] = {q, out, lse, wsum, workspace, token_pos,
+                        cache ? nullptr : k_new, cache ? nullptr : v_new};
   for (const void* p : ptrs)
     if (p && !aligned16(p)) return fail(H2O_EALIGN, "tensor pointer not 16-byte aligned");
   if (M > 0 && (!aligned16(k_cache) || !aligned16(v_cache)))
     return fail(H2O_EALIGN, "cache pointer not 16-byte aligned");
-  const Shape s{B, Hq, Hkv, T, M, d};
+  const Shape s{B, Hq, Hkv, T, M, d, cache};
   *plan = make_plan(s, dtype);
-  if (workspace_bytes < plan->bytes || (plan->bytes > 0 && !workspace))
-    return fail(H2O_EWORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes,
-                plan->bytes);
+  const size_t need = align256(plan->bytes) + extra_bytes;
+  if (workspace_bytes < need || (need > 0 && !workspace))
+    return fail(H2O_EWORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, need);
   return H2O_OK;
 }
 
 hipError_t launch_sdpa(const Shape& s, const Plan& p, int dtype, const void* q,
                        const void* k_cache, const void* v_cache, const void* k_new,
                        const void* v_new, void* out, float* lse, float* wsum, void* workspace,
-                       float scale, hipStream_t st) {
+                       float scale, hipStream_t st, KeyPos kp = KeyPos{nullptr, 0}) {
   char* ws = reinterpret_cast<char*>(workspace);
   switch (p.path) {
     case 1:
       return launch_sdpa_mfma(s, p, q, k_cache, v_cache, k_new, v_new, out, lse, wsum, ws,
-                              scale, st);
+                              scale, kp, st);
     case 2:
       return launch_sdpa_decode(s, p, q, k_cache, v_cache, k_new, v_new, out, lse, wsum, ws,
-                                scale, st);
+                                scale, kp, st);
     default:
       return launch_sdpa_generic(s, p, dtype, q, k_cache, v_cache, k_new, v_new, out, lse,
-                                 wsum, ws, scale, st);
+                                 wsum, ws, scale, kp, st);
   }
+}
+
+// Validation of the eviction arguments shared by the entry points that evict.
+int check_policy(int policy, const int32_t* token_pos) {
+  if (policy != H2O_POLICY_H2O && policy != H2O_POLICY_NORM && policy != H2O_POLICY_ORIG)
+    return fail(H2O_EINVAL, "policy %d unknown", policy);
+  if (policy == H2O_POLICY_NORM && !token_pos)
+    return fail(H2O_EINVAL, "h2o_norm needs token_pos (the slot ages)");
+  return H2O_OK;
+}
+
+// Ranking of `policy` (norm ages against t), bottom-k and insert of the
+// chunk; the inserted slots take score wsum[row, M+i] (row pitch M+T), or 0
+// when wsum is nullptr. ews is the policy's workspace (evict_workspace()).
+hipError_t launch_evict(int policy, void* k_cache, void* v_cache, float* scores,
+                        int32_t* token_pos, const void* k_new, const void* v_new,
+                        const float* wsum, int32_t* evict_idx, int B, int Hkv, int M, int T,
+                        int d, int k, int32_t pos0, int32_t t, int eb, char* ews,
+                        hipStream_t st) {
+  const int rows = B * Hkv;
+  const float* keys = scores;
+  int key_rows = 0;
+  float* wk = reinterpret_cast<float*>(ews);
+  hipError_t e = hipSuccess;
+  if (policy == H2O_POLICY_NORM) {
+    e = launch_norm_keys(scores, token_pos, wk, rows, M, t, st);
+    keys = wk;
+  } else if (policy == H2O_POLICY_ORIG) {
+    e = launch_orig_keys(scores, wk, B, Hkv, M, st);
+    keys = wk;
+    key_rows = Hkv;
+  }
+  if (e != hipSuccess) return e;
+  if (k == 1)
+    return launch_argmin_insert(k_cache, v_cache, scores, keys, key_rows, token_pos, k_new,
+                                v_new, wsum, evict_idx, rows, M, T, d, pos0, eb, st);
+  if (policy == H2O_POLICY_ORIG) {
+    int32_t* head_idx = reinterpret_cast<int32_t*>(ews + align256((size_t)Hkv * M * 4));
+    e = launch_bottomk(keys, Hkv, M, k, head_idx, st);
+    if (e == hipSuccess) e = launch_broadcast_rows(head_idx, evict_idx, B, Hkv * k, st);
+  } else {
+    e = launch_bottomk(keys, rows, M, k, evict_idx, st);
+  }
+  if (e != hipSuccess) return e;
+  return launch_insert(k_cache, v_cache, scores, token_pos, k_new, v_new, wsum, evict_idx, rows,
+                       M, T, d, k, pos0, eb, st);
 }
 
 }  // namespace
@@ -393,10 +446,8 @@ int h2o_evict_insert_policy(void* k_cache, void* v_cache, float* scores, int32_t
     return fail(H2O_ESHAPE, "too large");
   if (!k_cache || !v_cache || !scores || !k_new || !v_new || !wsum || !evict_idx)
     return fail(H2O_EINVAL, "null tensor pointer");
-  if (policy != H2O_POLICY_H2O && policy != H2O_POLICY_NORM && policy != H2O_POLICY_ORIG)
-    return fail(H2O_EINVAL, "policy %d unknown", policy);
-  if (policy == H2O_POLICY_NORM && !token_pos)
-    return fail(H2O_EINVAL, "h2o_norm needs token_pos (the slot ages)");
+  int rc = check_policy(policy, token_pos);
+  if (rc) return rc;
   const size_t need = evict_workspace(B, Hkv, M, k, policy);
   if (workspace_bytes < need)
     return fail(H2O_EWORKSPACE, "workspace %zu bytes, need %zu", workspace_bytes, need);
@@ -405,41 +456,79 @@ int h2o_evict_insert_policy(void* k_cache, void* v_cache, float* scores, int32_t
                         workspace};
   for (const void* p : ptrs)
     if (p && !aligned16(p)) return fail(H2O_EALIGN, "tensor pointer not 16-byte aligned");
-  int rc = check_device();
+  rc = check_device();
   if (rc) return rc;
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  const int eb = dtype == H2O_F32 ? 4 : 2, rows = B * Hkv;
-  // The ranked keys: the scores themselves, or the policy's keys in the
-  // workspace (h2o_orig: one row per kv head, shared by the batch).
-  const float* keys = scores;
-  int key_rows = 0;
-  float* wk = reinterpret_cast<float*>(workspace);
-  hipError_t e = hipSuccess;
-  if (policy == H2O_POLICY_NORM) {
-    e = launch_norm_keys(scores, token_pos, wk, rows, M, pos0 + T, st);
-    keys = wk;
-  } else if (policy == H2O_POLICY_ORIG) {
-    e = launch_orig_keys(scores, wk, B, Hkv, M, st);
-    keys = wk;
-    key_rows = Hkv;
-  }
-  if (e == hipSuccess && k == 1) {
-    e = launch_argmin_insert(k_cache, v_cache, scores, keys, key_rows, token_pos, k_new, v_new,
-                             wsum, evict_idx, rows, M, T, d, pos0, eb, st);
-  } else if (e == hipSuccess && policy == H2O_POLICY_ORIG) {
-    int32_t* head_idx = reinterpret_cast<int32_t*>(
-        reinterpret_cast<char*>(workspace) + align256((size_t)Hkv * M * 4));
-    e = launch_bottomk(keys, Hkv, M, k, head_idx, st);
-    if (e == hipSuccess) e = launch_broadcast_rows(head_idx, evict_idx, B, Hkv * k, st);
-    if (e == hipSuccess)
-      e = launch_insert(k_cache, v_cache, scores, token_pos, k_new, v_new, wsum, evict_idx,
-                        rows, M, T, d, k, pos0, eb, st);
-  } else if (e == hipSuccess) {
-    e = launch_bottomk(keys, rows, M, k, evict_idx, st);
-    if (e == hipSuccess)
-      e = launch_insert(k_cache, v_cache, scores, token_pos, k_new, v_new, wsum, evict_idx,
-                        rows, M, T, d, k, pos0, eb, st);
-  }
+  const int eb = dtype == H2O_F32 ? 4 : 2;
+  // h2o_norm ranks after the chunk has been attended: t = pos0 + T
+  hipError_t e = launch_evict(policy, k_cache, v_cache, scores, token_pos, k_new, v_new, wsum,
+                              evict_idx, B, Hkv, M, T, d, k, pos0, pos0 + T, eb,
+                              reinterpret_cast<char*>(workspace), st);
+  if (e != hipSuccess) return fail(H2O_ELAUNCH, "kernel launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+size_t h2o_cache_workspace_bytes(int B, int Hq, int Hkv, int T, int M, int d, int dtype,
+                                 int policy) {
+  if (dtype != H2O_F32 && dtype != H2O_BF16) return 0;
+  if (check_shape(B, Hq, Hkv, T, M, d) != H2O_OK || M < 1) return 0;
+  if (policy != H2O_POLICY_H2O && policy != H2O_POLICY_NORM && policy != H2O_POLICY_ORIG)
+    return 0;
+  const Shape s{B, Hq, Hkv, T, M, d, true};
+  return align256(make_plan(s, dtype).bytes) + evict_workspace(B, Hkv, M, T, policy);
+}
+
+int h2o_sdpa_cache(const void* q, const void* k_cache, const void* v_cache,
+                   const int32_t* token_pos, void* out, float* lse, float* wsum,
+                   void* workspace, size_t workspace_bytes, int B, int Hq, int Hkv, int T, int M,
+                   int d, float scale, int32_t pos0, int dtype, void* stream) {
+  if (!token_pos) return fail(H2O_EINVAL, "null tensor pointer (token_pos)");
+  Plan p;
+  int rc = check_sdpa(q, k_cache, v_cache, nullptr, nullptr, out, lse, wsum, workspace,
+                      workspace_bytes, B, Hq, Hkv, T, M, d, scale, dtype, &p, token_pos);
+  if (!rc) rc = check_device();
+  if (rc) return rc;
+  const Shape s{B, Hq, Hkv, T, M, d, true};
+  hipError_t e = launch_sdpa(s, p, dtype, q, k_cache, v_cache, nullptr, nullptr, out, lse, wsum,
+                             workspace, scale, reinterpret_cast<hipStream_t>(stream),
+                             KeyPos{token_pos, pos0});
+  if (e != hipSuccess) return fail(H2O_ELAUNCH, "kernel launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int h2o_chunk_step_insert_first(const void* q, void* k_cache, void* v_cache, float* scores,
+                                int32_t* token_pos, const void* k_new, const void* v_new,
+                                void* out, float* lse, float* wsum, int32_t* evict_idx,
+                                void* workspace, size_t workspace_bytes, int B, int Hq, int Hkv,
+                                int T, int M, int d, float scale, int32_t pos0, int dtype,
+                                int policy, void* stream) {
+  if (!token_pos || !scores || !evict_idx || !k_new || !v_new)
+    return fail(H2O_EINVAL, "null tensor pointer");
+  if (M < T) return fail(H2O_EINVAL, "cache length M (%d) must be >= T (%d)", M, T);
+  int rc = check_policy(policy, token_pos);
+  if (rc) return rc;
+  const size_t ews_bytes = evict_workspace(B, Hkv, M, T, policy);
+  Plan p;
+  rc = check_sdpa(q, k_cache, v_cache, nullptr, nullptr, out, lse, wsum, workspace,
+                  workspace_bytes, B, Hq, Hkv, T, M, d, scale, dtype, &p, token_pos, ews_bytes);
+  if (rc) return rc;
+  if (!aligned16(scores) || !aligned16(evict_idx) || !aligned16(k_new) || !aligned16(v_new))
+    return fail(H2O_EALIGN, "tensor pointer not 16-byte aligned");
+  rc = check_device();
+  if (rc) return rc;
+  const Shape s{B, Hq, Hkv, T, M, d, true};
+  hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  char* ws = reinterpret_cast<char*>(workspace);
+  const int eb = dtype == H2O_F32 ? 4 : 2;
+  // rank by the scores after pos0 tokens, then write the chunk into the
+  // chosen slots with score 0 and positions pos0 + i
+  hipError_t e = launch_evict(policy, k_cache, v_cache, scores, token_pos, k_new, v_new, nullptr,
+                              evict_idx, B, Hkv, M, T, d, T, pos0, pos0, eb,
+                              ws + align256(p.bytes), st);
+  if (e == hipSuccess)
+    e = launch_sdpa(s, p, dtype, q, k_cache, v_cache, nullptr, nullptr, out, lse, wsum, ws,
+                    scale, st, KeyPos{token_pos, pos0});
+  if (e == hipSuccess) e = launch_accumulate(scores, wsum, B * Hkv, M, 0, st);
   if (e != hipSuccess) return fail(H2O_ELAUNCH, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
 }

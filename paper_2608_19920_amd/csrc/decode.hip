@@ -12,6 +12,10 @@
 //   combine  block bh merges the splits with the chunk's own key (column M),
 //            writes out and lse, and wsum[j] = sum_g exp2(logit_gj - lambda_g)
 //            from the stored logits.
+//
+// In cache mode the chunk's key is already in the cache: there is no column
+// M, and a slot whose token position is later than the query's (pos0) is
+// masked; its stored logit is -inf.
 #include "internal.h"
 
 namespace h2o {
@@ -81,11 +85,12 @@ __device__ __forceinline__ bf16x8 v_operand(const bf16_t* vs, int db, int lane) 
 // and V come in through buffer loads whose range is the head, so slots past
 // the cache read as zero; they are masked, and their logit stores go to a
 // sink.
-template <int D, int G>
+template <int D, int G, bool CACHE>
 __global__ __launch_bounds__(kThreads) void decode_split(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
     int Hq, int Hkv, int M, float c_log2, float* __restrict__ logits,
-    float2* __restrict__ dstat, float* __restrict__ dO, float* __restrict__ sink) {
+    float2* __restrict__ dstat, float* __restrict__ dO, float* __restrict__ sink,
+    const int32_t* __restrict__ tp, int32_t pos0) {
   constexpr int DH = D / 32;                 // MFMA k-chunks of a row
   constexpr int NK = 2 * DH;                 // K loads per step (two 16-slot blocks)
   constexpr int RPL = 512 / D;               // V rows per wave load
@@ -108,6 +113,10 @@ __global__ __launch_bounds__(kThreads) void decode_split(
   const uint32_t head_bytes = (uint32_t)M * (uint32_t)(D * 2);
   const __amdgpu_buffer_rsrc_t krs = buffer_rsrc(kc + bh * (size_t)M * D, head_bytes);
   const __amdgpu_buffer_rsrc_t vrs = buffer_rsrc(vc + bh * (size_t)M * D, head_bytes);
+  // cache mode: token positions of the head (slots past the cache read as 0;
+  // they are masked by the slot bound)
+  const __amdgpu_buffer_rsrc_t trs =
+      buffer_rsrc(CACHE ? tp + bh * (size_t)M : tp, CACHE ? (uint32_t)M * 4u : 0u);
   bf16_t* vs = vs_all[wave];
   const int vrow = lane / (D / 8), vcol = 8 * (lane % (D / 8));
   const uint32_t koff = (uint32_t)(col * D + 8 * grp) * 2u;   // + block / chunk offsets
@@ -119,8 +128,16 @@ __global__ __launch_bounds__(kThreads) void decode_split(
   // consumed, so every wait leaves the other slot's loads in flight. Steps
   // past the head read as zero (buffer range) and are masked.
   u32x4 kr[2][NK], vr[2][NV];
+  int32_t tr[2][8];
   auto issue = [&](int k, int u) {
     const uint32_t base = (uint32_t)((stream + k * nstreams) * kStep) * (uint32_t)(D * 2);
+    if (CACHE) {   // this lane's 8 slots: 4 consecutive ones per 16-slot block
+      const uint32_t tb = (uint32_t)((stream + k * nstreams) * kStep + 4 * grp) * 4u;
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        tr[u][i] = (int32_t)__builtin_amdgcn_raw_buffer_load_b32(
+            trs, (int)(tb + 64u * (i >> 2) + 4u * (i & 3)), 0, 0);
+    }
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -164,6 +181,10 @@ __global__ __launch_bounds__(kThreads) void decode_split(
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       lg[i] = sacc[i >> 2][i & 3] * c_log2;
+      if (CACHE) {
+        const int key = key0 + 16 * (i >> 2) + 4 * grp + (i & 3);
+        if (key >= M || !pos_visible(tr[u][i], pos0, 0)) lg[i] = -INFINITY;
+      }
       mx = fmaxf(mx, lg[i]);
     }
 #pragma unroll
@@ -188,7 +209,8 @@ __global__ __launch_bounds__(kThreads) void decode_split(
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const int key = key0 + 16 * (i >> 2) + 4 * grp + (i & 3);
-      const float p = key < M ? __builtin_amdgcn_exp2f(lg[i] - m) : 0.f;
+      const float p = key < M && (!CACHE || lg[i] > -INFINITY)
+                          ? __builtin_amdgcn_exp2f(lg[i] - m) : 0.f;
       l += p;
       pb[i] = (__bf16)p;
     }
@@ -255,35 +277,43 @@ struct HeadStats {
 // normaliser, 1 / normaliser and each split's weight, with wave reductions
 // (lane s holds split s; at most 64 splits). Writes lse when asked. Ends
 // synced.
+// Without the chunk key (cache mode, has_chunk false) lnew is -inf, and a
+// query that sees no slot gets lam = +inf (every weight 0), linv = 0 and
+// lse = -inf.
 template <int D, int NT>
 __device__ __forceinline__ void head_stats(HeadStats& hs, const bf16_t* q, const bf16_t* kn,
                                            const float2* dstat, int Hq, int Hkv, int G,
-                                           int nsplit, float c_log2, size_t bh, float* lse) {
+                                           int nsplit, float c_log2, size_t bh, float* lse,
+                                           bool has_chunk = true) {
   const int b = (int)(bh / Hkv), h = (int)(bh % Hkv);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   for (int g = wave; g < G; g += NT / 64) {
     const float2 st = lane < nsplit ? dstat[(bh * nsplit + lane) * G + g]
                                     : make_float2(-INFINITY, 0.f);
-    float a = 0.f;
-    for (int dd = lane; dd < D; dd += 64)
-      a = fmaf(bf16_to_f32(q[(size_t)(b * Hq + h * G + g) * D + dd]),
-               bf16_to_f32(kn[bh * D + dd]), a);
-    for (int o = 32; o > 0; o >>= 1) a += __shfl_xor(a, o, 64);
-    const float lnew = a * c_log2;
+    float lnew = -INFINITY;
+    if (has_chunk) {
+      float a = 0.f;
+      for (int dd = lane; dd < D; dd += 64)
+        a = fmaf(bf16_to_f32(q[(size_t)(b * Hq + h * G + g) * D + dd]),
+                 bf16_to_f32(kn[bh * D + dd]), a);
+      for (int o = 32; o > 0; o >>= 1) a += __shfl_xor(a, o, 64);
+      lnew = a * c_log2;
+    }
     float mx = fmaxf(lnew, st.x);
     for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
     const float wt = st.y > 0.f ? __builtin_amdgcn_exp2f(st.x - mx) : 0.f;
     float L = st.y * wt;
     for (int o = 32; o > 0; o >>= 1) L += __shfl_xor(L, o, 64);
-    L += __builtin_amdgcn_exp2f(lnew - mx);
+    if (has_chunk) L += __builtin_amdgcn_exp2f(lnew - mx);
     if (lane < nsplit) hs.wt[lane * G + g] = wt;
     if (lane == 0) {
-      const float lm = mx + __log2f(L);
+      const bool any = L > 0.f;
+      const float lm = any ? mx + __log2f(L) : INFINITY;
       hs.lnew[g] = lnew;
       hs.lam[g] = lm;
       hs.mfin[g] = mx;
-      hs.linv[g] = 1.f / L;
-      if (lse) lse[(size_t)(b * Hq + h * G + g)] = lm * kLn2;
+      hs.linv[g] = any ? 1.f / L : 0.f;
+      if (lse) lse[(size_t)(b * Hq + h * G + g)] = any ? lm * kLn2 : -INFINITY;
     }
   }
   __syncthreads();
@@ -297,7 +327,8 @@ __device__ __forceinline__ float out_elem(const HeadStats& hs, const bf16_t* vn,
                                           const float* dO, const float* pre, int G,
                                           int nsplit, size_t bh, int c) {
   const int g = c / D, dd = c % D;
-  float a = __builtin_amdgcn_exp2f(hs.lnew[g] - hs.mfin[g]) * bf16_to_f32(vn[bh * D + dd]);
+  float a = vn ? __builtin_amdgcn_exp2f(hs.lnew[g] - hs.mfin[g]) * bf16_to_f32(vn[bh * D + dd])
+               : 0.f;
 #pragma unroll
   for (int s = 0; s < PRE; ++s)
     if (s < nsplit) a = fmaf(pre[s], hs.wt[s * G + g], a);
@@ -332,7 +363,8 @@ __device__ __forceinline__ float chunk_weight(const HeadStats& hs, int G) {
 }
 
 // Block (x, bh) writes wsum for columns [x*kCols, +kCols) of head bh; block
-// x == 0 also writes out, lse and the chunk key's column.
+// x == 0 also writes out, lse and the chunk key's column (chunk mode: kn and
+// vn non-null, wsum rows of M + 1; cache mode: both null, rows of M).
 constexpr int kCols = 1024;
 
 template <int D>
@@ -344,15 +376,16 @@ __global__ __launch_bounds__(kThreads) void decode_combine(
   __shared__ HeadStats hs;
   const int G = Hq / Hkv;
   const size_t bh = blockIdx.y;
+  const bool has_chunk = kn != nullptr;
   head_stats<D, kThreads>(hs, q, kn, dstat, Hq, Hkv, G, nsplit, c_log2, bh,
-                          blockIdx.x == 0 ? lse : nullptr);
+                          blockIdx.x == 0 ? lse : nullptr, has_chunk);
   if (blockIdx.x == 0) head_out<D, kThreads>(hs, vn, dO, out, Hq, Hkv, G, nsplit, bh);
-  float* w = wsum + bh * (size_t)(M + 1);
+  float* w = wsum + bh * (size_t)(M + (has_chunk ? 1 : 0));
   const float* lgb = logits + bh * (size_t)G * logit_pitch(M);
   const int c0 = blockIdx.x * kCols, c1 = min(M, c0 + kCols);
   for (int j = c0 + threadIdx.x; j < c1; j += kThreads)
     w[j] = slot_weight(hs, lgb, logit_pitch(M), G, j);
-  if (blockIdx.x == 0 && threadIdx.x == 0) w[M] = chunk_weight(hs, G);
+  if (has_chunk && blockIdx.x == 0 && threadIdx.x == 0) w[M] = chunk_weight(hs, G);
 }
 
 // Fused end of a token step, one block per head: the combine above, then
@@ -466,13 +499,13 @@ __global__ __launch_bounds__(kFinThreads) void decode_finish(
 // Split blocks per head such that all blocks of the grid are resident at
 // once (blocks per CU of this kernel instance x CUs), at most kMaxSplit and
 // at most one wave per step of slots.
-template <int D, int G>
+template <int D, int G, bool CACHE>
 int split_count(int M, int BH) {
   static int resident = 0;
   if (!resident) {
     int per_cu = 0, dev = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, decode_split<D, G>, kThreads,
-                                                     0) != hipSuccess || per_cu < 1)
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, decode_split<D, G, CACHE>,
+                                                     kThreads, 0) != hipSuccess || per_cu < 1)
       per_cu = 2;
     if (hipGetDevice(&dev) != hipSuccess ||
         hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
@@ -492,11 +525,18 @@ int split_count(int M, int BH) {
 template <int D, int G>
 hipError_t launch_split(hipStream_t st, int BH, const void* q, const void* kc, const void* vc,
                         int Hq, int Hkv, int M, float c, float* logits, float2* dstat, float* dO,
-                        float* sink, int* ns) {
-  *ns = split_count<D, G>(M, BH);
-  return launch_kernel(K_DECODE_SPLIT, decode_split<D, G>, dim3(*ns, BH), dim3(kThreads), st,
-                       (const bf16_t*)q, (const bf16_t*)kc, (const bf16_t*)vc, Hq, Hkv, M, c,
-                       logits, dstat, dO, sink);
+                        float* sink, KeyPos kp, int* ns) {
+  if (kp.tp) {
+    *ns = split_count<D, G, true>(M, BH);
+    return launch_kernel(K_DECODE_SPLIT, decode_split<D, G, true>, dim3(*ns, BH),
+                         dim3(kThreads), st, (const bf16_t*)q, (const bf16_t*)kc,
+                         (const bf16_t*)vc, Hq, Hkv, M, c, logits, dstat, dO, sink, kp.tp,
+                         kp.pos0);
+  }
+  *ns = split_count<D, G, false>(M, BH);
+  return launch_kernel(K_DECODE_SPLIT, decode_split<D, G, false>, dim3(*ns, BH), dim3(kThreads),
+                       st, (const bf16_t*)q, (const bf16_t*)kc, (const bf16_t*)vc, Hq, Hkv, M, c,
+                       logits, dstat, dO, sink, (const int32_t*)nullptr, (int32_t)0);
 }
 
 }  // namespace
@@ -513,7 +553,8 @@ namespace {
 
 // The split kernel over the cache (if any); returns the split count in *ns.
 hipError_t launch_decode_split(const Shape& s, const Plan& p, const void* q, const void* kc,
-                               const void* vc, char* ws, float c, hipStream_t st, int* ns) {
+                               const void* vc, char* ws, float c, KeyPos kp, hipStream_t st,
+                               int* ns) {
   float* logits = reinterpret_cast<float*>(ws + p.off_logits);
   float2* dstat = reinterpret_cast<float2*>(ws + p.off_stats);
   float* dO = reinterpret_cast<float*>(ws + p.off_opart);
@@ -523,7 +564,8 @@ hipError_t launch_decode_split(const Shape& s, const Plan& p, const void* q, con
   const int G = s.G();
   hipError_t e = hipErrorInvalidValue;
 #define H2O_SPLIT(DD, GG) \
-  e = launch_split<DD, GG>(st, s.BH(), q, kc, vc, s.Hq, s.Hkv, s.M, c, logits, dstat, dO, sink, ns)
+  e = launch_split<DD, GG>(st, s.BH(), q, kc, vc, s.Hq, s.Hkv, s.M, c, logits, dstat, dO, sink, \
+                           kp, ns)
   if (s.d == 64) {
     if (G == 1) H2O_SPLIT(64, 1);
     else if (G == 2) H2O_SPLIT(64, 2);
@@ -542,15 +584,18 @@ hipError_t launch_decode_split(const Shape& s, const Plan& p, const void* q, con
 
 hipError_t launch_sdpa_decode(const Shape& s, const Plan& p, const void* q, const void* kc,
                               const void* vc, const void* kn, const void* vn, void* out,
-                              float* lse, float* wsum, char* ws, float scale, hipStream_t st) {
+                              float* lse, float* wsum, char* ws, float scale, KeyPos kp,
+                              hipStream_t st) {
   const float c = scale * kLog2e;
   int ns = 0;
-  hipError_t e = launch_decode_split(s, p, q, kc, vc, ws, c, st, &ns);
+  hipError_t e = launch_decode_split(s, p, q, kc, vc, ws, c, kp, st, &ns);
   if (e != hipSuccess) return e;
   const dim3 cgrid(s.M > 0 ? (s.M + kCols - 1) / kCols : 1, s.BH());
   auto combine = s.d == 64 ? decode_combine<64> : decode_combine<128>;
+  const bool chunk = !s.cache_only;
   return launch_kernel(K_DECODE_COMBINE, combine, cgrid, dim3(kThreads), st, (const bf16_t*)q,
-                       (const bf16_t*)kn, (const bf16_t*)vn, s.Hq, s.Hkv, s.M, ns, c,
+                       chunk ? (const bf16_t*)kn : nullptr, chunk ? (const bf16_t*)vn : nullptr,
+                       s.Hq, s.Hkv, s.M, ns, c,
                        (const float*)(ws + p.off_logits), (const float2*)(ws + p.off_stats),
                        (const float*)(ws + p.off_opart), (bf16_t*)out, lse, wsum);
 }
@@ -561,7 +606,7 @@ hipError_t launch_decode_step(const Shape& s, const Plan& p, const void* q, void
                               int32_t pos0, char* ws, float scale, hipStream_t st) {
   const float c = scale * kLog2e;
   int ns = 0;
-  hipError_t e = launch_decode_split(s, p, q, kc, vc, ws, c, st, &ns);
+  hipError_t e = launch_decode_split(s, p, q, kc, vc, ws, c, KeyPos{nullptr, 0}, st, &ns);
   if (e != hipSuccess) return e;
   const int G = s.G();
   auto go = [&](auto kern) {

@@ -46,22 +46,45 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
 // ----------------------------------------------------------- problem shape
+// Two arrangements of the keys a chunk attends:
+//  - chunk mode: [M cache slots, all visible || the T chunk keys, causal], the
+//    chunk's keys and values passed separately (attend, then evict);
+//  - cache mode (cache_only): the M cache slots alone, the chunk already
+//    written into them, slot j visible to chunk query i iff
+//    token_pos[j] - pos0 <= i (insert, then attend).
 struct Shape {
   int B, Hq, Hkv, T, M, d;
+  bool cache_only = false;
   int G() const { return Hq / Hkv; }
   int R() const { return G() * T; }      // packed query rows per KV head
-  int Nk() const { return M + T; }       // key columns per KV head
+  int Tk() const { return cache_only ? 0 : T; }   // chunk key columns
+  int Nk() const { return M + Tk(); }    // key columns per KV head
   int BH() const { return B * Hkv; }
 };
 
+// Token positions of cache mode: tp = token_pos (nullptr in chunk mode), pos0
+// = the position of the chunk's first query.
+struct KeyPos {
+  const int32_t* tp;
+  int32_t pos0;
+};
+
 // Packed row r of a KV head is (chunk position i = r / G, group member g = r % G).
-// The keys a chunk position i may see are columns [0, M + i + 1).
+// In chunk mode the keys a chunk position i may see are columns [0, M + i + 1).
 // A partial-sum slot that covers packed rows [r0, r1) therefore sees key
-// columns [0, kv_end) with kv_end = M + min(T-1, (r1-1)/G) + 1.
-__host__ __device__ __forceinline__ int kv_end_for_rows(int r1, int G, int T, int M) {
+// columns [0, kv_end) with kv_end = M + min(T-1, (r1-1)/G) + 1; with no chunk
+// key columns (Tk = 0, cache mode) it is M.
+__host__ __device__ __forceinline__ int kv_end_for_rows(int r1, int G, int T, int M, int Tk) {
+  if (Tk == 0) return M;
   int i_max = (r1 - 1) / G;
   if (i_max > T - 1) i_max = T - 1;
   return M + i_max + 1;
+}
+
+// Cache-mode visibility of slot j to chunk position i (positions are compared
+// in 64 bits, so any int32 token position works).
+__device__ __forceinline__ bool pos_visible(int32_t tpj, int32_t pos0, int i) {
+  return (long long)tpj - (long long)pos0 <= (long long)i;
 }
 
 // ---------------------------------------------------------- workspace plan
@@ -117,16 +140,19 @@ hipError_t launch_kernel(int kernel_id, F kern, dim3 grid, dim3 block, hipStream
 
 // ------------------------------------------------------------- launchers
 // Each returns hipSuccess or the launch error. They assume validated inputs.
+// In cache mode (s.cache_only) kn and vn are unused and kp holds the token
+// positions; in chunk mode kp.tp is nullptr.
 hipError_t launch_sdpa_generic(const Shape& s, const Plan& p, int dtype, const void* q,
                                const void* kc, const void* vc, const void* kn,
                                const void* vn, void* out, float* lse, float* wsum,
-                               char* ws, float scale, hipStream_t st);
+                               char* ws, float scale, KeyPos kp, hipStream_t st);
 hipError_t launch_sdpa_mfma(const Shape& s, const Plan& p, const void* q, const void* kc,
                             const void* vc, const void* kn, const void* vn, void* out,
-                            float* lse, float* wsum, char* ws, float scale, hipStream_t st);
+                            float* lse, float* wsum, char* ws, float scale, KeyPos kp,
+                            hipStream_t st);
 hipError_t launch_sdpa_decode(const Shape& s, const Plan& p, const void* q, const void* kc,
                               const void* vc, const void* kn, const void* vn, void* out,
-                              float* lse, float* wsum, char* ws, float scale,
+                              float* lse, float* wsum, char* ws, float scale, KeyPos kp,
                               hipStream_t st);
 // T == 1, one call for the whole step: split kernel, then one block per head
 // merges the splits, accumulates the scores, picks the slot and inserts.
@@ -152,6 +178,8 @@ hipError_t launch_orig_keys(const float* scores, float* keys, int B, int Hkv, in
                             hipStream_t st);
 hipError_t launch_broadcast_rows(const int32_t* src, int32_t* dst, int B, int n,
                                  hipStream_t st);
+// The inserted slots take score wsum[row, M + i] (row pitch M + T), or 0
+// when wsum is nullptr (insert before attending).
 hipError_t launch_insert(void* kc, void* vc, float* scores, int32_t* token_pos,
                          const void* kn, const void* vn, const float* wsum,
                          const int32_t* idx, int rows, int M, int T, int d, int k,

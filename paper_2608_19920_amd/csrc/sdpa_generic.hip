@@ -11,6 +11,10 @@
 //           per row tile, column partials sum_{r in tile} m_rj
 //   reduce  wsum_j = sum over row tiles of the partials
 //
+// In cache mode the keys are the M cache slots alone, slot j visible to chunk
+// position i iff token_pos[j] - pos0 <= i; a row that sees no slot gets
+// lse = -inf, out = 0 and adds nothing to the column sums.
+//
 // Rows of a KV head are packed position-major: r = i*G + g (chunk position i,
 // query head hq = h*G + g). One thread owns one packed row; key tiles of
 // kTile keys are staged in LDS and shared by the 64 rows of the block.
@@ -43,9 +47,9 @@ template <typename E, int D>
 __global__ __launch_bounds__(kRows) void pass_a(const E* __restrict__ q, const E* __restrict__ kc,
                                                 const E* __restrict__ kn, float* __restrict__ lse,
                                                 float* __restrict__ lse_ws, int Hq, int Hkv,
-                                                int T, int M, float scale) {
+                                                int T, int M, int Tk, float scale, KeyPos kp) {
   __shared__ float ks[kTile * (D + 1)];
-  const int G = Hq / Hkv, R = G * T, Nk = M + T;
+  const int G = Hq / Hkv, R = G * T, Nk = M + Tk;
   const size_t bh = blockIdx.y;
   const int b = (int)(bh / Hkv), h = (int)(bh % Hkv);
   const int r0 = blockIdx.x * kRows, r = r0 + threadIdx.x;
@@ -56,7 +60,8 @@ __global__ __launch_bounds__(kRows) void pass_a(const E* __restrict__ q, const E
 #pragma unroll
   for (int c = 0; c < D; ++c) qv[c] = valid ? load_elem(q, qrow + c) * scale : 0.f;
   const int r1 = min(r0 + kRows, R);
-  const int kv_end = kv_end_for_rows(r1, G, T, M);
+  const int kv_end = kv_end_for_rows(r1, G, T, M, Tk);
+  const int32_t* tp = kp.tp ? kp.tp + bh * (size_t)M : nullptr;
   float m = -INFINITY, l = 0.f;
   for (int j0 = 0; j0 < kv_end; j0 += kTile) {
     __syncthreads();
@@ -66,6 +71,7 @@ __global__ __launch_bounds__(kRows) void pass_a(const E* __restrict__ q, const E
     for (int jj = 0; jj < jn; ++jj) {
       const int j = j0 + jj;
       if (j >= M && j - M > i) break;          // later chunk keys are invisible too
+      if (tp && !pos_visible(tp[j], kp.pos0, i)) continue;
       float s = 0.f;
 #pragma unroll
       for (int c = 0; c < D; ++c) s = fmaf(qv[c], ks[jj * (D + 1) + c], s);
@@ -90,11 +96,11 @@ __global__ __launch_bounds__(kRows) void pass_b(const E* __restrict__ q, const E
                                                 const E* __restrict__ vn, E* __restrict__ out,
                                                 const float* __restrict__ lse_ws,
                                                 float* __restrict__ parts, int Hq, int Hkv, int T,
-                                                int M, float scale) {
+                                                int M, int Tk, float scale, KeyPos kp) {
   __shared__ float ks[kTile * (D + 1)];
   __shared__ float vs[kTile * (D + 1)];
   __shared__ float ps[kRows * (kTile + 1)];
-  const int G = Hq / Hkv, R = G * T, Nk = M + T;
+  const int G = Hq / Hkv, R = G * T, Nk = M + Tk;
   const size_t bh = blockIdx.y;
   const int b = (int)(bh / Hkv), h = (int)(bh % Hkv);
   const int r0 = blockIdx.x * kRows, r = r0 + threadIdx.x;
@@ -108,8 +114,10 @@ __global__ __launch_bounds__(kRows) void pass_b(const E* __restrict__ q, const E
     o[c] = 0.f;
   }
   const float lam = valid ? lse_ws[bh * R + r] : 0.f;
+  const bool live = valid && lam > -INFINITY;   // the row sees at least one key
   const int r1 = min(r0 + kRows, R);
-  const int kv_end = kv_end_for_rows(r1, G, T, M);
+  const int kv_end = kv_end_for_rows(r1, G, T, M, Tk);
+  const int32_t* tp = kp.tp ? kp.tp + bh * (size_t)M : nullptr;
   float* prow = parts + ((size_t)blockIdx.x * gridDim.y + bh) * Nk;
   for (int j0 = 0; j0 < kv_end; j0 += kTile) {
     __syncthreads();
@@ -120,7 +128,7 @@ __global__ __launch_bounds__(kRows) void pass_b(const E* __restrict__ q, const E
     for (int jj = 0; jj < kTile; ++jj) {
       const int j = j0 + jj;
       float p = 0.f;
-      if (valid && jj < jn && (j < M || j - M <= i)) {
+      if (live && jj < jn && (j < M ? !tp || pos_visible(tp[j], kp.pos0, i) : j - M <= i)) {
         float s = 0.f;
 #pragma unroll
         for (int c = 0; c < D; ++c) s = fmaf(qv[c], ks[jj * (D + 1) + c], s);
@@ -147,17 +155,17 @@ __global__ __launch_bounds__(kRows) void pass_b(const E* __restrict__ q, const E
 template <typename E, int D>
 hipError_t run(const Shape& s, const Plan& p, const void* q, const void* kc, const void* vc,
                const void* kn, const void* vn, void* out, float* lse, float* wsum, char* ws,
-               float scale, hipStream_t st) {
+               float scale, KeyPos kp, hipStream_t st) {
   dim3 grid((s.R() + kRows - 1) / kRows, s.BH());
   float* lse_ws = reinterpret_cast<float*>(ws + p.off_stats);
   float* parts = reinterpret_cast<float*>(ws + p.off_parts);
   hipError_t e = launch_kernel(K_GENERIC_LSE, pass_a<E, D>, grid, dim3(kRows), st, (const E*)q,
                                (const E*)kc, (const E*)kn, lse, lse_ws, s.Hq, s.Hkv, s.T, s.M,
-                               scale);
+                               s.Tk(), scale, kp);
   if (e != hipSuccess) return e;
   e = launch_kernel(K_GENERIC_MAIN, pass_b<E, D>, grid, dim3(kRows), st, (const E*)q,
                     (const E*)kc, (const E*)vc, (const E*)kn, (const E*)vn, (E*)out,
-                    (const float*)lse_ws, parts, s.Hq, s.Hkv, s.T, s.M, scale);
+                    (const float*)lse_ws, parts, s.Hq, s.Hkv, s.T, s.M, s.Tk(), scale, kp);
   if (e != hipSuccess) return e;
   return launch_colsum_reduce(s, p, parts, wsum, st);
 }
@@ -167,13 +175,15 @@ hipError_t run(const Shape& s, const Plan& p, const void* q, const void* kc, con
 hipError_t launch_sdpa_generic(const Shape& s, const Plan& p, int dtype, const void* q,
                                const void* kc, const void* vc, const void* kn, const void* vn,
                                void* out, float* lse, float* wsum, char* ws, float scale,
-                               hipStream_t st) {
+                               KeyPos kp, hipStream_t st) {
   if (dtype == 0) {
-    return s.d == 64 ? run<float, 64>(s, p, q, kc, vc, kn, vn, out, lse, wsum, ws, scale, st)
-                     : run<float, 128>(s, p, q, kc, vc, kn, vn, out, lse, wsum, ws, scale, st);
+    return s.d == 64
+               ? run<float, 64>(s, p, q, kc, vc, kn, vn, out, lse, wsum, ws, scale, kp, st)
+               : run<float, 128>(s, p, q, kc, vc, kn, vn, out, lse, wsum, ws, scale, kp, st);
   }
-  return s.d == 64 ? run<bf16_t, 64>(s, p, q, kc, vc, kn, vn, out, lse, wsum, ws, scale, st)
-                   : run<bf16_t, 128>(s, p, q, kc, vc, kn, vn, out, lse, wsum, ws, scale, st);
+  return s.d == 64
+             ? run<bf16_t, 64>(s, p, q, kc, vc, kn, vn, out, lse, wsum, ws, scale, kp, st)
+             : run<bf16_t, 128>(s, p, q, kc, vc, kn, vn, out, lse, wsum, ws, scale, kp, st);
 }
 
 }  // namespace h2o

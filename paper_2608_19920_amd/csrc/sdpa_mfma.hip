@@ -102,9 +102,11 @@ __device__ __forceinline__ bf16x8 v_operand(const bf16_t* Vs, int db, int lane) 
 }
 
 struct Geo {
-  int G, T, M, R, Nk;
+  int G, T, M, R, Nk, Tk;   // Tk: chunk key columns (T, or 0 in cache mode)
   const bf16_t* q;
   const bf16_t *kc, *vc, *kn, *vn;
+  const int32_t* tp;        // cache mode: token positions [BH][M]
+  int32_t pos0;
 };
 
 // ------------------------------------------------------------ tile staging
@@ -202,6 +204,45 @@ __device__ __forceinline__ void scores_tile(f32x4 (&sacc)[2][NQB], const bf16_t*
 // Key column j of a chunk is visible to chunk position i iff j < M or j-M <= i.
 __device__ __forceinline__ bool visible(int j, int M, int i) { return j < M || j - M <= i; }
 
+// Masking of a tile: MK = 0 none, 1 the chunk's causal rule (visible()), 2
+// cache mode, where each key's position relative to the chunk, rp =
+// token_pos - pos0 (a value above every chunk position past the cache), is
+// staged in LDS with the tile and the key is visible to position i iff
+// rp <= i. Rel holds the rp of this lane's 8 keys of the tile.
+struct Rel {
+  int rp[2][4];
+};
+constexpr int kRpFar = 1 << 30;   // above every chunk position
+
+__device__ __forceinline__ void load_rel(Rel& rl, const int* rps, int lane) {
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+    const int4 v = *reinterpret_cast<const int4*>(rps + 16 * kb + 4 * (lane >> 4));
+    rl.rp[kb][0] = v.x;
+    rl.rp[kb][1] = v.y;
+    rl.rp[kb][2] = v.z;
+    rl.rp[kb][3] = v.w;
+  }
+}
+
+template <int MK>
+__device__ __forceinline__ bool key_hidden(const Rel& rl, int kb, int r, int j, int M, int i) {
+  if (MK == 1) return !visible(j, M, i);
+  if (MK == 2) return rl.rp[kb][r] > i;
+  return false;
+}
+
+// Cache mode: thread tid < BN fetches the relative position of key j0 + tid.
+__device__ __forceinline__ int load_rp(const int32_t* tp_bh, int32_t pos0, int j0, int M) {
+  const int j = j0 + (int)threadIdx.x;
+  if (threadIdx.x >= BN || j >= M) return kRpFar;
+  const long long r = (long long)tp_bh[j] - pos0;
+  return r > kRpFar ? kRpFar : (r < -kRpFar ? -kRpFar : (int)r);
+}
+__device__ __forceinline__ void store_rp(int* rps, int v) {
+  if (threadIdx.x < BN) rps[threadIdx.x] = v;
+}
+
 // Tiles [t0, t1) of a row tile's key range [0, ntiles*BN) for split sp.
 __device__ __forceinline__ void split_range(int ntiles, int nsplit, int sp, int& t0, int& t1) {
   const int per = (ntiles + nsplit - 1) / nsplit;
@@ -272,10 +313,11 @@ __device__ __forceinline__ BlockId block_id(int nsplit) {
 // running maximum m is kept in raw score units (c > 0 keeps the order);
 // l sums exp2(c*(s - m)). Unmasked tiles have finite scores, so only masked
 // tiles need the guard for a maximum that is still -inf.
-template <bool MASKED, int NQB>
+template <int MK, int NQB>
 __device__ __forceinline__ void lse_update(const f32x4 (&sacc)[2][NQB], float (&m)[NQB],
                                            float (&l)[NQB], const int (&qi)[NQB], int j0, int M,
-                                           int lane, float c) {
+                                           int lane, float c, const Rel& rl) {
+  constexpr bool MASKED = MK != 0;
 #pragma unroll
   for (int qb = 0; qb < NQB; ++qb) {
     float x[8];
@@ -284,7 +326,8 @@ __device__ __forceinline__ void lse_update(const f32x4 (&sacc)[2][NQB], float (&
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         float v = sacc[kb][qb][r];
-        if (MASKED && !visible(j0 + kb * 16 + 4 * (lane >> 4) + r, M, qi[qb])) v = -INFINITY;
+        if (key_hidden<MK>(rl, kb, r, j0 + kb * 16 + 4 * (lane >> 4) + r, M, qi[qb]))
+          v = -INFINITY;
         x[kb * 4 + r] = v;
       }
     const float mn = __builtin_fmaxf(__builtin_fmaxf(__builtin_fmaxf(x[0], x[1]), x[2]),
@@ -299,83 +342,104 @@ __device__ __forceinline__ void lse_update(const f32x4 (&sacc)[2][NQB], float (&
   }
 }
 
-// Loop state of pass A. At the start of tile t: sa holds S(t), and ka holds
-// the global rows of tile t+2, loaded but not yet written to LDS; kb is free.
+// Loop state of pass A. At the start of tile t: sa holds S(t), and ka (ra in
+// cache mode: the relative positions) holds the global rows of tile t+2,
+// loaded but not yet written to LDS; kb (rb) is free.
 template <int D, int NT, int NQB>
 struct LseState {
   f32x4 sa[2][NQB], sb[2][NQB];
   u32x4 ka[Tile<D, NT>::N], kb[Tile<D, NT>::N];
+  int ra, rb;
 };
 
 // One tile of pass A: the loads of tile t+3 go to `fill` while the MFMAs of
 // S(t+1) and the update with S(t) run; then tile t+2 (in `put`) goes to the
 // LDS buffer tile t-1 used. The loads of tile t+3 are waited for only one
 // tile later.
-template <bool MASKED, int D, int NT, int NQB>
+template <int MK, int D, int NT, int NQB>
 __device__ __forceinline__ void lse_tile(int t, int t0, int t1, const f32x4 (&s_cur)[2][NQB],
                                          f32x4 (&s_nxt)[2][NQB], u32x4 (&fill)[Tile<D, NT>::N],
-                                         const u32x4 (&put)[Tile<D, NT>::N],
-                                         const Tile<D, NT>& tl, bf16_t (*Ks)[BN * kstride(D)],
+                                         const u32x4 (&put)[Tile<D, NT>::N], int& rfill,
+                                         int rput, const Tile<D, NT>& tl,
+                                         bf16_t (*Ks)[BN * kstride(D)], int (*rps)[BN],
                                          const bf16x8 (&qf)[NQB][D / 32], float (&m)[NQB],
                                          float (&l)[NQB], const int (&qi)[NQB],
-                                         const bf16_t* kc_bh, const bf16_t* kn_bh, const Geo& g,
-                                         int lane, float c) {
-  const int b1 = (t + 1 - t0) % NBUF, b2 = (t + 2 - t0) % NBUF;
-  load_tile<D, NT>(fill, tl, kc_bh, kn_bh, min(t + 3, t1 - 1) * BN, g.M, g.Nk);
+                                         const bf16_t* kc_bh, const bf16_t* kn_bh,
+                                         const int32_t* tp_bh, const Geo& g, int lane, float c) {
+  const int b0 = (t - t0) % NBUF, b1 = (t + 1 - t0) % NBUF, b2 = (t + 2 - t0) % NBUF;
+  const int jn = min(t + 3, t1 - 1) * BN;
+  load_tile<D, NT>(fill, tl, kc_bh, kn_bh, jn, g.M, g.Nk);
+  if (MK == 2) rfill = load_rp(tp_bh, g.pos0, jn, g.M);
+  Rel rl;
+  if (MK == 2) load_rel(rl, rps[b0], lane);
   scores_tile<D, NQB>(s_nxt, Ks[b1], qf, lane);
-  lse_update<MASKED, NQB>(s_cur, m, l, qi, t * BN, g.M, lane, c);
-  interleave<2 * NQB * (D / 32), MASKED ? 8 : 5>();
+  lse_update<MK, NQB>(s_cur, m, l, qi, t * BN, g.M, lane, c, rl);
+  interleave<2 * NQB * (D / 32), MK ? 8 : 5>();
   store_tile<D, NT>(Ks[b2], tl.loff, put);
+  if (MK == 2) store_rp(rps[b2], rput);
   __syncthreads();
 }
 
 // Tiles [ta, tb): two tiles per trip with the roles of the register sets
 // swapped, so no accumulator or staging register is copied; an odd last
 // tile restores the state invariant with one copy.
-template <bool MASKED, int D, int NT, int NQB>
+template <int MK, int D, int NT, int NQB>
 __device__ __forceinline__ void lse_loop(int ta, int tb, int t0, int t1, LseState<D, NT, NQB>& S,
                                          const Tile<D, NT>& tl,
-                                         bf16_t (*Ks)[BN * kstride(D)],
+                                         bf16_t (*Ks)[BN * kstride(D)], int (*rps)[BN],
                                          const bf16x8 (&qf)[NQB][D / 32], float (&m)[NQB],
                                          float (&l)[NQB], const int (&qi)[NQB],
-                                         const bf16_t* kc_bh, const bf16_t* kn_bh, const Geo& g,
-                                         int lane, float c) {
+                                         const bf16_t* kc_bh, const bf16_t* kn_bh,
+                                         const int32_t* tp_bh, const Geo& g, int lane, float c) {
   int t = ta;
   for (; t + 1 < tb; t += 2) {
-    lse_tile<MASKED, D, NT, NQB>(t, t0, t1, S.sa, S.sb, S.kb, S.ka, tl, Ks, qf, m, l, qi, kc_bh,
-                                 kn_bh, g, lane, c);
-    lse_tile<MASKED, D, NT, NQB>(t + 1, t0, t1, S.sb, S.sa, S.ka, S.kb, tl, Ks, qf, m, l, qi,
-                                 kc_bh, kn_bh, g, lane, c);
+    lse_tile<MK, D, NT, NQB>(t, t0, t1, S.sa, S.sb, S.kb, S.ka, S.rb, S.ra, tl, Ks, rps, qf, m, l,
+                             qi, kc_bh, kn_bh, tp_bh, g, lane, c);
+    lse_tile<MK, D, NT, NQB>(t + 1, t0, t1, S.sb, S.sa, S.ka, S.kb, S.ra, S.rb, tl, Ks, rps, qf,
+                             m, l, qi, kc_bh, kn_bh, tp_bh, g, lane, c);
   }
   if (t < tb) {
-    lse_tile<MASKED, D, NT, NQB>(t, t0, t1, S.sa, S.sb, S.kb, S.ka, tl, Ks, qf, m, l, qi, kc_bh,
-                                 kn_bh, g, lane, c);
+    lse_tile<MK, D, NT, NQB>(t, t0, t1, S.sa, S.sb, S.kb, S.ka, S.rb, S.ra, tl, Ks, rps, qf, m, l,
+                             qi, kc_bh, kn_bh, tp_bh, g, lane, c);
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int qb = 0; qb < NQB; ++qb) S.sa[kb][qb] = S.sb[kb][qb];
 #pragma unroll
     for (int e = 0; e < Tile<D, NT>::N; ++e) S.ka[e] = S.kb[e];
+    S.ra = S.rb;
   }
 }
 
-template <int D, int NW, int NQB>
+// First tile index at which a row tile starting at packed row row0 needs a
+// mask: in chunk mode the first tile reaching a chunk key some row cannot
+// see, in cache mode (CACHE) every tile.
+template <bool CACHE>
+__device__ __forceinline__ int mask_start(const Geo& g, int row0, int t0, int t1) {
+  if (CACHE) return t0;
+  return min(t1, max(t0, first_masked_tile(g.M, min(row0, g.R - 1) / g.G)));
+}
+
+template <int D, int NW, int NQB, bool CACHE>
 __global__ __launch_bounds__(NW * 64) void lse_pass(Geo g, int Hq, int Hkv, int nsplit,
                                                     float c_log2, float2* __restrict__ stats) {
   constexpr int NT = NW * 64, ROWS = NW * NQB * 16;
+  constexpr int MKM = CACHE ? 2 : 1;   // mask mode of the masked tiles
   __shared__ __attribute__((aligned(16))) bf16_t Ks[NBUF][BN * kstride(D)];
+  __shared__ __attribute__((aligned(16))) int rps[NBUF][BN];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const BlockId id = block_id(nsplit);
   const int rt = id.rt, sp = id.sp;
   const size_t bh = id.bh;
   const int b = (int)(bh / Hkv), h = (int)(bh % Hkv);
   const int row0 = rt * ROWS, wrow0 = row0 + wave * NQB * 16;
-  const int kv_end = kv_end_for_rows(min(row0 + ROWS, g.R), g.G, g.T, g.M);
+  const int kv_end = kv_end_for_rows(min(row0 + ROWS, g.R), g.G, g.T, g.M, g.Tk);
   int t0, t1;
   split_range((kv_end + BN - 1) / BN, nsplit, sp, t0, t1);
-  const int t_mask = min(t1, max(t0, first_masked_tile(g.M, min(row0, g.R - 1) / g.G)));
+  const int t_mask = mask_start<CACHE>(g, row0, t0, t1);
   const bf16_t* kc_bh = g.kc + bh * (size_t)g.M * D;
-  const bf16_t* kn_bh = g.kn + bh * (size_t)g.T * D;
+  const bf16_t* kn_bh = CACHE ? nullptr : g.kn + bh * (size_t)g.T * D;
+  const int32_t* tp_bh = CACHE ? g.tp + bh * (size_t)g.M : nullptr;
 
   bf16x8 qf[NQB][D / 32];
   load_q<D, NQB>(qf, g, b, h, Hq, wrow0, lane);
@@ -391,17 +455,23 @@ __global__ __launch_bounds__(NW * 64) void lse_pass(Geo g, int Hq, int Hkv, int 
   LseState<D, NT, NQB> S;
   const Tile<D, NT> tl;
   if (t0 < t1) {
+    const int j1 = min(t0 + 1, t1 - 1) * BN, j2 = min(t0 + 2, t1 - 1) * BN;
     load_tile<D, NT>(S.ka, tl, kc_bh, kn_bh, t0 * BN, g.M, g.Nk);
-    load_tile<D, NT>(S.kb, tl, kc_bh, kn_bh, min(t0 + 1, t1 - 1) * BN, g.M, g.Nk);
+    load_tile<D, NT>(S.kb, tl, kc_bh, kn_bh, j1, g.M, g.Nk);
+    if (CACHE) {
+      store_rp(rps[0], load_rp(tp_bh, g.pos0, t0 * BN, g.M));
+      store_rp(rps[1], load_rp(tp_bh, g.pos0, j1, g.M));
+      S.ra = load_rp(tp_bh, g.pos0, j2, g.M);
+    }
     store_tile<D, NT>(Ks[0], tl.loff, S.ka);
     store_tile<D, NT>(Ks[1], tl.loff, S.kb);
-    load_tile<D, NT>(S.ka, tl, kc_bh, kn_bh, min(t0 + 2, t1 - 1) * BN, g.M, g.Nk);
+    load_tile<D, NT>(S.ka, tl, kc_bh, kn_bh, j2, g.M, g.Nk);
     __syncthreads();
     scores_tile<D, NQB>(S.sa, Ks[0], qf, lane);
-    lse_loop<false, D, NT, NQB>(t0, t_mask, t0, t1, S, tl, Ks, qf, m, l, qi, kc_bh, kn_bh, g, lane,
-                                c_log2);
-    lse_loop<true, D, NT, NQB>(t_mask, t1, t0, t1, S, tl, Ks, qf, m, l, qi, kc_bh, kn_bh, g, lane,
-                               c_log2);
+    lse_loop<0, D, NT, NQB>(t0, t_mask, t0, t1, S, tl, Ks, rps, qf, m, l, qi, kc_bh, kn_bh,
+                            tp_bh, g, lane, c_log2);
+    lse_loop<MKM, D, NT, NQB>(t_mask, t1, t0, t1, S, tl, Ks, rps, qf, m, l, qi, kc_bh, kn_bh,
+                              tp_bh, g, lane, c_log2);
   }
   // merge the four lane groups (disjoint key subsets of the same query)
 #pragma unroll
@@ -424,10 +494,11 @@ __global__ __launch_bounds__(NW * 64) void lse_pass(Geo g, int Hq, int Hkv, int 
 // Probabilities of one tile (bf16 B operands of the PV product) and their
 // column partials over this wave's rows, into the wave's LDS row for the
 // tile (the four lanes holding one column's total all store it).
-template <bool MASKED, int NQB>
+template <int MK, int NQB>
 __device__ __forceinline__ void probs_tile(const f32x4 (&sacc)[2][NQB], bf16x8 (&pb)[NQB],
                                            const float (&lam)[NQB], const int (&qi)[NQB],
-                                           float* cs_row, int j0, int M, int lane, float c) {
+                                           float* cs_row, int j0, int M, int lane, float c,
+                                           const Rel& rl) {
   float cs[2][4];
 #pragma unroll
   for (int qb = 0; qb < NQB; ++qb) {
@@ -436,7 +507,7 @@ __device__ __forceinline__ void probs_tile(const f32x4 (&sacc)[2][NQB], bf16x8 (
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         float p = __builtin_amdgcn_exp2f(fmaf(sacc[kb][qb][r], c, -lam[qb]));
-        if (MASKED && !visible(j0 + kb * 16 + 4 * (lane >> 4) + r, M, qi[qb])) p = 0.f;
+        if (key_hidden<MK>(rl, kb, r, j0 + kb * 16 + 4 * (lane >> 4) + r, M, qi[qb])) p = 0.f;
         cs[kb][r] = qb == 0 ? p : cs[kb][r] + p;
         pb[qb][kb * 4 + r] = (__bf16)p;
       }
@@ -467,21 +538,23 @@ struct MainState {
   f32x4 sa[2][NQB], sb[2][NQB];
   f32x4 oacc[D / 16][NQB];
   u32x4 ka[Tile<D, NT>::N], va[Tile<D, NT>::N], kb[Tile<D, NT>::N], vb[Tile<D, NT>::N];
+  int ra, rb;   // cache mode: relative positions of tile t+2 / free
 };
 
 // One tile of pass B. The waves' column partials of the tile meet in
 // cs_lds[tile parity][wave]; after the tile's barrier, threads 0..BN-1 add
 // them in wave order and store the block's partial row (one partial per
 // block and row tile).
-template <bool MASKED, int D, int NT, int NQB>
+template <int MK, int D, int NT, int NQB>
 __device__ __forceinline__ void main_tile(
     int t, int t0, int t1, const f32x4 (&s_cur)[2][NQB], f32x4 (&s_nxt)[2][NQB],
     f32x4 (&oacc)[D / 16][NQB], u32x4 (&kfill)[Tile<D, NT>::N],
     u32x4 (&vfill)[Tile<D, NT>::N], const u32x4 (&kput)[Tile<D, NT>::N],
-    const u32x4 (&vput)[Tile<D, NT>::N], const Tile<D, NT>& tl, bf16_t (*Ks)[BN * kstride(D)],
-    bf16_t (*Vs)[BN * vstride(D)], const bf16x8 (&qf)[NQB][D / 32], const float (&lam)[NQB],
-    const int (&qi)[NQB], float (*cs_lds)[NT / 64][BN], float* prow, const bf16_t* kc_bh,
-    const bf16_t* kn_bh, const bf16_t* vc_bh, const bf16_t* vn_bh, const Geo& g, int lane,
+    const u32x4 (&vput)[Tile<D, NT>::N], int& rfill, int rput, const Tile<D, NT>& tl,
+    bf16_t (*Ks)[BN * kstride(D)], bf16_t (*Vs)[BN * vstride(D)], int (*rps)[BN],
+    const bf16x8 (&qf)[NQB][D / 32], const float (&lam)[NQB], const int (&qi)[NQB],
+    float (*cs_lds)[NT / 64][BN], float* prow, const bf16_t* kc_bh, const bf16_t* kn_bh,
+    const bf16_t* vc_bh, const bf16_t* vn_bh, const int32_t* tp_bh, const Geo& g, int lane,
     float c) {
   const int wave = threadIdx.x >> 6;
   const int j0 = t * BN;
@@ -489,14 +562,18 @@ __device__ __forceinline__ void main_tile(
   const int jn = min(t + 3, t1 - 1) * BN;
   load_tile<D, NT>(kfill, tl, kc_bh, kn_bh, jn, g.M, g.Nk);
   load_tile<D, NT>(vfill, tl, vc_bh, vn_bh, jn, g.M, g.Nk);
+  if (MK == 2) rfill = load_rp(tp_bh, g.pos0, jn, g.M);
+  Rel rl;
+  if (MK == 2) load_rel(rl, rps[b0], lane);
   bf16x8 pb[NQB];
   scores_tile<D, NQB>(s_nxt, Ks[b1], qf, lane);
-  probs_tile<MASKED, NQB>(s_cur, pb, lam, qi, cs_lds[(t - t0) & 1][wave], j0, g.M, lane, c);
+  probs_tile<MK, NQB>(s_cur, pb, lam, qi, cs_lds[(t - t0) & 1][wave], j0, g.M, lane, c, rl);
   pv_tile<D, NQB>(oacc, pb, Vs[b0], lane);
-  interleave<2 * NQB * (D / 32), MASKED ? 5 : 4>();
+  interleave<2 * NQB * (D / 32), MK ? 5 : 4>();
   interleave<NQB * (D / 16), 1>();
   store_tile<D, NT>(Ks[b2], tl.loff, kput);
   store_tile<D, NT>(Vs[b2], tl.vloff, vput);
+  if (MK == 2) store_rp(rps[b2], rput);
   __syncthreads();
   if (threadIdx.x < BN) {
     const float (*cs)[BN] = cs_lds[(t - t0) & 1];
@@ -507,30 +584,30 @@ __device__ __forceinline__ void main_tile(
   }
 }
 
-template <bool MASKED, int D, int NT, int NQB>
+template <int MK, int D, int NT, int NQB>
 __device__ __forceinline__ void main_loop(int ta, int tb, int t0, int t1, MainState<D, NT, NQB>& S,
                                           const Tile<D, NT>& tl,
                                           bf16_t (*Ks)[BN * kstride(D)],
-                                          bf16_t (*Vs)[BN * vstride(D)],
+                                          bf16_t (*Vs)[BN * vstride(D)], int (*rps)[BN],
                                           const bf16x8 (&qf)[NQB][D / 32],
                                           const float (&lam)[NQB], const int (&qi)[NQB],
                                           float (*cs_lds)[NT / 64][BN], float* prow,
                                           const bf16_t* kc_bh, const bf16_t* kn_bh,
-                                          const bf16_t* vc_bh, const bf16_t* vn_bh, const Geo& g,
-                                          int lane, float c) {
+                                          const bf16_t* vc_bh, const bf16_t* vn_bh,
+                                          const int32_t* tp_bh, const Geo& g, int lane, float c) {
   int t = ta;
   for (; t + 1 < tb; t += 2) {
-    main_tile<MASKED, D, NT, NQB>(t, t0, t1, S.sa, S.sb, S.oacc, S.kb, S.vb, S.ka, S.va, tl, Ks,
-                                  Vs, qf, lam, qi, cs_lds, prow, kc_bh, kn_bh, vc_bh, vn_bh, g,
-                                  lane, c);
-    main_tile<MASKED, D, NT, NQB>(t + 1, t0, t1, S.sb, S.sa, S.oacc, S.ka, S.va, S.kb, S.vb, tl,
-                                  Ks, Vs, qf, lam, qi, cs_lds, prow, kc_bh, kn_bh, vc_bh, vn_bh,
-                                  g, lane, c);
+    main_tile<MK, D, NT, NQB>(t, t0, t1, S.sa, S.sb, S.oacc, S.kb, S.vb, S.ka, S.va, S.rb, S.ra,
+                              tl, Ks, Vs, rps, qf, lam, qi, cs_lds, prow, kc_bh, kn_bh, vc_bh,
+                              vn_bh, tp_bh, g, lane, c);
+    main_tile<MK, D, NT, NQB>(t + 1, t0, t1, S.sb, S.sa, S.oacc, S.ka, S.va, S.kb, S.vb, S.ra,
+                              S.rb, tl, Ks, Vs, rps, qf, lam, qi, cs_lds, prow, kc_bh, kn_bh,
+                              vc_bh, vn_bh, tp_bh, g, lane, c);
   }
   if (t < tb) {
-    main_tile<MASKED, D, NT, NQB>(t, t0, t1, S.sa, S.sb, S.oacc, S.kb, S.vb, S.ka, S.va, tl, Ks,
-                                  Vs, qf, lam, qi, cs_lds, prow, kc_bh, kn_bh, vc_bh, vn_bh, g,
-                                  lane, c);
+    main_tile<MK, D, NT, NQB>(t, t0, t1, S.sa, S.sb, S.oacc, S.kb, S.vb, S.ka, S.va, S.rb, S.ra,
+                              tl, Ks, Vs, rps, qf, lam, qi, cs_lds, prow, kc_bh, kn_bh, vc_bh,
+                              vn_bh, tp_bh, g, lane, c);
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -540,10 +617,11 @@ __device__ __forceinline__ void main_loop(int ta, int tb, int t0, int t1, MainSt
       S.ka[e] = S.kb[e];
       S.va[e] = S.vb[e];
     }
+    S.ra = S.rb;
   }
 }
 
-template <int D, int NW, int NQB>
+template <int D, int NW, int NQB, bool CACHE>
 __global__ __launch_bounds__(NW * 64) void main_pass(Geo g, int Hq, int Hkv, int nsplit,
                                                      int nsplit_lse, float c_log2,
                                                      const float2* __restrict__ stats,
@@ -552,8 +630,10 @@ __global__ __launch_bounds__(NW * 64) void main_pass(Geo g, int Hq, int Hkv, int
                                                      float* __restrict__ opart,
                                                      float* __restrict__ lse_out) {
   constexpr int NT = NW * 64, ROWS = NW * NQB * 16;
+  constexpr int MKM = CACHE ? 2 : 1;   // mask mode of the masked tiles
   __shared__ __attribute__((aligned(16))) bf16_t Ks[NBUF][BN * kstride(D)];
   __shared__ __attribute__((aligned(16))) bf16_t Vs[NBUF][BN * vstride(D)];
+  __shared__ __attribute__((aligned(16))) int rps[NBUF][BN];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const BlockId id = block_id(nsplit);
   const int rt = id.rt, sp = id.sp;
@@ -561,14 +641,15 @@ __global__ __launch_bounds__(NW * 64) void main_pass(Geo g, int Hq, int Hkv, int
   const int BH = gridDim.y;
   const int b = (int)(bh / Hkv), h = (int)(bh % Hkv);
   const int row0 = rt * ROWS, wrow0 = row0 + wave * NQB * 16;
-  const int kv_end = kv_end_for_rows(min(row0 + ROWS, g.R), g.G, g.T, g.M);
+  const int kv_end = kv_end_for_rows(min(row0 + ROWS, g.R), g.G, g.T, g.M, g.Tk);
   int t0, t1;
   split_range((kv_end + BN - 1) / BN, nsplit, sp, t0, t1);
-  const int t_mask = min(t1, max(t0, first_masked_tile(g.M, min(row0, g.R - 1) / g.G)));
+  const int t_mask = mask_start<CACHE>(g, row0, t0, t1);
   const bf16_t* kc_bh = g.kc + bh * (size_t)g.M * D;
-  const bf16_t* kn_bh = g.kn + bh * (size_t)g.T * D;
+  const bf16_t* kn_bh = CACHE ? nullptr : g.kn + bh * (size_t)g.T * D;
   const bf16_t* vc_bh = g.vc + bh * (size_t)g.M * D;
-  const bf16_t* vn_bh = g.vn + bh * (size_t)g.T * D;
+  const bf16_t* vn_bh = CACHE ? nullptr : g.vn + bh * (size_t)g.T * D;
+  const int32_t* tp_bh = CACHE ? g.tp + bh * (size_t)g.M : nullptr;
 
   bf16x8 qf[NQB][D / 32];
   load_q<D, NQB>(qf, g, b, h, Hq, wrow0, lane);
@@ -587,13 +668,16 @@ __global__ __launch_bounds__(NW * 64) void main_pass(Geo g, int Hq, int Hkv, int
         const float2 st = stats[((size_t)s * BH + bh) * g.R + r];
         if (st.y > 0.f) L += st.y * __builtin_amdgcn_exp2f(st.x - mx);
       }
-      lam[qb] = mx + __log2f(L);
+      // a row that sees no key (cache mode only) has no softmax: every
+      // probability is 0 and its lse is -inf
+      lam[qb] = L > 0.f ? mx + __log2f(L) : INFINITY;
     } else {
       lam[qb] = INFINITY;   // padding rows: every probability is 0
     }
     if (sp == 0 && lane < 16 && r < g.R) {
       const int i = r / g.G, gg = r % g.G;
-      lse_out[(size_t)(b * Hq + h * g.G + gg) * g.T + i] = lam[qb] * kLn2;
+      lse_out[(size_t)(b * Hq + h * g.G + gg) * g.T + i] =
+          lam[qb] == INFINITY ? -INFINITY : lam[qb] * kLn2;
     }
   }
 
@@ -613,6 +697,11 @@ __global__ __launch_bounds__(NW * 64) void main_pass(Geo g, int Hq, int Hkv, int
     load_tile<D, NT>(S.va, tl, vc_bh, vn_bh, t0 * BN, g.M, g.Nk);
     load_tile<D, NT>(S.kb, tl, kc_bh, kn_bh, j1, g.M, g.Nk);
     load_tile<D, NT>(S.vb, tl, vc_bh, vn_bh, j1, g.M, g.Nk);
+    if (CACHE) {
+      store_rp(rps[0], load_rp(tp_bh, g.pos0, t0 * BN, g.M));
+      store_rp(rps[1], load_rp(tp_bh, g.pos0, j1, g.M));
+      S.ra = load_rp(tp_bh, g.pos0, j2, g.M);
+    }
     store_tile<D, NT>(Ks[0], tl.loff, S.ka);
     store_tile<D, NT>(Vs[0], tl.vloff, S.va);
     store_tile<D, NT>(Ks[1], tl.loff, S.kb);
@@ -621,12 +710,10 @@ __global__ __launch_bounds__(NW * 64) void main_pass(Geo g, int Hq, int Hkv, int
     load_tile<D, NT>(S.va, tl, vc_bh, vn_bh, j2, g.M, g.Nk);
     __syncthreads();
     scores_tile<D, NQB>(S.sa, Ks[0], qf, lane);
-    main_loop<false, D, NT, NQB>(t0, t_mask, t0, t1, S, tl, Ks, Vs, qf, lam, qi, cs_lds, prow,
-                                 kc_bh, kn_bh,
-                                 vc_bh, vn_bh, g, lane, c_log2);
-    main_loop<true, D, NT, NQB>(t_mask, t1, t0, t1, S, tl, Ks, Vs, qf, lam, qi, cs_lds, prow,
-                                kc_bh, kn_bh,
-                                vc_bh, vn_bh, g, lane, c_log2);
+    main_loop<0, D, NT, NQB>(t0, t_mask, t0, t1, S, tl, Ks, Vs, rps, qf, lam, qi, cs_lds, prow,
+                             kc_bh, kn_bh, vc_bh, vn_bh, tp_bh, g, lane, c_log2);
+    main_loop<MKM, D, NT, NQB>(t_mask, t1, t0, t1, S, tl, Ks, Vs, rps, qf, lam, qi, cs_lds,
+                               prow, kc_bh, kn_bh, vc_bh, vn_bh, tp_bh, g, lane, c_log2);
   }
   // write O (lane: query qb*16 + l%16, d = db*16 + 4*(l/16) + r)
 #pragma unroll
@@ -687,23 +774,28 @@ static_assert(kLseWaves * kLseQB == kMainWaves * kMainQB, "one row tiling");
 template <int D>
 hipError_t run(const Shape& s, const Plan& p, const void* q, const void* kc, const void* vc,
                const void* kn, const void* vn, void* out, float* lse, float* wsum, char* ws,
-               float scale, hipStream_t st) {
+               float scale, KeyPos kp, hipStream_t st) {
   constexpr int ROWS = kMainWaves * kMainQB * 16;
-  Geo g{s.G(), s.T, s.M, s.R(), s.Nk(), (const bf16_t*)q, (const bf16_t*)kc,
-        (const bf16_t*)vc, (const bf16_t*)kn, (const bf16_t*)vn};
+  Geo g{s.G(), s.T, s.M, s.R(), s.Nk(), s.Tk(), (const bf16_t*)q, (const bf16_t*)kc,
+        (const bf16_t*)vc, (const bf16_t*)kn, (const bf16_t*)vn, kp.tp, kp.pos0};
+  const bool cache = s.cache_only;
   const int nrt = (s.R() + ROWS - 1) / ROWS;
   dim3 grid(nrt * p.nsplit, s.BH()), grid_lse(nrt * p.nsplit_lse, s.BH());
   const float c = scale * kLog2e;
   float2* stats = reinterpret_cast<float2*>(ws + p.off_stats);
   float* parts = reinterpret_cast<float*>(ws + p.off_parts);
   float* opart = reinterpret_cast<float*>(ws + p.off_opart);
-  hipError_t e = launch_kernel(K_MFMA_LSE, lse_pass<D, kLseWaves, kLseQB>, grid_lse,
-                               dim3(kLseWaves * 64), st, g, s.Hq, s.Hkv, p.nsplit_lse, c, stats);
+  hipError_t e = launch_kernel(K_MFMA_LSE,
+                               cache ? lse_pass<D, kLseWaves, kLseQB, true>
+                                     : lse_pass<D, kLseWaves, kLseQB, false>,
+                               grid_lse, dim3(kLseWaves * 64), st, g, s.Hq, s.Hkv, p.nsplit_lse, c,
+                               stats);
   if (e != hipSuccess) return e;
-  e = launch_kernel(K_MFMA_MAIN, main_pass<D, kMainWaves, kMainQB>, grid, dim3(kMainWaves * 64),
-                    st, g, s.Hq, s.Hkv,
-                    p.nsplit, p.nsplit_lse, c, (const float2*)stats, parts, p.parts_ld,
-                    (bf16_t*)out, opart, lse);
+  e = launch_kernel(K_MFMA_MAIN,
+                    cache ? main_pass<D, kMainWaves, kMainQB, true>
+                          : main_pass<D, kMainWaves, kMainQB, false>,
+                    grid, dim3(kMainWaves * 64), st, g, s.Hq, s.Hkv, p.nsplit, p.nsplit_lse, c,
+                    (const float2*)stats, parts, p.parts_ld, (bf16_t*)out, opart, lse);
   if (e != hipSuccess) return e;
   if (p.nsplit > 1) {
     const size_t n4 = (size_t)s.BH() * s.R() * s.d / 4;
@@ -724,9 +816,9 @@ int mfma_rows_per_part() { return kMainWaves * kMainQB * 16; }
 
 hipError_t launch_sdpa_mfma(const Shape& s, const Plan& p, const void* q, const void* kc,
                             const void* vc, const void* kn, const void* vn, void* out, float* lse,
-                            float* wsum, char* ws, float scale, hipStream_t st) {
-  if (s.d == 64) return run<64>(s, p, q, kc, vc, kn, vn, out, lse, wsum, ws, scale, st);
-  return run<128>(s, p, q, kc, vc, kn, vn, out, lse, wsum, ws, scale, st);
+                            float* wsum, char* ws, float scale, KeyPos kp, hipStream_t st) {
+  if (s.d == 64) return run<64>(s, p, q, kc, vc, kn, vn, out, lse, wsum, ws, scale, kp, st);
+  return run<128>(s, p, q, kc, vc, kn, vn, out, lse, wsum, ws, scale, kp, st);
 }
 
 }  // namespace h2o

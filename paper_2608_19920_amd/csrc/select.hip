@@ -10,7 +10,8 @@ namespace {
 __global__ __launch_bounds__(256) void colsum_reduce_kernel(const float* __restrict__ parts,
                                                             float* __restrict__ wsum, int nparts,
                                                             int rows_per_part, int BH, int Nk,
-                                                            int ld, int G, int T, int M) {
+                                                            int ld, int G, int T, int M,
+                                                            int Tk) {
   const int j = blockIdx.x * blockDim.x + threadIdx.x;
   const int bh = blockIdx.y;
   if (j >= Nk) return;
@@ -18,7 +19,7 @@ __global__ __launch_bounds__(256) void colsum_reduce_kernel(const float* __restr
   float s = 0.f;
   for (int p = 0; p < nparts; ++p) {
     const int r1 = min((p + 1) * rows_per_part, R);
-    if (j < kv_end_for_rows(r1, G, T, M)) s += parts[((size_t)p * BH + bh) * ld + j];
+    if (j < kv_end_for_rows(r1, G, T, M, Tk)) s += parts[((size_t)p * BH + bh) * ld + j];
   }
   wsum[(size_t)bh * Nk + j] = s;
 }
@@ -167,7 +168,7 @@ __global__ __launch_bounds__(kInsThreads) void insert_kernel(
     const int i = i0 + e;
     const int slot = idx[row * k + i];
     if ((unsigned)slot >= (unsigned)M) continue;
-    scores[row * M + slot] = wsum[row * (size_t)(M + T) + M + i];
+    scores[row * M + slot] = wsum ? wsum[row * (size_t)(M + T) + M + i] : 0.f;
     if (token_pos) token_pos[row * M + slot] = pos0 + i;
   }
 }
@@ -221,7 +222,7 @@ __global__ __launch_bounds__(kArgThreads) void argmin_insert_kernel(
     sh_slot = slot;
     idx[row] = slot;
     if ((unsigned)slot < (unsigned)M) {
-      scores[row * M + slot] = wsum[row * (size_t)(M + T) + M];
+      scores[row * M + slot] = wsum ? wsum[row * (size_t)(M + T) + M] : 0.f;
       if (token_pos) token_pos[row * M + slot] = pos0;
     }
   }
@@ -319,7 +320,8 @@ hipError_t launch_colsum_reduce(const Shape& s, const Plan& p, const float* part
                                 hipStream_t st) {
   dim3 grid((s.Nk() + 255) / 256, s.BH());
   return launch_kernel(K_COLSUM_REDUCE, colsum_reduce_kernel, grid, dim3(256), st, parts, wsum,
-                       p.nparts, p.rows_per_part, s.BH(), s.Nk(), p.parts_ld, s.G(), s.T, s.M);
+                       p.nparts, p.rows_per_part, s.BH(), s.Nk(), p.parts_ld, s.G(), s.T, s.M,
+                       s.Tk());
 }
 
 hipError_t launch_accumulate(float* scores, const float* wsum, int rows, int M, int T,

@@ -24,7 +24,8 @@ STATUS_NAMES = ["H2O_OK", "H2O_EINVAL", "H2O_ESHAPE", "H2O_EDTYPE", "H2O_EALIGN"
                 "H2O_EWORKSPACE", "H2O_ENODEVICE", "H2O_ELAUNCH"]
 EXPORTED = ["h2o_workspace_bytes", "h2o_sdpa_chunk", "h2o_accumulate_scores",
             "h2o_evict_insert", "h2o_evict_workspace_bytes", "h2o_evict_insert_policy",
-            "h2o_chunk_step", "h2o_bottomk", "h2o_last_error", "h2o_debug_force_path",
+            "h2o_chunk_step", "h2o_cache_workspace_bytes", "h2o_sdpa_cache",
+            "h2o_chunk_step_insert_first", "h2o_bottomk", "h2o_last_error", "h2o_debug_force_path",
             "h2o_debug_timing", "h2o_debug_kernel_time", "h2o_version"]
 KERNEL_IDS = {"generic_lse": 0, "generic_main": 1, "mfma_lse": 2, "mfma_main": 3,
               "split_reduce": 4, "colsum_reduce": 5, "accumulate": 6, "bottomk": 7,
@@ -69,6 +70,13 @@ def lib() -> ctypes.CDLL:
     L.h2o_evict_insert_policy.restype = i
     L.h2o_chunk_step.argtypes = [vp] * 12 + [sz] + [i] * 6 + [f, ctypes.c_int32, i, vp]
     L.h2o_chunk_step.restype = i
+    L.h2o_cache_workspace_bytes.argtypes = [i] * 8
+    L.h2o_cache_workspace_bytes.restype = sz
+    L.h2o_sdpa_cache.argtypes = [vp] * 8 + [sz] + [i] * 6 + [f, ctypes.c_int32, i, vp]
+    L.h2o_sdpa_cache.restype = i
+    L.h2o_chunk_step_insert_first.argtypes = [vp] * 12 + [sz] + [i] * 6 + \
+        [f, ctypes.c_int32, i, i, vp]
+    L.h2o_chunk_step_insert_first.restype = i
     L.h2o_bottomk.argtypes = [vp, i, i, i, vp, vp]
     L.h2o_bottomk.restype = i
     L.h2o_last_error.argtypes = []
@@ -280,6 +288,73 @@ def h2o_chunk_step(q, k_cache, v_cache, scores, token_pos, k_new, v_new, out, ls
         B, Hq, Hkv, T, M, d, float(scale), int(pos0), dt, _stream(stream)))
 
 
+def h2o_cache_workspace_bytes(B, Hq, Hkv, T, M, d, dtype, policy="h2o") -> int:
+    code = dtype if isinstance(dtype, int) else _dtype_code(torch.empty(0, dtype=dtype))
+    return int(lib().h2o_cache_workspace_bytes(B, Hq, Hkv, T, M, d, code,
+                                               _policy_code(policy)))
+
+
+def _cache_args(q, k_cache, v_cache, token_pos, out, lse, wsum):
+    B, Hq, T, d = q.shape
+    Hkv, M = k_cache.shape[1], k_cache.shape[2]
+    for name, t in (("k_cache", k_cache), ("v_cache", v_cache), ("out", out)):
+        if t.dtype != q.dtype:
+            raise TypeError(f"{name} dtype {t.dtype} != q dtype {q.dtype}")
+    if tuple(k_cache.shape) != (B, Hkv, M, d) or tuple(v_cache.shape) != (B, Hkv, M, d) or \
+            tuple(out.shape) != (B, Hq, T, d):
+        raise ValueError("shape mismatch")
+    if token_pos is None or token_pos.dtype != torch.int32 or \
+            tuple(token_pos.shape) != (B, Hkv, M):
+        raise ValueError("token_pos must be int32 [B,Hkv,M]")
+    if tuple(lse.shape) != (B, Hq, T) or lse.dtype != torch.float32:
+        raise ValueError("lse must be float32 [B,Hq,T]")
+    if tuple(wsum.shape) != (B, Hkv, M) or wsum.dtype != torch.float32:
+        raise ValueError("wsum must be float32 [B,Hkv,M]")
+    return B, Hq, Hkv, T, M, d
+
+
+def h2o_sdpa_cache(q, k_cache, v_cache, token_pos, out, lse, wsum, workspace, pos0: int,
+                   scale: Optional[float] = None, stream=None) -> None:
+    """Attention of the T queries (positions pos0..) over the cache slots,
+    masked by token_pos; wsum [B,Hkv,M] f32; workspace uint8 of
+    h2o_cache_workspace_bytes(...) bytes."""
+    B, Hq, Hkv, T, M, d = _cache_args(q, k_cache, v_cache, token_pos, out, lse, wsum)
+    if scale is None:
+        scale = d ** -0.5
+    nbytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(lib().h2o_sdpa_cache(
+        _dev(q, "q"), _dev(k_cache, "k_cache"), _dev(v_cache, "v_cache"),
+        _dev(token_pos, "token_pos"), _dev(out, "out"), _dev(lse, "lse"), _dev(wsum, "wsum"),
+        _dev(workspace, "workspace"), nbytes, B, Hq, Hkv, T, M, d, float(scale), int(pos0),
+        _dtype_code(q), _stream(stream)))
+
+
+def h2o_chunk_step_insert_first(q, k_cache, v_cache, scores, token_pos, k_new, v_new, out, lse,
+                                wsum, evict_idx, workspace, pos0: int,
+                                scale: Optional[float] = None, policy="h2o",
+                                stream=None) -> None:
+    """Evict by ``policy`` (scores after pos0 tokens), insert the chunk, attend
+    with the token-position mask, accumulate; wsum [B,Hkv,M]."""
+    B, Hq, Hkv, T, M, d = _cache_args(q, k_cache, v_cache, token_pos, out, lse, wsum)
+    if k_new.dtype != q.dtype or v_new.dtype != q.dtype or \
+            tuple(k_new.shape) != (B, Hkv, T, d) or tuple(v_new.shape) != (B, Hkv, T, d):
+        raise ValueError("k_new/v_new must be [B,Hkv,T,d] in q's dtype")
+    if tuple(scores.shape) != (B, Hkv, M) or scores.dtype != torch.float32:
+        raise ValueError("scores must be float32 [B,Hkv,M]")
+    if tuple(evict_idx.shape) != (B, Hkv, T) or evict_idx.dtype != torch.int32:
+        raise ValueError("evict_idx must be int32 [B,Hkv,T]")
+    if scale is None:
+        scale = d ** -0.5
+    nbytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    _check(lib().h2o_chunk_step_insert_first(
+        _dev(q, "q"), _dev(k_cache, "k_cache"), _dev(v_cache, "v_cache"),
+        _dev(scores, "scores"), _dev(token_pos, "token_pos"), _dev(k_new, "k_new"),
+        _dev(v_new, "v_new"), _dev(out, "out"), _dev(lse, "lse"), _dev(wsum, "wsum"),
+        _dev(evict_idx, "evict_idx"), _dev(workspace, "workspace"), nbytes,
+        B, Hq, Hkv, T, M, d, float(scale), int(pos0), _dtype_code(q), _policy_code(policy),
+        _stream(stream)))
+
+
 def h2o_bottomk(scores, k: int, idx_out, stream=None) -> None:
     """scores [..., M] f32; idx_out [..., k] int32 (ascending indices)."""
     M = scores.shape[-1]
@@ -293,17 +368,23 @@ def h2o_bottomk(scores, k: int, idx_out, stream=None) -> None:
 
 
 # ------------------------------------------------------------ conveniences
-def alloc_step(B, Hq, Hkv, T, M, d, dtype, device="cuda", policy="h2o"):
+def alloc_step(B, Hq, Hkv, T, M, d, dtype, device="cuda", policy="h2o",
+               insert_first: bool = False):
     """Output and scratch tensors for one chunk step (``policy``'s eviction
-    workspace included)."""
+    workspace included); ``insert_first``: for the paper's order
+    (h2o_chunk_step_insert_first / h2o_sdpa_cache, wsum of M columns)."""
     code = _dtype_code(torch.empty(0, dtype=dtype))
-    ws = h2o_workspace_bytes(B, Hq, Hkv, T, M, d, code)
+    if insert_first:
+        ws = h2o_cache_workspace_bytes(B, Hq, Hkv, T, M, d, code, policy)
+    else:
+        ws = h2o_workspace_bytes(B, Hq, Hkv, T, M, d, code)
     ews = h2o_evict_workspace_bytes(B, Hkv, M, T, policy)
     return dict(
         evict_workspace=torch.empty(max(ews, 16), dtype=torch.uint8, device=device),
         out=torch.empty(B, Hq, T, d, dtype=dtype, device=device),
         lse=torch.empty(B, Hq, T, dtype=torch.float32, device=device),
-        wsum=torch.empty(B, Hkv, M + T, dtype=torch.float32, device=device),
+        wsum=torch.empty(B, Hkv, M + (0 if insert_first else T), dtype=torch.float32,
+                         device=device),
         workspace=torch.empty(max(ws, 16), dtype=torch.uint8, device=device),
         evict_idx=torch.empty(B, Hkv, T, dtype=torch.int32, device=device),
     )

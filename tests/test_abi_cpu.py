@@ -175,6 +175,70 @@ def test_chunk_step_rejects(L, kw, code):
     assert len(L.h2o_last_error()) > 0
 
 
+def _cache(L, **kw):
+    a = dict(q=P, kc=P, vc=P, tp=P, out=P, lse=P, w=P, ws=P, wsb=1 << 40, B=1, Hq=4, Hkv=2, T=8,
+             M=16, d=64, scale=0.125, pos0=100, dt=1, st=None)
+    a.update(kw)
+    return L.h2o_sdpa_cache(a["q"], a["kc"], a["vc"], a["tp"], a["out"], a["lse"], a["w"],
+                            a["ws"], a["wsb"], a["B"], a["Hq"], a["Hkv"], a["T"], a["M"], a["d"],
+                            a["scale"], a["pos0"], a["dt"], a["st"])
+
+
+def _step_if(L, **kw):
+    a = dict(q=P, kc=P, vc=P, sc=P, tp=P, kn=P, vn=P, out=P, lse=P, w=P, idx=P, ws=P,
+             wsb=1 << 40, B=1, Hq=4, Hkv=2, T=4, M=16, d=64, scale=0.125, pos0=16, dt=1, pol=0,
+             st=None)
+    a.update(kw)
+    return L.h2o_chunk_step_insert_first(
+        a["q"], a["kc"], a["vc"], a["sc"], a["tp"], a["kn"], a["vn"], a["out"], a["lse"],
+        a["w"], a["idx"], a["ws"], a["wsb"], a["B"], a["Hq"], a["Hkv"], a["T"], a["M"], a["d"],
+        a["scale"], a["pos0"], a["dt"], a["pol"], a["st"])
+
+
+def test_cache_workspace_bytes(L):
+    base = L.h2o_cache_workspace_bytes(2, 8, 2, 16, 1000, 64, 1, 0)
+    assert base > 0 and base % 256 == 0
+    # the policy's eviction scratch comes on top (h2o_norm: B*Hkv*M floats)
+    assert L.h2o_cache_workspace_bytes(2, 8, 2, 16, 1000, 64, 1, 1) == base + 16128
+    assert L.h2o_cache_workspace_bytes(2, 8, 2, 16, 0, 64, 1, 0) == 0      # M >= 1
+    assert L.h2o_cache_workspace_bytes(2, 8, 2, 16, 1000, 64, 1, 5) == 0   # policy
+    assert L.h2o_cache_workspace_bytes(2, 8, 3, 16, 1000, 64, 1, 0) == 0   # Hq % Hkv
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(tp=None), H.H2O_EINVAL),
+    (dict(M=0), H.H2O_EINVAL),
+    (dict(q=None), H.H2O_EINVAL),
+    (dict(w=None), H.H2O_EINVAL),
+    (dict(tp=MIS), H.H2O_EALIGN),
+    (dict(lse=MIS), H.H2O_EALIGN),
+    (dict(dt=4), H.H2O_EDTYPE),
+    (dict(d=80), H.H2O_ESHAPE),
+    (dict(scale=float("inf")), H.H2O_EINVAL),
+    (dict(wsb=32), H.H2O_EWORKSPACE),
+])
+def test_sdpa_cache_rejects(L, kw, code):
+    assert _cache(L, **kw) == code
+    assert len(L.h2o_last_error()) > 0
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(tp=None), H.H2O_EINVAL),
+    (dict(sc=None), H.H2O_EINVAL),
+    (dict(kn=None), H.H2O_EINVAL),
+    (dict(idx=None), H.H2O_EINVAL),
+    (dict(M=3), H.H2O_EINVAL),
+    (dict(pol=9), H.H2O_EINVAL),
+    (dict(sc=MIS), H.H2O_EALIGN),
+    (dict(vn=MIS), H.H2O_EALIGN),
+    (dict(pol=1, wsb=64), H.H2O_EWORKSPACE),
+    (dict(dt=2), H.H2O_EDTYPE),
+])
+def test_step_insert_first_rejects(L, kw, code):
+    assert _step_if(L, **kw) == code
+    assert len(L.h2o_last_error()) > 0
+
+
 @pytest.mark.parametrize("args,code", [
     ((P, 4, 10, 11, P, None), H.H2O_EINVAL),
     ((P, 4, 10, -1, P, None), H.H2O_EINVAL),
@@ -207,6 +271,9 @@ def test_no_device_is_reported(L):
         assert _evict_policy(L, pol=pol) == H.H2O_ENODEVICE
     assert _evict_policy(L, pol=0, ws=None, wsb=0) == H.H2O_ENODEVICE
     assert _evict_policy(L, pol=2, tp=None) == H.H2O_ENODEVICE
+    assert _cache(L) == H.H2O_ENODEVICE
+    for pol in (0, 1, 2):
+        assert _step_if(L, pol=pol) == H.H2O_ENODEVICE
 
 
 def test_binding_raises_typed_errors(L):

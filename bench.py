@@ -11,7 +11,9 @@ bytes per second (GB/s) over the timed steps.
 The chunked-prefill shapes (d=128: B1 Hq32 Hkv8 M8192 T1024; B4 Hq32 Hkv8
 M32768 T512; B2 Hq28 Hkv4 M16384 T2048) are timed too and reported under
 "prefill" as TFLOP/s of algorithmic attention work W = 4 d P B Hq,
-P = T*M + T(T+1)/2.
+P = T*M + T(T+1)/2. "insert_first" times the paper's own order of a step
+(insert the chunk, then attend with the token-position mask) on the same
+shapes, with P = (M - T)*T + T(T+1)/2 there.
 
 Prints one JSON line. ``--gpus N`` with N > 1 exits: this build runs on one GPU.
 """
@@ -196,6 +198,104 @@ def bench_prefill(name, args, torch, H, W):
                               "traffic": traffic_for("mfma_main", w.name)}}
 
 
+# --------------------------------------------- the paper's order: insert first
+def insert_first_flops(w) -> float:
+    """Attention work of h2o_sdpa_cache after the chunk is in the cache: the
+    M - T older slots are seen by all T queries, chunk key i by queries >= i."""
+    P = (w.M - w.T) * w.T + w.T * (w.T + 1) / 2
+    return 4.0 * w.d * P * w.B * w.Hq
+
+
+def insert_first_step_bytes(w) -> int:
+    """Algorithmic HBM bytes of one insert-first token step (T = 1)."""
+    return decode_step_bytes(w) + w.B * w.Hkv * w.M * 4     # + the token positions read
+
+
+def bench_insert_first(args, torch, H, W):
+    """h2o_chunk_step_insert_first on the decode workload (8 layer states, one
+    HIP graph) and h2o_sdpa_cache / the whole insert-first step on the
+    prefill workloads."""
+    bf = torch.bfloat16
+    w = W.WORKLOADS["decode_bf16"]
+    layers = []
+    for layer in range(LAYERS):
+        x = W.make_inputs(w, seed=layer)
+        st = _dev_state(x, torch)
+        to = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to("cuda").to(bf)
+        inp = (to(x["q_steps"][0]), to(x["k_new_steps"][0]), to(x["v_new_steps"][0]),
+               int(x["pos0"]), float(x["scale"]))
+        layers.append((st, inp, H.alloc_step(w.B, w.Hq, w.Hkv, w.T, w.M, w.d, bf,
+                                             insert_first=True)))
+    del x
+
+    def step():
+        for st, (q, kn, vn, pos0, scale), b in layers:
+            H.h2o_chunk_step_insert_first(q, st["k_cache"], st["v_cache"], st["scores"],
+                                          st["token_pos"], kn, vn, b["out"], b["lse"], b["wsum"],
+                                          b["evict_idx"], b["workspace"], pos0, scale)
+
+    stream = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    with torch.cuda.stream(stream):
+        step()
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=stream):
+        step()
+    torch.cuda.synchronize()
+    for _ in range(args.warmup):
+        graph.replay()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(args.steps):
+        graph.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    gbs = insert_first_step_bytes(w) * LAYERS / (ms * 1e-3) / 1e9
+    out = {"decode": {"workload": w.describe() + f", {LAYERS} layer states",
+                      "us_per_step": round(ms * 1e3, 1), "gbs": round(gbs, 1),
+                      "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4)},
+           "prefill": []}
+    del layers, graph
+    torch.cuda.empty_cache()
+    for name in PREFILL:
+        w = W.WORKLOADS[name]
+        x = W.make_inputs(w, seed=0)
+        st = _dev_state(x, torch)
+        to = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to("cuda").to(bf)
+        q, kn, vn = to(x["q"]), to(x["k_new"]), to(x["v_new"])
+        pos0, scale = int(x["pos0"]), float(x["scale"])
+        del x
+        b = H.alloc_step(w.B, w.Hq, w.Hkv, w.T, w.M, w.d, bf, insert_first=True)
+        full = lambda: H.h2o_chunk_step_insert_first(
+            q, st["k_cache"], st["v_cache"], st["scores"], st["token_pos"], kn, vn, b["out"],
+            b["lse"], b["wsum"], b["evict_idx"], b["workspace"], pos0, scale)
+        sdpa = lambda: H.h2o_sdpa_cache(q, st["k_cache"], st["v_cache"], st["token_pos"],
+                                        b["out"], b["lse"], b["wsum"], b["workspace"], pos0,
+                                        scale)
+        full()                     # the chunk is in the cache from here on
+        reps = max(3, args.steps // 5)
+        res = {}
+        for tag, fn in (("sdpa_cache", sdpa), ("full_step", full)):
+            fn()
+            torch.cuda.synchronize()
+            e0.record()
+            for _ in range(reps):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            res[tag] = e0.elapsed_time(e1) / reps
+        tf = insert_first_flops(w) / (res["sdpa_cache"] * 1e-3) / 1e12
+        out["prefill"].append({"workload": w.describe(), "tflops": round(tf, 1),
+                               "frac_of_bf16_peak": round(tf / BF16_PEAK_TFLOPS, 4),
+                               "ms_sdpa_cache": round(res["sdpa_cache"], 4),
+                               "ms_full_step": round(res["full_step"], 4)})
+        del st, q, kn, vn, b
+        torch.cuda.empty_cache()
+    return out
+
+
 # -------------------------------------------------------------- CPU baseline
 def cpu_baseline(w, budget_s, W):
     import oracle
@@ -252,6 +352,11 @@ def main():
             print(f"# {name}: {r['tflops']} TFLOP/s", file=sys.stderr, flush=True)
             prefill.append(r)
             torch.cuda.empty_cache()
+    ins = None
+    if not args.no_prefill:
+        ins = bench_insert_first(args, torch, H, W)
+        print(f"# insert-first decode: {ins['decode']['gbs']} GB/s; prefill "
+              f"{[r['tflops'] for r in ins['prefill']]} TFLOP/s", file=sys.stderr, flush=True)
     w = dec["w"]
     cpu = None
     if args.cpu_budget > 0:
@@ -271,6 +376,7 @@ def main():
         "roofline": dec["roofline"],
         "cpu_baseline": cpu,
         "prefill": prefill,
+        "insert_first": ins,
     }
     print(json.dumps(rec))
 

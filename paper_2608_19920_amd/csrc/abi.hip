@@ -525,10 +525,15 @@ int h2o_chunk_step_insert_first(const void* q, void* k_cache, void* v_cache, flo
   hipError_t e = launch_evict(policy, k_cache, v_cache, scores, token_pos, k_new, v_new, nullptr,
                               evict_idx, B, Hkv, M, T, d, T, pos0, pos0, eb,
                               ws + align256(p.bytes), st);
-  if (e == hipSuccess)
+  if (e == hipSuccess && p.path == 2) {
+    // the decode combine adds the summed weights to the scores itself
+    e = launch_sdpa_decode(s, p, q, k_cache, v_cache, nullptr, nullptr, out, lse, wsum, ws,
+                           scale, KeyPos{token_pos, pos0}, st, scores);
+  } else if (e == hipSuccess) {
     e = launch_sdpa(s, p, dtype, q, k_cache, v_cache, nullptr, nullptr, out, lse, wsum, ws,
                     scale, st, KeyPos{token_pos, pos0});
-  if (e == hipSuccess) e = launch_accumulate(scores, wsum, B * Hkv, M, 0, st);
+    if (e == hipSuccess) e = launch_accumulate(scores, wsum, B * Hkv, M, 0, st);
+  }
   if (e != hipSuccess) return fail(H2O_ELAUNCH, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
 }

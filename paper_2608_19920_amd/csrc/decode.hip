@@ -367,12 +367,14 @@ __device__ __forceinline__ float chunk_weight(const HeadStats& hs, int G) {
 // vn non-null, wsum rows of M + 1; cache mode: both null, rows of M).
 constexpr int kCols = 1024;
 
+// With scores non-null (cache mode only) it also adds each slot's summed
+// weight to its score: scores[j] += wsum[j], one float32 addition.
 template <int D>
 __global__ __launch_bounds__(kThreads) void decode_combine(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ kn, const bf16_t* __restrict__ vn,
     int Hq, int Hkv, int M, int nsplit, float c_log2, const float* __restrict__ logits,
     const float2* __restrict__ dstat, const float* __restrict__ dO, bf16_t* __restrict__ out,
-    float* __restrict__ lse, float* __restrict__ wsum) {
+    float* __restrict__ lse, float* __restrict__ wsum, float* __restrict__ scores) {
   __shared__ HeadStats hs;
   const int G = Hq / Hkv;
   const size_t bh = blockIdx.y;
@@ -383,8 +385,12 @@ __global__ __launch_bounds__(kThreads) void decode_combine(
   float* w = wsum + bh * (size_t)(M + (has_chunk ? 1 : 0));
   const float* lgb = logits + bh * (size_t)G * logit_pitch(M);
   const int c0 = blockIdx.x * kCols, c1 = min(M, c0 + kCols);
-  for (int j = c0 + threadIdx.x; j < c1; j += kThreads)
-    w[j] = slot_weight(hs, lgb, logit_pitch(M), G, j);
+  float* sc = scores ? scores + bh * (size_t)M : nullptr;
+  for (int j = c0 + threadIdx.x; j < c1; j += kThreads) {
+    const float wj = slot_weight(hs, lgb, logit_pitch(M), G, j);
+    w[j] = wj;
+    if (sc) sc[j] = sc[j] + wj;
+  }
   if (has_chunk && blockIdx.x == 0 && threadIdx.x == 0) w[M] = chunk_weight(hs, G);
 }
 
@@ -585,7 +591,7 @@ hipError_t launch_decode_split(const Shape& s, const Plan& p, const void* q, con
 hipError_t launch_sdpa_decode(const Shape& s, const Plan& p, const void* q, const void* kc,
                               const void* vc, const void* kn, const void* vn, void* out,
                               float* lse, float* wsum, char* ws, float scale, KeyPos kp,
-                              hipStream_t st) {
+                              hipStream_t st, float* scores_acc) {
   const float c = scale * kLog2e;
   int ns = 0;
   hipError_t e = launch_decode_split(s, p, q, kc, vc, ws, c, kp, st, &ns);
@@ -597,7 +603,8 @@ hipError_t launch_sdpa_decode(const Shape& s, const Plan& p, const void* q, cons
                        chunk ? (const bf16_t*)kn : nullptr, chunk ? (const bf16_t*)vn : nullptr,
                        s.Hq, s.Hkv, s.M, ns, c,
                        (const float*)(ws + p.off_logits), (const float2*)(ws + p.off_stats),
-                       (const float*)(ws + p.off_opart), (bf16_t*)out, lse, wsum);
+                       (const float*)(ws + p.off_opart), (bf16_t*)out, lse, wsum,
+                       chunk ? nullptr : scores_acc);
 }
 
 hipError_t launch_decode_step(const Shape& s, const Plan& p, const void* q, void* kc, void* vc,

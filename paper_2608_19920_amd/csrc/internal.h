@@ -150,10 +150,12 @@ hipError_t launch_sdpa_mfma(const Shape& s, const Plan& p, const void* q, const 
                             const void* vc, const void* kn, const void* vn, void* out,
                             float* lse, float* wsum, char* ws, float scale, KeyPos kp,
                             hipStream_t st);
+// scores_acc (cache mode only, may be nullptr): scores to which the summed
+// weights are added in the same pass (the accumulate of an insert-first step).
 hipError_t launch_sdpa_decode(const Shape& s, const Plan& p, const void* q, const void* kc,
                               const void* vc, const void* kn, const void* vn, void* out,
                               float* lse, float* wsum, char* ws, float scale, KeyPos kp,
-                              hipStream_t st);
+                              hipStream_t st, float* scores_acc = nullptr);
 // T == 1, one call for the whole step: split kernel, then one block per head
 // merges the splits, accumulates the scores, picks the slot and inserts.
 hipError_t launch_decode_step(const Shape& s, const Plan& p, const void* q, void* kc, void* vc,

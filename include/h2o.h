@@ -136,6 +136,32 @@ int h2o_evict_insert(void* k_cache, void* v_cache, float* scores,
                      int M, int T, int d, int k, int32_t pos0, int dtype,
                      void* stream);
 
+/* h2o_chunk_step in two calls with the same arguments, for callers that
+ * overlap the cache maintenance of one layer with the attention of the next
+ * (the eviction of a layer is not needed by the next layer's queries):
+ *   h2o_chunk_step_attend  writes out and lse (and, except on the T == 1
+ *                          bf16 path, wsum);
+ *   h2o_chunk_step_evict   completes wsum, accumulates the scores, picks the
+ *                          slots and inserts the chunk.
+ * The evict call reads what the attend call left in the workspace: it must
+ * run after the attend call (same stream, or an event between streams), and
+ * nothing may use the workspace, scores, cache or token_pos of this state in
+ * between. Together they give the bits of h2o_chunk_step. */
+int h2o_chunk_step_attend(const void* q, void* k_cache, void* v_cache,
+                          float* scores, int32_t* token_pos, const void* k_new,
+                          const void* v_new, void* out, float* lse, float* wsum,
+                          int32_t* evict_idx, void* workspace,
+                          size_t workspace_bytes, int B, int Hq, int Hkv, int T,
+                          int M, int d, float scale, int32_t pos0, int dtype,
+                          void* stream);
+int h2o_chunk_step_evict(const void* q, void* k_cache, void* v_cache,
+                         float* scores, int32_t* token_pos, const void* k_new,
+                         const void* v_new, void* out, float* lse, float* wsum,
+                         int32_t* evict_idx, void* workspace,
+                         size_t workspace_bytes, int B, int Hq, int Hkv, int T,
+                         int M, int d, float scale, int32_t pos0, int dtype,
+                         void* stream);
+
 /* Bytes of device scratch h2o_evict_insert_policy needs (0 for
  * H2O_POLICY_H2O and on invalid arguments): the ranked keys (NORM: B*Hkv*M
  * floats; ORIG: Hkv*M floats plus Hkv*k indices). */

@@ -348,11 +348,20 @@ int h2o_sdpa_chunk(const void* q, const void* k_cache, const void* v_cache, cons
   return ok();
 }
 
-int h2o_chunk_step(const void* q, void* k_cache, void* v_cache, float* scores,
-                   int32_t* token_pos, const void* k_new, const void* v_new, void* out,
-                   float* lse, float* wsum, int32_t* evict_idx, void* workspace,
-                   size_t workspace_bytes, int B, int Hq, int Hkv, int T, int M, int d,
-                   float scale, int32_t pos0, int dtype, void* stream) {
+}  // extern "C"
+
+namespace h2o {
+namespace {
+
+enum StepPart { STEP_ALL, STEP_ATTEND, STEP_EVICT };
+
+// h2o_chunk_step and its two halves: validation shared, then the kernels of
+// the part asked for.
+int chunk_step(StepPart part, const void* q, void* k_cache, void* v_cache, float* scores,
+               int32_t* token_pos, const void* k_new, const void* v_new, void* out, float* lse,
+               float* wsum, int32_t* evict_idx, void* workspace, size_t workspace_bytes, int B,
+               int Hq, int Hkv, int T, int M, int d, float scale, int32_t pos0, int dtype,
+               void* stream) {
   Plan p;
   int rc = check_sdpa(q, k_cache, v_cache, k_new, v_new, out, lse, wsum, workspace,
                       workspace_bytes, B, Hq, Hkv, T, M, d, scale, dtype, &p);
@@ -366,27 +375,71 @@ int h2o_chunk_step(const void* q, void* k_cache, void* v_cache, float* scores,
   const Shape s{B, Hq, Hkv, T, M, d};
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   char* ws = reinterpret_cast<char*>(workspace);
-  hipError_t e;
+  hipError_t e = hipSuccess;
   if (p.path == 2) {
-    e = launch_decode_step(s, p, q, k_cache, v_cache, k_new, v_new, out, lse, wsum, scores,
-                           token_pos, evict_idx, pos0, ws, scale, st);
+    if (part == STEP_ALL)
+      e = launch_decode_step(s, p, q, k_cache, v_cache, k_new, v_new, out, lse, wsum, scores,
+                             token_pos, evict_idx, pos0, ws, scale, st);
+    else if (part == STEP_ATTEND)
+      e = launch_decode_attend(s, p, q, k_cache, v_cache, k_new, v_new, out, lse, ws, scale, st);
+    else
+      e = launch_decode_evict(s, p, q, k_cache, v_cache, k_new, v_new, wsum, scores, token_pos,
+                              evict_idx, pos0, ws, scale, st);
   } else {
     const int rows = B * Hkv, eb = dtype == H2O_F32 ? 4 : 2;
-    e = launch_sdpa(s, p, dtype, q, k_cache, v_cache, k_new, v_new, out, lse, wsum, workspace,
-                    scale, st);
-    if (e == hipSuccess) e = launch_accumulate(scores, wsum, rows, M, T, st);
-    if (e == hipSuccess && T == 1) {
-      e = launch_argmin_insert(k_cache, v_cache, scores, scores, 0, token_pos, k_new, v_new, wsum,
-                               evict_idx, rows, M, T, d, pos0, eb, st);
-    } else if (e == hipSuccess) {
-      e = launch_bottomk(scores, rows, M, T, evict_idx, st);
-      if (e == hipSuccess)
-        e = launch_insert(k_cache, v_cache, scores, token_pos, k_new, v_new, wsum, evict_idx,
-                          rows, M, T, d, T, pos0, eb, st);
+    if (part != STEP_EVICT)
+      e = launch_sdpa(s, p, dtype, q, k_cache, v_cache, k_new, v_new, out, lse, wsum, workspace,
+                      scale, st);
+    if (part != STEP_ATTEND) {
+      if (e == hipSuccess) e = launch_accumulate(scores, wsum, rows, M, T, st);
+      if (e == hipSuccess && T == 1) {
+        e = launch_argmin_insert(k_cache, v_cache, scores, scores, 0, token_pos, k_new, v_new,
+                                 wsum, evict_idx, rows, M, T, d, pos0, eb, st);
+      } else if (e == hipSuccess) {
+        e = launch_bottomk(scores, rows, M, T, evict_idx, st);
+        if (e == hipSuccess)
+          e = launch_insert(k_cache, v_cache, scores, token_pos, k_new, v_new, wsum, evict_idx,
+                            rows, M, T, d, T, pos0, eb, st);
+      }
     }
   }
   if (e != hipSuccess) return fail(H2O_ELAUNCH, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
+}
+
+}  // namespace
+}  // namespace h2o
+
+extern "C" {
+
+int h2o_chunk_step(const void* q, void* k_cache, void* v_cache, float* scores,
+                   int32_t* token_pos, const void* k_new, const void* v_new, void* out,
+                   float* lse, float* wsum, int32_t* evict_idx, void* workspace,
+                   size_t workspace_bytes, int B, int Hq, int Hkv, int T, int M, int d,
+                   float scale, int32_t pos0, int dtype, void* stream) {
+  return chunk_step(STEP_ALL, q, k_cache, v_cache, scores, token_pos, k_new, v_new, out, lse,
+                    wsum, evict_idx, workspace, workspace_bytes, B, Hq, Hkv, T, M, d, scale,
+                    pos0, dtype, stream);
+}
+
+int h2o_chunk_step_attend(const void* q, void* k_cache, void* v_cache, float* scores,
+                          int32_t* token_pos, const void* k_new, const void* v_new, void* out,
+                          float* lse, float* wsum, int32_t* evict_idx, void* workspace,
+                          size_t workspace_bytes, int B, int Hq, int Hkv, int T, int M, int d,
+                          float scale, int32_t pos0, int dtype, void* stream) {
+  return chunk_step(STEP_ATTEND, q, k_cache, v_cache, scores, token_pos, k_new, v_new, out, lse,
+                    wsum, evict_idx, workspace, workspace_bytes, B, Hq, Hkv, T, M, d, scale,
+                    pos0, dtype, stream);
+}
+
+int h2o_chunk_step_evict(const void* q, void* k_cache, void* v_cache, float* scores,
+                         int32_t* token_pos, const void* k_new, const void* v_new, void* out,
+                         float* lse, float* wsum, int32_t* evict_idx, void* workspace,
+                         size_t workspace_bytes, int B, int Hq, int Hkv, int T, int M, int d,
+                         float scale, int32_t pos0, int dtype, void* stream) {
+  return chunk_step(STEP_EVICT, q, k_cache, v_cache, scores, token_pos, k_new, v_new, out, lse,
+                    wsum, evict_idx, workspace, workspace_bytes, B, Hq, Hkv, T, M, d, scale,
+                    pos0, dtype, stream);
 }
 
 int h2o_accumulate_scores(float* scores, const float* wsum, int B, int Hkv, int M, int T,

@@ -364,7 +364,8 @@ __device__ __forceinline__ float chunk_weight(const HeadStats& hs, int G) {
 
 // Block (x, bh) writes wsum for columns [x*kCols, +kCols) of head bh; block
 // x == 0 also writes out, lse and the chunk key's column (chunk mode: kn and
-// vn non-null, wsum rows of M + 1; cache mode: both null, rows of M).
+// vn non-null, wsum rows of M + 1; cache mode: both null, rows of M). With
+// wsum null only out and lse are written (grid x = 1).
 constexpr int kCols = 1024;
 
 // With scores non-null (cache mode only) it also adds each slot's summed
@@ -382,6 +383,7 @@ __global__ __launch_bounds__(kThreads) void decode_combine(
   head_stats<D, kThreads>(hs, q, kn, dstat, Hq, Hkv, G, nsplit, c_log2, bh,
                           blockIdx.x == 0 ? lse : nullptr, has_chunk);
   if (blockIdx.x == 0) head_out<D, kThreads>(hs, vn, dO, out, Hq, Hkv, G, nsplit, bh);
+  if (!wsum) return;   // out and lse only (the attend half of a step)
   float* w = wsum + bh * (size_t)(M + (has_chunk ? 1 : 0));
   const float* lgb = logits + bh * (size_t)G * logit_pitch(M);
   const int c0 = blockIdx.x * kCols, c1 = min(M, c0 + kCols);
@@ -405,7 +407,9 @@ __global__ __launch_bounds__(kThreads) void decode_combine(
 constexpr int kFinThreads = 1024;
 constexpr int kFinCols = 8;   // slots per thread and pass
 
-template <int D, int G>
+// With OUT false the block skips out and lse (written by decode_combine in
+// an attend call): the eviction half of the step.
+template <int D, int G, bool OUT>
 __global__ __launch_bounds__(kFinThreads) void decode_finish(
     const bf16_t* __restrict__ q, bf16_t* __restrict__ kc, bf16_t* __restrict__ vc,
     const bf16_t* __restrict__ kn, const bf16_t* __restrict__ vn, int Hq, int Hkv, int M,
@@ -443,12 +447,12 @@ __global__ __launch_bounds__(kFinThreads) void decode_finish(
   // partials come in with the other early loads
   constexpr int kPre = 16;
   float pre[kPre];
-  const bool has_c = tid < G * D;
+  const bool has_c = OUT && tid < G * D;
 #pragma unroll
   for (int s = 0; s < kPre; ++s)
     pre[s] = has_c && s < nsplit ? dO[(bh * nsplit + s) * (size_t)(G * D) + tid] : 0.f;
   load_pass(0);
-  head_stats<D, NT>(hs, q, kn, dstat, Hq, Hkv, G, nsplit, c_log2, bh, lse);
+  head_stats<D, NT>(hs, q, kn, dstat, Hq, Hkv, G, nsplit, c_log2, bh, OUT ? lse : nullptr);
   if (has_c) {
     const float v = out_elem<D, kPre>(hs, vn, dO, pre, G, nsplit, bh, tid);
     const int b = (int)(bh / Hkv), h = (int)(bh % Hkv);
@@ -607,14 +611,13 @@ hipError_t launch_sdpa_decode(const Shape& s, const Plan& p, const void* q, cons
                        chunk ? nullptr : scores_acc);
 }
 
-hipError_t launch_decode_step(const Shape& s, const Plan& p, const void* q, void* kc, void* vc,
-                              const void* kn, const void* vn, void* out, float* lse,
-                              float* wsum, float* scores, int32_t* token_pos, int32_t* evict_idx,
-                              int32_t pos0, char* ws, float scale, hipStream_t st) {
-  const float c = scale * kLog2e;
-  int ns = 0;
-  hipError_t e = launch_decode_split(s, p, q, kc, vc, ws, c, KeyPos{nullptr, 0}, st, &ns);
-  if (e != hipSuccess) return e;
+namespace {
+
+// The finish kernel for this (d, G); out_too selects the fused form.
+hipError_t launch_finish(const Shape& s, const Plan& p, bool out_too, int ns, const void* q,
+                         void* kc, void* vc, const void* kn, const void* vn, void* out,
+                         float* lse, float* wsum, float* scores, int32_t* token_pos,
+                         int32_t* evict_idx, int32_t pos0, char* ws, float c, hipStream_t st) {
   const int G = s.G();
   auto go = [&](auto kern) {
     return launch_kernel(K_DECODE_FINISH, kern, dim3(s.BH()), dim3(kFinThreads), st,
@@ -624,17 +627,74 @@ hipError_t launch_decode_step(const Shape& s, const Plan& p, const void* q, void
                          (const float*)(ws + p.off_opart), (bf16_t*)out, lse, wsum, scores,
                          token_pos, evict_idx, pos0);
   };
+#define H2O_FIN(DD, GG) \
+  return out_too ? go(decode_finish<DD, GG, true>) : go(decode_finish<DD, GG, false>)
   if (s.d == 64) {
-    if (G == 1) return go(decode_finish<64, 1>);
-    if (G == 2) return go(decode_finish<64, 2>);
-    if (G == 4) return go(decode_finish<64, 4>);
-    if (G == 8) return go(decode_finish<64, 8>);
+    if (G == 1) H2O_FIN(64, 1);
+    if (G == 2) H2O_FIN(64, 2);
+    if (G == 4) H2O_FIN(64, 4);
+    if (G == 8) H2O_FIN(64, 8);
   } else {
-    if (G == 1) return go(decode_finish<128, 1>);
-    if (G == 2) return go(decode_finish<128, 2>);
-    if (G == 4) return go(decode_finish<128, 4>);
+    if (G == 1) H2O_FIN(128, 1);
+    if (G == 2) H2O_FIN(128, 2);
+    if (G == 4) H2O_FIN(128, 4);
   }
+#undef H2O_FIN
   return hipErrorInvalidValue;
+}
+
+// The split count the split kernel used for this shape (chunk mode).
+int split_count_for(const Shape& s) {
+  const int G = s.G();
+  if (s.M == 0) return 0;
+  if (s.d == 64) {
+    if (G == 1) return split_count<64, 1, false>(s.M, s.BH());
+    if (G == 2) return split_count<64, 2, false>(s.M, s.BH());
+    if (G == 4) return split_count<64, 4, false>(s.M, s.BH());
+    if (G == 8) return split_count<64, 8, false>(s.M, s.BH());
+  } else {
+    if (G == 1) return split_count<128, 1, false>(s.M, s.BH());
+    if (G == 2) return split_count<128, 2, false>(s.M, s.BH());
+    if (G == 4) return split_count<128, 4, false>(s.M, s.BH());
+  }
+  return 0;
+}
+
+}  // namespace
+
+hipError_t launch_decode_attend(const Shape& s, const Plan& p, const void* q, const void* kc,
+                                const void* vc, const void* kn, const void* vn, void* out,
+                                float* lse, char* ws, float scale, hipStream_t st) {
+  const float c = scale * kLog2e;
+  int ns = 0;
+  hipError_t e = launch_decode_split(s, p, q, kc, vc, ws, c, KeyPos{nullptr, 0}, st, &ns);
+  if (e != hipSuccess) return e;
+  auto combine = s.d == 64 ? decode_combine<64> : decode_combine<128>;
+  return launch_kernel(K_DECODE_COMBINE, combine, dim3(1, s.BH()), dim3(kThreads), st,
+                       (const bf16_t*)q, (const bf16_t*)kn, (const bf16_t*)vn, s.Hq, s.Hkv,
+                       s.M, ns, c, (const float*)(ws + p.off_logits),
+                       (const float2*)(ws + p.off_stats), (const float*)(ws + p.off_opart),
+                       (bf16_t*)out, lse, (float*)nullptr, (float*)nullptr);
+}
+
+hipError_t launch_decode_evict(const Shape& s, const Plan& p, const void* q, void* kc, void* vc,
+                               const void* kn, const void* vn, float* wsum, float* scores,
+                               int32_t* token_pos, int32_t* evict_idx, int32_t pos0, char* ws,
+                               float scale, hipStream_t st) {
+  return launch_finish(s, p, false, split_count_for(s), q, kc, vc, kn, vn, nullptr, nullptr,
+                       wsum, scores, token_pos, evict_idx, pos0, ws, scale * kLog2e, st);
+}
+
+hipError_t launch_decode_step(const Shape& s, const Plan& p, const void* q, void* kc, void* vc,
+                              const void* kn, const void* vn, void* out, float* lse,
+                              float* wsum, float* scores, int32_t* token_pos, int32_t* evict_idx,
+                              int32_t pos0, char* ws, float scale, hipStream_t st) {
+  const float c = scale * kLog2e;
+  int ns = 0;
+  hipError_t e = launch_decode_split(s, p, q, kc, vc, ws, c, KeyPos{nullptr, 0}, st, &ns);
+  if (e != hipSuccess) return e;
+  return launch_finish(s, p, true, ns, q, kc, vc, kn, vn, out, lse, wsum, scores, token_pos,
+                       evict_idx, pos0, ws, c, st);
 }
 
 }  // namespace h2o

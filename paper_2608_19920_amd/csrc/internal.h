@@ -162,6 +162,16 @@ hipError_t launch_decode_step(const Shape& s, const Plan& p, const void* q, void
                               const void* kn, const void* vn, void* out, float* lse,
                               float* wsum, float* scores, int32_t* token_pos, int32_t* evict_idx,
                               int32_t pos0, char* ws, float scale, hipStream_t st);
+// The same step as two calls: the attention (split, then out and lse) and
+// the eviction (summed weights, accumulate, argmin, insert) from the split
+// partials the attention left in the workspace. Same bits as the fused step.
+hipError_t launch_decode_attend(const Shape& s, const Plan& p, const void* q, const void* kc,
+                                const void* vc, const void* kn, const void* vn, void* out,
+                                float* lse, char* ws, float scale, hipStream_t st);
+hipError_t launch_decode_evict(const Shape& s, const Plan& p, const void* q, void* kc, void* vc,
+                               const void* kn, const void* vn, float* wsum, float* scores,
+                               int32_t* token_pos, int32_t* evict_idx, int32_t pos0, char* ws,
+                               float scale, hipStream_t st);
 hipError_t launch_colsum_reduce(const Shape& s, const Plan& p, const float* parts,
                                 float* wsum, hipStream_t st);
 hipError_t launch_accumulate(float* scores, const float* wsum, int rows, int M, int T,

@@ -24,7 +24,8 @@ STATUS_NAMES = ["H2O_OK", "H2O_EINVAL", "H2O_ESHAPE", "H2O_EDTYPE", "H2O_EALIGN"
                 "H2O_EWORKSPACE", "H2O_ENODEVICE", "H2O_ELAUNCH"]
 EXPORTED = ["h2o_workspace_bytes", "h2o_sdpa_chunk", "h2o_accumulate_scores",
             "h2o_evict_insert", "h2o_evict_workspace_bytes", "h2o_evict_insert_policy",
-            "h2o_chunk_step", "h2o_cache_workspace_bytes", "h2o_sdpa_cache",
+            "h2o_chunk_step", "h2o_chunk_step_attend", "h2o_chunk_step_evict",
+            "h2o_cache_workspace_bytes", "h2o_sdpa_cache",
             "h2o_chunk_step_insert_first", "h2o_bottomk", "h2o_last_error", "h2o_debug_force_path",
             "h2o_debug_timing", "h2o_debug_kernel_time", "h2o_version"]
 KERNEL_IDS = {"generic_lse": 0, "generic_main": 1, "mfma_lse": 2, "mfma_main": 3,
@@ -70,6 +71,9 @@ def lib() -> ctypes.CDLL:
     L.h2o_evict_insert_policy.restype = i
     L.h2o_chunk_step.argtypes = [vp] * 12 + [sz] + [i] * 6 + [f, ctypes.c_int32, i, vp]
     L.h2o_chunk_step.restype = i
+    for name in ("h2o_chunk_step_attend", "h2o_chunk_step_evict"):
+        getattr(L, name).argtypes = L.h2o_chunk_step.argtypes
+        getattr(L, name).restype = i
     L.h2o_cache_workspace_bytes.argtypes = [i] * 8
     L.h2o_cache_workspace_bytes.restype = sz
     L.h2o_sdpa_cache.argtypes = [vp] * 8 + [sz] + [i] * 6 + [f, ctypes.c_int32, i, vp]
@@ -252,9 +256,12 @@ def h2o_evict_insert_policy(k_cache, v_cache, scores, token_pos, k_new, v_new, w
 
 def h2o_chunk_step(q, k_cache, v_cache, scores, token_pos, k_new, v_new, out, lse, wsum,
                    evict_idx, workspace, pos0: int, scale: Optional[float] = None,
-                   stream=None) -> None:
+                   stream=None, part: str = "all") -> None:
     """h2o_sdpa_chunk + h2o_accumulate_scores + h2o_evict_insert (k = T) in one
-    call; shapes as there."""
+    call; shapes as there. ``part`` "attend" / "evict" calls one half
+    (h2o_chunk_step_attend / h2o_chunk_step_evict)."""
+    fn = {"all": "h2o_chunk_step", "attend": "h2o_chunk_step_attend",
+          "evict": "h2o_chunk_step_evict"}[part]
     B, Hq, T, d = q.shape
     Hkv, M = k_cache.shape[1], k_cache.shape[2]
     dt = _dtype_code(q)
@@ -280,7 +287,7 @@ def h2o_chunk_step(q, k_cache, v_cache, scores, token_pos, k_new, v_new, out, ls
     if scale is None:
         scale = d ** -0.5
     nbytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
-    _check(lib().h2o_chunk_step(
+    _check(getattr(lib(), fn)(
         _dev(q, "q"), _dev(k_cache, "k_cache"), _dev(v_cache, "v_cache"),
         _dev(scores, "scores"), _dev(token_pos, "token_pos"), _dev(k_new, "k_new"),
         _dev(v_new, "v_new"), _dev(out, "out"), _dev(lse, "lse"), _dev(wsum, "wsum"),

@@ -147,14 +147,17 @@ def test_evict_policy_rejects(L, kw, code):
     assert len(L.h2o_last_error()) > 0
 
 
-def _step(L, **kw):
+STEP_FNS = ["h2o_chunk_step", "h2o_chunk_step_attend", "h2o_chunk_step_evict"]
+
+
+def _step(L, fn="h2o_chunk_step", **kw):
     a = dict(q=P, kc=P, vc=P, sc=P, tp=P, kn=P, vn=P, out=P, lse=P, w=P, idx=P, ws=P,
              wsb=1 << 40, B=1, Hq=4, Hkv=2, T=4, M=16, d=64, scale=0.125, pos0=16, dt=1, st=None)
     a.update(kw)
-    return L.h2o_chunk_step(a["q"], a["kc"], a["vc"], a["sc"], a["tp"], a["kn"], a["vn"],
-                            a["out"], a["lse"], a["w"], a["idx"], a["ws"], a["wsb"], a["B"],
-                            a["Hq"], a["Hkv"], a["T"], a["M"], a["d"], a["scale"], a["pos0"],
-                            a["dt"], a["st"])
+    return getattr(L, fn)(a["q"], a["kc"], a["vc"], a["sc"], a["tp"], a["kn"], a["vn"],
+                          a["out"], a["lse"], a["w"], a["idx"], a["ws"], a["wsb"], a["B"],
+                          a["Hq"], a["Hkv"], a["T"], a["M"], a["d"], a["scale"], a["pos0"],
+                          a["dt"], a["st"])
 
 
 @pytest.mark.parametrize("kw,code", [
@@ -170,8 +173,9 @@ def _step(L, **kw):
     (dict(lse=MIS), H.H2O_EALIGN),
     (dict(wsb=8), H.H2O_EWORKSPACE),
 ])
-def test_chunk_step_rejects(L, kw, code):
-    assert _step(L, **kw) == code
+@pytest.mark.parametrize("fn", STEP_FNS)
+def test_chunk_step_rejects(L, kw, code, fn):
+    assert _step(L, fn, **kw) == code
     assert len(L.h2o_last_error()) > 0
 
 
@@ -266,7 +270,8 @@ def test_no_device_is_reported(L):
     assert _evict(L) == H.H2O_ENODEVICE
     assert L.h2o_bottomk(P, 4, 10, 3, P, None) == H.H2O_ENODEVICE
     assert L.h2o_accumulate_scores(P, P, 1, 2, 8, 1, None) == H.H2O_ENODEVICE
-    assert _step(L) == H.H2O_ENODEVICE
+    for fn in STEP_FNS:
+        assert _step(L, fn) == H.H2O_ENODEVICE
     for pol in (0, 1, 2):
         assert _evict_policy(L, pol=pol) == H.H2O_ENODEVICE
     assert _evict_policy(L, pol=0, ws=None, wsb=0) == H.H2O_ENODEVICE

@@ -308,6 +308,41 @@ def test_chunk_step_equals_three_calls(shape):
     _check_attention(x, dt, (res[1]["out"], res[1]["lse"], res[1]["wsum"]), extra="fused")
 
 
+@pytest.mark.parametrize("shape", STEP_SHAPES)
+def test_attend_then_evict_equals_step(shape):
+    """h2o_chunk_step_attend then h2o_chunk_step_evict, the second on another
+    stream after an event, give the bits of h2o_chunk_step."""
+    B, Hq, Hkv, d, M, T, dt = shape
+    wl = W.custom("halves", B=B, Hq=Hq, Hkv=Hkv, d=d, M=M, T=T, dtype=dt, heavy_frac=0.02)
+    say(f"attend + evict {wl.describe()}")
+    x = W.make_inputs(wl, seed=13)
+    tdt = torch.float32 if dt == "f32" else torch.bfloat16
+    q, kn, vn = (U.to_dev(x[n], tdt) for n in ("q", "k_new", "v_new"))
+    pos0, scale = int(x["pos0"]), float(x["scale"])
+    res = []
+    for halves in (False, True):
+        st = U.device_state(x, dt)
+        b = H.alloc_step(B, Hq, Hkv, T, M, d, tdt)
+        args = (q, st["k_cache"], st["v_cache"], st["scores"], st["token_pos"], kn, vn, b["out"],
+                b["lse"], b["wsum"], b["evict_idx"], b["workspace"], pos0, scale)
+        torch.cuda.synchronize()
+        if halves:
+            side = torch.cuda.Stream()
+            H.h2o_chunk_step(*args, part="attend")
+            ev = torch.cuda.Event()
+            ev.record()
+            side.wait_event(ev)
+            with torch.cuda.stream(side):
+                H.h2o_chunk_step(*args, part="evict")
+        else:
+            H.h2o_chunk_step(*args)
+        torch.cuda.synchronize()
+        res.append({**{n: U.to_np(b[n]) for n in ("out", "lse", "wsum", "evict_idx")},
+                    **{n: U.to_np(st[n]) for n in ("k_cache", "v_cache", "scores", "token_pos")}})
+    for n in res[0]:
+        np.testing.assert_array_equal(res[1][n], res[0][n], err_msg=n)
+
+
 @pytest.mark.parametrize("shape", [(8, 32, 8, 64, 4096, 1, "bf16"), (1, 8, 2, 128, 300, 70, "bf16")])
 def test_graph_replays_match_eager(shape):
     """The chunk step captured in a HIP graph and replayed three times (the

@@ -4,9 +4,11 @@ TEST INFRASTRUCTURE ONLY: imported by ``tests/``, ``__graft_entry__.smoke()``
 and the ``cpu_baseline`` leg of ``bench.py``, never by the library.
 """
 from .h2o_oracle import (POLICIES, accumulate_scores, bottomk, decode, evict_insert,
-                         h2o_step, h2o_step_insert_first, rel_err, sdpa_cache, sdpa_chunk,
-                         selection_keys, visible, visible_by_position)
+                         h2o_step, h2o_step_insert_first, kv_gather, kv_scatter, rel_err,
+                         sdpa_cache, sdpa_chunk, sdpa_chunk_backward, selection_keys, visible,
+                         visible_by_position)
 
 __all__ = ["POLICIES", "accumulate_scores", "bottomk", "decode", "evict_insert",
-           "h2o_step", "h2o_step_insert_first", "rel_err", "sdpa_cache", "sdpa_chunk",
-           "selection_keys", "visible", "visible_by_position"]
+           "h2o_step", "h2o_step_insert_first", "kv_gather", "kv_scatter", "rel_err",
+           "sdpa_cache", "sdpa_chunk", "sdpa_chunk_backward", "selection_keys", "visible",
+           "visible_by_position"]

@@ -338,6 +338,101 @@ def h2o_step_insert_first(k_cache, v_cache, scores, token_pos, q, k_new, v_new,
                 k_cache=kc, v_cache=vc, scores=accumulate_scores(sc, wsum), token_pos=tp)
 
 
+# ------------------------------------------- backward (fine-tuning) and deltas
+def _head_backward(Qh, K, V, allowed, scale, dO):
+    """Gradients of one query head's output Y = softmax(scale Q K^T, masked) V
+    for the loss sum(dO * Y): returns (dQ [T,d], dK [Nk,d], dV [Nk,d]).
+
+    The softmax vector-Jacobian product row by row: with p = softmax(a) and
+    g = dL/dp, dL/da = p * (g - <p, g>). A row that sees no key has no
+    gradient."""
+    A = scale * (Qh @ K.T)
+    A = np.where(allowed, A, -np.inf)
+    some = allowed.any(axis=1)
+    amax = np.where(some, A.max(axis=1), 0.0)[:, None]
+    E = np.where(allowed, np.exp(A - amax), 0.0)
+    Z = E.sum(axis=1, keepdims=True)
+    P = np.where(some[:, None], E / np.where(Z > 0, Z, 1.0), 0.0)     # attention weights
+    dV = P.T @ dO
+    dP = dO @ V.T                                                      # dL/dP
+    dA = P * (dP - (P * dP).sum(axis=1, keepdims=True))                # softmax VJP
+    dQ = scale * (dA @ K)
+    dK = scale * (dA.T @ Qh)
+    return dQ, dK, dV
+
+
+def sdpa_chunk_backward(q, k_cache, v_cache, k_new, v_new, dout, scale: Optional[float] = None,
+                        token_pos=None, pos0: int = 0):
+    """Gradients of the chunk attention's output for the loss sum(dout * out),
+    the backward of the SDPA of a fine-tuning step (Sec. "Fine-Tuning for
+    Sparse Attention"). The summed weights carry no gradient: they only steer
+    the discrete eviction.
+
+    Chunk mode (token_pos None): keys [cache || chunk] as in ``sdpa_chunk``;
+    returns float64 (dq [B,Hq,T,d], dk_cache, dv_cache [B,Hkv,M,d], dk_new,
+    dv_new [B,Hkv,T,d]). Cache mode (token_pos given): the keys are the cache
+    slots with the token-position mask of ``sdpa_cache``; dk_new and dv_new
+    are None. Gradients of a KV head sum over its group's query heads.
+    """
+    q = np.asarray(q)
+    B, Hq, T, d = q.shape
+    Hkv, M = k_cache.shape[1], k_cache.shape[2]
+    G = Hq // Hkv
+    if scale is None:
+        scale = 1.0 / np.sqrt(d)
+    scale = float(scale)
+    cache_mode = token_pos is not None
+    Nk = M if cache_mode else M + T
+    dq = np.zeros((B, Hq, T, d))
+    dk = np.zeros((B, Hkv, Nk, d))
+    dv = np.zeros((B, Hkv, Nk, d))
+    for b in range(B):
+        for h in range(Hkv):
+            if cache_mode:
+                K = np.asarray(k_cache[b, h], F64)
+                V = np.asarray(v_cache[b, h], F64)
+                allowed = visible_by_position(token_pos[b, h], pos0, T)
+            else:
+                K = np.concatenate([k_cache[b, h], k_new[b, h]]).astype(F64)
+                V = np.concatenate([v_cache[b, h], v_new[b, h]]).astype(F64)
+                allowed = visible(M, T)
+            for g in range(G):
+                hq = h * G + g
+                gq, gk, gv = _head_backward(q[b, hq].astype(F64), K, V, allowed, scale,
+                                            np.asarray(dout[b, hq], F64))
+                dq[b, hq] = gq
+                dk[b, h] += gk
+                dv[b, h] += gv
+    if cache_mode:
+        return dq, dk, dv, None, None
+    return dq, dk[:, :, :M], dv[:, :, :M], dk[:, :, M:], dv[:, :, M:]
+
+
+def kv_gather(cache, idx) -> np.ndarray:
+    """delta[b, h, i] = cache[b, h, idx[b, h, i]]: the rows a chunk's insert is
+    about to overwrite, the delta encoding of the KV recurrence (Eq.
+    recurrence-reverse, Sec. "Buffer Read/Write Access by torch.scatter,
+    torch.gather")."""
+    cache = np.asarray(cache)
+    idx = np.asarray(idx)
+    out = np.empty(idx.shape + cache.shape[3:], cache.dtype)
+    for b in range(idx.shape[0]):
+        for h in range(idx.shape[1]):
+            out[b, h] = cache[b, h, idx[b, h]]
+    return out
+
+
+def kv_scatter(cache, idx, src) -> np.ndarray:
+    """A copy of cache with cache[b, h, idx[b, h, i]] = src[b, h, i]: the insert
+    of a chunk, and, with src = kv_gather(old cache, idx), its inverse."""
+    out = np.array(cache, copy=True)
+    idx = np.asarray(idx)
+    for b in range(idx.shape[0]):
+        for h in range(idx.shape[1]):
+            out[b, h, idx[b, h]] = src[b, h]
+    return out
+
+
 def decode(k_cache, v_cache, scores, token_pos, q_steps, k_new_steps,
            v_new_steps, pos0: int, scale: Optional[float] = None):
     """Token generation: ``len(q_steps)`` chunk steps of length T (usually 1),

@@ -251,3 +251,36 @@ def torch_sdpa_positions(q, kc, vc, tp, pos0, scale):
                     Q[None], K[None], V[None], attn_mask=mask[None], scale=float(scale))[0].numpy()
                 lse[b, h * G + g] = _lse_torch(Q, K, mask, float(scale)).numpy()
     return out, lse
+
+
+def torch_attention_grads(q, kc, vc, kn, vn, dout, scale, token_pos=None, pos0=0):
+    """Gradients of sum(dout * out) by torch autograd (float64, CPU) through an
+    explicit masked softmax attention, head by head (GQA heads share the KV
+    tensors, so their gradients add up by autograd itself)."""
+    B, Hq, T, d = q.shape
+    Hkv, M = kc.shape[1], kc.shape[2]
+    G = Hq // Hkv
+    t = lambda a: torch.tensor(np.asarray(a, np.float64), requires_grad=True)
+    Q, KC, VC = t(q), t(kc), t(vc)
+    cache_mode = token_pos is not None
+    KN, VN = (None, None) if cache_mode else (t(kn), t(vn))
+    loss = 0.0
+    for b in range(B):
+        for h in range(Hkv):
+            if cache_mode:
+                K, V = KC[b, h], VC[b, h]
+                mask = torch.from_numpy(np.asarray(token_pos[b, h], np.int64))[None, :] <= \
+                    (torch.arange(T)[:, None] + int(pos0))
+            else:
+                K = torch.cat([KC[b, h], KN[b, h]])
+                V = torch.cat([VC[b, h], VN[b, h]])
+                mask = _mask(M, T)
+            for g in range(G):
+                A = float(scale) * (Q[b, h * G + g] @ K.T)
+                A = A.masked_fill(~mask, float("-inf"))
+                P = torch.softmax(A, dim=-1)
+                loss = loss + (torch.from_numpy(np.asarray(dout[b, h * G + g], np.float64)) *
+                               (P @ V)).sum()
+    loss.backward()
+    g = lambda x: None if x is None else x.grad.numpy()
+    return g(Q), g(KC), g(VC), g(KN), g(VN)

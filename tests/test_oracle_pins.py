@@ -645,3 +645,113 @@ def test_insert_first_mistakes_are_caught(monkeypatch):
             m.setattr(oracle, name, fn)
             with pytest.raises(AssertionError):
                 test()
+
+
+# ----------------------------------------------- backward and delta encoding
+BWD_SHAPES = [(1, 2, 1, 4, 5, 3), (2, 4, 2, 8, 7, 4), (1, 3, 1, 6, 0, 4), (1, 4, 2, 16, 33, 9)]
+
+
+def _dout(x, seed):
+    return np.random.default_rng(seed).standard_normal(x["q"].shape)
+
+
+@pytest.mark.parametrize("shape", BWD_SHAPES)
+def test_backward_matches_torch_autograd(shape):
+    x = _inputs(*shape, seed=sum(shape))
+    do = _dout(x, 1)
+    got = oracle.sdpa_chunk_backward(*_args(x), do, x["scale"])
+    ref = P.torch_attention_grads(*_args(x), do, x["scale"])
+    for a, r, n in zip(got, ref, ("dq", "dk_cache", "dv_cache", "dk_new", "dv_new")):
+        np.testing.assert_allclose(a, r, rtol=1e-11, atol=1e-12, err_msg=n)
+
+
+def test_backward_cache_mode_matches_torch_autograd():
+    B, Hq, Hkv, d, M, T = 2, 4, 2, 8, 12, 3
+    x = _inputs(B, Hq, Hkv, d, M, T, seed=3)
+    rng = np.random.default_rng(3)
+    tp = rng.integers(95, 105, size=(B, Hkv, M)).astype(np.int32)
+    tp[:, :, 0] = 100                      # every query sees at least slot 0
+    do = _dout(x, 2)
+    got = oracle.sdpa_chunk_backward(x["q"], x["k_cache"], x["v_cache"], None, None, do,
+                                     x["scale"], token_pos=tp, pos0=100)
+    ref = P.torch_attention_grads(x["q"], x["k_cache"], x["v_cache"], None, None, do,
+                                  x["scale"], token_pos=tp, pos0=100)
+    for a, r in zip(got[:3], ref[:3]):
+        np.testing.assert_allclose(a, r, rtol=1e-11, atol=1e-12)
+    assert got[3] is None and got[4] is None
+
+
+def test_backward_finite_differences():
+    """Central differences of the forward oracle's loss sum(dout * out)."""
+    x = _inputs(1, 2, 1, 3, 3, 2, seed=5)
+    do = _dout(x, 5)
+    grads = oracle.sdpa_chunk_backward(*_args(x), do, x["scale"])
+    names = ("q", "k_cache", "v_cache", "k_new", "v_new")
+    loss = lambda xx: float((do * oracle.sdpa_chunk(*_args(xx), x["scale"])[0]).sum())
+    h = 1e-6
+    for n, gr in zip(names, grads):
+        base = {k: np.asarray(v, np.float64) for k, v in x.items() if k in names}
+        for idx in np.ndindex(base[n].shape):
+            up, dn = dict(x), dict(x)
+            up[n] = base[n].copy(); up[n][idx] += h
+            dn[n] = base[n].copy(); dn[n][idx] -= h
+            fd = (loss(up) - loss(dn)) / (2 * h)
+            assert abs(fd - gr[idx]) <= 1e-6 * max(1.0, abs(fd)), (n, idx, fd, gr[idx])
+
+
+@pytest.mark.parametrize("shape", BWD_SHAPES)
+def test_backward_invariants(shape):
+    """Softmax is invariant to a common shift of a row's scores, so the key
+    gradients of a KV head sum to zero; the weights of a row sum to one, so the
+    value gradients sum to the sum of the output gradients of the group."""
+    B, Hq, Hkv, d, M, T = shape
+    x = _inputs(*shape, seed=7)
+    do = _dout(x, 7)
+    dq, dkc, dvc, dkn, dvn = oracle.sdpa_chunk_backward(*_args(x), do, x["scale"])
+    G = Hq // Hkv
+    for b in range(B):
+        for h in range(Hkv):
+            sk = dkc[b, h].sum(0) + dkn[b, h].sum(0)
+            assert np.abs(sk).max() < 1e-12
+            sv = dvc[b, h].sum(0) + dvn[b, h].sum(0)
+            np.testing.assert_allclose(sv, do[b, h * G:(h + 1) * G].sum((0, 1)), rtol=1e-12,
+                                       atol=1e-12)
+
+
+def test_kv_delta_round_trip():
+    """The recurrence of the KV buffers and its inverse (Eq. recurrence-reverse):
+    keys' = scatter(keys, index, new) and keys = scatter(keys', index,
+    gather(keys, index)), bit for bit."""
+    rng = np.random.default_rng(0)
+    B, H, M, k, d = 2, 3, 40, 7, 8
+    keys = rng.standard_normal((B, H, M, d)).astype(np.float32)
+    new = rng.standard_normal((B, H, k, d)).astype(np.float32)
+    idx = np.stack([np.stack([np.sort(rng.choice(M, k, replace=False)) for _ in range(H)])
+                    for _ in range(B)]).astype(np.int32)
+    delta = oracle.kv_gather(keys, idx)
+    after = oracle.kv_scatter(keys, idx, new)
+    np.testing.assert_array_equal(oracle.kv_gather(after, idx), new)
+    np.testing.assert_array_equal(oracle.kv_scatter(after, idx, delta), keys)
+    # the same as torch's gather/scatter along the slot axis
+    np.testing.assert_array_equal(_gather_torch(keys, idx), delta)
+    np.testing.assert_array_equal(_scatter_torch(keys, idx, new), after)
+
+
+def test_backward_mistakes_are_caught(monkeypatch):
+    orig = O._head_backward
+
+    def no_centering(Qh, K, V, allowed, scale, dO):
+        A = np.where(allowed, scale * (Qh @ K.T), -np.inf)
+        Pm = np.exp(A - A.max(1, keepdims=True)); Pm /= Pm.sum(1, keepdims=True)
+        dA = Pm * (dO @ V.T)                           # missing the - <p, g> term
+        return scale * dA @ K, scale * dA.T @ Qh, Pm.T @ dO
+
+    def no_scale_dk(Qh, K, V, allowed, scale, dO):
+        dQ, dK, dV = orig(Qh, K, V, allowed, scale, dO)
+        return dQ, dK / scale, dV
+
+    for fn in (no_centering, no_scale_dk):
+        with monkeypatch.context() as m:
+            m.setattr(O, "_head_backward", fn)
+            with pytest.raises(AssertionError):
+                test_backward_matches_torch_autograd((2, 4, 2, 8, 7, 4))

@@ -249,6 +249,49 @@ int h2o_chunk_step_insert_first(const void* q, void* k_cache, void* v_cache,
                                 int Hq, int Hkv, int T, int M, int d, float scale,
                                 int32_t pos0, int dtype, int policy, void* stream);
 
+/* ---- Fine-tuning (Sec. "Fine-Tuning for Sparse Attention"). */
+
+/* Bytes of device scratch for h2o_sdpa_chunk_backward (one float per query
+ * row; 0 on invalid arguments). */
+size_t h2o_backward_workspace_bytes(int B, int Hq, int Hkv, int T, int M, int d,
+                                    int dtype);
+
+/* Backward of h2o_sdpa_chunk (token_pos NULL: keys [cache || chunk], causal in
+ * the chunk) or of h2o_sdpa_cache (token_pos non-NULL, positions pos0..: the
+ * cache slots with the token-position mask; k_new, v_new, dk_new and dv_new
+ * are not used and may be NULL). Given the forward's lse and the output
+ * gradient dout [B,Hq,T,d], writes the gradients of the loss sum(dout * out):
+ *   dq [B,Hq,T,d]; dk_cache, dv_cache [B,Hkv,M,d]; dk_new, dv_new [B,Hkv,T,d]
+ * (written, not accumulated; a KV head's gradients sum over its GQA group).
+ * With P = softmax(scale Q K^T) (masked, rebuilt from lse), dP = dout V^T
+ * and D_r = sum_j P_rj dP_rj (from P and dP, not from a rounded output):
+ *   dV = P^T dout,  dS = P * (dP - D),  dQ = scale dS K,  dK = scale dS^T Q.
+ * The summed weights of the forward carry no gradient (they only steer the
+ * discrete eviction). Float32 arithmetic; gradients are stored in dtype
+ * (bf16 nearest-even). Workspace of h2o_backward_workspace_bytes(). */
+int h2o_sdpa_chunk_backward(const void* q, const void* k_cache,
+                            const void* v_cache, const void* k_new,
+                            const void* v_new, const int32_t* token_pos,
+                            const float* lse, const void* dout,
+                            void* dq, void* dk_cache, void* dv_cache, void* dk_new,
+                            void* dv_new, void* workspace, size_t workspace_bytes,
+                            int B, int Hq, int Hkv, int T, int M, int d,
+                            float scale, int32_t pos0, int dtype, void* stream);
+
+/* Delta encoding of the KV recurrence (Eq. recurrence-reverse, Sec. "Buffer
+ * Read/Write Access by torch.scatter, torch.gather"): with idx [B,Hkv,k]
+ * (int32 slots, out-of-range entries skipped),
+ *   h2o_kv_gather:   delta[b,h,i,:] = cache[b,h,idx[b,h,i],:]
+ *   h2o_kv_scatter:  cache[b,h,idx[b,h,i],:] = src[b,h,i,:]
+ * cache [B,Hkv,M,d], delta/src [B,Hkv,k,d], in dtype. The gather of the slots
+ * a chunk is about to overwrite, scattered back after the insert, restores
+ * the cache bit for bit. Slots in one row of idx must be distinct for the
+ * scatter. */
+int h2o_kv_gather(const void* cache, const int32_t* idx, void* delta, int B,
+                  int Hkv, int M, int k, int d, int dtype, void* stream);
+int h2o_kv_scatter(void* cache, const int32_t* idx, const void* src, int B,
+                   int Hkv, int M, int k, int d, int dtype, void* stream);
+
 /* The selection of h2o_evict_insert alone: for each of `rows` rows of M
  * float32 scores, the k smallest by (score, index), ascending indices, into
  * idx_out [rows, k]. 0 <= k <= M. */
@@ -278,7 +321,9 @@ int h2o_debug_force_path(int path);
  *   6 accumulate         7 bottom-k            8 insert
  *   9 decode split      10 decode combine     11 argmin + insert (k == 1)
  *  12 decode finish (h2o_chunk_step, T == 1)
- *  13 score-variant keys and index broadcast (h2o_evict_insert_policy) */
+ *  13 score-variant keys and index broadcast (h2o_evict_insert_policy)
+ *  14 backward dQ (and the rows' D)  15 backward dK/dV
+ *  16 KV gather / scatter */
 int h2o_debug_timing(int on);
 int h2o_debug_kernel_time(int kernel_id, double* total_ms, long* count);
 

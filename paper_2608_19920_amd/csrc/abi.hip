@@ -591,4 +591,79 @@ int h2o_chunk_step_insert_first(const void* q, void* k_cache, void* v_cache, flo
   return ok();
 }
 
+size_t h2o_backward_workspace_bytes(int B, int Hq, int Hkv, int T, int M, int d, int dtype) {
+  if (dtype != H2O_F32 && dtype != H2O_BF16) return 0;
+  if (check_shape(B, Hq, Hkv, T, M, d) != H2O_OK) return 0;
+  return align256((size_t)B * Hkv * (Hq / Hkv) * T * sizeof(float));
+}
+
+int h2o_sdpa_chunk_backward(const void* q, const void* k_cache, const void* v_cache,
+                            const void* k_new, const void* v_new, const int32_t* token_pos,
+                            const float* lse, const void* dout, void* dq,
+                            void* dk_cache, void* dv_cache, void* dk_new, void* dv_new,
+                            void* workspace, size_t workspace_bytes, int B, int Hq, int Hkv,
+                            int T, int M, int d, float scale, int32_t pos0, int dtype,
+                            void* stream) {
+  if (dtype != H2O_F32 && dtype != H2O_BF16) return fail(H2O_EDTYPE, "dtype %d unknown", dtype);
+  int rc = check_shape(B, Hq, Hkv, T, M, d);
+  if (rc) return rc;
+  const bool cache = token_pos != nullptr;
+  if (cache && M < 1) return fail(H2O_EINVAL, "cache length M must be >= 1");
+  if (!(std::isfinite(scale) && scale > 0.f)) return fail(H2O_EINVAL, "scale must be finite > 0");
+  if (!q || !lse || !dout || !dq ||
+      (M > 0 && (!k_cache || !v_cache || !dk_cache || !dv_cache)) ||
+      (!cache && (!k_new || !v_new || !dk_new || !dv_new)))
+    return fail(H2O_EINVAL, "null tensor pointer");
+  const void* ptrs[] = {q, k_cache, v_cache, lse, dout, dq, dk_cache, dv_cache, workspace,
+                        token_pos, cache ? nullptr : k_new, cache ? nullptr : v_new,
+                        cache ? nullptr : dk_new, cache ? nullptr : dv_new};
+  for (const void* p : ptrs)
+    if (p && !aligned16(p)) return fail(H2O_EALIGN, "tensor pointer not 16-byte aligned");
+  const size_t need = h2o_backward_workspace_bytes(B, Hq, Hkv, T, M, d, dtype);
+  if (workspace_bytes < need || !workspace)
+    return fail(H2O_EWORKSPACE, "workspace has %zu bytes, needs %zu", workspace_bytes, need);
+  rc = check_device();
+  if (rc) return rc;
+  const Shape s{B, Hq, Hkv, T, M, d, cache};
+  hipError_t e = launch_sdpa_backward(s, dtype, q, k_cache, v_cache, k_new, v_new,
+                                      KeyPos{token_pos, pos0}, lse, dout, dq, dk_cache,
+                                      dv_cache, dk_new, dv_new,
+                                      reinterpret_cast<float*>(workspace), scale,
+                                      reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(H2O_ELAUNCH, "kernel launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+namespace {
+int kv_copy_call(bool gather, void* cache, const int32_t* idx, void* rows, int B, int Hkv, int M,
+                 int k, int d, int dtype, void* stream) {
+  if (dtype != H2O_F32 && dtype != H2O_BF16) return fail(H2O_EDTYPE, "dtype %d unknown", dtype);
+  if (B < 1 || Hkv < 1 || M < 1 || k < 0 || k > M)
+    return fail(H2O_ESHAPE, "need B, Hkv, M >= 1 and 0 <= k <= M");
+  if (d != 64 && d != 128) return fail(H2O_ESHAPE, "head dim d=%d not supported (64 or 128)", d);
+  if ((long long)B * Hkv * M * d >= (1ll << 40)) return fail(H2O_ESHAPE, "too large");
+  if (k > 0 && (!cache || !idx || !rows)) return fail(H2O_EINVAL, "null tensor pointer");
+  if ((cache && !aligned16(cache)) || (idx && !aligned16(idx)) || (rows && !aligned16(rows)))
+    return fail(H2O_EALIGN, "tensor pointer not 16-byte aligned");
+  int rc = check_device();
+  if (rc) return rc;
+  const int eb = dtype == H2O_F32 ? 4 : 2;
+  hipError_t e = launch_kv_copy(gather, cache, idx, rows, B * Hkv, M, k, d * eb / 16,
+                                reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(H2O_ELAUNCH, "kernel launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+}  // namespace
+
+int h2o_kv_gather(const void* cache, const int32_t* idx, void* delta, int B, int Hkv, int M,
+                  int k, int d, int dtype, void* stream) {
+  return kv_copy_call(true, const_cast<void*>(cache), idx, delta, B, Hkv, M, k, d, dtype,
+                      stream);
+}
+
+int h2o_kv_scatter(void* cache, const int32_t* idx, const void* src, int B, int Hkv, int M, int k,
+                   int d, int dtype, void* stream) {
+  return kv_copy_call(false, cache, idx, const_cast<void*>(src), B, Hkv, M, k, d, dtype, stream);
+}
+
 }  // extern "C"

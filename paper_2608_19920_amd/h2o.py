@@ -25,13 +25,15 @@ STATUS_NAMES = ["H2O_OK", "H2O_EINVAL", "H2O_ESHAPE", "H2O_EDTYPE", "H2O_EALIGN"
 EXPORTED = ["h2o_workspace_bytes", "h2o_sdpa_chunk", "h2o_accumulate_scores",
             "h2o_evict_insert", "h2o_evict_workspace_bytes", "h2o_evict_insert_policy",
             "h2o_chunk_step", "h2o_chunk_step_attend", "h2o_chunk_step_evict",
-            "h2o_cache_workspace_bytes", "h2o_sdpa_cache",
+            "h2o_cache_workspace_bytes", "h2o_sdpa_cache", "h2o_backward_workspace_bytes",
+            "h2o_sdpa_chunk_backward", "h2o_kv_gather", "h2o_kv_scatter",
             "h2o_chunk_step_insert_first", "h2o_bottomk", "h2o_last_error", "h2o_debug_force_path",
             "h2o_debug_timing", "h2o_debug_kernel_time", "h2o_version"]
 KERNEL_IDS = {"generic_lse": 0, "generic_main": 1, "mfma_lse": 2, "mfma_main": 3,
               "split_reduce": 4, "colsum_reduce": 5, "accumulate": 6, "bottomk": 7,
               "insert": 8, "decode_split": 9, "decode_combine": 10,
-              "argmin_insert": 11, "decode_finish": 12, "variant_keys": 13}
+              "argmin_insert": 11, "decode_finish": 12, "variant_keys": 13,
+              "bwd_dq": 14, "bwd_dkdv": 15, "kv_copy": 16}
 # eviction rankings (Sec. "Variants of Heavy-Hitter Oracle"), as h2o_policy
 POLICIES = {"h2o": 0, "h2o_norm": 1, "h2o_orig": 2}
 
@@ -81,6 +83,13 @@ def lib() -> ctypes.CDLL:
     L.h2o_chunk_step_insert_first.argtypes = [vp] * 12 + [sz] + [i] * 6 + \
         [f, ctypes.c_int32, i, i, vp]
     L.h2o_chunk_step_insert_first.restype = i
+    L.h2o_backward_workspace_bytes.argtypes = [i] * 7
+    L.h2o_backward_workspace_bytes.restype = sz
+    L.h2o_sdpa_chunk_backward.argtypes = [vp] * 14 + [sz] + [i] * 6 + [f, ctypes.c_int32, i, vp]
+    L.h2o_sdpa_chunk_backward.restype = i
+    for name in ("h2o_kv_gather", "h2o_kv_scatter"):
+        getattr(L, name).argtypes = [vp] * 3 + [i] * 6 + [vp]
+        getattr(L, name).restype = i
     L.h2o_bottomk.argtypes = [vp, i, i, i, vp, vp]
     L.h2o_bottomk.restype = i
     L.h2o_last_error.argtypes = []
@@ -360,6 +369,77 @@ def h2o_chunk_step_insert_first(q, k_cache, v_cache, scores, token_pos, k_new, v
         _dev(evict_idx, "evict_idx"), _dev(workspace, "workspace"), nbytes,
         B, Hq, Hkv, T, M, d, float(scale), int(pos0), _dtype_code(q), _policy_code(policy),
         _stream(stream)))
+
+
+def h2o_backward_workspace_bytes(B, Hq, Hkv, T, M, d, dtype) -> int:
+    code = dtype if isinstance(dtype, int) else _dtype_code(torch.empty(0, dtype=dtype))
+    return int(lib().h2o_backward_workspace_bytes(B, Hq, Hkv, T, M, d, code))
+
+
+def h2o_sdpa_chunk_backward(q, k_cache, v_cache, k_new, v_new, lse, dout, dq, dk_cache,
+                            dv_cache, dk_new, dv_new, workspace, scale: Optional[float] = None,
+                            token_pos=None, pos0: int = 0, stream=None) -> None:
+    """Gradients of sum(dout * out) for the chunk attention (token_pos None)
+    or the cache attention with the token-position mask (token_pos given;
+    k_new, v_new, dk_new, dv_new unused). Gradients in q's dtype."""
+    B, Hq, T, d = q.shape
+    Hkv, M = k_cache.shape[1], k_cache.shape[2]
+    cache = token_pos is not None
+    for name, t in (("k_cache", k_cache), ("v_cache", v_cache), ("dout", dout),
+                    ("dq", dq), ("dk_cache", dk_cache), ("dv_cache", dv_cache)):
+        if t.dtype != q.dtype:
+            raise TypeError(f"{name} dtype {t.dtype} != q dtype {q.dtype}")
+    for name, t in (("dout", dout), ("dq", dq)):
+        if tuple(t.shape) != (B, Hq, T, d):
+            raise ValueError(f"{name} must be [B,Hq,T,d]")
+    for name, t in (("k_cache", k_cache), ("v_cache", v_cache), ("dk_cache", dk_cache),
+                    ("dv_cache", dv_cache)):
+        if tuple(t.shape) != (B, Hkv, M, d):
+            raise ValueError(f"{name} must be [B,Hkv,M,d]")
+    if not cache:
+        for name, t in (("k_new", k_new), ("v_new", v_new), ("dk_new", dk_new),
+                        ("dv_new", dv_new)):
+            if t is None or t.dtype != q.dtype or tuple(t.shape) != (B, Hkv, T, d):
+                raise ValueError(f"{name} must be [B,Hkv,T,d] in q's dtype")
+    elif token_pos.dtype != torch.int32 or tuple(token_pos.shape) != (B, Hkv, M):
+        raise ValueError("token_pos must be int32 [B,Hkv,M]")
+    if tuple(lse.shape) != (B, Hq, T) or lse.dtype != torch.float32:
+        raise ValueError("lse must be float32 [B,Hq,T]")
+    if scale is None:
+        scale = d ** -0.5
+    nbytes = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    n = (lambda t, name: None) if cache else _dev
+    _check(lib().h2o_sdpa_chunk_backward(
+        _dev(q, "q"), _dev(k_cache, "k_cache"), _dev(v_cache, "v_cache"), n(k_new, "k_new"),
+        n(v_new, "v_new"), _dev(token_pos, "token_pos"), _dev(lse, "lse"),
+        _dev(dout, "dout"), _dev(dq, "dq"), _dev(dk_cache, "dk_cache"),
+        _dev(dv_cache, "dv_cache"), n(dk_new, "dk_new"), n(dv_new, "dv_new"),
+        _dev(workspace, "workspace"), nbytes, B, Hq, Hkv, T, M, d, float(scale), int(pos0),
+        _dtype_code(q), _stream(stream)))
+
+
+def _kv_rows(cache, idx, rows):
+    B, Hkv, M, d = cache.shape
+    k = idx.shape[2]
+    if idx.dtype != torch.int32 or tuple(idx.shape) != (B, Hkv, k):
+        raise ValueError("idx must be int32 [B,Hkv,k]")
+    if rows.dtype != cache.dtype or tuple(rows.shape) != (B, Hkv, k, d):
+        raise ValueError("rows must be [B,Hkv,k,d] in the cache's dtype")
+    return B, Hkv, M, k, d
+
+
+def h2o_kv_gather(cache, idx, delta, stream=None) -> None:
+    """delta[b,h,i] = cache[b,h,idx[b,h,i]]."""
+    B, Hkv, M, k, d = _kv_rows(cache, idx, delta)
+    _check(lib().h2o_kv_gather(_dev(cache, "cache"), _dev(idx, "idx"), _dev(delta, "delta"),
+                               B, Hkv, M, k, d, _dtype_code(cache), _stream(stream)))
+
+
+def h2o_kv_scatter(cache, idx, src, stream=None) -> None:
+    """cache[b,h,idx[b,h,i]] = src[b,h,i]."""
+    B, Hkv, M, k, d = _kv_rows(cache, idx, src)
+    _check(lib().h2o_kv_scatter(_dev(cache, "cache"), _dev(idx, "idx"), _dev(src, "src"),
+                                B, Hkv, M, k, d, _dtype_code(cache), _stream(stream)))
 
 
 def h2o_bottomk(scores, k: int, idx_out, stream=None) -> None:

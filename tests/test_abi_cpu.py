@@ -243,6 +243,51 @@ def test_step_insert_first_rejects(L, kw, code):
     assert len(L.h2o_last_error()) > 0
 
 
+def _bwd(L, **kw):
+    a = dict(q=P, kc=P, vc=P, kn=P, vn=P, tp=None, lse=P, do=P, dq=P, dkc=P, dvc=P, dkn=P,
+             dvn=P, ws=P, wsb=1 << 40, B=1, Hq=4, Hkv=2, T=8, M=16, d=64, scale=0.125, pos0=0,
+             dt=1, st=None)
+    a.update(kw)
+    return L.h2o_sdpa_chunk_backward(
+        a["q"], a["kc"], a["vc"], a["kn"], a["vn"], a["tp"], a["lse"], a["do"],
+        a["dq"], a["dkc"], a["dvc"], a["dkn"], a["dvn"], a["ws"], a["wsb"], a["B"], a["Hq"],
+        a["Hkv"], a["T"], a["M"], a["d"], a["scale"], a["pos0"], a["dt"], a["st"])
+
+
+def test_backward_workspace_bytes(L):
+    # one float per query row (B*Hkv*G*T = 2*8*16 rows), in 256-byte units
+    assert L.h2o_backward_workspace_bytes(2, 8, 2, 16, 100, 64, 1) == 1024
+    assert L.h2o_backward_workspace_bytes(2, 8, 3, 16, 100, 64, 1) == 0
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dt=3), H.H2O_EDTYPE),
+    (dict(d=48), H.H2O_ESHAPE),
+    (dict(Hq=5), H.H2O_ESHAPE),
+    (dict(dq=None), H.H2O_EINVAL),
+    (dict(dkn=None), H.H2O_EINVAL),
+    (dict(lse=None), H.H2O_EINVAL),
+    (dict(tp=P, M=0), H.H2O_EINVAL),
+    (dict(do=MIS), H.H2O_EALIGN),
+    (dict(tp=MIS), H.H2O_EALIGN),
+    (dict(wsb=16), H.H2O_EWORKSPACE),
+    (dict(scale=0.0), H.H2O_EINVAL),
+])
+def test_backward_rejects(L, kw, code):
+    assert _bwd(L, **kw) == code
+    assert len(L.h2o_last_error()) > 0
+
+
+@pytest.mark.parametrize("fn", ["h2o_kv_gather", "h2o_kv_scatter"])
+def test_kv_copy_rejects(L, fn):
+    f = getattr(L, fn)
+    assert f(P, P, P, 1, 2, 16, 17, 64, 1, None) == H.H2O_ESHAPE     # k > M
+    assert f(P, P, P, 1, 2, 16, 4, 32, 1, None) == H.H2O_ESHAPE      # d
+    assert f(P, P, P, 1, 2, 16, 4, 64, 7, None) == H.H2O_EDTYPE
+    assert f(None, P, P, 1, 2, 16, 4, 64, 1, None) == H.H2O_EINVAL
+    assert f(P, MIS, P, 1, 2, 16, 4, 64, 1, None) == H.H2O_EALIGN
+
+
 @pytest.mark.parametrize("args,code", [
     ((P, 4, 10, 11, P, None), H.H2O_EINVAL),
     ((P, 4, 10, -1, P, None), H.H2O_EINVAL),
@@ -277,6 +322,10 @@ def test_no_device_is_reported(L):
     assert _evict_policy(L, pol=0, ws=None, wsb=0) == H.H2O_ENODEVICE
     assert _evict_policy(L, pol=2, tp=None) == H.H2O_ENODEVICE
     assert _cache(L) == H.H2O_ENODEVICE
+    assert _bwd(L) == H.H2O_ENODEVICE
+    assert _bwd(L, tp=P, kn=None, vn=None, dkn=None, dvn=None) == H.H2O_ENODEVICE
+    assert L.h2o_kv_gather(P, P, P, 1, 2, 16, 4, 64, 1, None) == H.H2O_ENODEVICE
+    assert L.h2o_kv_scatter(P, P, P, 1, 2, 16, 4, 64, 1, None) == H.H2O_ENODEVICE
     for pol in (0, 1, 2):
         assert _step_if(L, pol=pol) == H.H2O_ENODEVICE
 

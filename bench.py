@@ -296,6 +296,41 @@ def bench_insert_first(args, torch, H, W):
     return out
 
 
+# ----------------------------------------------------------------- backward
+def bench_backward(args, torch, H, W):
+    """h2o_sdpa_chunk_backward on the first prefill workload, after its
+    forward: TFLOP/s of the algorithmic backward work 2.5 W (the five
+    products QK^T, dout V^T, P^T dout, dS K, dS^T Q over the visible pairs)."""
+    w = W.WORKLOADS["prefill_bf16"]
+    bf = torch.bfloat16
+    x = W.make_inputs(w, seed=0)
+    to = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to("cuda").to(bf)
+    q, kc, vc, kn, vn = (to(x[n]) for n in ("q", "k_cache", "v_cache", "k_new", "v_new"))
+    scale = float(x["scale"])
+    del x
+    b = H.alloc_step(w.B, w.Hq, w.Hkv, w.T, w.M, w.d, bf)
+    H.h2o_sdpa_chunk(q, kc, vc, kn, vn, b["out"], b["lse"], b["wsum"], b["workspace"], scale)
+    dout = torch.randn_like(q)
+    grads = [torch.empty_like(t) for t in (q, kc, vc, kn, vn)]
+    ws = torch.empty(max(H.h2o_backward_workspace_bytes(w.B, w.Hq, w.Hkv, w.T, w.M, w.d, bf), 16),
+                     dtype=torch.uint8, device="cuda")
+    fn = lambda: H.h2o_sdpa_chunk_backward(q, kc, vc, kn, vn, b["lse"], dout, *grads, ws, scale)
+    fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    reps = 3
+    e0.record()
+    for _ in range(reps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    tf = 2.5 * attention_flops(w) / (ms * 1e-3) / 1e12
+    return {"workload": w.describe(), "ms": round(ms, 3), "tflops": round(tf, 1),
+            "frac_of_bf16_peak": round(tf / BF16_PEAK_TFLOPS, 4),
+            "kernels": "generic VALU (float32 arithmetic)"}
+
+
 # -------------------------------------------------------------- CPU baseline
 def cpu_baseline(w, budget_s, W):
     import oracle
@@ -357,6 +392,11 @@ def main():
         ins = bench_insert_first(args, torch, H, W)
         print(f"# insert-first decode: {ins['decode']['gbs']} GB/s; prefill "
               f"{[r['tflops'] for r in ins['prefill']]} TFLOP/s", file=sys.stderr, flush=True)
+    bwd = None
+    if not args.no_prefill:
+        bwd = bench_backward(args, torch, H, W)
+        print(f"# backward {bwd['workload']}: {bwd['ms']} ms, {bwd['tflops']} TFLOP/s",
+              file=sys.stderr, flush=True)
     w = dec["w"]
     cpu = None
     if args.cpu_budget > 0:
@@ -377,6 +417,7 @@ def main():
         "cpu_baseline": cpu,
         "prefill": prefill,
         "insert_first": ins,
+        "backward": bwd,
     }
     print(json.dumps(rec))
 

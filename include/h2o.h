@@ -267,8 +267,11 @@ size_t h2o_backward_workspace_bytes(int B, int Hq, int Hkv, int T, int M, int d,
  * and D_r = sum_j P_rj dP_rj (from P and dP, not from a rounded output):
  *   dV = P^T dout,  dS = P * (dP - D),  dQ = scale dS K,  dK = scale dS^T Q.
  * The summed weights of the forward carry no gradient (they only steer the
- * discrete eviction). Float32 arithmetic; gradients are stored in dtype
- * (bf16 nearest-even). Workspace of h2o_backward_workspace_bytes(). */
+ * discrete eviction). Float32 arithmetic for float32 data; bf16 data runs
+ * on bf16 MFMA with float32 accumulation, P and dS (formed in float32 with
+ * the row's D) rounded to bf16 as the operands of the dV, dK and dQ
+ * products. Gradients are stored in dtype (bf16 nearest-even). Workspace of
+ * h2o_backward_workspace_bytes(). */
 int h2o_sdpa_chunk_backward(const void* q, const void* k_cache,
                             const void* v_cache, const void* k_new,
                             const void* v_new, const int32_t* token_pos,
@@ -305,8 +308,9 @@ const char* h2o_last_error(void);
 /* Testing hook, not needed in normal use: force the bf16 SDPA kernel path of
  * h2o_sdpa_chunk for every later call in the process (-1 automatic, 0 the
  * generic VALU kernels, 1 the MFMA prefill kernels, 2 the decode kernels,
- * which need T == 1). float32 always uses the generic kernels. Returns
- * H2O_EINVAL for other values. */
+ * which need T == 1). float32 always uses the generic kernels. 0 also puts
+ * h2o_sdpa_chunk_backward on its VALU kernels. Returns H2O_EINVAL for other
+ * values. */
 int h2o_debug_force_path(int path);
 
 /* Benchmark hook, not needed in normal use. h2o_debug_timing(1) makes every
@@ -322,8 +326,8 @@ int h2o_debug_force_path(int path);
  *   9 decode split      10 decode combine     11 argmin + insert (k == 1)
  *  12 decode finish (h2o_chunk_step, T == 1)
  *  13 score-variant keys and index broadcast (h2o_evict_insert_policy)
- *  14 backward dQ (and the rows' D)  15 backward dK/dV
- *  16 KV gather / scatter */
+ *  14 backward dQ (VALU: and the rows' D)  15 backward dK/dV
+ *  16 KV gather / scatter   17 backward rows' D (MFMA path) */
 int h2o_debug_timing(int on);
 int h2o_debug_kernel_time(int kernel_id, double* total_ms, long* count);
 

@@ -34,6 +34,7 @@ FLAGS = [
 FILE_FLAGS = {
     "decode.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
     "sdpa_mfma.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form", "-fno-honor-nans"],
+    "backward_mfma.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
 }
 
 

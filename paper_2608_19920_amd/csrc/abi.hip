@@ -625,11 +625,16 @@ int h2o_sdpa_chunk_backward(const void* q, const void* k_cache, const void* v_ca
   rc = check_device();
   if (rc) return rc;
   const Shape s{B, Hq, Hkv, T, M, d, cache};
-  hipError_t e = launch_sdpa_backward(s, dtype, q, k_cache, v_cache, k_new, v_new,
-                                      KeyPos{token_pos, pos0}, lse, dout, dq, dk_cache,
-                                      dv_cache, dk_new, dv_new,
-                                      reinterpret_cast<float*>(workspace), scale,
-                                      reinterpret_cast<hipStream_t>(stream));
+  // bf16 runs on the MFMA kernels unless the generic path is forced
+  const bool mfma = dtype == H2O_BF16 && g_forced_path.load() != 0;
+  float* dot = reinterpret_cast<float*>(workspace);
+  const hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  const KeyPos kp{token_pos, pos0};
+  hipError_t e =
+      mfma ? launch_sdpa_backward_mfma(s, q, k_cache, v_cache, k_new, v_new, kp, lse, dout, dq,
+                                       dk_cache, dv_cache, dk_new, dv_new, dot, scale, st)
+           : launch_sdpa_backward(s, dtype, q, k_cache, v_cache, k_new, v_new, kp, lse, dout,
+                                  dq, dk_cache, dv_cache, dk_new, dv_new, dot, scale, st);
   if (e != hipSuccess) return fail(H2O_ELAUNCH, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
 }

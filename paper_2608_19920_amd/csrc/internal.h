@@ -114,7 +114,7 @@ bool decode_supports(int d, int G);   // (d, G) pairs the decode kernels handle
 enum KernelId {
   K_GENERIC_LSE = 0, K_GENERIC_MAIN, K_MFMA_LSE, K_MFMA_MAIN, K_SPLIT_REDUCE, K_COLSUM_REDUCE,
   K_ACCUMULATE, K_BOTTOMK, K_INSERT, K_DECODE_SPLIT, K_DECODE_COMBINE, K_ARGMIN_INSERT,
-  K_DECODE_FINISH, K_KEYS, K_BWD_DQ, K_BWD_DKDV, K_KV_COPY, K_COUNT
+  K_DECODE_FINISH, K_KEYS, K_BWD_DQ, K_BWD_DKDV, K_KV_COPY, K_BWD_DOT, K_COUNT
 };
 // While timing is switched on (h2o_debug_timing), kernels go out through
 // hipExtLaunchKernel with a start and a stop event: the runtime stamps them
@@ -205,6 +205,13 @@ hipError_t launch_sdpa_backward(const Shape& s, int dtype, const void* q, const 
                                 const float* lse, const void* dout, void* dq, void* dkc,
                                 void* dvc, void* dkn, void* dvn, float* dot, float scale,
                                 hipStream_t st);
+// The same gradients on bf16 MFMA (bf16 data, d = 64 or 128): a rows pass
+// for D_r, a rows pass for dq, a keys pass for dk and dv.
+hipError_t launch_sdpa_backward_mfma(const Shape& s, const void* q, const void* kc,
+                                     const void* vc, const void* kn, const void* vn, KeyPos kp,
+                                     const float* lse, const void* dout, void* dq, void* dkc,
+                                     void* dvc, void* dkn, void* dvn, float* dot, float scale,
+                                     hipStream_t st);
 // rows[r, i] = cache[r, idx[r, i]] (gather) or cache[r, idx[r, i]] = rows[r, i]
 // (scatter), `vecs` 16-byte vectors per cache row.
 hipError_t launch_kv_copy(bool gather, void* cache, const int32_t* idx, void* rows, int nrows,

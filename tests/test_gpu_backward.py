@@ -5,7 +5,8 @@ the float64 oracle.
 
 Gradients: normwise relative error per (b, head) slice <= 1e-5 (float32) and
 <= 2e-2 (bf16, gradients stored in bf16). The forward's lse comes from the
-library's own forward, as in training. Gather and scatter are bitwise.
+library's own forward, as in training. bf16 runs on the MFMA kernels, and
+again on the VALU kernels (path 0). Gather and scatter are bitwise.
 """
 import numpy as np
 import pytest
@@ -23,13 +24,21 @@ pytestmark = pytest.mark.gpu
 SHAPES = [  # B, Hq, Hkv, d, M, T, dtype
     (1, 4, 2, 64, 256, 64, "f32"),
     (2, 4, 2, 64, 100, 1, "f32"),
-    (1, 8, 2, 128, 300, 70, "bf16"),
+    (1, 8, 2, 128, 300, 70, "bf16"),        # ragged row and key blocks
     (2, 8, 2, 64, 333, 17, "bf16"),
-    (1, 28, 4, 128, 257, 40, "bf16"),
-    (1, 4, 1, 128, 0, 20, "bf16"),
-    (8, 32, 8, 64, 512, 1, "bf16"),
+    (1, 28, 4, 128, 257, 40, "bf16"),       # GQA 7
+    (1, 4, 1, 128, 0, 20, "bf16"),          # empty cache
+    (8, 32, 8, 64, 512, 1, "bf16"),         # one query, heavy hitters
     (1, 8, 2, 128, 1000, 128, "bf16"),
+    (2, 32, 8, 128, 700, 64, "bf16"),       # 16 heads: XCD-grouped block order
 ]
+PATHS = [-1, 0]   # bf16: -1 the MFMA kernels, 0 the VALU kernels
+
+
+@pytest.fixture
+def force(request):
+    yield
+    H.h2o_debug_force_path(-1)
 
 
 def _grads_check(dt, got, ref, names):
@@ -43,11 +52,15 @@ def _grads_check(dt, got, ref, names):
         assert e <= tol, n
 
 
+@pytest.mark.parametrize("path", PATHS)
 @pytest.mark.parametrize("shape", SHAPES)
-def test_backward_chunk_mode(shape):
+def test_backward_chunk_mode(shape, path, force):
     B, Hq, Hkv, d, M, T, dt = shape
+    if dt == "f32" and path != -1:
+        pytest.skip("float32 has one path")
+    H.h2o_debug_force_path(path)
     wl = W.custom("bwd", B=B, Hq=Hq, Hkv=Hkv, d=d, M=M, T=T, dtype=dt, heavy_frac=0.02)
-    say(f"backward {wl.describe()}")
+    say(f"backward {wl.describe()} path {path}")
     x = W.make_inputs(wl, seed=M + 3 * T)
     tdt = U.TDT[dt]
     q, kc, vc, kn, vn = (U.to_dev(x[n], tdt) for n in ("q", "k_cache", "v_cache", "k_new",
@@ -70,14 +83,19 @@ def test_backward_chunk_mode(shape):
                  ("dq", "dk_cache", "dv_cache", "dk_new", "dv_new"))
 
 
+@pytest.mark.parametrize("path", PATHS)
 @pytest.mark.parametrize("shape", [(1, 4, 2, 64, 256, 64, "f32"), (2, 8, 2, 128, 300, 33, "bf16"),
-                                   (4, 8, 4, 64, 200, 1, "bf16")])
-def test_backward_cache_mode(shape):
+                                   (4, 8, 4, 64, 200, 1, "bf16"),
+                                   (1, 32, 8, 128, 500, 40, "bf16")])
+def test_backward_cache_mode(shape, path, force):
     """Backward of h2o_sdpa_cache: the chunk sits in scattered slots, the mask
     comes from the token positions (some rows of head (0, 0) see nothing)."""
     B, Hq, Hkv, d, M, T, dt = shape
+    if dt == "f32" and path != -1:
+        pytest.skip("float32 has one path")
+    H.h2o_debug_force_path(path)
     wl = W.custom("bwdc", B=B, Hq=Hq, Hkv=Hkv, d=d, M=M, T=T, dtype=dt)
-    say(f"backward, cache mode {wl.describe()}")
+    say(f"backward, cache mode {wl.describe()} path {path}")
     x = W.make_inputs(wl, seed=5)
     rng = np.random.default_rng(5)
     pos0 = 1000
@@ -102,6 +120,40 @@ def test_backward_cache_mode(shape):
     ref = oracle.sdpa_chunk_backward(x["q"], x["k_cache"], x["v_cache"], None, None, do_np, scale,
                                      token_pos=tp, pos0=pos0)
     _grads_check(dt, [U.to_np(g) for g in (dq, dkc, dvc)], ref[:3], ("dq", "dk", "dv"))
+
+
+def test_backward_full_size_sampled_head():
+    """The backward at the 1024-token prefill size (B1 Hq32 Hkv8 d128 M8192
+    T1024, bf16) in the launch configuration the benchmark times; the oracle
+    recomputes the gradients of one KV head (its group's query heads and its
+    keys) from that head's slice of the inputs."""
+    wl = W.WORKLOADS["prefill_bf16"]
+    say(f"backward, full size {wl.describe()}")
+    x = W.make_inputs(wl, seed=1)
+    tdt = torch.bfloat16
+    q, kc, vc, kn, vn = (U.to_dev(x[n], tdt) for n in ("q", "k_cache", "v_cache", "k_new",
+                                                        "v_new"))
+    do_np = W.bf16_bits_to_f32(W.f32_to_bf16_bits(
+        np.random.default_rng(11).standard_normal(x["q"].shape).astype(np.float32)))
+    dout = U.to_dev(do_np, tdt)
+    b = H.alloc_step(wl.B, wl.Hq, wl.Hkv, wl.T, wl.M, wl.d, tdt)
+    scale = float(x["scale"])
+    H.h2o_sdpa_chunk(q, kc, vc, kn, vn, b["out"], b["lse"], b["wsum"], b["workspace"], scale)
+    grads = [torch.empty_like(t) for t in (q, kc, vc, kn, vn)]
+    ws = torch.empty(H.h2o_backward_workspace_bytes(wl.B, wl.Hq, wl.Hkv, wl.T, wl.M, wl.d, tdt),
+                     dtype=torch.uint8, device=U.DEV)
+    H.h2o_sdpa_chunk_backward(q, kc, vc, kn, vn, b["lse"], dout, *grads, ws, scale)
+    torch.cuda.synchronize()
+    got = [U.to_np(g) for g in grads]
+    for g in got:
+        assert np.isfinite(g).all()
+    G, h = wl.G, 5
+    qs = slice(h * G, (h + 1) * G)
+    ref = oracle.sdpa_chunk_backward(x["q"][:, qs], x["k_cache"][:, h:h + 1],
+                                     x["v_cache"][:, h:h + 1], x["k_new"][:, h:h + 1],
+                                     x["v_new"][:, h:h + 1], do_np[:, qs], scale)
+    sel = [got[0][:, qs]] + [g[:, h:h + 1] for g in got[1:]]
+    _grads_check("bf16", sel, ref, ("dq", "dk_cache", "dv_cache", "dk_new", "dv_new"))
 
 
 @pytest.mark.parametrize("dt", ["f32", "bf16"])

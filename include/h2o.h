@@ -251,8 +251,11 @@ int h2o_chunk_step_insert_first(const void* q, void* k_cache, void* v_cache,
 
 /* ---- Fine-tuning (Sec. "Fine-Tuning for Sparse Attention"). */
 
-/* Bytes of device scratch for h2o_sdpa_chunk_backward (one float per query
- * row; 0 on invalid arguments). */
+/* Bytes of device scratch for h2o_sdpa_chunk_backward (0 on invalid
+ * arguments): one float per packed query row for float32; for bf16 one per
+ * row and key-range split, plus float32 partials of dq [splits,B,Hq,T,d] when
+ * the shape has too few query rows to fill the GPU (e.g. 2 splits, 32 MiB at
+ * B1 Hq32 T1024 d128). */
 size_t h2o_backward_workspace_bytes(int B, int Hq, int Hkv, int T, int M, int d,
                                     int dtype);
 
@@ -327,7 +330,8 @@ int h2o_debug_force_path(int path);
  *  12 decode finish (h2o_chunk_step, T == 1)
  *  13 score-variant keys and index broadcast (h2o_evict_insert_policy)
  *  14 backward dQ (VALU: and the rows' D)  15 backward dK/dV
- *  16 KV gather / scatter   17 backward rows' D (MFMA path) */
+ *  16 KV gather / scatter   17 backward rows' D (MFMA path)
+ *  18 backward dQ split reduce (MFMA path) */
 int h2o_debug_timing(int on);
 int h2o_debug_kernel_time(int kernel_id, double* total_ms, long* count);
 

@@ -594,7 +594,8 @@ int h2o_chunk_step_insert_first(const void* q, void* k_cache, void* v_cache, flo
 size_t h2o_backward_workspace_bytes(int B, int Hq, int Hkv, int T, int M, int d, int dtype) {
   if (dtype != H2O_F32 && dtype != H2O_BF16) return 0;
   if (check_shape(B, Hq, Hkv, T, M, d) != H2O_OK) return 0;
-  return align256((size_t)B * Hkv * (Hq / Hkv) * T * sizeof(float));
+  const Shape s{B, Hq, Hkv, T, M, d};
+  return backward_plan(s, dtype == H2O_BF16 ? 1 : 0).bytes;
 }
 
 int h2o_sdpa_chunk_backward(const void* q, const void* k_cache, const void* v_cache,
@@ -627,14 +628,15 @@ int h2o_sdpa_chunk_backward(const void* q, const void* k_cache, const void* v_ca
   const Shape s{B, Hq, Hkv, T, M, d, cache};
   // bf16 runs on the MFMA kernels unless the generic path is forced
   const bool mfma = dtype == H2O_BF16 && g_forced_path.load() != 0;
-  float* dot = reinterpret_cast<float*>(workspace);
   const hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   const KeyPos kp{token_pos, pos0};
   hipError_t e =
       mfma ? launch_sdpa_backward_mfma(s, q, k_cache, v_cache, k_new, v_new, kp, lse, dout, dq,
-                                       dk_cache, dv_cache, dk_new, dv_new, dot, scale, st)
+                                       dk_cache, dv_cache, dk_new, dv_new,
+                                       reinterpret_cast<char*>(workspace), scale, st)
            : launch_sdpa_backward(s, dtype, q, k_cache, v_cache, k_new, v_new, kp, lse, dout,
-                                  dq, dk_cache, dv_cache, dk_new, dv_new, dot, scale, st);
+                                  dq, dk_cache, dv_cache, dk_new, dv_new,
+                                  reinterpret_cast<float*>(workspace), scale, st);
   if (e != hipSuccess) return fail(H2O_ELAUNCH, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();
 }

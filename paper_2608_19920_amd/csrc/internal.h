@@ -87,6 +87,8 @@ __device__ __forceinline__ bool pos_visible(int32_t tpj, int32_t pos0, int i) {
   return (long long)tpj - (long long)pos0 <= (long long)i;
 }
 
+__host__ __device__ __forceinline__ size_t align256_size(size_t n) { return (n + 255) & ~size_t(255); }
+
 // ---------------------------------------------------------- workspace plan
 // Layout of the scratch buffer used by h2o_sdpa_chunk. All offsets are byte
 // offsets, 256-byte aligned.
@@ -114,7 +116,7 @@ bool decode_supports(int d, int G);   // (d, G) pairs the decode kernels handle
 enum KernelId {
   K_GENERIC_LSE = 0, K_GENERIC_MAIN, K_MFMA_LSE, K_MFMA_MAIN, K_SPLIT_REDUCE, K_COLSUM_REDUCE,
   K_ACCUMULATE, K_BOTTOMK, K_INSERT, K_DECODE_SPLIT, K_DECODE_COMBINE, K_ARGMIN_INSERT,
-  K_DECODE_FINISH, K_KEYS, K_BWD_DQ, K_BWD_DKDV, K_KV_COPY, K_BWD_DOT, K_COUNT
+  K_DECODE_FINISH, K_KEYS, K_BWD_DQ, K_BWD_DKDV, K_KV_COPY, K_BWD_DOT, K_BWD_DQ_REDUCE, K_COUNT
 };
 // While timing is switched on (h2o_debug_timing), kernels go out through
 // hipExtLaunchKernel with a start and a stop event: the runtime stamps them
@@ -205,12 +207,22 @@ hipError_t launch_sdpa_backward(const Shape& s, int dtype, const void* q, const 
                                 const float* lse, const void* dout, void* dq, void* dkc,
                                 void* dvc, void* dkn, void* dvn, float* dot, float scale,
                                 hipStream_t st);
+// Workspace of the backward: D partials [ns_dot][BH][R] floats at offset 0
+// (the VALU kernels use the first plane) and, with several, one more plane
+// for their sum; then, when the dq pass is split, dq partials
+// [ns_dq][BH][R][d] floats at off_part. dtype 0 (float32) has no splits.
+struct BackwardPlan {
+  int ns_dot, ns_dq;
+  size_t off_part, bytes;
+};
+BackwardPlan backward_plan(const Shape& s, int dtype);
 // The same gradients on bf16 MFMA (bf16 data, d = 64 or 128): a rows pass
-// for D_r, a rows pass for dq, a keys pass for dk and dv.
+// for D_r, a rows pass for dq (plus the reduce of its split partials), a
+// keys pass for dk and dv. ws: a workspace of backward_plan(s, 1).bytes.
 hipError_t launch_sdpa_backward_mfma(const Shape& s, const void* q, const void* kc,
                                      const void* vc, const void* kn, const void* vn, KeyPos kp,
                                      const float* lse, const void* dout, void* dq, void* dkc,
-                                     void* dvc, void* dkn, void* dvn, float* dot, float scale,
+                                     void* dvc, void* dkn, void* dvn, char* ws, float scale,
                                      hipStream_t st);
 // rows[r, i] = cache[r, idx[r, i]] (gather) or cache[r, idx[r, i]] = rows[r, i]
 // (scatter), `vecs` 16-byte vectors per cache row.

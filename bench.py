@@ -318,17 +318,26 @@ def bench_backward(args, torch, H, W):
     fn()
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    reps = 3
+    reps = 5
     e0.record()
     for _ in range(reps):
         fn()
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / reps
+    # per-kernel times from the library's timing hook, over the same calls
+    H.h2o_debug_timing(True)
+    for _ in range(reps):
+        fn()
+    torch.cuda.synchronize()
+    kern = {k: round(H.h2o_debug_kernel_time(k)[0] / reps * 1e3, 1)
+            for k in ("bwd_dot", "bwd_dq", "bwd_dq_reduce", "bwd_dkdv")}
+    H.h2o_debug_timing(False)
     tf = 2.5 * attention_flops(w) / (ms * 1e-3) / 1e12
     return {"workload": w.describe(), "ms": round(ms, 3), "tflops": round(tf, 1),
-            "frac_of_bf16_peak": round(tf / BF16_PEAK_TFLOPS, 4),
-            "kernels": "bf16 MFMA: rows pass for D, rows pass for dq, keys pass for dk/dv"}
+            "frac_of_bf16_peak": round(tf / BF16_PEAK_TFLOPS, 4), "kernel_us": kern,
+            "kernels": "bf16 MFMA: rows pass for D, rows pass for dq (+ split reduce), "
+                       "keys pass for dk/dv"}
 
 
 # -------------------------------------------------------------- CPU baseline

@@ -255,9 +255,18 @@ def _bwd(L, **kw):
 
 
 def test_backward_workspace_bytes(L):
-    # one float per query row (B*Hkv*G*T = 2*8*16 rows), in 256-byte units
+    # one float per query row (B*Hkv*G*T = 2*8*16 rows), in 256-byte units: too
+    # few key tiles (4) for a key-range split
     assert L.h2o_backward_workspace_bytes(2, 8, 2, 16, 100, 64, 1) == 1024
+    assert L.h2o_backward_workspace_bytes(2, 8, 2, 16, 100, 64, 0) == 1024
     assert L.h2o_backward_workspace_bytes(2, 8, 3, 16, 100, 64, 1) == 0
+    # B1 Hq32 Hkv8 d128 M8192 T1024: 256 row blocks of 128 rows, so the bf16
+    # rows passes split the keys, 3 ways for D (plus a plane for the sum) and
+    # 2 ways for dq (float32 partials); float32 keeps one float per row
+    rows = 8 * 4096
+    assert L.h2o_backward_workspace_bytes(1, 32, 8, 1024, 8192, 128, 1) == \
+        (3 + 1) * rows * 4 + 2 * rows * 128 * 4
+    assert L.h2o_backward_workspace_bytes(1, 32, 8, 1024, 8192, 128, 0) == rows * 4
 
 
 @pytest.mark.parametrize("kw,code", [

@@ -32,7 +32,9 @@ SHAPES = [  # B, Hq, Hkv, d, M, T, dtype
     (1, 8, 2, 128, 1000, 128, "bf16"),
     (2, 32, 8, 128, 700, 64, "bf16"),       # 16 heads: XCD-grouped block order
 ]
-PATHS = [-1, 0]   # bf16: -1 the MFMA kernels, 0 the VALU kernels
+# bf16 shapes run on the MFMA kernels (-1) and on the VALU kernels (0);
+# float32 has only the VALU kernels
+CASES = [(sh, p) for sh in SHAPES for p in ((-1, 0) if sh[-1] == "bf16" else (-1,))]
 
 
 @pytest.fixture
@@ -52,12 +54,9 @@ def _grads_check(dt, got, ref, names):
         assert e <= tol, n
 
 
-@pytest.mark.parametrize("path", PATHS)
-@pytest.mark.parametrize("shape", SHAPES)
+@pytest.mark.parametrize("shape,path", CASES)
 def test_backward_chunk_mode(shape, path, force):
     B, Hq, Hkv, d, M, T, dt = shape
-    if dt == "f32" and path != -1:
-        pytest.skip("float32 has one path")
     H.h2o_debug_force_path(path)
     wl = W.custom("bwd", B=B, Hq=Hq, Hkv=Hkv, d=d, M=M, T=T, dtype=dt, heavy_frac=0.02)
     say(f"backward {wl.describe()} path {path}")
@@ -83,16 +82,16 @@ def test_backward_chunk_mode(shape, path, force):
                  ("dq", "dk_cache", "dv_cache", "dk_new", "dv_new"))
 
 
-@pytest.mark.parametrize("path", PATHS)
-@pytest.mark.parametrize("shape", [(1, 4, 2, 64, 256, 64, "f32"), (2, 8, 2, 128, 300, 33, "bf16"),
-                                   (4, 8, 4, 64, 200, 1, "bf16"),
-                                   (1, 32, 8, 128, 500, 40, "bf16")])
+CACHE_SHAPES = [(1, 4, 2, 64, 256, 64, "f32"), (2, 8, 2, 128, 300, 33, "bf16"),
+                (4, 8, 4, 64, 200, 1, "bf16"), (1, 32, 8, 128, 500, 40, "bf16")]
+
+
+@pytest.mark.parametrize("shape,path", [(sh, p) for sh in CACHE_SHAPES
+                                        for p in ((-1, 0) if sh[-1] == "bf16" else (-1,))])
 def test_backward_cache_mode(shape, path, force):
     """Backward of h2o_sdpa_cache: the chunk sits in scattered slots, the mask
     comes from the token positions (some rows of head (0, 0) see nothing)."""
     B, Hq, Hkv, d, M, T, dt = shape
-    if dt == "f32" and path != -1:
-        pytest.skip("float32 has one path")
     H.h2o_debug_force_path(path)
     wl = W.custom("bwdc", B=B, Hq=Hq, Hkv=Hkv, d=d, M=M, T=T, dtype=dt)
     say(f"backward, cache mode {wl.describe()} path {path}")

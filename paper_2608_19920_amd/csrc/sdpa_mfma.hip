@@ -232,15 +232,24 @@ __device__ __forceinline__ bool key_hidden(const Rel& rl, int kb, int r, int j, 
   return false;
 }
 
-// Cache mode: thread tid < BN fetches the relative position of key j0 + tid.
-__device__ __forceinline__ int load_rp(const int32_t* tp_bh, int32_t pos0, int j0, int M) {
+// Cache mode: thread tid < BN fetches the token position of key j0 + tid.
+// It becomes a relative position (kRpFar past the cache) only when the tile
+// is stored: arithmetic on the loaded value where the load is issued would
+// wait for it, and with it for the K/V loads issued just before.
+__device__ __forceinline__ int32_t load_tp(const int32_t* tp_bh, int j0, int M) {
   const int j = j0 + (int)threadIdx.x;
-  if (threadIdx.x >= BN || j >= M) return kRpFar;
-  const long long r = (long long)tp_bh[j] - pos0;
-  return r > kRpFar ? kRpFar : (r < -kRpFar ? -kRpFar : (int)r);
+  return (threadIdx.x < BN && j < M) ? tp_bh[j] : 0;
 }
-__device__ __forceinline__ void store_rp(int* rps, int v) {
-  if (threadIdx.x < BN) rps[threadIdx.x] = v;
+__device__ __forceinline__ void store_rp(int* rps, int32_t tpj, int32_t pos0, int j0, int M) {
+  // an empty asm that takes and returns the value: the conversion below
+  // cannot be moved (or folded into the load) ahead of this point
+  asm volatile("" : "+v"(tpj));
+  if (threadIdx.x < BN) {
+    const int j = j0 + (int)threadIdx.x;
+    const long long r = (long long)tpj - pos0;
+    rps[threadIdx.x] =
+        j >= M ? kRpFar : (r > kRpFar ? kRpFar : (r < -kRpFar ? -kRpFar : (int)r));
+  }
 }
 
 // Tiles [t0, t1) of a row tile's key range [0, ntiles*BN) for split sp.
@@ -369,14 +378,14 @@ __device__ __forceinline__ void lse_tile(int t, int t0, int t1, const f32x4 (&s_
   const int b0 = (t - t0) % NBUF, b1 = (t + 1 - t0) % NBUF, b2 = (t + 2 - t0) % NBUF;
   const int jn = min(t + 3, t1 - 1) * BN;
   load_tile<D, NT>(fill, tl, kc_bh, kn_bh, jn, g.M, g.Nk);
-  if (MK == 2) rfill = load_rp(tp_bh, g.pos0, jn, g.M);
+  if (MK == 2) rfill = load_tp(tp_bh, jn, g.M);
   Rel rl;
   if (MK == 2) load_rel(rl, rps[b0], lane);
   scores_tile<D, NQB>(s_nxt, Ks[b1], qf, lane);
   lse_update<MK, NQB>(s_cur, m, l, qi, t * BN, g.M, lane, c, rl);
   interleave<2 * NQB * (D / 32), MK ? 8 : 5>();
   store_tile<D, NT>(Ks[b2], tl.loff, put);
-  if (MK == 2) store_rp(rps[b2], rput);
+  if (MK == 2) store_rp(rps[b2], rput, g.pos0, min(t + 2, t1 - 1) * BN, g.M);
   __syncthreads();
 }
 
@@ -459,9 +468,9 @@ __global__ __launch_bounds__(NW * 64) void lse_pass(Geo g, int Hq, int Hkv, int 
     load_tile<D, NT>(S.ka, tl, kc_bh, kn_bh, t0 * BN, g.M, g.Nk);
     load_tile<D, NT>(S.kb, tl, kc_bh, kn_bh, j1, g.M, g.Nk);
     if (CACHE) {
-      store_rp(rps[0], load_rp(tp_bh, g.pos0, t0 * BN, g.M));
-      store_rp(rps[1], load_rp(tp_bh, g.pos0, j1, g.M));
-      S.ra = load_rp(tp_bh, g.pos0, j2, g.M);
+      store_rp(rps[0], load_tp(tp_bh, t0 * BN, g.M), g.pos0, t0 * BN, g.M);
+      store_rp(rps[1], load_tp(tp_bh, j1, g.M), g.pos0, j1, g.M);
+      S.ra = load_tp(tp_bh, j2, g.M);
     }
     store_tile<D, NT>(Ks[0], tl.loff, S.ka);
     store_tile<D, NT>(Ks[1], tl.loff, S.kb);
@@ -562,7 +571,7 @@ __device__ __forceinline__ void main_tile(
   const int jn = min(t + 3, t1 - 1) * BN;
   load_tile<D, NT>(kfill, tl, kc_bh, kn_bh, jn, g.M, g.Nk);
   load_tile<D, NT>(vfill, tl, vc_bh, vn_bh, jn, g.M, g.Nk);
-  if (MK == 2) rfill = load_rp(tp_bh, g.pos0, jn, g.M);
+  if (MK == 2) rfill = load_tp(tp_bh, jn, g.M);
   Rel rl;
   if (MK == 2) load_rel(rl, rps[b0], lane);
   bf16x8 pb[NQB];
@@ -573,7 +582,7 @@ __device__ __forceinline__ void main_tile(
   interleave<NQB * (D / 16), 1>();
   store_tile<D, NT>(Ks[b2], tl.loff, kput);
   store_tile<D, NT>(Vs[b2], tl.vloff, vput);
-  if (MK == 2) store_rp(rps[b2], rput);
+  if (MK == 2) store_rp(rps[b2], rput, g.pos0, min(t + 2, t1 - 1) * BN, g.M);
   __syncthreads();
   if (threadIdx.x < BN) {
     const float (*cs)[BN] = cs_lds[(t - t0) & 1];
@@ -698,9 +707,9 @@ __global__ __launch_bounds__(NW * 64) void main_pass(Geo g, int Hq, int Hkv, int
     load_tile<D, NT>(S.kb, tl, kc_bh, kn_bh, j1, g.M, g.Nk);
     load_tile<D, NT>(S.vb, tl, vc_bh, vn_bh, j1, g.M, g.Nk);
     if (CACHE) {
-      store_rp(rps[0], load_rp(tp_bh, g.pos0, t0 * BN, g.M));
-      store_rp(rps[1], load_rp(tp_bh, g.pos0, j1, g.M));
-      S.ra = load_rp(tp_bh, g.pos0, j2, g.M);
+      store_rp(rps[0], load_tp(tp_bh, t0 * BN, g.M), g.pos0, t0 * BN, g.M);
+      store_rp(rps[1], load_tp(tp_bh, j1, g.M), g.pos0, j1, g.M);
+      S.ra = load_tp(tp_bh, j2, g.M);
     }
     store_tile<D, NT>(Ks[0], tl.loff, S.ka);
     store_tile<D, NT>(Vs[0], tl.vloff, S.va);

@@ -573,6 +573,16 @@ int h2o_chunk_step_insert_first(const void* q, void* k_cache, void* v_cache, flo
   hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   char* ws = reinterpret_cast<char*>(workspace);
   const int eb = dtype == H2O_F32 ? 4 : 2;
+  // T == 1 on the decode kernels with the h2o ranking: the split kernel picks
+  // and fills the slot itself (two launches, same results)
+  if (p.path == 2 && policy == H2O_POLICY_H2O) {
+    const hipError_t e = launch_decode_step_insert_first(s, p, q, k_cache, v_cache, scores,
+                                                         token_pos, k_new, v_new, out, lse,
+                                                         wsum, evict_idx, pos0, ws, scale, st);
+    if (e != hipSuccess)
+      return fail(H2O_ELAUNCH, "kernel launch failed: %s", hipGetErrorString(e));
+    return ok();
+  }
   // rank by the scores after pos0 tokens, then write the chunk into the
   // chosen slots with score 0 and positions pos0 + i
   hipError_t e = launch_evict(policy, k_cache, v_cache, scores, token_pos, k_new, v_new, nullptr,

@@ -85,12 +85,31 @@ __device__ __forceinline__ bf16x8 v_operand(const bf16_t* vs, int db, int lane) 
 // and V come in through buffer loads whose range is the head, so slots past
 // the cache read as zero; they are masked, and their logit stores go to a
 // sink.
-template <int D, int G, bool CACHE>
+//
+// INS (cache mode, the insert-first step with the h2o ranking): the block
+// first picks the head's evicted slot, the (score, slot)-smallest of the
+// scores before the step (every block of the head finds the same one), and
+// attends as if the chunk's key, value and position pos0 were already in
+// that slot: the rows read from the cache are replaced in registers. Split
+// block 0 also writes them into the cache and the slot into evict_idx; the
+// scores are left to the combine (slot: 0 + its summed weight). Other blocks
+// may read the slot while block 0 overwrites it; they never use what they
+// read there.
+struct InsArgs {
+  const float* scores;    // [BH][M], read only here
+  const bf16_t* kn;       // [BH][d] the chunk's key and value
+  const bf16_t* vn;
+  int32_t* evict_idx;     // [BH]
+};
+constexpr int kScPre = 16;   // scores per thread prefetched before the first K/V loads
+
+template <int D, int G, bool CACHE, bool INS = false>
 __global__ __launch_bounds__(kThreads) void decode_split(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
     int Hq, int Hkv, int M, float c_log2, float* __restrict__ logits,
     float2* __restrict__ dstat, float* __restrict__ dO, float* __restrict__ sink,
-    const int32_t* __restrict__ tp, int32_t pos0) {
+    const int32_t* __restrict__ tp, int32_t pos0, InsArgs ins) {
+  static_assert(!INS || CACHE, "the insert-first step runs in cache mode");
   constexpr int DH = D / 32;                 // MFMA k-chunks of a row
   constexpr int NK = 2 * DH;                 // K loads per step (two 16-slot blocks)
   constexpr int RPL = 512 / D;               // V rows per wave load
@@ -100,6 +119,8 @@ __global__ __launch_bounds__(kThreads) void decode_split(
   __shared__ __attribute__((aligned(16))) bf16_t vs_all[kWaves][kStep * VP];
   __shared__ float red_m[kWaves][16], red_l[kWaves][16];
   __shared__ float ored[kWaves][G][D];
+  __shared__ uint32_t red_k[kWaves], red_j[kWaves];
+  __shared__ int sh_slot;
   const int s = blockIdx.x, nsplit = gridDim.x;
   const size_t bh = blockIdx.y;
   const int b = (int)(bh / Hkv), h = (int)(bh % Hkv);
@@ -163,8 +184,25 @@ __global__ __launch_bounds__(kThreads) void decode_split(
 #pragma unroll
   for (int db = 0; db < D / 16; ++db) oacc[db] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  int slot = -1;                                // INS: the head's evicted slot
+  u32x4 knr[DH], vnr = u32x4{0u, 0u, 0u, 0u};   // INS: this lane's parts of the chunk's K, V rows
   auto consume = [&](int k, int u) {
     const int key0 = (stream + k * nstreams) * kStep;
+    if (INS && (unsigned)(slot - key0) < (unsigned)kStep) {   // wave-uniform, one step per head
+      const int rs = slot - key0;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+        if (16 * kb + col == rs) {
+#pragma unroll
+          for (int dh = 0; dh < DH; ++dh) kr[u][kb * DH + dh] = knr[dh];
+        }
+#pragma unroll
+      for (int t = 0; t < NV; ++t)
+        if (t * RPL + vrow == rs) vr[u][t] = vnr;
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+        if (16 * (i >> 2) + 4 * grp + (i & 3) == rs) tr[u][i] = pos0;
+    }
 #pragma unroll
     for (int t = 0; t < NV; ++t)
       *reinterpret_cast<u32x4*>(vs + (t * RPL + vrow) * VP + vcol) = vr[u][t];
@@ -219,7 +257,61 @@ __global__ __launch_bounds__(kThreads) void decode_split(
     for (int db = 0; db < D / 16; ++db) oacc[db] = mfma(v_operand<D>(vs, db, lane), pb, oacc[db]);
   };
 
+  // INS: the scores and the chunk's rows are requested before the first K/V
+  // loads, so the choice of the slot waits for them alone
+  float scp[INS ? kScPre : 1];
+  if (INS) {
+    const float* sc_bh = ins.scores + bh * (size_t)M;
+#pragma unroll
+    for (int u = 0; u < kScPre; ++u) {
+      const int j = tid + u * kThreads;
+      scp[u] = j < M ? sc_bh[j] : 0.f;
+    }
+#pragma unroll
+    for (int dh = 0; dh < DH; ++dh) knr[dh] = load16(ins.kn + bh * (size_t)D + 32 * dh + 8 * grp);
+    vnr = load16(ins.vn + bh * (size_t)D + vcol);
+  }
   issue(0, 0);
+  if (INS) {
+    // (key, slot)-smallest, slots visited in increasing order per thread so
+    // that a strict < keeps the lowest slot among equal keys
+    uint32_t bk = 0xFFFFFFFFu, bj = 0xFFFFFFFFu;
+#pragma unroll
+    for (int u = 0; u < kScPre; ++u) {
+      const int j = tid + u * kThreads;
+      const uint32_t key = order_key(scp[u]);
+      if (j < M && key < bk) { bk = key; bj = (uint32_t)j; }
+    }
+    for (int j = tid + kScPre * kThreads; j < M; j += kThreads) {
+      const uint32_t key = order_key(ins.scores[bh * (size_t)M + j]);
+      if (key < bk) { bk = key; bj = (uint32_t)j; }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const uint32_t ok = __shfl_xor(bk, o, 64), oj = __shfl_xor(bj, o, 64);
+      if (ok < bk || (ok == bk && oj < bj)) { bk = ok; bj = oj; }
+    }
+    if (lane == 0) { red_k[wave] = bk; red_j[wave] = bj; }
+    __syncthreads();
+    if (tid == 0) {
+      for (int w = 1; w < kWaves; ++w)
+        if (red_k[w] < bk || (red_k[w] == bk && red_j[w] < bj)) { bk = red_k[w]; bj = red_j[w]; }
+      sh_slot = (int)bj;
+    }
+    __syncthreads();
+    slot = sh_slot;
+    if (s == 0) {   // one block per head writes the insert
+      if (tid == 0) {
+        ins.evict_idx[bh] = slot;
+        const_cast<int32_t*>(tp)[bh * (size_t)M + slot] = pos0;
+      }
+      if (tid < D / 8) {
+        const size_t o = (bh * (size_t)M + slot) * D + 8 * tid;
+        *reinterpret_cast<u32x4*>(const_cast<bf16_t*>(kc) + o) = load16(ins.kn + bh * (size_t)D + 8 * tid);
+        *reinterpret_cast<u32x4*>(const_cast<bf16_t*>(vc) + o) = load16(ins.vn + bh * (size_t)D + 8 * tid);
+      }
+    }
+  }
   for (int k = 0; k < nst; k += 2) {
     issue(k + 1, 1);
     consume(k, 0);
@@ -369,13 +461,16 @@ __device__ __forceinline__ float chunk_weight(const HeadStats& hs, int G) {
 constexpr int kCols = 1024;
 
 // With scores non-null (cache mode only) it also adds each slot's summed
-// weight to its score: scores[j] += wsum[j], one float32 addition.
+// weight to its score: scores[j] += wsum[j], one float32 addition; with
+// ins_idx non-null the head's slot ins_idx[bh] (just inserted, by the fused
+// insert-first split) takes 0 + wsum[j] instead.
 template <int D>
 __global__ __launch_bounds__(kThreads) void decode_combine(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ kn, const bf16_t* __restrict__ vn,
     int Hq, int Hkv, int M, int nsplit, float c_log2, const float* __restrict__ logits,
     const float2* __restrict__ dstat, const float* __restrict__ dO, bf16_t* __restrict__ out,
-    float* __restrict__ lse, float* __restrict__ wsum, float* __restrict__ scores) {
+    float* __restrict__ lse, float* __restrict__ wsum, float* __restrict__ scores,
+    const int32_t* __restrict__ ins_idx) {
   __shared__ HeadStats hs;
   const int G = Hq / Hkv;
   const size_t bh = blockIdx.y;
@@ -388,10 +483,11 @@ __global__ __launch_bounds__(kThreads) void decode_combine(
   const float* lgb = logits + bh * (size_t)G * logit_pitch(M);
   const int c0 = blockIdx.x * kCols, c1 = min(M, c0 + kCols);
   float* sc = scores ? scores + bh * (size_t)M : nullptr;
+  const int ins = ins_idx ? ins_idx[bh] : -1;
   for (int j = c0 + threadIdx.x; j < c1; j += kThreads) {
     const float wj = slot_weight(hs, lgb, logit_pitch(M), G, j);
     w[j] = wj;
-    if (sc) sc[j] = sc[j] + wj;
+    if (sc) sc[j] = (j == ins ? 0.f : sc[j]) + wj;
   }
   if (has_chunk && blockIdx.x == 0 && threadIdx.x == 0) w[M] = chunk_weight(hs, G);
 }
@@ -509,12 +605,12 @@ __global__ __launch_bounds__(kFinThreads) void decode_finish(
 // Split blocks per head such that all blocks of the grid are resident at
 // once (blocks per CU of this kernel instance x CUs), at most kMaxSplit and
 // at most one wave per step of slots.
-template <int D, int G, bool CACHE>
+template <int D, int G, bool CACHE, bool INS = false>
 int split_count(int M, int BH) {
   static int resident = 0;
   if (!resident) {
     int per_cu = 0, dev = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, decode_split<D, G, CACHE>,
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, decode_split<D, G, CACHE, INS>,
                                                      kThreads, 0) != hipSuccess || per_cu < 1)
       per_cu = 2;
     if (hipGetDevice(&dev) != hipSuccess ||
@@ -532,21 +628,29 @@ int split_count(int M, int BH) {
   return ns < 1 ? 1 : ns;
 }
 
+// ins.scores non-null: the fused insert-first form (cache mode).
 template <int D, int G>
 hipError_t launch_split(hipStream_t st, int BH, const void* q, const void* kc, const void* vc,
                         int Hq, int Hkv, int M, float c, float* logits, float2* dstat, float* dO,
-                        float* sink, KeyPos kp, int* ns) {
+                        float* sink, KeyPos kp, int* ns, InsArgs ins) {
+  if (kp.tp && ins.scores) {
+    *ns = split_count<D, G, true, true>(M, BH);
+    return launch_kernel(K_DECODE_SPLIT, decode_split<D, G, true, true>, dim3(*ns, BH),
+                         dim3(kThreads), st, (const bf16_t*)q, (const bf16_t*)kc,
+                         (const bf16_t*)vc, Hq, Hkv, M, c, logits, dstat, dO, sink, kp.tp,
+                         kp.pos0, ins);
+  }
   if (kp.tp) {
     *ns = split_count<D, G, true>(M, BH);
     return launch_kernel(K_DECODE_SPLIT, decode_split<D, G, true>, dim3(*ns, BH),
                          dim3(kThreads), st, (const bf16_t*)q, (const bf16_t*)kc,
                          (const bf16_t*)vc, Hq, Hkv, M, c, logits, dstat, dO, sink, kp.tp,
-                         kp.pos0);
+                         kp.pos0, ins);
   }
   *ns = split_count<D, G, false>(M, BH);
   return launch_kernel(K_DECODE_SPLIT, decode_split<D, G, false>, dim3(*ns, BH), dim3(kThreads),
                        st, (const bf16_t*)q, (const bf16_t*)kc, (const bf16_t*)vc, Hq, Hkv, M, c,
-                       logits, dstat, dO, sink, (const int32_t*)nullptr, (int32_t)0);
+                       logits, dstat, dO, sink, (const int32_t*)nullptr, (int32_t)0, ins);
 }
 
 }  // namespace
@@ -564,7 +668,7 @@ namespace {
 // The split kernel over the cache (if any); returns the split count in *ns.
 hipError_t launch_decode_split(const Shape& s, const Plan& p, const void* q, const void* kc,
                                const void* vc, char* ws, float c, KeyPos kp, hipStream_t st,
-                               int* ns) {
+                               int* ns, InsArgs ins = InsArgs{nullptr, nullptr, nullptr, nullptr}) {
   float* logits = reinterpret_cast<float*>(ws + p.off_logits);
   float2* dstat = reinterpret_cast<float2*>(ws + p.off_stats);
   float* dO = reinterpret_cast<float*>(ws + p.off_opart);
@@ -575,7 +679,7 @@ hipError_t launch_decode_split(const Shape& s, const Plan& p, const void* q, con
   hipError_t e = hipErrorInvalidValue;
 #define H2O_SPLIT(DD, GG) \
   e = launch_split<DD, GG>(st, s.BH(), q, kc, vc, s.Hq, s.Hkv, s.M, c, logits, dstat, dO, sink, \
-                           kp, ns)
+                           kp, ns, ins)
   if (s.d == 64) {
     if (G == 1) H2O_SPLIT(64, 1);
     else if (G == 2) H2O_SPLIT(64, 2);
@@ -608,7 +712,27 @@ hipError_t launch_sdpa_decode(const Shape& s, const Plan& p, const void* q, cons
                        s.Hq, s.Hkv, s.M, ns, c,
                        (const float*)(ws + p.off_logits), (const float2*)(ws + p.off_stats),
                        (const float*)(ws + p.off_opart), (bf16_t*)out, lse, wsum,
-                       chunk ? nullptr : scores_acc);
+                       chunk ? nullptr : scores_acc, (const int32_t*)nullptr);
+}
+
+hipError_t launch_decode_step_insert_first(const Shape& s, const Plan& p, const void* q,
+                                           void* kc, void* vc, float* scores, int32_t* token_pos,
+                                           const void* kn, const void* vn, void* out, float* lse,
+                                           float* wsum, int32_t* evict_idx, int32_t pos0,
+                                           char* ws, float scale, hipStream_t st) {
+  const float c = scale * kLog2e;
+  int ns = 0;
+  hipError_t e = launch_decode_split(
+      s, p, q, kc, vc, ws, c, KeyPos{token_pos, pos0}, st, &ns,
+      InsArgs{scores, (const bf16_t*)kn, (const bf16_t*)vn, evict_idx});
+  if (e != hipSuccess) return e;
+  const dim3 cgrid((s.M + kCols - 1) / kCols, s.BH());
+  auto combine = s.d == 64 ? decode_combine<64> : decode_combine<128>;
+  return launch_kernel(K_DECODE_COMBINE, combine, cgrid, dim3(kThreads), st, (const bf16_t*)q,
+                       (const bf16_t*)nullptr, (const bf16_t*)nullptr, s.Hq, s.Hkv, s.M, ns, c,
+                       (const float*)(ws + p.off_logits), (const float2*)(ws + p.off_stats),
+                       (const float*)(ws + p.off_opart), (bf16_t*)out, lse, wsum, scores,
+                       (const int32_t*)evict_idx);
 }
 
 namespace {
@@ -674,7 +798,8 @@ hipError_t launch_decode_attend(const Shape& s, const Plan& p, const void* q, co
                        (const bf16_t*)q, (const bf16_t*)kn, (const bf16_t*)vn, s.Hq, s.Hkv,
                        s.M, ns, c, (const float*)(ws + p.off_logits),
                        (const float2*)(ws + p.off_stats), (const float*)(ws + p.off_opart),
-                       (bf16_t*)out, lse, (float*)nullptr, (float*)nullptr);
+                       (bf16_t*)out, lse, (float*)nullptr, (float*)nullptr,
+                       (const int32_t*)nullptr);
 }
 
 hipError_t launch_decode_evict(const Shape& s, const Plan& p, const void* q, void* kc, void* vc,

@@ -174,6 +174,17 @@ hipError_t launch_decode_evict(const Shape& s, const Plan& p, const void* q, voi
                                const void* kn, const void* vn, float* wsum, float* scores,
                                int32_t* token_pos, int32_t* evict_idx, int32_t pos0, char* ws,
                                float scale, hipStream_t st);
+// The insert-first step with the h2o ranking for T == 1 (cache mode), in two
+// launches: the split kernel picks each head's evicted slot itself (the
+// (score, slot)-smallest of the scores before the step), attends as if the
+// chunk's key, value and position were already in that slot and writes them
+// there; the combine adds the summed weights to the scores, the new slot's
+// to 0. Same results as evict, insert, attend and accumulate in turn.
+hipError_t launch_decode_step_insert_first(const Shape& s, const Plan& p, const void* q,
+                                           void* kc, void* vc, float* scores, int32_t* token_pos,
+                                           const void* kn, const void* vn, void* out, float* lse,
+                                           float* wsum, int32_t* evict_idx, int32_t pos0,
+                                           char* ws, float scale, hipStream_t st);
 hipError_t launch_colsum_reduce(const Shape& s, const Plan& p, const float* parts,
                                 float* wsum, hipStream_t st);
 hipError_t launch_accumulate(float* scores, const float* wsum, int rows, int M, int T,

@@ -13,11 +13,16 @@
 // Rows passes: a wave owns 32 packed rows (their Q and dO are B operands in
 // registers); the block's four waves share 32-key K/V tiles in LDS; the
 // transposed K operand of the dQ product comes from ds_read_b64_tr_b16.
-// Keys pass: a wave owns 32 keys and the waves share 32-row Q/dO tiles. Its
-// S and dP are computed in the key-per-lane orientation, so P and dS leave
-// the accumulators already laid out as the B operands of the dV and dK
-// products (two 16-row blocks per operand), and the transposed dO and Q
-// operands again come from transposing LDS reads.
+// Keys pass: a wave owns 16 keys (H2O_BWD_NKB blocks of 16; 16 keep the
+// wave at 200 registers, two waves per SIMD) and the waves share 32-row
+// Q/dO tiles. Its S and dP are computed in the key-per-lane orientation, so
+// P and dS leave the accumulators already laid out as the B operands of the
+// dV and dK products (two 16-row blocks per operand), and the transposed dO
+// and Q operands again come from transposing LDS reads.
+// When the rows passes would have too few blocks to fill the CUs they split
+// the key range: D partials are summed in split order (the dq pass's first
+// split leaves the sum for the keys pass), dq partials are float32 and
+// bwd_dq_reduce adds them in split order.
 //
 // Masking: key j is visible to chunk position i iff rel_j <= i, with rel_j =
 // -1 for a cache slot (chunk mode), j - M for a chunk key, and the slot's
@@ -37,7 +42,8 @@ constexpr int kW = 4;          // waves per block
 constexpr int kNT = 64 * kW;   // threads per block
 constexpr int kTile = 32;      // keys (rows passes) or packed rows (keys pass) per LDS tile
 constexpr int kPad = 16;       // bf16 past d per LDS row (pitch 288 B at d = 128)
-#ifndef H2O_BWD_NKB
+constexpr int kRB = kW * 32;   // packed rows per block of the rows passes (32 per wave)
+#ifndef H2O_BWD_NKB   // key blocks of 16 per wave in the keys pass
 #define H2O_BWD_NKB 1
 #endif
 
@@ -218,8 +224,8 @@ __global__ __launch_bounds__(kNT) void bwd_rows(BArgs a) {
   const int b = bhi / a.Hkv, h = bhi % a.Hkv;
   // x = split * (row tiles) + row tile: the blocks of one key range are
   // consecutive, so they share their K/V tiles in one L2
-  const int nrt = (a.R + kW * 32 - 1) / (kW * 32);
-  const int sp = xb / nrt, rblk = (xb % nrt) * (kW * 32), wrow0 = rblk + wave * 32;
+  const int nrt = (a.R + kRB - 1) / kRB;
+  const int sp = xb / nrt, rblk = (xb % nrt) * kRB, wrow0 = rblk + wave * 32;
   const bool live = wrow0 < a.R;
   const int imin = wrow0 / a.G;
 
@@ -247,7 +253,7 @@ __global__ __launch_bounds__(kNT) void bwd_rows(BArgs a) {
   }
 
   const int kv_end =
-      CACHE ? a.M : kv_end_for_rows(min(rblk + kW * 32, a.R), a.G, a.T, a.M, a.Nk - a.M);
+      CACHE ? a.M : kv_end_for_rows(min(rblk + kRB, a.R), a.G, a.T, a.M, a.Nk - a.M);
   // this split's share of the block's key tiles (possibly none)
   const int ntiles_all = (kv_end + kTile - 1) / kTile;
   const int tb = (int)((long long)sp * ntiles_all / a.ns);
@@ -507,7 +513,7 @@ __global__ __launch_bounds__(256) void bwd_dq_reduce(BArgs a) {
 
 template <int D, bool CACHE>
 hipError_t run(const Shape& s, const BackwardPlan& pl, BArgs a, hipStream_t st) {
-  const int BH = s.BH(), nrt = (s.R() + kW * 32 - 1) / (kW * 32);
+  const int BH = s.BH(), nrt = (s.R() + kRB - 1) / kRB;
   a.ns = pl.ns_dot;
   hipError_t e = launch_kernel(K_BWD_DOT, bwd_rows<D, false, CACHE>, dim3(nrt * a.ns, BH),
                                dim3(kNT), st, a);
@@ -537,7 +543,7 @@ BackwardPlan backward_plan(const Shape& s, int dtype) {
   const size_t BH = s.BH(), R = s.R();
   size_t bytes = align256_size(BH * R * sizeof(float));
   if (dtype == 1 && R > 0) {
-    const long long blocks = (long long)((R + kW * 32 - 1) / (kW * 32)) * (long long)BH;
+    const long long blocks = (long long)((R + kRB - 1) / kRB) * (long long)BH;
     const long long ntiles = (s.Nk() + kTile - 1) / kTile;
     auto pick = [&](long long target) {
       long long ns = (target + blocks - 1) / blocks;

@@ -240,7 +240,10 @@ int h2o_sdpa_cache(const void* q, const void* k_cache, const void* v_cache,
  *   3. h2o_sdpa_cache over the updated cache (out, lse, wsum [B,Hkv,M]);
  *   4. scores[b,h,j] += wsum[b,h,j] for all M slots (one float32 addition).
  * token_pos is required. Workspace of h2o_cache_workspace_bytes(..., policy);
- * its contents on entry are ignored. */
+ * its contents on entry are ignored. For T == 1 in bf16 with H2O_POLICY_H2O
+ * the step is two kernel launches (the attention kernel picks the slot and
+ * attends with the chunk's row already in place, then one kernel merges the
+ * splits and accumulates), with the same results as steps 1-4 in turn. */
 int h2o_chunk_step_insert_first(const void* q, void* k_cache, void* v_cache,
                                 float* scores, int32_t* token_pos,
                                 const void* k_new, const void* v_new, void* out,

@@ -121,6 +121,67 @@ def test_backward_cache_mode(shape, path, force):
     _grads_check(dt, [U.to_np(g) for g in (dq, dkc, dvc)], ref[:3], ("dq", "dk", "dv"))
 
 
+def _random_shapes(n, seed):
+    """Seeded random small shapes: GQA groups 1-8, both head sizes, ragged M
+    and T (M = 0 included), chunk or cache mode."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for _ in range(n):
+        G = int(rng.choice([1, 2, 4, 7, 8]))
+        Hkv = int(rng.integers(1, 4))
+        d = int(rng.choice([64, 128]))
+        T = int(rng.integers(1, 90))
+        cache = bool(rng.integers(0, 2))
+        M = int(rng.integers(1 if cache else 0, 400))
+        out.append((int(rng.integers(1, 3)), G * Hkv, Hkv, d, M, T, cache))
+    return out
+
+
+@pytest.mark.parametrize("shape", _random_shapes(10, 2024) + [(1, 8, 2, 64, 0, 37, False),
+                                                              (3, 8, 4, 128, 260, 1, True)])
+def test_backward_random_shapes(shape):
+    """The MFMA backward (bf16) on seeded random shapes, chunk or cache mode,
+    against the oracle."""
+    B, Hq, Hkv, d, M, T, cache = shape
+    wl = W.custom("bwdr", B=B, Hq=Hq, Hkv=Hkv, d=d, M=M, T=T, dtype="bf16", heavy_frac=0.02)
+    say(f"backward random {wl.describe()} cache={cache}")
+    x = W.make_inputs(wl, seed=M + T + d)
+    tdt = torch.bfloat16
+    rng = np.random.default_rng(M * 7 + T)
+    do_np = W.bf16_bits_to_f32(W.f32_to_bf16_bits(
+        rng.standard_normal(x["q"].shape).astype(np.float32)))
+    q, kc, vc = (U.to_dev(x[n], tdt) for n in ("q", "k_cache", "v_cache"))
+    dout = U.to_dev(do_np, tdt)
+    scale = float(x["scale"])
+    ws = torch.empty(max(H.h2o_backward_workspace_bytes(B, Hq, Hkv, T, M, d, tdt), 16),
+                     dtype=torch.uint8, device=U.DEV)
+    if cache:
+        pos0 = 500
+        tp = rng.integers(pos0 - 30, pos0 + T + 2, size=(B, Hkv, M)).astype(np.int32)
+        tpd = U.to_dev(tp, torch.int32)
+        b = H.alloc_step(B, Hq, Hkv, T, M, d, tdt, insert_first=True)
+        H.h2o_sdpa_cache(q, kc, vc, tpd, b["out"], b["lse"], b["wsum"], b["workspace"], pos0,
+                         scale)
+        grads = [torch.empty_like(t) for t in (q, kc, vc)]
+        H.h2o_sdpa_chunk_backward(q, kc, vc, None, None, b["lse"], dout, *grads, None, None, ws,
+                                  scale, token_pos=tpd, pos0=pos0)
+        torch.cuda.synchronize()
+        ref = oracle.sdpa_chunk_backward(x["q"], x["k_cache"], x["v_cache"], None, None, do_np,
+                                         scale, token_pos=tp, pos0=pos0)[:3]
+        names = ("dq", "dk", "dv")
+    else:
+        kn, vn = U.to_dev(x["k_new"], tdt), U.to_dev(x["v_new"], tdt)
+        b = H.alloc_step(B, Hq, Hkv, T, M, d, tdt)
+        H.h2o_sdpa_chunk(q, kc, vc, kn, vn, b["out"], b["lse"], b["wsum"], b["workspace"], scale)
+        grads = [torch.empty_like(t) for t in (q, kc, vc, kn, vn)]
+        H.h2o_sdpa_chunk_backward(q, kc, vc, kn, vn, b["lse"], dout, *grads, ws, scale)
+        torch.cuda.synchronize()
+        ref = oracle.sdpa_chunk_backward(x["q"], x["k_cache"], x["v_cache"], x["k_new"],
+                                         x["v_new"], do_np, scale)
+        names = ("dq", "dk_cache", "dv_cache", "dk_new", "dv_new")
+    _grads_check("bf16", [U.to_np(g) for g in grads], ref, names)
+
+
 def test_backward_full_size_sampled_head():
     """The backward at the 1024-token prefill size (B1 Hq32 Hkv8 d128 M8192
     T1024, bf16) in the launch configuration the benchmark times; the oracle

@@ -96,6 +96,8 @@ def test_sdpa_cache(shape, kind, force):
 
 STEP_SHAPES = [  # B, Hq, Hkv, d, M, T, dtype
     (8, 32, 8, 64, 4096, 1, "bf16"),
+    (2, 8, 2, 64, 5000, 1, "bf16"),     # T = 1, more slots than the fused kernel prefetches
+    (1, 8, 2, 128, 4133, 1, "bf16"),    # T = 1, d = 128, ragged last step
     (2, 8, 2, 128, 700, 64, "bf16"),
     (1, 4, 2, 64, 256, 64, "f32"),
     (2, 4, 2, 64, 300, 1, "f32"),

@@ -15,12 +15,24 @@ __global__ __launch_bounds__(256) void colsum_reduce_kernel(const float* __restr
   const int j = blockIdx.x * blockDim.x + threadIdx.x;
   const int bh = blockIdx.y;
   if (j >= Nk) return;
-  const int R = G * T;
+  // The partials that see column j are p0 .. nparts-1 (kv_end grows with
+  // p): all of them for a cache column, and for chunk key i = j - M those
+  // whose last row (r1 - 1) / G reaches i, i.e. (p + 1) * rows_per_part > i * G.
+  int p0 = 0;
+  if (Tk > 0 && j >= M) p0 = ((j - M) * G) / rows_per_part;
+  const float* src = parts + ((size_t)p0 * BH + bh) * ld + j;
+  const size_t stride = (size_t)BH * ld;
   float s = 0.f;
-  for (int p = 0; p < nparts; ++p) {
-    const int r1 = min((p + 1) * rows_per_part, R);
-    if (j < kv_end_for_rows(r1, G, T, M, Tk)) s += parts[((size_t)p * BH + bh) * ld + j];
+  int p = p0;
+  // loads four ahead, additions in increasing p (bitwise reproducible)
+  for (; p + 3 < nparts; p += 4, src += 4 * stride) {
+    const float a0 = src[0], a1 = src[stride], a2 = src[2 * stride], a3 = src[3 * stride];
+    s += a0;
+    s += a1;
+    s += a2;
+    s += a3;
   }
+  for (; p < nparts; ++p, src += stride) s += src[0];
   wsum[(size_t)bh * Nk + j] = s;
 }
 

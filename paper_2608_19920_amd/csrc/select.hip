@@ -81,25 +81,59 @@ __device__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* tmp, uint32_t* to
   return res;
 }
 
+// Rows of at most this many slots are staged in LDS as order keys (one pad
+// word after every 32, so that a thread's contiguous chunk in the compaction
+// and the strided reads of the histogram passes are both free of bank
+// conflicts); longer rows are read from global memory in every pass.
+constexpr int kSelLdsMax = 32768;
+__device__ __forceinline__ int sel_lds_index(int j) { return j + (j >> 5); }
+
+// hist[bin] += 1 for every active lane. Lanes of a wave that share a bin are
+// counted with one atomic (the leading bins of a wave first, at most four
+// rounds; the rest add one each): the first radix passes put most keys of a
+// row into a few bins, where plain LDS atomics would serialise.
+__device__ __forceinline__ void hist_add(uint32_t* hist, uint32_t bin, bool active) {
+  const int lane = threadIdx.x & 63;
+  uint64_t pending = __ballot(active);
+#pragma unroll
+  for (int it = 0; it < 4 && pending; ++it) {
+    const int leader = __ffsll((unsigned long long)pending) - 1;
+    const uint32_t lb = __shfl(bin, leader, 64);
+    const uint64_t same = __ballot(((pending >> lane) & 1ull) && bin == lb);
+    if (lane == leader) atomicAdd(&hist[lb], (uint32_t)__popcll(same));
+    pending &= ~same;
+  }
+  if ((pending >> lane) & 1ull) atomicAdd(&hist[bin], 1u);
+}
+
 // One block per row. Radix-select the k-th smallest key tau (8 bits per pass,
 // most significant first), then emit, in ascending slot order, every slot with
 // key < tau and the lowest-index (k - #less) slots with key == tau.
+template <bool LDS>
 __global__ __launch_bounds__(kSelThreads) void bottomk_kernel(const float* __restrict__ scores,
                                                               int M, int k,
                                                               int32_t* __restrict__ idx) {
+  __shared__ uint32_t keys[LDS ? kSelLdsMax + kSelLdsMax / 32 : 1];
   __shared__ uint32_t hist[256];
   __shared__ uint32_t tmp[2 * kSelWaves + 1];
   __shared__ uint32_t sh_prefix, sh_krem;
   const float* s = scores + (size_t)blockIdx.x * M;
   int32_t* out = idx + (size_t)blockIdx.x * k;
   if (k <= 0) return;
+  if (LDS) {
+    for (int j = threadIdx.x; j < M; j += kSelThreads) keys[sel_lds_index(j)] = order_key(s[j]);
+  }
+  auto key_at = [&](int j) { return LDS ? keys[sel_lds_index(j)] : order_key(s[j]); };
   uint32_t prefix = 0, mask = 0, krem = (uint32_t)k;
   for (int shift = 24; shift >= 0; shift -= 8) {
     for (int b = threadIdx.x; b < 256; b += kSelThreads) hist[b] = 0u;
     __syncthreads();
-    for (int j = threadIdx.x; j < M; j += kSelThreads) {
-      const uint32_t key = order_key(s[j]);
-      if ((key & mask) == prefix) atomicAdd(&hist[(key >> shift) & 255u], 1u);
+    // rounds of the whole block (the trip count is uniform: hist_add is a
+    // wave-level operation)
+    for (int j0 = 0; j0 < M; j0 += kSelThreads) {
+      const int j = j0 + (int)threadIdx.x;
+      const uint32_t key = j < M ? key_at(j) : 0u;
+      hist_add(hist, (key >> shift) & 255u, j < M && (key & mask) == prefix);
     }
     __syncthreads();
     if (threadIdx.x < 64) {
@@ -138,7 +172,7 @@ __global__ __launch_bounds__(kSelThreads) void bottomk_kernel(const float* __res
   const int j0 = min(M, (int)threadIdx.x * C), j1 = min(M, j0 + C);
   uint32_t n_less = 0, n_eq = 0;
   for (int j = j0; j < j1; ++j) {
-    const uint32_t key = order_key(s[j]);
+    const uint32_t key = key_at(j);
     n_less += key < tau;
     n_eq += key == tau;
   }
@@ -149,7 +183,7 @@ __global__ __launch_bounds__(kSelThreads) void bottomk_kernel(const float* __res
   const uint32_t pos = block_exclusive_scan(n_less + take_eq, tmp, &tot);
   uint32_t w = pos, eq_seen = 0;
   for (int j = j0; j < j1; ++j) {
-    const uint32_t key = order_key(s[j]);
+    const uint32_t key = key_at(j);
     bool sel = key < tau;
     if (key == tau) { sel = eq_seen < take_eq; ++eq_seen; }
     if (sel && w < (uint32_t)k) out[w++] = j;
@@ -347,8 +381,11 @@ hipError_t launch_accumulate(float* scores, const float* wsum, int rows, int M, 
 hipError_t launch_bottomk(const float* scores, int rows, int M, int k, int32_t* idx,
                           hipStream_t st) {
   if (rows == 0 || k == 0) return hipSuccess;
-  return launch_kernel(K_BOTTOMK, bottomk_kernel, dim3(rows), dim3(kSelThreads), st, scores, M, k,
-                       idx);
+  if (M <= kSelLdsMax)
+    return launch_kernel(K_BOTTOMK, bottomk_kernel<true>, dim3(rows), dim3(kSelThreads), st,
+                         scores, M, k, idx);
+  return launch_kernel(K_BOTTOMK, bottomk_kernel<false>, dim3(rows), dim3(kSelThreads), st,
+                       scores, M, k, idx);
 }
 
 hipError_t launch_insert(void* kc, void* vc, float* scores, int32_t* token_pos, const void* kn,

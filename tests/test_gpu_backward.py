@@ -243,3 +243,39 @@ def test_kv_delta_round_trip(B, Hkv, M, k, d, dt):
     H.h2o_kv_scatter(cache, idx, delta)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(U.to_np(cache), cache_np)
+
+
+def test_backward_graph_replays_match_eager():
+    """The bf16 backward (split rows passes and their reduce included)
+    captured in a HIP graph and replayed three times, with eager calls and
+    synchronisation between the replays: every replay gives the eager bits."""
+    B, Hq, Hkv, d, M, T = 1, 8, 2, 128, 1000, 128
+    wl = W.custom("bwdg", B=B, Hq=Hq, Hkv=Hkv, d=d, M=M, T=T, dtype="bf16", heavy_frac=0.02)
+    say(f"backward graph replay {wl.describe()}")
+    x = W.make_inputs(wl, seed=4)
+    tdt = torch.bfloat16
+    q, kc, vc, kn, vn = (U.to_dev(x[n], tdt) for n in ("q", "k_cache", "v_cache", "k_new",
+                                                        "v_new"))
+    dout = U.to_dev(np.random.default_rng(3).standard_normal(x["q"].shape).astype(np.float32), tdt)
+    scale = float(x["scale"])
+    b = H.alloc_step(B, Hq, Hkv, T, M, d, tdt)
+    H.h2o_sdpa_chunk(q, kc, vc, kn, vn, b["out"], b["lse"], b["wsum"], b["workspace"], scale)
+    nbytes = H.h2o_backward_workspace_bytes(B, Hq, Hkv, T, M, d, tdt)
+    wg = torch.empty(nbytes, dtype=torch.uint8, device=U.DEV)
+    we = torch.empty(nbytes, dtype=torch.uint8, device=U.DEV)
+    gg = [torch.empty_like(t) for t in (q, kc, vc, kn, vn)]
+    ge = [torch.empty_like(t) for t in (q, kc, vc, kn, vn)]
+    stream = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=stream):
+        H.h2o_sdpa_chunk_backward(q, kc, vc, kn, vn, b["lse"], dout, *gg, wg, scale)
+    torch.cuda.synchronize()
+    for r in range(3):
+        for g in gg:
+            g.fill_(7)            # stale outputs must be overwritten by the replay
+        graph.replay()
+        H.h2o_sdpa_chunk_backward(q, kc, vc, kn, vn, b["lse"], dout, *ge, we, scale)
+        torch.cuda.synchronize()
+        for a_, e_, n in zip(gg, ge, ("dq", "dk_cache", "dv_cache", "dk_new", "dv_new")):
+            np.testing.assert_array_equal(U.to_np(a_), U.to_np(e_), err_msg=f"replay {r} {n}")

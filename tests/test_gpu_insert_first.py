@@ -175,3 +175,40 @@ def test_full_size_insert_first_sampled_heads(name, nheads):
     go, gl, gw = (U.to_np(bufs[n]) for n in ("out", "lse", "wsum"))
     _check("bf16", (sel(go, hq), sel(gl, hq), sel(gw, heads)),
            (sel(o, hq), sel(l, hq), sel(w, heads)), extra=f"heads {heads}")
+
+
+@pytest.mark.parametrize("shape", [(8, 32, 8, 64, 4096, 1, "bf16"), (2, 8, 2, 128, 700, 64, "bf16")])
+def test_insert_first_graph_replays_match_eager(shape):
+    """The insert-first step captured in a HIP graph and replayed three times
+    (the state advancing each time, eager steps and synchronisation between
+    the replays) gives the same bits as the same steps run eagerly."""
+    B, Hq, Hkv, d, M, T, dt = shape
+    wl = W.custom("ifgraph", B=B, Hq=Hq, Hkv=Hkv, d=d, M=M, T=T, dtype=dt, heavy_frac=0.02)
+    say(f"insert-first graph replay {wl.describe()}")
+    x = W.make_inputs(wl, seed=9)
+    tdt = U.TDT[dt]
+    q, kn, vn = (U.to_dev(x[n], tdt) for n in ("q", "k_new", "v_new"))
+    pos0, scale = int(x["pos0"]), float(x["scale"])
+    sg, se = U.device_state(x, dt), U.device_state(x, dt)
+    bg = H.alloc_step(B, Hq, Hkv, T, M, d, tdt, insert_first=True)
+    be = H.alloc_step(B, Hq, Hkv, T, M, d, tdt, insert_first=True)
+
+    def run(st, b):
+        H.h2o_chunk_step_insert_first(q, st["k_cache"], st["v_cache"], st["scores"],
+                                      st["token_pos"], kn, vn, b["out"], b["lse"], b["wsum"],
+                                      b["evict_idx"], b["workspace"], pos0, scale)
+
+    stream = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph, stream=stream):
+        run(sg, bg)
+    torch.cuda.synchronize()          # capture does not run the step
+    for r in range(3):
+        graph.replay()
+        run(se, be)
+        torch.cuda.synchronize()
+        for n in ("out", "lse", "wsum", "evict_idx"):
+            np.testing.assert_array_equal(U.to_np(bg[n]), U.to_np(be[n]), err_msg=f"replay {r} {n}")
+        for n in ("k_cache", "v_cache", "scores", "token_pos"):
+            np.testing.assert_array_equal(U.to_np(sg[n]), U.to_np(se[n]), err_msg=f"replay {r} {n}")

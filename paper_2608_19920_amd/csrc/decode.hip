@@ -41,6 +41,58 @@ __device__ __forceinline__ u32x4 load16(const bf16_t* p) {
   return *reinterpret_cast<const u32x4*>(p);
 }
 
+// Whole-wave reductions, the result in every lane: four DPP steps inside each
+// 16-lane row (quad xor 1, quad xor 2, half-row mirror, row mirror: after
+// them every lane holds its row's total), then two cross-row shuffles. The
+// DPP steps replace four of the six LDS permutes a shuffle tree would take
+// on the latency-bound path of the per-head kernels.
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t x) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, true);
+}
+constexpr int kDppQuadXor1 = 0xB1, kDppQuadXor2 = 0x4E, kDppHalfMirror = 0x141,
+              kDppMirror = 0x140;
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float x) {
+  return __uint_as_float(dpp_u32<CTRL>(__float_as_uint(x)));
+}
+__device__ __forceinline__ float wave_sum(float v) {
+  v += dpp_f32<kDppQuadXor1>(v);
+  v += dpp_f32<kDppQuadXor2>(v);
+  v += dpp_f32<kDppHalfMirror>(v);
+  v += dpp_f32<kDppMirror>(v);
+  v += __shfl_xor(v, 16, 64);
+  v += __shfl_xor(v, 32, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+  v = fmaxf(v, dpp_f32<kDppQuadXor1>(v));
+  v = fmaxf(v, dpp_f32<kDppQuadXor2>(v));
+  v = fmaxf(v, dpp_f32<kDppHalfMirror>(v));
+  v = fmaxf(v, dpp_f32<kDppMirror>(v));
+  v = fmaxf(v, __shfl_xor(v, 16, 64));
+  v = fmaxf(v, __shfl_xor(v, 32, 64));
+  return v;
+}
+// (key, slot) lexicographic minimum over the wave.
+template <int CTRL>
+__device__ __forceinline__ void argmin_step_dpp(uint32_t& k, uint32_t& j) {
+  const uint32_t ok = dpp_u32<CTRL>(k), oj = dpp_u32<CTRL>(j);
+  if (ok < k || (ok == k && oj < j)) { k = ok; j = oj; }
+}
+__device__ __forceinline__ void argmin_step_xor(uint32_t& k, uint32_t& j, int o) {
+  const uint32_t ok = __shfl_xor(k, o, 64), oj = __shfl_xor(j, o, 64);
+  if (ok < k || (ok == k && oj < j)) { k = ok; j = oj; }
+}
+__device__ __forceinline__ void wave_argmin(uint32_t& k, uint32_t& j) {
+  argmin_step_dpp<kDppQuadXor1>(k, j);
+  argmin_step_dpp<kDppQuadXor2>(k, j);
+  argmin_step_dpp<kDppHalfMirror>(k, j);
+  argmin_step_dpp<kDppMirror>(k, j);
+  argmin_step_xor(k, j, 16);
+  argmin_step_xor(k, j, 32);
+}
+
 // floats per row of the stored logits ([bh][g][slot]; 16-byte aligned rows)
 __host__ __device__ constexpr int logit_pitch(int M) { return (M + 3) & ~3; }
 
@@ -388,14 +440,14 @@ __device__ __forceinline__ void head_stats(HeadStats& hs, const bf16_t* q, const
       for (int dd = lane; dd < D; dd += 64)
         a = fmaf(bf16_to_f32(q[(size_t)(b * Hq + h * G + g) * D + dd]),
                  bf16_to_f32(kn[bh * D + dd]), a);
-      for (int o = 32; o > 0; o >>= 1) a += __shfl_xor(a, o, 64);
+      a = wave_sum(a);
       lnew = a * c_log2;
     }
     float mx = fmaxf(lnew, st.x);
-    for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+    mx = wave_max(mx);
     const float wt = st.y > 0.f ? __builtin_amdgcn_exp2f(st.x - mx) : 0.f;
     float L = st.y * wt;
-    for (int o = 32; o > 0; o >>= 1) L += __shfl_xor(L, o, 64);
+    L = wave_sum(L);
     if (has_chunk) L += __builtin_amdgcn_exp2f(lnew - mx);
     if (lane < nsplit) hs.wt[lane * G + g] = wt;
     if (lane == 0) {
@@ -574,11 +626,7 @@ __global__ __launch_bounds__(kFinThreads) void decode_finish(
       }
     }
   }
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) {
-    const uint32_t ok = __shfl_xor(bk, o, 64), oj = __shfl_xor(bj, o, 64);
-    if (ok < bk || (ok == bk && oj < bj)) { bk = ok; bj = oj; }
-  }
+  wave_argmin(bk, bj);
   if (lane == 0) { red_k[wave] = bk; red_j[wave] = bj; }
   __syncthreads();
   if (tid == 0) {

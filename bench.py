@@ -15,7 +15,7 @@ P = T*M + T(T+1)/2. "insert_first" times the paper's own order of a step
 (insert the chunk, then attend with the token-position mask) on the same
 shapes, with P = (M - T)*T + T(T+1)/2 there.
 
-Prints one JSON line. ``--gpus N`` with N > 1 exits: this build runs on one GPU.
+Prints one JSON line. ``--gpus N`` with N > 1 exits: the benchmark runs on one GPU.
 """
 from __future__ import annotations
 
@@ -376,7 +376,7 @@ def main():
     ap.add_argument("--no-prefill", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py: this build runs on one GPU only; use --gpus 1", file=sys.stderr)
+        print("bench.py: the benchmark runs on one GPU only; use --gpus 1", file=sys.stderr)
         sys.exit(2)
     import torch
     from paper_2608_19920_amd import h2o as H

@@ -43,9 +43,37 @@ __device__ __forceinline__ u32x4 load16(const bf16_t* p) {
 
 // Whole-wave reductions, the result in every lane: four DPP steps inside each
 // 16-lane row (quad xor 1, quad xor 2, half-row mirror, row mirror: after
-// them every lane holds its row's total), then two cross-row shuffles. The
-// DPP steps replace four of the six LDS permutes a shuffle tree would take
-// on the latency-bound path of the per-head kernels.
+// them every lane holds its row's total), then two cross-row exchanges. All
+// six steps are VALU operations, no LDS permutes.
+//
+// Cross-row exchange: v_permlane16_swap / v_permlane32_swap with x as both
+// operands leave (a, b) = x of lanes (l, l ^ 16) or (l, l ^ 32), the lower
+// lane first in both lanes of a pair, so a commutative combine of a and b
+// gives equal bits in the two lanes.
+template <bool ROW16>
+__device__ __forceinline__ void xrow(uint32_t x, uint32_t& a, uint32_t& b) {
+  if constexpr (ROW16) {
+    const auto r = __builtin_amdgcn_permlane16_swap(x, x, false, false);
+    a = r[0];
+    b = r[1];
+  } else {
+    const auto r = __builtin_amdgcn_permlane32_swap(x, x, false, false);
+    a = r[0];
+    b = r[1];
+  }
+}
+template <bool ROW16>
+__device__ __forceinline__ float xrow_sum(float v) {
+  uint32_t a, b;
+  xrow<ROW16>(__float_as_uint(v), a, b);
+  return __uint_as_float(a) + __uint_as_float(b);
+}
+template <bool ROW16>
+__device__ __forceinline__ float xrow_max(float v) {
+  uint32_t a, b;
+  xrow<ROW16>(__float_as_uint(v), a, b);
+  return fmaxf(__uint_as_float(a), __uint_as_float(b));
+}
 template <int CTRL>
 __device__ __forceinline__ uint32_t dpp_u32(uint32_t x) {
   return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, CTRL, 0xF, 0xF, true);
@@ -61,18 +89,14 @@ __device__ __forceinline__ float wave_sum(float v) {
   v += dpp_f32<kDppQuadXor2>(v);
   v += dpp_f32<kDppHalfMirror>(v);
   v += dpp_f32<kDppMirror>(v);
-  v += __shfl_xor(v, 16, 64);
-  v += __shfl_xor(v, 32, 64);
-  return v;
+  return xrow_sum<false>(xrow_sum<true>(v));
 }
 __device__ __forceinline__ float wave_max(float v) {
   v = fmaxf(v, dpp_f32<kDppQuadXor1>(v));
   v = fmaxf(v, dpp_f32<kDppQuadXor2>(v));
   v = fmaxf(v, dpp_f32<kDppHalfMirror>(v));
   v = fmaxf(v, dpp_f32<kDppMirror>(v));
-  v = fmaxf(v, __shfl_xor(v, 16, 64));
-  v = fmaxf(v, __shfl_xor(v, 32, 64));
-  return v;
+  return xrow_max<false>(xrow_max<true>(v));
 }
 // (key, slot) lexicographic minimum over the wave.
 template <int CTRL>
@@ -80,17 +104,22 @@ __device__ __forceinline__ void argmin_step_dpp(uint32_t& k, uint32_t& j) {
   const uint32_t ok = dpp_u32<CTRL>(k), oj = dpp_u32<CTRL>(j);
   if (ok < k || (ok == k && oj < j)) { k = ok; j = oj; }
 }
-__device__ __forceinline__ void argmin_step_xor(uint32_t& k, uint32_t& j, int o) {
-  const uint32_t ok = __shfl_xor(k, o, 64), oj = __shfl_xor(j, o, 64);
-  if (ok < k || (ok == k && oj < j)) { k = ok; j = oj; }
+template <bool ROW16>
+__device__ __forceinline__ void argmin_step_xrow(uint32_t& k, uint32_t& j) {
+  uint32_t k0, k1, j0, j1;
+  xrow<ROW16>(k, k0, k1);
+  xrow<ROW16>(j, j0, j1);
+  const bool second = k1 < k0 || (k1 == k0 && j1 < j0);
+  k = second ? k1 : k0;
+  j = second ? j1 : j0;
 }
 __device__ __forceinline__ void wave_argmin(uint32_t& k, uint32_t& j) {
   argmin_step_dpp<kDppQuadXor1>(k, j);
   argmin_step_dpp<kDppQuadXor2>(k, j);
   argmin_step_dpp<kDppHalfMirror>(k, j);
   argmin_step_dpp<kDppMirror>(k, j);
-  argmin_step_xor(k, j, 16);
-  argmin_step_xor(k, j, 32);
+  argmin_step_xrow<true>(k, j);
+  argmin_step_xrow<false>(k, j);
 }
 
 // floats per row of the stored logits ([bh][g][slot]; 16-byte aligned rows)
@@ -338,11 +367,7 @@ __global__ __launch_bounds__(kThreads) void decode_split(
       const uint32_t key = order_key(ins.scores[bh * (size_t)M + j]);
       if (key < bk) { bk = key; bj = (uint32_t)j; }
     }
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const uint32_t ok = __shfl_xor(bk, o, 64), oj = __shfl_xor(bj, o, 64);
-      if (ok < bk || (ok == bk && oj < bj)) { bk = ok; bj = oj; }
-    }
+    wave_argmin(bk, bj);
     if (lane == 0) { red_k[wave] = bk; red_j[wave] = bj; }
     __syncthreads();
     if (tid == 0) {

@@ -184,8 +184,8 @@ struct InsArgs {
 };
 constexpr int kScPre = 16;   // scores per thread prefetched before the first K/V loads
 
-template <int D, int G, bool CACHE, bool INS = false>
-__global__ __launch_bounds__(kThreads) void decode_split(
+template <int D, int G, bool CACHE, bool INS>
+__device__ __forceinline__ void split_body(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ kc, const bf16_t* __restrict__ vc,
     int Hq, int Hkv, int M, float c_log2, float* __restrict__ logits,
     float2* __restrict__ dstat, float* __restrict__ dO, float* __restrict__ sink,
@@ -297,12 +297,17 @@ __global__ __launch_bounds__(kThreads) void decode_split(
     }
     float lg[8];
     float mx = -INFINITY;
+    // wave-uniform: a step reaching past the cache (the ragged last one, or
+    // a padding step), whose zero rows must not raise the reference maximum
+    const bool tail = key0 + kStep > M;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       lg[i] = sacc[i >> 2][i & 3] * c_log2;
+      const int key = key0 + 16 * (i >> 2) + 4 * grp + (i & 3);
       if (CACHE) {
-        const int key = key0 + 16 * (i >> 2) + 4 * grp + (i & 3);
         if (key >= M || !pos_visible(tr[u][i], pos0, 0)) lg[i] = -INFINITY;
+      } else if (tail && key >= M) {
+        lg[i] = -INFINITY;
       }
       mx = fmaxf(mx, lg[i]);
     }
@@ -389,46 +394,88 @@ __global__ __launch_bounds__(kThreads) void decode_split(
       }
     }
   }
+  // Without token positions the loop runs whole trips of two steps: with an
+  // odd count the last trip's second step lies past the head (zero rows,
+  // every key masked) and changes nothing. An exit between the two halves
+  // makes the compiler wait for the other ring slot's loads at the top of
+  // every trip, and so does a use of a step's data scheduled above the next
+  // step's loads (the scheduling barriers). The cache-mode kernels, which
+  // run at fewer waves per SIMD, measured faster with the exit.
   for (int k = 0; k < nst; k += 2) {
     issue(k + 1, 1);
+    if (!CACHE) __builtin_amdgcn_sched_barrier(0);
     consume(k, 0);
-    if (k + 1 >= nst) break;
+    if (CACHE && k + 1 >= nst) break;
     issue(k + 2, 0);
+    if (!CACHE) __builtin_amdgcn_sched_barrier(0);
     consume(k + 1, 1);
   }
-  // block merge: per column, the common maximum over the waves
+  // block merge, one barrier: every wave leaves its column statistics and
+  // its unscaled O accumulators; then per head the common maximum over the
+  // waves, each wave's weight, and the sums in wave order
   l += __shfl_xor(l, 16, 64);
   l += __shfl_xor(l, 32, 64);
   if (grp == 0) {
     red_m[wave][col] = m;
     red_l[wave][col] = l;
   }
-  __syncthreads();
-  float mb = red_m[0][col];
-#pragma unroll
-  for (int w = 1; w < kWaves; ++w) mb = fmaxf(mb, red_m[w][col]);
-  const float sc = m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - mb);
   if (col < G) {
 #pragma unroll
     for (int db = 0; db < D / 16; ++db)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) ored[wave][col][16 * db + 4 * grp + r] = oacc[db][r] * sc;
+      for (int r = 0; r < 4; ++r) ored[wave][col][16 * db + 4 * grp + r] = oacc[db][r];
   }
   __syncthreads();
-  if (tid < G) {
-    float mg = red_m[0][tid];
-    for (int w = 1; w < kWaves; ++w) mg = fmaxf(mg, red_m[w][tid]);
-    float lt = 0.f;
-    for (int w = 0; w < kWaves; ++w)
-      if (red_m[w][tid] != -INFINITY) lt += red_l[w][tid] * __builtin_amdgcn_exp2f(red_m[w][tid] - mg);
-    dstat[(bh * nsplit + s) * G + tid] = make_float2(mg, lt);
-  }
   for (int c = tid; c < G * D; c += kThreads) {
-    float a = 0.f;
+    const int g = c / D;
+    float mg = red_m[0][g];
 #pragma unroll
-    for (int w = 0; w < kWaves; ++w) a += ored[w][c / D][c % D];
+    for (int w = 1; w < kWaves; ++w) mg = fmaxf(mg, red_m[w][g]);
+    float a = 0.f, lt = 0.f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      const float mw = red_m[w][g];
+      const float sw = mw == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mw - mg);
+      a += ored[w][g][c % D] * sw;
+      lt += red_l[w][g] * sw;
+    }
     dO[(bh * nsplit + s) * (size_t)(G * D) + c] = a;
+    if (c % D == 0) dstat[(bh * nsplit + s) * G + g] = make_float2(mg, lt);
   }
+}
+
+// Register budgets at d = 64, where the kernels fit them without spilling:
+// four waves per SIMD (128 registers) without token positions, three for the
+// insert-first kernel. Cache mode, and d = 128, keep the compiler's own.
+#define H2O_SPLIT_PARAMS                                                                     \
+  const bf16_t *__restrict__ q, const bf16_t *__restrict__ kc, const bf16_t *__restrict__ vc, \
+      int Hq, int Hkv, int M, float c_log2, float *__restrict__ logits,                       \
+      float2 *__restrict__ dstat, float *__restrict__ dO, float *__restrict__ sink,           \
+      const int32_t *__restrict__ tp, int32_t pos0, InsArgs ins
+template <int D, int G>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(D == 64 ? 4 : 1)))
+void decode_split(H2O_SPLIT_PARAMS) {
+  split_body<D, G, false, false>(q, kc, vc, Hq, Hkv, M, c_log2, logits, dstat, dO, sink, tp,
+                                 pos0, ins);
+}
+template <int D, int G>
+__global__ __launch_bounds__(kThreads) void decode_split_cache(H2O_SPLIT_PARAMS) {
+  split_body<D, G, true, false>(q, kc, vc, Hq, Hkv, M, c_log2, logits, dstat, dO, sink, tp, pos0,
+                                ins);
+}
+template <int D, int G>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(D == 64 ? 3 : 1)))
+void decode_split_ins(H2O_SPLIT_PARAMS) {
+  split_body<D, G, true, true>(q, kc, vc, Hq, Hkv, M, c_log2, logits, dstat, dO, sink, tp, pos0,
+                               ins);
+}
+#undef H2O_SPLIT_PARAMS
+
+template <int D, int G, bool CACHE, bool INS>
+const void* split_kernel() {
+  if constexpr (INS) return reinterpret_cast<const void*>(decode_split_ins<D, G>);
+  else if constexpr (CACHE) return reinterpret_cast<const void*>(decode_split_cache<D, G>);
+  else return reinterpret_cast<const void*>(decode_split<D, G>);
 }
 
 // ------------------------------------------------------------------ combine
@@ -683,7 +730,7 @@ int split_count(int M, int BH) {
   static int resident = 0;
   if (!resident) {
     int per_cu = 0, dev = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, decode_split<D, G, CACHE, INS>,
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, split_kernel<D, G, CACHE, INS>(),
                                                      kThreads, 0) != hipSuccess || per_cu < 1)
       per_cu = 2;
     if (hipGetDevice(&dev) != hipSuccess ||
@@ -708,20 +755,20 @@ hipError_t launch_split(hipStream_t st, int BH, const void* q, const void* kc, c
                         float* sink, KeyPos kp, int* ns, InsArgs ins) {
   if (kp.tp && ins.scores) {
     *ns = split_count<D, G, true, true>(M, BH);
-    return launch_kernel(K_DECODE_SPLIT, decode_split<D, G, true, true>, dim3(*ns, BH),
+    return launch_kernel(K_DECODE_SPLIT, decode_split_ins<D, G>, dim3(*ns, BH),
                          dim3(kThreads), st, (const bf16_t*)q, (const bf16_t*)kc,
                          (const bf16_t*)vc, Hq, Hkv, M, c, logits, dstat, dO, sink, kp.tp,
                          kp.pos0, ins);
   }
   if (kp.tp) {
     *ns = split_count<D, G, true>(M, BH);
-    return launch_kernel(K_DECODE_SPLIT, decode_split<D, G, true>, dim3(*ns, BH),
+    return launch_kernel(K_DECODE_SPLIT, decode_split_cache<D, G>, dim3(*ns, BH),
                          dim3(kThreads), st, (const bf16_t*)q, (const bf16_t*)kc,
                          (const bf16_t*)vc, Hq, Hkv, M, c, logits, dstat, dO, sink, kp.tp,
                          kp.pos0, ins);
   }
   *ns = split_count<D, G, false>(M, BH);
-  return launch_kernel(K_DECODE_SPLIT, decode_split<D, G, false>, dim3(*ns, BH), dim3(kThreads),
+  return launch_kernel(K_DECODE_SPLIT, decode_split<D, G>, dim3(*ns, BH), dim3(kThreads),
                        st, (const bf16_t*)q, (const bf16_t*)kc, (const bf16_t*)vc, Hq, Hkv, M, c,
                        logits, dstat, dO, sink, (const int32_t*)nullptr, (int32_t)0, ins);
 }

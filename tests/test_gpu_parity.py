@@ -166,6 +166,32 @@ def test_sdpa_decode_path(shape):
         H.h2o_debug_force_path(-1)
 
 
+@pytest.mark.parametrize("M", [1000, 4096])
+def test_sdpa_decode_path_very_negative_logits(M):
+    # Every logit near -128 (about -185 in log2 units): exp2 of any logit
+    # relative to a maximum of 0 underflows float32. The zero rows read past
+    # the cache's end (M = 1000: a ragged last step of 32 slots) must not
+    # count as logits of 0 in a split's running maximum.
+    H.h2o_debug_force_path(2)
+    try:
+        shape = dict(B=1, Hq=4, Hkv=1, d=64, M=M, T=1)
+        say(f"decode path, very negative logits {shape}")
+        w = W.custom(**shape, dtype="bf16")
+        x = W.make_inputs(w, seed=11)
+        rng = np.random.Generator(np.random.PCG64(12))
+        def fill(a, sign):
+            v = (sign * (4.0 + 0.1 * rng.standard_normal(a.shape))).astype(np.float32)
+            return W.bf16_bits_to_f32(W.f32_to_bf16_bits(v))
+        x["q"] = fill(x["q"], 1.0)
+        for k in ("k_cache", "k_new"):
+            x[k] = fill(x[k], -1.0)
+        res = U.run_sdpa(x["q"], x["k_cache"], x["v_cache"], x["k_new"], x["v_new"],
+                         x["scale"], "bf16")
+        _check_attention(x, "bf16", res, extra="decode path, logits ~ -128")
+    finally:
+        H.h2o_debug_force_path(-1)
+
+
 @pytest.mark.parametrize("path", BF16_PATHS + [2], indirect=True)
 def test_bitwise_repeatable(path):
     say(f"repeatability path {path}")

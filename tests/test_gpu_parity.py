@@ -166,16 +166,17 @@ def test_sdpa_decode_path(shape):
         H.h2o_debug_force_path(-1)
 
 
-@pytest.mark.parametrize("M", [1000, 4096])
-def test_sdpa_decode_path_very_negative_logits(M):
+@pytest.mark.parametrize("path_id,M,T", [(2, 1000, 1), (2, 4096, 1), (1, 1000, 33),
+                                         (0, 1000, 33), (1, 4096, 64)])
+def test_sdpa_very_negative_logits(path_id, M, T):
     # Every logit near -128 (about -185 in log2 units): exp2 of any logit
     # relative to a maximum of 0 underflows float32. The zero rows read past
-    # the cache's end (M = 1000: a ragged last step of 32 slots) must not
-    # count as logits of 0 in a split's running maximum.
-    H.h2o_debug_force_path(2)
+    # the keys' end (a ragged last step or tile) must not count as logits of
+    # 0 in a running maximum. Paths: 2 decode, 1 MFMA, 0 generic.
+    H.h2o_debug_force_path(path_id)
     try:
-        shape = dict(B=1, Hq=4, Hkv=1, d=64, M=M, T=1)
-        say(f"decode path, very negative logits {shape}")
+        shape = dict(B=1, Hq=4, Hkv=1, d=64, M=M, T=T)
+        say(f"path {path_id}, very negative logits {shape}")
         w = W.custom(**shape, dtype="bf16")
         x = W.make_inputs(w, seed=11)
         rng = np.random.Generator(np.random.PCG64(12))
@@ -187,7 +188,7 @@ def test_sdpa_decode_path_very_negative_logits(M):
             x[k] = fill(x[k], -1.0)
         res = U.run_sdpa(x["q"], x["k_cache"], x["v_cache"], x["k_new"], x["v_new"],
                          x["scale"], "bf16")
-        _check_attention(x, "bf16", res, extra="decode path, logits ~ -128")
+        _check_attention(x, "bf16", res, extra=f"path {path_id}, logits ~ -128")
     finally:
         H.h2o_debug_force_path(-1)
 

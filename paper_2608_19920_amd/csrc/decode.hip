@@ -648,13 +648,22 @@ __global__ __launch_bounds__(kFinThreads) void decode_finish(
   float* sc = scores + bh * (size_t)M;
   const float* lgb = logits + bh * (size_t)G * pitch;
   float lg[kFinCols][G], sv[kFinCols];
-  auto load_pass = [&](int base) {   // M >= 1: clamped slots are in bounds
+  // One pass of slots: column groups wholly past the cache (a block-uniform
+  // test) are not loaded; in a ragged group the clamped slots are in bounds
+  // (M >= 1) and are not used.
+  auto load_pass = [&](int base) {
 #pragma unroll
     for (int u = 0; u < kFinCols; ++u) {
-      const int j = min(base + u * NT + tid, M - 1);
+      if (base + u * NT < M) {
+        const int j = min(base + u * NT + tid, M - 1);
 #pragma unroll
-      for (int g = 0; g < G; ++g) lg[u][g] = lgb[(size_t)g * pitch + j];
-      sv[u] = sc[j];
+        for (int g = 0; g < G; ++g) lg[u][g] = lgb[(size_t)g * pitch + j];
+        sv[u] = sc[j];
+      } else {
+#pragma unroll
+        for (int g = 0; g < G; ++g) lg[u][g] = 0.f;
+        sv[u] = 0.f;
+      }
     }
   };
   typedef uint32_t u4 __attribute__((ext_vector_type(4)));

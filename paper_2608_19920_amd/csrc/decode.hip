@@ -23,6 +23,7 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / 64;
+constexpr int kCombThreads = 1024;                       // threads of a combine block
 constexpr int kStep = 32;                                // cache slots per wave step
 constexpr int kMaxGD = 512;                              // G * D handled by these kernels
 constexpr int kMaxSplit = 64;                            // split blocks per head, at most
@@ -589,7 +590,7 @@ constexpr int kCols = 1024;
 // ins_idx non-null the head's slot ins_idx[bh] (just inserted, by the fused
 // insert-first split) takes 0 + wsum[j] instead.
 template <int D>
-__global__ __launch_bounds__(kThreads) void decode_combine(
+__global__ __launch_bounds__(kCombThreads) void decode_combine(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ kn, const bf16_t* __restrict__ vn,
     int Hq, int Hkv, int M, int nsplit, float c_log2, const float* __restrict__ logits,
     const float2* __restrict__ dstat, const float* __restrict__ dO, bf16_t* __restrict__ out,
@@ -599,16 +600,16 @@ __global__ __launch_bounds__(kThreads) void decode_combine(
   const int G = Hq / Hkv;
   const size_t bh = blockIdx.y;
   const bool has_chunk = kn != nullptr;
-  head_stats<D, kThreads>(hs, q, kn, dstat, Hq, Hkv, G, nsplit, c_log2, bh,
+  head_stats<D, kCombThreads>(hs, q, kn, dstat, Hq, Hkv, G, nsplit, c_log2, bh,
                           blockIdx.x == 0 ? lse : nullptr, has_chunk);
-  if (blockIdx.x == 0) head_out<D, kThreads>(hs, vn, dO, out, Hq, Hkv, G, nsplit, bh);
+  if (blockIdx.x == 0) head_out<D, kCombThreads>(hs, vn, dO, out, Hq, Hkv, G, nsplit, bh);
   if (!wsum) return;   // out and lse only (the attend half of a step)
   float* w = wsum + bh * (size_t)(M + (has_chunk ? 1 : 0));
   const float* lgb = logits + bh * (size_t)G * logit_pitch(M);
   const int c0 = blockIdx.x * kCols, c1 = min(M, c0 + kCols);
   float* sc = scores ? scores + bh * (size_t)M : nullptr;
   const int ins = ins_idx ? ins_idx[bh] : -1;
-  for (int j = c0 + threadIdx.x; j < c1; j += kThreads) {
+  for (int j = c0 + threadIdx.x; j < c1; j += kCombThreads) {
     const float wj = slot_weight(hs, lgb, logit_pitch(M), G, j);
     w[j] = wj;
     if (sc) sc[j] = (j == ins ? 0.f : sc[j]) + wj;
@@ -836,7 +837,7 @@ hipError_t launch_sdpa_decode(const Shape& s, const Plan& p, const void* q, cons
   const dim3 cgrid(s.M > 0 ? (s.M + kCols - 1) / kCols : 1, s.BH());
   auto combine = s.d == 64 ? decode_combine<64> : decode_combine<128>;
   const bool chunk = !s.cache_only;
-  return launch_kernel(K_DECODE_COMBINE, combine, cgrid, dim3(kThreads), st, (const bf16_t*)q,
+  return launch_kernel(K_DECODE_COMBINE, combine, cgrid, dim3(kCombThreads), st, (const bf16_t*)q,
                        chunk ? (const bf16_t*)kn : nullptr, chunk ? (const bf16_t*)vn : nullptr,
                        s.Hq, s.Hkv, s.M, ns, c,
                        (const float*)(ws + p.off_logits), (const float2*)(ws + p.off_stats),
@@ -857,7 +858,7 @@ hipError_t launch_decode_step_insert_first(const Shape& s, const Plan& p, const 
   if (e != hipSuccess) return e;
   const dim3 cgrid((s.M + kCols - 1) / kCols, s.BH());
   auto combine = s.d == 64 ? decode_combine<64> : decode_combine<128>;
-  return launch_kernel(K_DECODE_COMBINE, combine, cgrid, dim3(kThreads), st, (const bf16_t*)q,
+  return launch_kernel(K_DECODE_COMBINE, combine, cgrid, dim3(kCombThreads), st, (const bf16_t*)q,
                        (const bf16_t*)nullptr, (const bf16_t*)nullptr, s.Hq, s.Hkv, s.M, ns, c,
                        (const float*)(ws + p.off_logits), (const float2*)(ws + p.off_stats),
                        (const float*)(ws + p.off_opart), (bf16_t*)out, lse, wsum, scores,
@@ -923,7 +924,7 @@ hipError_t launch_decode_attend(const Shape& s, const Plan& p, const void* q, co
   hipError_t e = launch_decode_split(s, p, q, kc, vc, ws, c, KeyPos{nullptr, 0}, st, &ns);
   if (e != hipSuccess) return e;
   auto combine = s.d == 64 ? decode_combine<64> : decode_combine<128>;
-  return launch_kernel(K_DECODE_COMBINE, combine, dim3(1, s.BH()), dim3(kThreads), st,
+  return launch_kernel(K_DECODE_COMBINE, combine, dim3(1, s.BH()), dim3(kCombThreads), st,
                        (const bf16_t*)q, (const bf16_t*)kn, (const bf16_t*)vn, s.Hq, s.Hkv,
                        s.M, ns, c, (const float*)(ws + p.off_logits),
                        (const float2*)(ws + p.off_stats), (const float*)(ws + p.off_opart),

@@ -1,0 +1,81 @@
+"""GPU parity over seeded random shapes: h2o_sdpa_chunk (chunk mode) and
+h2o_sdpa_cache (cache mode, token-position mask) against the float64 oracle,
+on every kernel path a shape can take (automatic, generic VALU, MFMA, and the
+T = 1 decode kernels), GQA group sizes 1 to 8, cache lengths from 0 to a few
+thousand slots with ragged tails, chunk lengths from 1 to 160, bf16 and
+float32. Tolerances as in test_gpu_parity: normwise relative error per
+(b, head) slice <= 2e-2 (bf16) and 1e-5 (float32) for out, lse and wsum.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle import rel_err
+from paper_2608_19920_amd import h2o as H
+from paper_2608_19920_amd import workloads as W
+import _gpu as U
+from _gpu import say
+from test_gpu_insert_first import _positions
+
+pytestmark = pytest.mark.gpu
+
+N_CASES = 48
+
+
+def _case(i):
+    rng = np.random.default_rng(9000 + i)
+    G = int(rng.choice([1, 2, 3, 4, 7, 8]))
+    Hkv = int(rng.integers(1, 4))
+    B = int(rng.integers(1, 3))
+    d = int(rng.choice([64, 128]))
+    M = int(rng.choice([0, 1, 31, 33, int(rng.integers(2, 2500))]))
+    T = int(rng.choice([1, 1, int(rng.integers(2, 40)), int(rng.integers(40, 160))]))
+    dt = str(rng.choice(["bf16", "bf16", "f32"]))
+    paths = [-1, 0] + ([1] if dt == "bf16" else []) + ([2] if T == 1 and dt == "bf16" else [])
+    path = int(rng.choice(paths))
+    mode = str(rng.choice(["chunk", "cache"]))
+    if mode == "cache" and T > M:
+        mode = "chunk"
+    kind = str(rng.choice(["state", "wild"]))
+    return dict(B=B, G=G, Hkv=Hkv, d=d, M=M, T=T, dt=dt, path=path, mode=mode, kind=kind)
+
+
+@pytest.mark.parametrize("i", range(N_CASES))
+def test_random_shape(i):
+    c = _case(i)
+    B, G, Hkv, d, M, T, dt = (c[k] for k in ("B", "G", "Hkv", "d", "M", "T", "dt"))
+    say(f"sweep case {i}: {c}")
+    H.h2o_debug_force_path(c["path"])
+    try:
+        wl = W.custom("sweep", B=B, Hq=G * Hkv, Hkv=Hkv, d=d, M=M, T=T, dtype=dt,
+                      heavy_frac=0.02)
+        x = W.make_inputs(wl, seed=1000 + i)
+        if c["mode"] == "chunk":
+            res = U.run_sdpa(x["q"], x["k_cache"], x["v_cache"], x["k_new"], x["v_new"],
+                             x["scale"], dt)
+            ref = oracle.sdpa_chunk(x["q"], x["k_cache"], x["v_cache"], x["k_new"],
+                                    x["v_new"], x["scale"])
+        else:
+            tp, pos0 = _positions(B, Hkv, M, T, np.random.default_rng(i), c["kind"])
+            tdt = U.TDT[dt]
+            q, kc, vc = (U.to_dev(x[k], tdt) for k in ("q", "k_cache", "v_cache"))
+            bufs = H.alloc_step(B, G * Hkv, Hkv, T, M, d, tdt, insert_first=True)
+            H.h2o_sdpa_cache(q, kc, vc, U.to_dev(tp, torch.int32), bufs["out"], bufs["lse"],
+                             bufs["wsum"], bufs["workspace"], pos0, float(x["scale"]))
+            torch.cuda.synchronize()
+            res = tuple(U.to_np(bufs[k]) for k in ("out", "lse", "wsum"))
+            ref = oracle.sdpa_cache(x["q"], x["k_cache"], x["v_cache"], tp, pos0, x["scale"])
+    finally:
+        H.h2o_debug_force_path(-1)
+    o, l, w = ref
+    go, gl, gw = res
+    seen = np.isfinite(l)   # rows that see no key have lse -inf on both sides
+    assert np.array_equal(np.isfinite(gl), seen)
+    tol = U.TOL[dt]
+    e_o = rel_err(go, o, axes=(-2, -1))
+    e_l = rel_err(np.where(seen, gl, 0.0), np.where(seen, l, 0.0), axes=(-1,))
+    e_w = rel_err(gw, w, axes=(-1,))
+    say(f"  err out {e_o:.2e} lse {e_l:.2e} wsum {e_w:.2e} (tol {tol})")
+    assert np.isfinite(go).all() and np.isfinite(gw).all()
+    assert e_o <= tol and e_l <= tol and e_w <= tol

@@ -5,6 +5,8 @@ T = 1 decode kernels), GQA group sizes 1 to 8, cache lengths from 0 to a few
 thousand slots with ragged tails, chunk lengths from 1 to 160, bf16 and
 float32. Tolerances as in test_gpu_parity: normwise relative error per
 (b, head) slice <= 2e-2 (bf16) and 1e-5 (float32) for out, lse and wsum.
+The whole chunk step on random shapes: the fused call bit-equal to the three
+separate calls (attention, accumulate, evict and insert).
 """
 import numpy as np
 import pytest
@@ -78,4 +80,51 @@ def test_random_shape(i):
     e_w = rel_err(gw, w, axes=(-1,))
     say(f"  err out {e_o:.2e} lse {e_l:.2e} wsum {e_w:.2e} (tol {tol})")
     assert np.isfinite(go).all() and np.isfinite(gw).all()
+    assert e_o <= tol and e_l <= tol and e_w <= tol
+
+
+N_STEP_CASES = 24
+
+
+def _step_case(i):
+    rng = np.random.default_rng(7000 + i)
+    G = int(rng.choice([1, 2, 4, 7, 8]))
+    Hkv = int(rng.integers(1, 4))
+    B = int(rng.integers(1, 3))
+    d = int(rng.choice([64, 128]))
+    T = int(rng.choice([1, 1, 1, int(rng.integers(2, 100))]))
+    M = int(rng.integers(T, T + 3000))
+    dt = str(rng.choice(["bf16", "bf16", "f32"]))
+    return dict(B=B, G=G, Hkv=Hkv, d=d, M=M, T=T, dt=dt)
+
+
+@pytest.mark.parametrize("i", range(N_STEP_CASES))
+def test_random_step_fused_equals_calls(i):
+    """h2o_chunk_step gives the same bits as h2o_sdpa_chunk + h2o_accumulate_scores
+    + h2o_evict_insert on a random shape, and its attention matches the oracle."""
+    c = _step_case(i)
+    B, G, Hkv, d, M, T, dt = (c[k] for k in ("B", "G", "Hkv", "d", "M", "T", "dt"))
+    say(f"step sweep case {i}: {c}")
+    wl = W.custom("stepsweep", B=B, Hq=G * Hkv, Hkv=Hkv, d=d, M=M, T=T, dtype=dt,
+                  heavy_frac=0.02)
+    x = W.make_inputs(wl, seed=2000 + i)
+    tdt = U.TDT[dt]
+    q, kn, vn = (U.to_dev(x[n], tdt) for n in ("q", "k_new", "v_new"))
+    res = []
+    for fused in (False, True):
+        st = U.device_state(x, dt)
+        bufs = H.alloc_step(B, G * Hkv, Hkv, T, M, d, tdt)
+        H.step(st, q, kn, vn, bufs, int(x["pos0"]), float(x["scale"]), fused=fused)
+        torch.cuda.synchronize()
+        res.append({**{n: U.to_np(bufs[n]) for n in ("out", "lse", "wsum", "evict_idx")},
+                    **{n: U.to_np(st[n]) for n in ("k_cache", "v_cache", "scores", "token_pos")}})
+    for n in res[0]:
+        np.testing.assert_array_equal(res[1][n], res[0][n], err_msg=n)
+    o, l, w = oracle.sdpa_chunk(x["q"], x["k_cache"], x["v_cache"], x["k_new"], x["v_new"],
+                                x["scale"])
+    tol = U.TOL[dt]
+    e_o = rel_err(res[1]["out"], o, axes=(-2, -1))
+    e_l = rel_err(res[1]["lse"], l, axes=(-1,))
+    e_w = rel_err(res[1]["wsum"], w, axes=(-1,))
+    say(f"  err out {e_o:.2e} lse {e_l:.2e} wsum {e_w:.2e} (tol {tol})")
     assert e_o <= tol and e_l <= tol and e_w <= tol

@@ -6,7 +6,8 @@ thousand slots with ragged tails, chunk lengths from 1 to 160, bf16 and
 float32. Tolerances as in test_gpu_parity: normwise relative error per
 (b, head) slice <= 2e-2 (bf16) and 1e-5 (float32) for out, lse and wsum.
 The whole chunk step on random shapes: the fused call bit-equal to the three
-separate calls (attention, accumulate, evict and insert).
+separate calls (attention, accumulate, evict and insert); the insert-first
+step with each score policy, eviction and insert exact against the oracle.
 """
 import numpy as np
 import pytest
@@ -128,3 +129,44 @@ def test_random_step_fused_equals_calls(i):
     e_w = rel_err(res[1]["wsum"], w, axes=(-1,))
     say(f"  err out {e_o:.2e} lse {e_l:.2e} wsum {e_w:.2e} (tol {tol})")
     assert e_o <= tol and e_l <= tol and e_w <= tol
+
+
+N_INS_CASES = 18
+
+
+@pytest.mark.parametrize("i", range(N_INS_CASES))
+def test_random_step_insert_first(i):
+    """h2o_chunk_step_insert_first on a random shape with a random policy:
+    eviction and insert exact against the oracle, attention within tolerance,
+    scores one float32 addition of the GPU's own summed weights."""
+    c = _step_case(100 + i)
+    B, G, Hkv, d, M, T, dt = (c[k] for k in ("B", "G", "Hkv", "d", "M", "T", "dt"))
+    policy = ("h2o", "h2o_norm", "h2o_orig")[i % 3]
+    say(f"insert-first sweep case {i}: {c} {policy}")
+    wl = W.custom("inssweep", B=B, Hq=G * Hkv, Hkv=Hkv, d=d, M=M, T=T, dtype=dt,
+                  heavy_frac=0.02, age_decay=8192.0)
+    x = W.make_inputs(wl, seed=3000 + i)
+    tdt = U.TDT[dt]
+    st = U.device_state(x, dt)
+    q, kn, vn = (U.to_dev(x[n], tdt) for n in ("q", "k_new", "v_new"))
+    bufs = H.alloc_step(B, G * Hkv, Hkv, T, M, d, tdt, policy=policy, insert_first=True)
+    pos0 = int(x["pos0"])
+    H.h2o_chunk_step_insert_first(q, st["k_cache"], st["v_cache"], st["scores"], st["token_pos"],
+                                  kn, vn, bufs["out"], bufs["lse"], bufs["wsum"],
+                                  bufs["evict_idx"], bufs["workspace"], pos0, float(x["scale"]),
+                                  policy)
+    torch.cuda.synchronize()
+    r = oracle.h2o_step_insert_first(x["k_cache"], x["v_cache"], x["scores"], x["token_pos"],
+                                     x["q"], x["k_new"], x["v_new"], pos0, x["scale"], policy)
+    np.testing.assert_array_equal(bufs["evict_idx"].cpu().numpy(), r["evict_idx"])
+    for n in ("k_cache", "v_cache", "token_pos"):
+        np.testing.assert_array_equal(U.to_np(st[n]), np.asarray(r[n], U.to_np(st[n]).dtype),
+                                      err_msg=n)
+    g = tuple(U.to_np(bufs[n]) for n in ("out", "lse", "wsum"))
+    tol = U.TOL[dt]
+    e = [rel_err(a, b, axes=ax) for a, b, ax in
+         zip(g, (r["out"], r["lse"], r["wsum"]), ((-2, -1), (-1,), (-1,)))]
+    say(f"  err out {e[0]:.2e} lse {e[1]:.2e} wsum {e[2]:.2e} (tol {tol})")
+    assert all(v <= tol for v in e)
+    np.testing.assert_array_equal(st["scores"].cpu().numpy(),
+                                  oracle.accumulate_scores(r["scores_inserted"], g[2]))

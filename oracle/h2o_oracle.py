@@ -456,3 +456,55 @@ def rel_err(x, ref, axes: Sequence[int]) -> float:
     num = np.sqrt(((x - ref) ** 2).sum(axis=tuple(axes)))
     den = np.sqrt((ref ** 2).sum(axis=tuple(axes)))
     return float((num / np.maximum(den, np.finfo(F64).tiny)).max())
+
+
+def elem_err(x, ref, axes: Sequence[int], floor: float = 1e-6) -> float:
+    """Max over elements of |x - ref| / (|ref| + floor * max|ref|), the maximum
+    |ref| taken per slice over `axes`.
+
+    The summed weight and the score are defined per key (Eq. h2o-score), so
+    they are compared element by element: an element is held to a relative
+    error, and only elements below ``floor`` times the largest of their slice
+    to an absolute one. A slice whose reference is all zero must match
+    exactly."""
+    x = np.asarray(x, F64)
+    ref = np.asarray(ref, F64)
+    scale = np.abs(ref).max(axis=tuple(axes), keepdims=True)
+    den = np.abs(ref) + floor * scale
+    err = np.abs(x - ref)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        r = np.where(den > 0, err / np.where(den > 0, den, 1.0), np.where(err > 0, np.inf, 0.0))
+    return float(r.max()) if r.size else 0.0
+
+
+def eviction_agreement(evicted, scores_ref, k: int, tol: float):
+    """Compares a chosen eviction set with the oracle's for one row.
+
+    ``evicted``: the k slots some computation evicted, from its own float32
+    scores; ``scores_ref``: the oracle's accumulated scores of the row (all
+    non-negative). If that computation's scores are within ``tol`` of the
+    oracle's, relatively and element by element, then every slot it evicts
+    has an oracle score of at most tau * (1 + tol) / (1 - tol) and every slot
+    it keeps one of at least tau * (1 - tol) / (1 + tol), tau being the
+    oracle's k-th smallest score (Sec. "Variants of Heavy-Hitter Oracle":
+    the slots of smallest score are overwritten).
+
+    Returns (n_diff, n_band, valid): the number of evicted slots outside the
+    oracle's own eviction set, the number of oracle slots inside that band
+    (the only ones that may trade places), and whether every evicted and
+    every kept slot lies on its side of the band."""
+    s = np.asarray(scores_ref, F64)
+    M = s.shape[-1]
+    ev = np.asarray(evicted, np.int64)
+    own = bottomk(np.asarray(scores_ref, np.float32)[None], k)[0]
+    if k == 0:
+        return 0, 0, len(ev) == 0
+    tau = float(np.sort(s)[k - 1])
+    hi = tau * (1.0 + tol) / (1.0 - tol)
+    lo = tau * (1.0 - tol) / (1.0 + tol)
+    kept = np.setdiff1d(np.arange(M), ev)
+    valid = (len(np.unique(ev)) == k and ev.min() >= 0 and ev.max() < M
+             and bool((s[ev] <= hi).all()) and bool((s[kept] >= lo).all()))
+    n_diff = int(len(np.setdiff1d(ev, own)))
+    n_band = int(((s >= lo) & (s <= hi)).sum())
+    return n_diff, n_band, valid

@@ -1,16 +1,19 @@
 """GPU parity: the HIP path through the C ABI against the float64 oracle.
 
-Tolerances: normwise relative error per (b, head) slice <= 1e-5 for float32
-and <= 2e-2 for bf16, for out, lse, wsum and the accumulated scores.
-Selection is bit-exact when run on the oracle's float32 score vector; the
-insert is bitwise.
+Tolerances (1e-5 for float32, 2e-2 for bf16): out and lse normwise per
+(b, head) slice; wsum and the accumulated scores element by element
+(``_gpu.check``). Selection is bit-exact when run on the oracle's float32
+score vector; the insert is bitwise. End to end, the GPU's eviction (from
+its own scores) is compared with the oracle's: every slot that differs must
+lie inside a band around the oracle's k-th score whose width follows from
+the float32 score error bound (``_gpu.SEL_TOL``), which the scores are
+checked against first.
 """
 import numpy as np
 import pytest
 import torch
 
 import oracle
-from oracle import rel_err
 from paper_2608_19920_amd import h2o as H
 from paper_2608_19920_amd import workloads as W
 import _gpu as U
@@ -40,13 +43,8 @@ def _check_attention(x, dtype, res, heads=None, extra=""):
         sel = lambda a, hs: np.stack([a[b, h] for b, h in hs])
         o, go, l, gl = sel(o, hq), sel(go, hq), sel(l, hq), sel(gl, hq)
         w, gw = sel(w, heads), sel(gw, heads)
-    tol = U.TOL[dtype]
-    e_o = rel_err(go, o, axes=(-2, -1))
-    e_l = rel_err(gl, l, axes=(-1,))
-    e_w = rel_err(gw, w, axes=(-1,))
-    say(f"  {extra} err out {e_o:.2e} lse {e_l:.2e} wsum {e_w:.2e} (tol {tol})")
-    assert np.isfinite(go).all() and np.isfinite(gl).all() and np.isfinite(gw).all()
-    assert e_o <= tol and e_l <= tol and e_w <= tol
+    assert np.isfinite(gl).all()
+    U.check(dtype, out=(go, o), lse=(gl, l), wsum=(gw, w), extra=extra)
     return o_full
 
 
@@ -104,7 +102,7 @@ def test_tiny_f32_full_step():
     # bitwise: the kernel adds exactly the float32 values it was given
     np.testing.assert_array_equal(g_acc, oracle.accumulate_scores(x["scores"], res[2]))
     o_acc = oracle.accumulate_scores(x["scores"], w)
-    assert rel_err(g_acc, o_acc, axes=(-1,)) <= 1e-5
+    U.check("f32", scores=(g_acc, o_acc), extra="accumulated scores")
     # selection on the oracle's own float32 scores is bit-exact
     np.testing.assert_array_equal(U.gpu_bottomk(o_acc, wl.T), oracle.bottomk(o_acc, wl.T))
     # end-to-end eviction from the GPU's own scores + bitwise insert
@@ -236,9 +234,14 @@ def test_full_size_step_sampled_heads(name, nheads):
     # every query row's weights sum to one: per KV head, sum_j wsum = T*G
     np.testing.assert_allclose(res[2].sum(-1), wl.T * wl.G, rtol=2e-3)
     M, k = wl.M, wl.T
+    o_accs = {}
     for (b, h) in heads:
         o_acc = oracle.accumulate_scores(x["scores"][b, h], w[b, h])
-        assert rel_err(g_acc[b, h], o_acc, axes=(-1,)) <= 2e-2
+        o_accs[(b, h)] = o_acc
+        # the accumulated scores, element by element, at the stated tolerance
+        # and at the score error bound the eviction band below rests on
+        e_s = U.check("bf16", scores=(g_acc[b, h], o_acc), extra=f"scores {(b, h)}")["scores"]
+        assert e_s <= U.SEL_TOL, f"score error {e_s:.2e} above the bound {U.SEL_TOL}"
         np.testing.assert_array_equal(U.gpu_bottomk(o_acc[None], k)[0],
                                       oracle.bottomk(o_acc[None], k)[0])
     H.h2o_evict_insert(st["k_cache"], st["v_cache"], st["scores"], st["token_pos"], kn, vn,
@@ -246,13 +249,12 @@ def test_full_size_step_sampled_heads(name, nheads):
     torch.cuda.synchronize()
     g_idx = bufs["evict_idx"].cpu().numpy()
     np.testing.assert_array_equal(g_idx, oracle.bottomk(g_acc, k))     # on the GPU's scores
-    for (b, h) in heads:       # validity against the oracle's scores (near-ties only differ)
-        o_acc = oracle.accumulate_scores(x["scores"][b, h], w[b, h]).astype(np.float64)
-        tau = np.sort(o_acc)[k - 1]
-        delta = 4 * 2e-2 * o_acc.max()
-        ev = g_idx[b, h]
-        kept = np.setdiff1d(np.arange(M), ev)
-        assert (o_acc[ev] <= tau + delta).all() and (o_acc[kept] >= tau - delta).all()
+    for (b, h) in heads:       # against the oracle's eviction: only near-ties may differ
+        n_diff, n_band, ok = oracle.eviction_agreement(g_idx[b, h], o_accs[(b, h)], k,
+                                                       U.SEL_TOL)
+        say(f"  head {(b, h)}: {n_diff} of {k} evicted slots differ from the oracle's; "
+            f"{n_band} oracle slots lie within the band of {U.SEL_TOL} around the k-th score")
+        assert ok and n_diff <= n_band
     kc = st["k_cache"].float().cpu().numpy()
     for (b, h) in heads:
         np.testing.assert_array_equal(kc[b, h][g_idx[b, h]], x["k_new"][b, h])
@@ -283,21 +285,26 @@ def test_decode_trajectory_teacher_forced():
         ref = oracle.h2o_step(pre_k, pre_v, pre["scores"], pre["token_pos"], x["q_steps"][s],
                               x["k_new_steps"][s], x["v_new_steps"][s], pos, x["scale"])
         go, gw = U.to_np(bufs["out"]), U.to_np(bufs["wsum"])
-        assert rel_err(go, ref["out"], axes=(-2, -1)) <= 2e-2
-        assert rel_err(gw, ref["wsum"], axes=(-1,)) <= 2e-2
+        U.check("bf16", out=(go, ref["out"]), wsum=(gw, ref["wsum"]), extra=f"step {s}")
         g_idx = bufs["evict_idx"].cpu().numpy()
-        n_mismatch += int((g_idx != ref["evict_idx"]).sum())
         # the GPU's choice is the argmin of the GPU's own accumulated scores
         g_acc = oracle.accumulate_scores(pre["scores"], gw)
         np.testing.assert_array_equal(g_idx, oracle.bottomk(g_acc, 1))
+        assert oracle.elem_err(g_acc, ref["scores_acc"], (-1,)) <= U.SEL_TOL
+        # and agrees with the oracle's, up to near-ties of the band
+        for b in range(wl.B):
+            for h in range(wl.Hkv):
+                n_diff, _, ok = oracle.eviction_agreement(g_idx[b, h], ref["scores_acc"][b, h],
+                                                          1, U.SEL_TOL)
+                assert ok, f"step {s} head {(b, h)}: eviction outside the band"
+                n_mismatch += n_diff
         # and the inserted key is where the GPU says
         kc = st["k_cache"].float().cpu().numpy()
         for b in range(wl.B):
             for h in range(wl.Hkv):
                 np.testing.assert_array_equal(kc[b, h, g_idx[b, h, 0]], x["k_new_steps"][s, b, h, 0])
     say(f"  eviction choices differing from the oracle over 16 steps: {n_mismatch} / "
-        f"{16 * wl.B * wl.Hkv}")
-    assert n_mismatch <= 2
+        f"{16 * wl.B * wl.Hkv} (each inside the band)")
 
 
 STEP_SHAPES = [  # B, Hq, Hkv, d, M, T, dtype
@@ -333,6 +340,11 @@ def test_chunk_step_equals_three_calls(shape):
     for n in res[0]:
         np.testing.assert_array_equal(res[1][n], res[0][n], err_msg=n)
     _check_attention(x, dt, (res[1]["out"], res[1]["lse"], res[1]["wsum"]), extra="fused")
+    # the accumulated scores of the kept slots against the oracle's
+    ref = oracle.h2o_step(x["k_cache"], x["v_cache"], x["scores"], x["token_pos"], x["q"],
+                          x["k_new"], x["v_new"], int(x["pos0"]), x["scale"])
+    g_acc = oracle.accumulate_scores(x["scores"], res[1]["wsum"])
+    U.check(dt, scores=(g_acc, ref["scores_acc"]), extra="accumulated scores")
 
 
 @pytest.mark.parametrize("shape", STEP_SHAPES)

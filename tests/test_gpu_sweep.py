@@ -3,8 +3,8 @@ h2o_sdpa_cache (cache mode, token-position mask) against the float64 oracle,
 on every kernel path a shape can take (automatic, generic VALU, MFMA, and the
 T = 1 decode kernels), GQA group sizes 1 to 8, cache lengths from 0 to a few
 thousand slots with ragged tails, chunk lengths from 1 to 160, bf16 and
-float32. Tolerances as in test_gpu_parity: normwise relative error per
-(b, head) slice <= 2e-2 (bf16) and 1e-5 (float32) for out, lse and wsum.
+float32. Tolerances as in test_gpu_parity (2e-2 bf16, 1e-5 float32): out
+and lse normwise per (b, head) slice, wsum element by element.
 The whole chunk step on random shapes: the fused call bit-equal to the three
 separate calls (attention, accumulate, evict and insert); the insert-first
 step with each score policy, eviction and insert exact against the oracle.
@@ -14,7 +14,6 @@ import pytest
 import torch
 
 import oracle
-from oracle import rel_err
 from paper_2608_19920_amd import h2o as H
 from paper_2608_19920_amd import workloads as W
 import _gpu as U
@@ -73,15 +72,8 @@ def test_random_shape(i):
         H.h2o_debug_force_path(-1)
     o, l, w = ref
     go, gl, gw = res
-    seen = np.isfinite(l)   # rows that see no key have lse -inf on both sides
-    assert np.array_equal(np.isfinite(gl), seen)
-    tol = U.TOL[dt]
-    e_o = rel_err(go, o, axes=(-2, -1))
-    e_l = rel_err(np.where(seen, gl, 0.0), np.where(seen, l, 0.0), axes=(-1,))
-    e_w = rel_err(gw, w, axes=(-1,))
-    say(f"  err out {e_o:.2e} lse {e_l:.2e} wsum {e_w:.2e} (tol {tol})")
-    assert np.isfinite(go).all() and np.isfinite(gw).all()
-    assert e_o <= tol and e_l <= tol and e_w <= tol
+    # rows that see no key have lse -inf on both sides (checked in U.check)
+    U.check(dt, out=(go, o), lse=(gl, l), wsum=(gw, w))
 
 
 N_STEP_CASES = 24
@@ -123,12 +115,9 @@ def test_random_step_fused_equals_calls(i):
         np.testing.assert_array_equal(res[1][n], res[0][n], err_msg=n)
     o, l, w = oracle.sdpa_chunk(x["q"], x["k_cache"], x["v_cache"], x["k_new"], x["v_new"],
                                 x["scale"])
-    tol = U.TOL[dt]
-    e_o = rel_err(res[1]["out"], o, axes=(-2, -1))
-    e_l = rel_err(res[1]["lse"], l, axes=(-1,))
-    e_w = rel_err(res[1]["wsum"], w, axes=(-1,))
-    say(f"  err out {e_o:.2e} lse {e_l:.2e} wsum {e_w:.2e} (tol {tol})")
-    assert e_o <= tol and e_l <= tol and e_w <= tol
+    U.check(dt, out=(res[1]["out"], o), lse=(res[1]["lse"], l), wsum=(res[1]["wsum"], w),
+            scores=(oracle.accumulate_scores(x["scores"], res[1]["wsum"]),
+                    oracle.accumulate_scores(x["scores"], w)))
 
 
 N_INS_CASES = 18
@@ -163,10 +152,7 @@ def test_random_step_insert_first(i):
         np.testing.assert_array_equal(U.to_np(st[n]), np.asarray(r[n], U.to_np(st[n]).dtype),
                                       err_msg=n)
     g = tuple(U.to_np(bufs[n]) for n in ("out", "lse", "wsum"))
-    tol = U.TOL[dt]
-    e = [rel_err(a, b, axes=ax) for a, b, ax in
-         zip(g, (r["out"], r["lse"], r["wsum"]), ((-2, -1), (-1,), (-1,)))]
-    say(f"  err out {e[0]:.2e} lse {e[1]:.2e} wsum {e[2]:.2e} (tol {tol})")
-    assert all(v <= tol for v in e)
+    U.check(dt, out=(g[0], r["out"]), lse=(g[1], r["lse"]), wsum=(g[2], r["wsum"]),
+            scores=(U.to_np(st["scores"]), r["scores"]))
     np.testing.assert_array_equal(st["scores"].cpu().numpy(),
                                   oracle.accumulate_scores(r["scores_inserted"], g[2]))

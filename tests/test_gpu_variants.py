@@ -13,7 +13,6 @@ import pytest
 import torch
 
 import oracle
-from oracle import rel_err
 from paper_2608_19920_amd import h2o as H
 from paper_2608_19920_amd import workloads as W
 import _gpu as U
@@ -170,9 +169,7 @@ def test_step_with_policy(shape, policy):
     g_w = U.to_np(bufs["wsum"])
     o_out, o_lse, o_w = oracle.sdpa_chunk(x["q"], x["k_cache"], x["v_cache"], x["k_new"],
                                           x["v_new"], float(x["scale"]))
-    tol = U.TOL[dt]
-    assert rel_err(g_w, o_w, axes=(-1,)) <= tol
-    assert rel_err(U.to_np(bufs["out"]), o_out, axes=(-2, -1)) <= tol
+    U.check(dt, out=(U.to_np(bufs["out"]), o_out), wsum=(g_w, o_w))
     g_acc = oracle.accumulate_scores(x["scores"], g_w)
     kc, vc, sc, tp, idx = oracle.evict_insert(x["k_cache"], x["v_cache"], g_acc, x["token_pos"],
                                               x["k_new"], x["v_new"], g_w, T, pos0, policy)
@@ -180,15 +177,17 @@ def test_step_with_policy(shape, policy):
     got["evict_idx"] = bufs["evict_idx"].cpu().numpy()
     _assert_same(got, dict(k_cache=kc, v_cache=vc, scores=sc, token_pos=tp, evict_idx=idx),
                  policy)
-    # validity against the oracle's own keys
+    # against the oracle's own ranking: only near-ties may differ (the keys
+    # are the scores divided by an exact age, or batch sums of non-negative
+    # scores, so they carry the scores' relative error bound)
     o_keys = oracle.selection_keys(oracle.accumulate_scores(x["scores"], o_w), x["token_pos"],
-                                   policy, pos0 + T).astype(np.float64)
+                                   policy, pos0 + T)
+    g_keys = oracle.selection_keys(g_acc, x["token_pos"], policy, pos0 + T)
+    assert oracle.elem_err(g_keys, o_keys, (-1,)) <= U.SEL_TOL
     g_idx = got["evict_idx"][0] if policy == "h2o_orig" else got["evict_idx"]
-    rows = o_keys.reshape(-1, M)
-    for r, e in zip(rows, g_idx.reshape(-1, T)):
-        tau = np.sort(r)[T - 1]
-        delta = 4 * tol * np.abs(r).max()
-        kept = np.ones(M, bool)
-        kept[e] = False
-        assert r[e].max() <= tau + delta
-        assert r[kept].min() >= tau - delta if kept.any() else True
+    n_diff = 0
+    for r, e in zip(o_keys.reshape(-1, M), g_idx.reshape(-1, T)):
+        nd, _, ok = oracle.eviction_agreement(e, r, T, U.SEL_TOL)
+        assert ok, "eviction outside the band around the oracle's k-th key"
+        n_diff += nd
+    say(f"  {n_diff} evicted slots differ from the oracle's (each inside the band)")

@@ -755,3 +755,272 @@ def test_backward_mistakes_are_caught(monkeypatch):
             m.setattr(O, "_head_backward", fn)
             with pytest.raises(AssertionError):
                 test_backward_matches_torch_autograd((2, 4, 2, 8, 7, 4))
+
+
+# --------------------------------------------- the step's wiring, worked by hand
+# One-hot keys make every logit a chosen number: with key j = e_j, scale 1 and
+# query i = (ln a_i0, ln a_i1, ...), the logit of (i, j) is ln a_ij, so the
+# softmax weights are a_ij / sum_j' a_ij' (exact rationals) and everything the
+# step computes can be written down with fractions. Rows are chosen to sum to
+# powers of two, so every weight and score below is exact in float32.
+def _onehot_case():
+    """B1 Hq2 Hkv1 (G2), M5, T2, d7: integer weights a[g, i, j] over the keys
+    row i sees (cache slots 0..4, chunk key t <= i); prior scores S0; values
+    V[j] = j + 1 (cache) and 10 + t (chunk keys)."""
+    M, T, G = 5, 2, 2
+    a = {
+        (0, 0): [1, 1, 1, 1, 2, 2],
+        (0, 1): [2, 1, 1, 1, 1, 1, 1],
+        (1, 0): [1, 2, 1, 1, 1, 2],
+        (1, 1): [8, 1, 1, 1, 1, 2, 2],
+    }
+    d = M + T
+    q = np.zeros((1, G, T, d))
+    for (g, i), row in a.items():
+        q[0, g, i, :len(row)] = np.log(np.array(row, np.float64))
+    keys = np.eye(d)
+    kc, kn = keys[None, None, :M], keys[None, None, M:]
+    vc = np.arange(1, M + 1, dtype=np.float64)[None, None, :, None] * np.ones((1, 1, M, d))
+    vn = (10 + np.arange(T, dtype=np.float64))[None, None, :, None] * np.ones((1, 1, T, d))
+    s0 = np.array([[[0.0625, 1.0, 0.75, 0.5, 0.25]]], np.float32)
+    tp = np.array([[[7, 3, 9, 1, 4]]], np.int32)
+    return dict(a=a, M=M, T=T, G=G, q=q, kc=kc, vc=vc, kn=kn, vn=vn, s0=s0, tp=tp, pos0=20)
+
+
+def _onehot_expected(c):
+    """The step's results by exact rational arithmetic (no oracle code)."""
+    M, T, G, a = c["M"], c["T"], c["G"], c["a"]
+    vals = [Fraction(j + 1) for j in range(M)] + [Fraction(10 + t) for t in range(T)]
+    w = [Fraction(0)] * (M + T)
+    out = np.zeros((G, T))
+    lse = np.zeros((G, T))
+    for (g, i), row in a.items():
+        Z = sum(Fraction(x) for x in row)
+        lse[g, i] = float(np.log(float(Z)))
+        out[g, i] = float(sum(Fraction(x) / Z * vals[j] for j, x in enumerate(row)))
+        for j, x in enumerate(row):
+            w[j] += Fraction(x) / Z
+    acc = [Fraction(float(c["s0"][0, 0, j])) + w[j] for j in range(M)]
+    # bottom-T by (score, slot), ascending slots
+    evict = sorted(sorted(range(M), key=lambda j: (acc[j], j))[:T])
+    scores = [float(x) for x in acc]
+    tp = [int(x) for x in c["tp"][0, 0]]
+    for i, e in enumerate(evict):
+        scores[e] = float(w[M + i])
+        tp[e] = c["pos0"] + i
+    return dict(w=[float(x) for x in w], acc=[float(x) for x in acc], evict=evict,
+                scores=scores, tp=tp, out=out, lse=lse)
+
+
+def _check_onehot_step(step_fn):
+    """Runs ``step_fn`` (oracle.h2o_step's signature) on the worked case and
+    compares with the exact results; returns the list of what differs."""
+    c = _onehot_case()
+    e = _onehot_expected(c)
+    r = step_fn(c["kc"], c["vc"], c["s0"], c["tp"], c["q"], c["kn"], c["vn"], c["pos0"], 1.0)
+    bad = []
+    if not np.allclose(r["wsum"][0, 0], e["w"], rtol=1e-14, atol=0):
+        bad.append("wsum")
+    if not np.array_equal(np.asarray(r["scores_acc"])[0, 0], np.float32(e["acc"])):
+        bad.append("accumulated scores")
+    if not np.array_equal(r["evict_idx"][0, 0], e["evict"]):
+        bad.append("evicted slots")
+    if not np.array_equal(np.asarray(r["scores"])[0, 0], np.float32(e["scores"])):
+        bad.append("scores after the insert")
+    if not np.array_equal(r["token_pos"][0, 0], e["tp"]):
+        bad.append("token positions")
+    kc_new = np.array(c["kc"], copy=True)
+    for i, slot in enumerate(e["evict"]):
+        kc_new[0, 0, slot] = c["kn"][0, 0, i]
+    if not np.array_equal(r["k_cache"], kc_new):
+        bad.append("inserted keys")
+    if not (np.allclose(r["out"][0, :, :, 0], e["out"], rtol=1e-14)
+            and np.allclose(r["lse"][0], e["lse"], rtol=1e-14)):
+        bad.append("out/lse")
+    return bad
+
+
+def test_step_worked_example_exact():
+    """h2o_step on the worked case equals exact rational arithmetic: wsum
+    sums each key's weight over both query heads and both queries (the chunk
+    keys only over the queries that see them), the accumulated scores are
+    S0 + wsum (Eq. h2o-score), the eviction is the bottom-2 of the
+    *accumulated* scores - here {3, 4}, while the prior scores alone would
+    evict {0, 4} - and chunk key i lands in the i-th smallest evicted slot
+    with score wsum[M+i] (its own column sum) and position pos0 + i."""
+    e = _onehot_expected(_onehot_case())
+    assert e["evict"] == [3, 4]
+    assert e["w"] == [1.0, 9 / 16, 7 / 16, 7 / 16, 9 / 16, 12 / 16, 4 / 16]
+    assert e["scores"] == [1.0625, 1.5625, 1.1875, 0.75, 0.25]
+    assert sum(e["w"]) == 4.0                     # T * G: every row sums to one
+    assert _check_onehot_step(oracle.h2o_step) == []
+
+
+def test_step_wiring_mistakes_are_caught(monkeypatch):
+    """Mistakes in how h2o_step wires its parts fail the worked example."""
+    orig_step = O.h2o_step
+
+    def rank_prior(k_cache, v_cache, scores, token_pos, q, k_new, v_new, pos0, scale=None,
+                   policy="h2o"):
+        # ranks the scores before the chunk's weights are added
+        out, lse, wsum = O.sdpa_chunk(q, k_cache, v_cache, k_new, v_new, scale)
+        acc = O.accumulate_scores(scores, wsum)
+        T = q.shape[2]
+        idx = O.bottomk(scores, T)
+        kc, vc = k_cache.copy(), v_cache.copy()
+        sc, tp = acc.copy(), token_pos.copy()
+        M = sc.shape[-1]
+        for i, e in enumerate(idx[0, 0]):
+            kc[0, 0, e] = k_new[0, 0, i]
+            vc[0, 0, e] = v_new[0, 0, i]
+            sc[0, 0, e] = np.float32(wsum[0, 0, M + i])
+            tp[0, 0, e] = pos0 + i
+        return dict(out=out, lse=lse, wsum=wsum, scores_acc=acc, evict_idx=idx, k_cache=kc,
+                    v_cache=vc, scores=sc, token_pos=tp)
+
+    def with_insert(mutate):
+        def step(*a, **k):
+            r = orig_step(*a, **k)
+            mutate(r, a)
+            return r
+        return step
+
+    def insert_zero(r, a):          # new slots start from 0
+        for i, e in enumerate(r["evict_idx"][0, 0]):
+            r["scores"][0, 0, e] = 0.0
+
+    def insert_wrong_column(r, a):  # the first chunk columns instead of M + i
+        for i, e in enumerate(r["evict_idx"][0, 0]):
+            r["scores"][0, 0, e] = np.float32(r["wsum"][0, 0, i])
+
+    def insert_reversed(r, a):      # new key i into the i-th largest evicted slot
+        ev = r["evict_idx"][0, 0]
+        M = r["scores"].shape[-1]
+        for i, e in enumerate(ev[::-1]):
+            r["scores"][0, 0, e] = np.float32(r["wsum"][0, 0, M + i])
+            r["k_cache"][0, 0, e] = a[5][0, 0, i]
+
+    def keep_prior_scores(r, a):    # the kept slots not accumulated
+        keep = np.setdiff1d(np.arange(r["scores"].shape[-1]), r["evict_idx"][0, 0])
+        r["scores"][0, 0, keep] = np.asarray(a[2], np.float32)[0, 0, keep]
+
+    for name, fn in [("ranks prior scores", rank_prior),
+                     ("inserted score 0", with_insert(insert_zero)),
+                     ("inserted score from the wrong column", with_insert(insert_wrong_column)),
+                     ("new keys in reversed slots", with_insert(insert_reversed)),
+                     ("kept scores not accumulated", with_insert(keep_prior_scores))]:
+        assert _check_onehot_step(fn), f"planted wiring mistake not caught: {name}"
+
+
+def test_decode_threads_state_exact():
+    """Two single-token steps by hand (one-hot keys, G1, M3): step 1 evicts
+    slot 2 and writes key e3 there with score 1/2; step 2 must attend over that
+    new state (e3 in slot 2) and, with slots 1 and 2 tied at 3/4, evict the
+    lower slot 1. oracle.decode must thread the state from step to step."""
+    d = 5
+    keys = np.eye(d)
+    kc = keys[None, None, :3].copy()
+    vc = np.ones((1, 1, 3, d))
+    s0 = np.array([[[0.5, 0.5, 0.25]]], np.float32)
+    tp = np.array([[[0, 1, 2]]], np.int32)
+    # step 1 sees e0 e1 e2 | e3 with weights 2 1 1 | 4 (sum 8)
+    # step 2 sees e0 e1 e3 | e4 with weights 1 1 2 | 4 (sum 8); e2 is gone
+    q1 = np.log(np.array([2, 1, 1, 4, 1], np.float64))
+    q2 = np.log(np.array([1, 1, 1, 2, 4], np.float64))
+    qs = np.stack([q1, q2])[:, None, None, None, :]
+    kns = np.stack([keys[3], keys[4]])[:, None, None, None, :]
+    vns = np.ones((2, 1, 1, 1, d))
+    res = oracle.decode(kc, vc, s0, tp, qs, kns, vns, 3, 1.0)
+    np.testing.assert_allclose(res[0]["wsum"][0, 0], [0.25, 0.125, 0.125, 0.5], rtol=1e-14)
+    assert res[0]["evict_idx"][0, 0, 0] == 2
+    np.testing.assert_array_equal(res[0]["scores"][0, 0], np.float32([0.75, 0.625, 0.5]))
+    np.testing.assert_allclose(res[1]["wsum"][0, 0], [0.125, 0.125, 0.25, 0.5], rtol=1e-14)
+    assert res[1]["evict_idx"][0, 0, 0] == 1                 # the tie goes to the lower slot
+    np.testing.assert_array_equal(res[1]["scores"][0, 0], np.float32([0.875, 0.5, 0.75]))
+    np.testing.assert_array_equal(res[1]["token_pos"][0, 0], [0, 4, 3])
+    np.testing.assert_array_equal(res[1]["k_cache"][0, 0], keys[[0, 4, 3]])
+
+
+# ------------------------------------------------- the metrics the gates use
+def test_rel_err_hand_computed():
+    """||x - ref|| / ||ref|| per slice, maximum over slices: slice 0 differs
+    by (0, 0.5) against (3, 4) -> 0.1; slice 1 by (0, 0.2) against (1, 0)
+    -> 0.2."""
+    ref = np.array([[3.0, 4.0], [1.0, 0.0]])
+    x = np.array([[3.0, 4.5], [1.0, 0.2]])
+    assert oracle.rel_err(x, ref, axes=(-1,)) == pytest.approx(0.2, rel=1e-15)
+    # over both axes: ||(0, .5, 0, .2)|| / ||(3, 4, 1, 0)|| = sqrt(.29 / 26)
+    assert oracle.rel_err(x, ref, axes=(-2, -1)) == pytest.approx(np.sqrt(0.29 / 26), rel=1e-15)
+    assert oracle.rel_err(ref, ref, axes=(-1,)) == 0.0
+
+
+def test_elem_err_hand_computed():
+    """|x - ref| / (|ref| + floor * max|ref|) per element: (0.5 / 4.000004)
+    for the 4.0 entry of slice 0, 0.2 / (0 + 1e-6) for the 0.0 entry of
+    slice 1, whose largest |ref| is 1."""
+    ref = np.array([[3.0, 4.0], [1.0, 0.0]])
+    x = np.array([[3.0, 4.5], [1.0, 2e-7]])
+    assert oracle.elem_err(x, ref, axes=(-1,)) == pytest.approx(0.2, rel=1e-12)
+    x2 = np.array([[3.0, 4.5], [1.0, 0.0]])
+    assert oracle.elem_err(x2, ref, axes=(-1,)) == pytest.approx(0.5 / (4.0 + 4e-6), rel=1e-12)
+    assert oracle.elem_err(np.zeros(3), np.zeros(3), axes=(-1,)) == 0.0
+    assert oracle.elem_err(np.array([0, 1e-30, 0]), np.zeros(3), axes=(-1,)) == np.inf
+
+
+def _skewed_head(seed=0):
+    """One KV head with heavy hitters (a skewed wsum): the oracle's wsum and
+    accumulated scores of B1 Hq4 Hkv1 d64 M2048 T256, 2 % heavy keys."""
+    w = W.custom(B=1, Hq=4, Hkv=1, d=64, M=2048, T=256, dtype="bf16", heavy_frac=0.02)
+    x = W.make_inputs(w, seed)
+    _, _, ws = oracle.sdpa_chunk(*_args(x), x["scale"])
+    return x, ws, oracle.accumulate_scores(x["scores"], ws)
+
+
+def test_normwise_gate_misses_a_zeroed_tile_elementwise_gate_does_not():
+    """Zeroing the summed weights of one 32-key tile of ordinary slots (no
+    heavy hitter among them) passes a 2e-2 normwise check of the whole row -
+    the heavy hitters dominate its norm - but fails the element-by-element
+    check at the same tolerance, and changes the eviction."""
+    x, ws, acc = _skewed_head()
+    row = ws[0, 0, :2048]
+    med = np.median(row)
+    t0 = next(t for t in range(0, 2048, 32) if row[t:t + 32].max() < 4 * med)
+    bad = ws.copy()
+    bad[0, 0, t0:t0 + 32] = 0.0
+    assert oracle.rel_err(bad, ws, axes=(-1,)) <= 2e-2
+    assert oracle.elem_err(bad, ws, axes=(-1,)) > 2e-2
+    bad_acc = oracle.accumulate_scores(x["scores"], bad)
+    assert not np.array_equal(oracle.bottomk(bad_acc, 256), oracle.bottomk(acc, 256))
+
+
+def test_eviction_band_accepts_near_ties_and_rejects_far_slots():
+    """The band check: the oracle's own set is valid with no differences; a
+    set that swaps the k-th slot with the (k+1)-th (a near tie, both inside a
+    band of 1e-3 around the k-th score when they are that close) is valid; a
+    set that swaps in a slot far above the threshold is not."""
+    x, ws, acc = _skewed_head(1)
+    k = 256
+    s = acc[0, 0].astype(np.float64)
+    own = oracle.bottomk(acc, k)[0, 0]
+    n_diff, n_band, ok = oracle.eviction_agreement(own, s, k, 1e-3)
+    assert (n_diff, ok) == (0, True) and n_band >= 1
+    order = np.lexsort((np.arange(len(s)), s))
+    # a near tie: the (k+1)-th score set 1e-4 above the k-th; an eviction
+    # that takes it instead of the k-th slot is valid at a tolerance of 1e-3
+    sn = s.copy()
+    sn[order[k]] = s[order[k - 1]] * (1 + 1e-4)
+    near = np.sort(np.concatenate([own[own != order[k - 1]], [order[k]]]))
+    n_diff, n_band, ok = oracle.eviction_agreement(near, sn, k, 1e-3)
+    assert n_diff == 1 and ok and n_band >= 2
+    far = np.sort(np.concatenate([own[own != order[k - 1]], [order[-1]]]))   # the largest score
+    n_diff, _, ok = oracle.eviction_agreement(far, s, k, 1e-3)
+    assert n_diff == 1 and not ok
+    # a slot a quarter above the threshold: outside the relative band, but
+    # inside an absolute band of 4 * 2e-2 * max score (the heavy hitters
+    # make that band wider than the threshold itself)
+    tau = s[order[k - 1]]
+    j = order[np.searchsorted(s[order], 1.25 * tau)]
+    assert 1.2 * tau < s[j] <= tau + 4 * 2e-2 * s.max()
+    mid = np.sort(np.concatenate([own[own != order[k - 1]], [j]]))
+    n_diff, _, ok = oracle.eviction_agreement(mid, s, k, 1e-3)
+    assert n_diff == 1 and not ok

@@ -73,6 +73,31 @@ def traffic_for(kernel: str, workload: str):
 
 
 # ----------------------------------------------------------------- device side
+PREFILL_WARMUP = 3
+PREFILL_REPS = 20
+
+
+def interleaved_median_ms(fns, reps, warmup, torch):
+    """Median duration in ms of each call in ``fns`` (name -> callable): after
+    ``warmup`` untimed rounds, ``reps`` rounds that run the calls one after
+    the other, each bracketed by a pair of events on the current stream, so
+    every call is timed under the same conditions as the others."""
+    for _ in range(warmup):
+        for fn in fns.values():
+            fn()
+    torch.cuda.synchronize()
+    E = lambda: torch.cuda.Event(enable_timing=True)
+    ev = {k: [(E(), E()) for _ in range(reps)] for k in fns}
+    for r in range(reps):
+        for k, fn in fns.items():
+            a, b = ev[k][r]
+            a.record()
+            fn()
+            b.record()
+    torch.cuda.synchronize()
+    return {k: float(np.median([a.elapsed_time(b) for a, b in ev[k]])) for k in fns}
+
+
 def _dev_state(x, torch):
     bf = torch.bfloat16
     to = lambda a, dt: torch.from_numpy(np.ascontiguousarray(a)).to("cuda").to(dt)
@@ -131,6 +156,29 @@ def bench_decode(args, torch, H, W):
     H.h2o_debug_timing(False)
     step_bytes = decode_step_bytes(w) * LAYERS
     gbs = step_bytes / (ms_step * 1e-3) / 1e9
+
+    # The same token step on ONE layer state, captured LAYERS times in a row:
+    # its 69 MB stay in the 256 MB Infinity Cache between steps (hot MALL).
+    st0, inp0, bufs0 = layers[0]
+    hot = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(hot, stream=stream):
+        for _ in range(LAYERS):
+            H.step(st0, inp0["q"], inp0["k_new"], inp0["v_new"], bufs0, inp0["pos0"],
+                   inp0["scale"])
+    torch.cuda.synchronize()
+    for _ in range(args.warmup):
+        hot.replay()
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(args.steps):
+        hot.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    hot_us = e0.elapsed_time(e1) / args.steps / LAYERS * 1e3
+    hot_mall = {"workload": "the same token step on one layer state, replayed (its 69 MB "
+                            "stay in the 256 MB Infinity Cache)",
+                "us_per_layer_step": round(hot_us, 2),
+                "gbs": round(decode_step_bytes(w) / (hot_us * 1e-6) / 1e9, 1)}
     ms_split, n_split = ktimes["decode_split"]
     avg_split_ms = ms_split / max(n_split, 1)
     ach = decode_split_bytes(w) / (avg_split_ms * 1e-3) / 1e9
@@ -144,7 +192,7 @@ def bench_decode(args, torch, H, W):
                       "own begin and end) on the launch stream, over an eager pass of the "
                       "timed steps"}
     return dict(w=w, ms_step=ms_step, value=gbs, roofline=roof, wall_s=t_wall,
-                step_bytes=step_bytes)
+                step_bytes=step_bytes, hot_mall=hot_mall)
 
 
 def bench_prefill(name, args, torch, H, W):
@@ -159,31 +207,21 @@ def bench_prefill(name, args, torch, H, W):
     bufs = H.alloc_step(w.B, w.Hq, w.Hkv, w.T, w.M, w.d, bf)
     sdpa = lambda: H.h2o_sdpa_chunk(q, st["k_cache"], st["v_cache"], kn, vn, bufs["out"],
                                     bufs["lse"], bufs["wsum"], bufs["workspace"], scale)
-    reps = max(3, args.steps // 5)
-    for _ in range(max(2, args.warmup)):
-        sdpa()
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(reps):
-        sdpa()
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / reps
+    full = lambda: H.step(st, q, kn, vn, bufs, pos0, scale)
+    # the attention call and the whole step (attention, accumulate, evict and
+    # insert), interleaved, median of PREFILL_REPS after PREFILL_WARMUP
+    med = interleaved_median_ms({"sdpa": sdpa, "full_step": full}, PREFILL_REPS,
+                                PREFILL_WARMUP, torch)
+    ms, ms_step = med["sdpa"], med["full_step"]
+    # per-kernel durations of the same calls from the library's timing hook
     H.h2o_debug_timing(True)
-    for _ in range(reps):
-        sdpa()
+    for _ in range(PREFILL_REPS):
+        full()
     torch.cuda.synchronize()
     kt = {k: H.h2o_debug_kernel_time(k) for k in
-          ("mfma_lse", "mfma_main", "split_reduce", "colsum_reduce")}
+          ("mfma_lse", "mfma_main", "split_reduce", "colsum_reduce", "accumulate", "bottomk",
+           "insert")}
     H.h2o_debug_timing(False)
-    # whole step: attention + accumulate + evict/insert
-    e0.record()
-    for _ in range(reps):
-        H.step(st, q, kn, vn, bufs, pos0, scale)
-    e1.record()
-    torch.cuda.synchronize()
-    ms_step = e0.elapsed_time(e1) / reps
     Wf = attention_flops(w)
     tf = Wf / (ms * 1e-3) / 1e12
     main_ms = kt["mfma_main"][0] / max(kt["mfma_main"][1], 1)
@@ -191,6 +229,8 @@ def bench_prefill(name, args, torch, H, W):
     return {"workload": w.describe(), "tflops": round(tf, 1),
             "frac_of_bf16_peak": round(tf / BF16_PEAK_TFLOPS, 4),
             "ms_sdpa": round(ms, 4), "ms_full_step": round(ms_step, 4),
+            "timing": f"median of {PREFILL_REPS} after {PREFILL_WARMUP} warm-up rounds, "
+                      "the two calls interleaved",
             "kernel_us": {k: round(v[0] / max(v[1], 1) * 1e3, 1) for k, v in kt.items()},
             "roofline_main": {"kernel": "mfma_main", "bound": "mfma",
                               "achieved": round(ach_main, 1), "peak": BF16_PEAK_TFLOPS,
@@ -275,17 +315,8 @@ def bench_insert_first(args, torch, H, W):
                                         b["out"], b["lse"], b["wsum"], b["workspace"], pos0,
                                         scale)
         full()                     # the chunk is in the cache from here on
-        reps = max(3, args.steps // 5)
-        res = {}
-        for tag, fn in (("sdpa_cache", sdpa), ("full_step", full)):
-            fn()
-            torch.cuda.synchronize()
-            e0.record()
-            for _ in range(reps):
-                fn()
-            e1.record()
-            torch.cuda.synchronize()
-            res[tag] = e0.elapsed_time(e1) / reps
+        res = interleaved_median_ms({"sdpa_cache": sdpa, "full_step": full}, PREFILL_REPS,
+                                    PREFILL_WARMUP, torch)
         tf = insert_first_flops(w) / (res["sdpa_cache"] * 1e-3) / 1e12
         out["prefill"].append({"workload": w.describe(), "tflops": round(tf, 1),
                                "frac_of_bf16_peak": round(tf / BF16_PEAK_TFLOPS, 4),
@@ -315,16 +346,8 @@ def bench_backward(args, torch, H, W):
     ws = torch.empty(max(H.h2o_backward_workspace_bytes(w.B, w.Hq, w.Hkv, w.T, w.M, w.d, bf), 16),
                      dtype=torch.uint8, device="cuda")
     fn = lambda: H.h2o_sdpa_chunk_backward(q, kc, vc, kn, vn, b["lse"], dout, *grads, ws, scale)
-    fn()
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    reps = 5
-    e0.record()
-    for _ in range(reps):
-        fn()
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1) / reps
+    reps = PREFILL_REPS
+    ms = interleaved_median_ms({"bwd": fn}, reps, PREFILL_WARMUP, torch)["bwd"]
     # per-kernel times from the library's timing hook, over the same calls
     H.h2o_debug_timing(True)
     for _ in range(reps):
@@ -423,6 +446,7 @@ def main():
                    "bytes_per_step": dec["step_bytes"],
                    "frac_of_hbm_peak": round(dec["value"] / HBM_PEAK_GBS, 4)},
         "roofline": dec["roofline"],
+        "hot_mall": dec["hot_mall"],
         "cpu_baseline": cpu,
         "prefill": prefill,
         "insert_first": ins,

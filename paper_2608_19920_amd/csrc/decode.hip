@@ -497,22 +497,43 @@ struct HeadStats {
 // Without the chunk key (cache mode, has_chunk false) lnew is -inf, and a
 // query that sees no slot gets lam = +inf (every weight 0), linv = 0 and
 // lse = -inf.
-template <int D, int NT>
-__device__ __forceinline__ void head_stats(HeadStats& hs, const bf16_t* q, const bf16_t* kn,
-                                           const float2* dstat, int Hq, int Hkv, int G,
-                                           int nsplit, float c_log2, size_t bh, float* lse,
-                                           bool has_chunk = true) {
+// The loads (head_stats_load, for wave g < G) and the arithmetic
+// (head_stats_from) are separate so that a latency-bound kernel can issue the
+// loads together with its other early loads.
+template <int D>
+struct StatIn {
+  float2 st;                         // split `lane`'s (max, sum) of query head g
+  bf16_t qv[(D + 63) / 64], kv[(D + 63) / 64];   // elements lane, lane + 64 of q and k_new
+};
+template <int D>
+__device__ __forceinline__ void head_stats_load(StatIn<D>& in, const bf16_t* q, const bf16_t* kn,
+                                                const float2* dstat, int Hq, int Hkv, int G,
+                                                int nsplit, size_t bh, bool has_chunk) {
   const int b = (int)(bh / Hkv), h = (int)(bh % Hkv);
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  for (int g = wave; g < G; g += NT / 64) {
-    const float2 st = lane < nsplit ? dstat[(bh * nsplit + lane) * G + g]
-                                    : make_float2(-INFINITY, 0.f);
+  const int lane = threadIdx.x & 63, g = threadIdx.x >> 6;
+  in.st = lane < nsplit ? dstat[(bh * nsplit + lane) * G + g] : make_float2(-INFINITY, 0.f);
+#pragma unroll
+  for (int i = 0; i < (D + 63) / 64; ++i) {
+    const int dd = lane + 64 * i;
+    in.qv[i] = has_chunk && dd < D ? q[(size_t)(b * Hq + h * G + g) * D + dd] : (bf16_t)0;
+    in.kv[i] = has_chunk && dd < D ? kn[bh * D + dd] : (bf16_t)0;
+  }
+}
+template <int D, int NT>
+__device__ __forceinline__ void head_stats_from(HeadStats& hs, const StatIn<D>& in, int Hq,
+                                                int Hkv, int G, int nsplit, float c_log2,
+                                                size_t bh, float* lse, bool has_chunk) {
+  static_assert(NT / 64 >= kMaxG, "one wave per query head of the group");
+  const int b = (int)(bh / Hkv), h = (int)(bh % Hkv);
+  const int lane = threadIdx.x & 63, g = threadIdx.x >> 6;
+  if (g < G) {
+    const float2 st = in.st;
     float lnew = -INFINITY;
     if (has_chunk) {
       float a = 0.f;
-      for (int dd = lane; dd < D; dd += 64)
-        a = fmaf(bf16_to_f32(q[(size_t)(b * Hq + h * G + g) * D + dd]),
-                 bf16_to_f32(kn[bh * D + dd]), a);
+#pragma unroll
+      for (int i = 0; i < (D + 63) / 64; ++i)
+        if (lane + 64 * i < D) a = fmaf(bf16_to_f32(in.qv[i]), bf16_to_f32(in.kv[i]), a);
       a = wave_sum(a);
       lnew = a * c_log2;
     }
@@ -534,6 +555,16 @@ __device__ __forceinline__ void head_stats(HeadStats& hs, const bf16_t* q, const
     }
   }
   __syncthreads();
+}
+template <int D, int NT>
+__device__ __forceinline__ void head_stats(HeadStats& hs, const bf16_t* q, const bf16_t* kn,
+                                           const float2* dstat, int Hq, int Hkv, int G,
+                                           int nsplit, float c_log2, size_t bh, float* lse,
+                                           bool has_chunk = true) {
+  StatIn<D> in;
+  if ((int)(threadIdx.x >> 6) < G)
+    head_stats_load<D>(in, q, kn, dstat, Hq, Hkv, G, nsplit, bh, has_chunk);
+  head_stats_from<D, NT>(hs, in, Hq, Hkv, G, nsplit, c_log2, bh, lse, has_chunk);
 }
 
 // Output element c = g*D + dd of head bh: the chunk key's term plus the
@@ -622,11 +653,20 @@ __global__ __launch_bounds__(kCombThreads) void decode_combine(
 // (lower slot first among equal scores; -0 equals +0), and the insert of the
 // chunk's key, value, score wsum[M] and token position into that slot. Same
 // arithmetic as the combine, accumulate and argmin-insert kernels. The block
-// is latency-bound, so everything it reads (a pass of logits and scores, the
-// split statistics and O-partials, the chunk's key and value rows) is
-// requested before the first value is needed.
+// is latency-bound on 64 or so CUs: everything it reads (the logits and
+// scores of the first pass of slots, 16 bytes per load, the split
+// statistics and O-partials, the query and the chunk's key and value rows)
+// is requested before the first value is used; slot groups past the cache
+// do no arithmetic; and the slots of the last pass (the only pass at the
+// decode shapes) are stored only after the slot is chosen, so that the
+// chosen slot's score is written once, with its new value.
 constexpr int kFinThreads = 1024;
-constexpr int kFinCols = 8;   // slots per thread and pass
+constexpr int kFinVec = 4;                          // consecutive slots per thread and pass
+constexpr int kFinPass = kFinThreads * kFinVec;     // slots per pass
+
+__device__ __forceinline__ bool lex_less(uint32_t ka, uint32_t ja, uint32_t kb, uint32_t jb) {
+  return ka < kb || (ka == kb && ja < jb);
+}
 
 // With OUT false the block skips out and lse (written by decode_combine in
 // an attend call): the eviction half of the step.
@@ -638,32 +678,31 @@ __global__ __launch_bounds__(kFinThreads) void decode_finish(
     const float* __restrict__ dO, bf16_t* __restrict__ out, float* __restrict__ lse,
     float* __restrict__ wsum, float* __restrict__ scores, int32_t* __restrict__ token_pos,
     int32_t* __restrict__ evict_idx, int32_t pos0) {
-  constexpr int NT = kFinThreads, PASS = NT * kFinCols;
+  constexpr int NT = kFinThreads;
   __shared__ HeadStats hs;
   __shared__ uint32_t red_k[NT / 64], red_j[NT / 64];
-  __shared__ int sh_slot;
   const size_t bh = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int pitch = logit_pitch(M);
   float* w = wsum + bh * (size_t)(M + 1);
   float* sc = scores + bh * (size_t)M;
   const float* lgb = logits + bh * (size_t)G * pitch;
-  float lg[kFinCols][G], sv[kFinCols];
-  // One pass of slots: column groups wholly past the cache (a block-uniform
-  // test) are not loaded; in a ragged group the clamped slots are in bounds
-  // (M >= 1) and are not used.
+  const bool sc16 = (M & 3) == 0;     // score rows start 16-byte aligned
+  // This thread's slots of a pass are j0 .. j0 + 3, j0 = base + 4 * tid. A
+  // logit row is padded to a multiple of 4 slots, so a group that starts in
+  // the cache is read whole; its slots past the cache are not used.
+  f32x4 lg[G], sv;
   auto load_pass = [&](int base) {
+    const int j0 = base + kFinVec * tid;
+    if (j0 < M) {
 #pragma unroll
-    for (int u = 0; u < kFinCols; ++u) {
-      if (base + u * NT < M) {
-        const int j = min(base + u * NT + tid, M - 1);
-#pragma unroll
-        for (int g = 0; g < G; ++g) lg[u][g] = lgb[(size_t)g * pitch + j];
-        sv[u] = sc[j];
+      for (int g = 0; g < G; ++g)
+        lg[g] = *reinterpret_cast<const f32x4*>(lgb + (size_t)g * pitch + j0);
+      if (sc16) {
+        sv = *reinterpret_cast<const f32x4*>(sc + j0);
       } else {
 #pragma unroll
-        for (int g = 0; g < G; ++g) lg[u][g] = 0.f;
-        sv[u] = 0.f;
+        for (int r = 0; r < kFinVec; ++r) sv[r] = sc[min(j0 + r, M - 1)];
       }
     }
   };
@@ -674,59 +713,91 @@ __global__ __launch_bounds__(kFinThreads) void decode_finish(
     vrow = reinterpret_cast<const u4*>(vn + bh * (size_t)D)[tid];
   }
   // thread c < G*D owns output element c (G*D <= NT); its first kPre split
-  // partials come in with the other early loads
+  // partials come in with the other early loads, and so do the inputs of
+  // the head statistics
   constexpr int kPre = 16;
   float pre[kPre];
   const bool has_c = OUT && tid < G * D;
 #pragma unroll
   for (int s = 0; s < kPre; ++s)
     pre[s] = has_c && s < nsplit ? dO[(bh * nsplit + s) * (size_t)(G * D) + tid] : 0.f;
+  StatIn<D> sin;
+  if (wave < G) head_stats_load<D>(sin, q, kn, dstat, Hq, Hkv, G, nsplit, bh, true);
   load_pass(0);
-  head_stats<D, NT>(hs, q, kn, dstat, Hq, Hkv, G, nsplit, c_log2, bh, OUT ? lse : nullptr);
+  head_stats_from<D, NT>(hs, sin, Hq, Hkv, G, nsplit, c_log2, bh, OUT ? lse : nullptr, true);
   if (has_c) {
     const float v = out_elem<D, kPre>(hs, vn, dO, pre, G, nsplit, bh, tid);
     const int b = (int)(bh / Hkv), h = (int)(bh % Hkv);
     out[(size_t)(b * Hq + h * G) * D + tid] = f32_to_bf16(v);
   }
-  // slots visited in increasing order per thread: a strict < keeps the lowest
-  // slot among equal keys
+  // Passes in increasing slot order; a thread visits its slots in
+  // increasing order, so a strict < keeps the lowest slot among equal keys.
   uint32_t bk = 0xFFFFFFFFu, bj = 0xFFFFFFFFu;
-  for (int base = 0; base < M; base += PASS) {
-    if (base > 0) load_pass(base);
+  f32x4 wv, sa;
+  int base = 0;
+  for (;;) {
+    const int j0 = base + kFinVec * tid;
+    if (j0 < M) {
 #pragma unroll
-    for (int u = 0; u < kFinCols; ++u) {
-      const int j = base + u * NT + tid;
-      float wj = 0.f;
+      for (int r = 0; r < kFinVec; ++r) {
+        float wj = 0.f;
 #pragma unroll
-      for (int g = 0; g < G; ++g) wj += __builtin_amdgcn_exp2f(lg[u][g] - hs.lam[g]);
-      if (j < M) {
-        w[j] = wj;
-        const float s = sv[u] + wj;
-        sc[j] = s;
-        const uint32_t key = order_key(s);
-        if (key < bk) { bk = key; bj = (uint32_t)j; }
+        for (int g = 0; g < G; ++g) wj += __builtin_amdgcn_exp2f(lg[g][r] - hs.lam[g]);
+        wv[r] = wj;
+        sa[r] = sv[r] + wj;
+        const uint32_t key = order_key(sa[r]);
+        if (j0 + r < M && key < bk) { bk = key; bj = (uint32_t)(j0 + r); }
       }
     }
+    if (base + kFinPass >= M) break;   // the last pass is stored after the choice
+#pragma unroll
+    for (int r = 0; r < kFinVec; ++r)
+      if (j0 + r < M) {
+        w[j0 + r] = wv[r];
+        sc[j0 + r] = sa[r];
+      }
+    base += kFinPass;
+    load_pass(base);
   }
   wave_argmin(bk, bj);
   if (lane == 0) { red_k[wave] = bk; red_j[wave] = bj; }
   __syncthreads();
-  if (tid == 0) {
-    for (int v = 1; v < NT / 64; ++v)
-      if (red_k[v] < bk || (red_k[v] == bk && red_j[v] < bj)) { bk = red_k[v]; bj = red_j[v]; }
-    const int slot = (int)bj;
-    const float wnew = chunk_weight(hs, G);
-    w[M] = wnew;
-    sh_slot = slot;
-    evict_idx[bh] = slot;
-    if ((unsigned)slot < (unsigned)M) {
-      sc[slot] = wnew;
-      if (token_pos) token_pos[bh * M + slot] = pos0;
+  bk = red_k[0];
+  bj = red_j[0];
+#pragma unroll
+  for (int v = 1; v < NT / 64; ++v)
+    if (lex_less(red_k[v], red_j[v], bk, bj)) { bk = red_k[v]; bj = red_j[v]; }
+  const int slot = (int)bj;
+  const float wnew = chunk_weight(hs, G);
+  {
+    const int j0 = base + kFinVec * tid;
+#pragma unroll
+    for (int r = 0; r < kFinVec; ++r)
+      if (j0 + r < M) w[j0 + r] = wv[r];
+#pragma unroll
+    for (int r = 0; r < kFinVec; ++r)
+      if (j0 + r == slot) sa[r] = wnew;
+    if (sc16 && j0 < M) {
+      *reinterpret_cast<f32x4*>(sc + j0) = sa;
+    } else {
+#pragma unroll
+      for (int r = 0; r < kFinVec; ++r)
+        if (j0 + r < M) sc[j0 + r] = sa[r];
     }
   }
-  __syncthreads();
-  const int slot = sh_slot;
-  if ((unsigned)slot < (unsigned)M && tid < D / 8) {
+  if (slot < base) {
+    // (more than one pass) the slot's accumulated score was stored with an
+    // earlier pass: every thread's stores complete before it is replaced
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (tid == 0) sc[slot] = wnew;
+  }
+  if (tid == 0) {
+    w[M] = wnew;
+    evict_idx[bh] = slot;
+    if (token_pos) token_pos[bh * M + slot] = pos0;
+  }
+  if (tid < D / 8) {
     reinterpret_cast<u4*>(kc + (bh * M + slot) * (size_t)D)[tid] = krow;
     reinterpret_cast<u4*>(vc + (bh * M + slot) * (size_t)D)[tid] = vrow;
   }

@@ -202,6 +202,26 @@ int h2o_chunk_step(const void* q, void* k_cache, void* v_cache, float* scores,
                    int Hkv, int T, int M, int d, float scale, int32_t pos0,
                    int dtype, void* stream);
 
+/* h2o_chunk_step without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation). Arguments, results and errors are those
+ * of h2o_chunk_step (same kernels, same bits), with the scratch taken from a
+ * fixed array of h2o_noalloc_scratch_bytes() bytes (32 MiB) inside the
+ * library instead: one array per GPU the library runs on, held until the
+ * process ends. No call allocates or frees memory. A shape whose
+ * h2o_workspace_bytes() exceeds the array returns H2O_EWORKSPACE before
+ * anything is enqueued (the decode shape B8 Hq32 Hkv8 d64 M4096 needs about
+ * 8 MiB). Every call on one GPU shares that GPU's array, and the array keeps
+ * what the last call left there (no kernel reads it before writing it), so
+ * calls that can overlap on one GPU - different streams, host threads -
+ * race and must be ordered by the caller. */
+size_t h2o_noalloc_scratch_bytes(void);
+int h2o_chunk_step_noalloc(const void* q, void* k_cache, void* v_cache, float* scores,
+                           int32_t* token_pos, const void* k_new, const void* v_new, void* out,
+                           float* lse, float* wsum, int32_t* evict_idx, int B, int Hq, int Hkv,
+                           int T, int M, int d, float scale, int32_t pos0, int dtype,
+                           void* stream);
+
 /* ---- The paper's order of a chunk step: insert, then attend (Sec.
  * "Discussion: SDPA Kernels for Sparse Attention"). The chunk is written into
  * the cache first and the attention masks each slot by its token position:

@@ -422,6 +422,70 @@ int h2o_chunk_step(const void* q, void* k_cache, void* v_cache, float* scores,
                     pos0, dtype, stream);
 }
 
+}  // extern "C"
+
+namespace h2o {
+namespace {
+
+// Scratch of h2o_chunk_step_noalloc, in place of a caller's workspace: one
+// array on every device the library runs on, held until the process ends.
+// In host code `scratch` names a host-side stand-in, not device memory:
+// kernels get the address hipGetSymbolAddress returns for the current device.
+constexpr size_t kScratchBytes = size_t(32) << 20;
+static __device__ __align__(256) char scratch[kScratchBytes];
+
+// Device address of `scratch` on the current device, looked up on the first
+// call on that device (with it current) and kept.
+int scratch_address(void** out) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return fail(H2O_ENODEVICE, "hipGetDevice failed");
+  if (dev < 0 || dev >= 64) return fail(H2O_ENODEVICE, "device %d out of range", dev);
+  static std::mutex mu;
+  static void* addr[64] = {};
+  std::lock_guard<std::mutex> lk(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) {
+      (void)hipGetLastError();
+      return fail(H2O_ELAUNCH, "hipGetSymbolAddress(scratch) failed: %s", hipGetErrorString(e));
+    }
+    addr[dev] = p;
+  }
+  *out = addr[dev];
+  return H2O_OK;
+}
+
+}  // namespace
+}  // namespace h2o
+
+extern "C" {
+
+size_t h2o_noalloc_scratch_bytes(void) { return kScratchBytes; }
+
+int h2o_chunk_step_noalloc(const void* q, void* k_cache, void* v_cache, float* scores,
+                           int32_t* token_pos, const void* k_new, const void* v_new, void* out,
+                           float* lse, float* wsum, int32_t* evict_idx, int B, int Hq, int Hkv,
+                           int T, int M, int d, float scale, int32_t pos0, int dtype,
+                           void* stream) {
+  if (dtype != H2O_F32 && dtype != H2O_BF16) return fail(H2O_EDTYPE, "dtype %d unknown", dtype);
+  int rc = check_shape(B, Hq, Hkv, T, M, d);
+  if (rc) return rc;
+  const size_t need = make_plan(Shape{B, Hq, Hkv, T, M, d}, dtype).bytes;
+  if (need > kScratchBytes)
+    return fail(H2O_EWORKSPACE,
+                "this shape needs %zu bytes of scratch; h2o_chunk_step_noalloc has %zu "
+                "(use h2o_chunk_step with a workspace)", need, kScratchBytes);
+  rc = check_device();
+  if (rc) return rc;
+  void* ws = nullptr;
+  rc = scratch_address(&ws);
+  if (rc) return rc;
+  return chunk_step(STEP_ALL, q, k_cache, v_cache, scores, token_pos, k_new, v_new, out, lse,
+                    wsum, evict_idx, ws, kScratchBytes, B, Hq, Hkv, T, M, d, scale, pos0, dtype,
+                    stream);
+}
+
 int h2o_chunk_step_attend(const void* q, void* k_cache, void* v_cache, float* scores,
                           int32_t* token_pos, const void* k_new, const void* v_new, void* out,
                           float* lse, float* wsum, int32_t* evict_idx, void* workspace,

@@ -25,6 +25,7 @@ STATUS_NAMES = ["H2O_OK", "H2O_EINVAL", "H2O_ESHAPE", "H2O_EDTYPE", "H2O_EALIGN"
 EXPORTED = ["h2o_workspace_bytes", "h2o_sdpa_chunk", "h2o_accumulate_scores",
             "h2o_evict_insert", "h2o_evict_workspace_bytes", "h2o_evict_insert_policy",
             "h2o_chunk_step", "h2o_chunk_step_attend", "h2o_chunk_step_evict",
+            "h2o_noalloc_scratch_bytes", "h2o_chunk_step_noalloc",
             "h2o_cache_workspace_bytes", "h2o_sdpa_cache", "h2o_backward_workspace_bytes",
             "h2o_sdpa_chunk_backward", "h2o_kv_gather", "h2o_kv_scatter",
             "h2o_chunk_step_insert_first", "h2o_bottomk", "h2o_last_error", "h2o_debug_force_path",
@@ -77,6 +78,10 @@ def lib() -> ctypes.CDLL:
     for name in ("h2o_chunk_step_attend", "h2o_chunk_step_evict"):
         getattr(L, name).argtypes = L.h2o_chunk_step.argtypes
         getattr(L, name).restype = i
+    L.h2o_noalloc_scratch_bytes.argtypes = []
+    L.h2o_noalloc_scratch_bytes.restype = sz
+    L.h2o_chunk_step_noalloc.argtypes = [vp] * 11 + [i] * 6 + [f, ctypes.c_int32, i, vp]
+    L.h2o_chunk_step_noalloc.restype = i
     L.h2o_cache_workspace_bytes.argtypes = [i] * 8
     L.h2o_cache_workspace_bytes.restype = sz
     L.h2o_sdpa_cache.argtypes = [vp] * 8 + [sz] + [i] * 6 + [f, ctypes.c_int32, i, vp]
@@ -343,6 +348,32 @@ def h2o_sdpa_cache(q, k_cache, v_cache, token_pos, out, lse, wsum, workspace, po
         _dev(q, "q"), _dev(k_cache, "k_cache"), _dev(v_cache, "v_cache"),
         _dev(token_pos, "token_pos"), _dev(out, "out"), _dev(lse, "lse"), _dev(wsum, "wsum"),
         _dev(workspace, "workspace"), nbytes, B, Hq, Hkv, T, M, d, float(scale), int(pos0),
+        _dtype_code(q), _stream(stream)))
+
+
+def h2o_noalloc_scratch_bytes() -> int:
+    return int(lib().h2o_noalloc_scratch_bytes())
+
+
+def h2o_chunk_step_noalloc(q, k_cache, v_cache, scores, token_pos, k_new, v_new, out, lse, wsum,
+                           evict_idx, pos0: int, scale: Optional[float] = None,
+                           stream=None) -> None:
+    """h2o_chunk_step without a workspace: the library's own scratch array
+    (h2o_noalloc_scratch_bytes) serves instead; shapes as in h2o_chunk_step."""
+    B, Hq, T, d = q.shape
+    Hkv, M = k_cache.shape[1], k_cache.shape[2]
+    if tuple(wsum.shape) != (B, Hkv, M + T) or tuple(evict_idx.shape) != (B, Hkv, T) or \
+            tuple(scores.shape) != (B, Hkv, M) or tuple(out.shape) != (B, Hq, T, d) or \
+            tuple(k_new.shape) != (B, Hkv, T, d) or tuple(v_new.shape) != (B, Hkv, T, d) or \
+            tuple(lse.shape) != (B, Hq, T):
+        raise ValueError("shape mismatch")
+    if scale is None:
+        scale = d ** -0.5
+    _check(lib().h2o_chunk_step_noalloc(
+        _dev(q, "q"), _dev(k_cache, "k_cache"), _dev(v_cache, "v_cache"),
+        _dev(scores, "scores"), _dev(token_pos, "token_pos"), _dev(k_new, "k_new"),
+        _dev(v_new, "v_new"), _dev(out, "out"), _dev(lse, "lse"), _dev(wsum, "wsum"),
+        _dev(evict_idx, "evict_idx"), B, Hq, Hkv, T, M, d, float(scale), int(pos0),
         _dtype_code(q), _stream(stream)))
 
 

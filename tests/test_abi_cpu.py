@@ -179,6 +179,29 @@ def test_chunk_step_rejects(L, kw, code, fn):
     assert len(L.h2o_last_error()) > 0
 
 
+def _noalloc(L, **kw):
+    a = dict(q=P, kc=P, vc=P, sc=P, tp=P, kn=P, vn=P, out=P, lse=P, w=P, idx=P, B=1, Hq=4,
+             Hkv=2, T=4, M=16, d=64, scale=0.125, pos0=16, dt=1, st=None)
+    a.update(kw)
+    return L.h2o_chunk_step_noalloc(a["q"], a["kc"], a["vc"], a["sc"], a["tp"], a["kn"],
+                                    a["vn"], a["out"], a["lse"], a["w"], a["idx"], a["B"],
+                                    a["Hq"], a["Hkv"], a["T"], a["M"], a["d"], a["scale"],
+                                    a["pos0"], a["dt"], a["st"])
+
+
+def test_noalloc_scratch_limit(L):
+    """The allocation-free step has a fixed 32 MiB scratch array: a shape
+    whose workspace exceeds it (the long-cache shape needs 66 MiB) is refused
+    on the host before anything else; the decode shape fits."""
+    assert L.h2o_noalloc_scratch_bytes() == 32 << 20
+    assert L.h2o_workspace_bytes(4, 32, 8, 512, 32768, 128, 1) > 32 << 20
+    assert _noalloc(L, B=4, Hq=32, Hkv=8, T=512, M=32768, d=128) == H.H2O_EWORKSPACE
+    assert b"h2o_chunk_step_noalloc" in L.h2o_last_error()
+    assert L.h2o_workspace_bytes(8, 32, 8, 1, 4096, 64, 1) <= 32 << 20
+    assert _noalloc(L, dt=3) == H.H2O_EDTYPE
+    assert _noalloc(L, Hq=6, Hkv=4) == H.H2O_ESHAPE
+
+
 def _cache(L, **kw):
     a = dict(q=P, kc=P, vc=P, tp=P, out=P, lse=P, w=P, ws=P, wsb=1 << 40, B=1, Hq=4, Hkv=2, T=8,
              M=16, d=64, scale=0.125, pos0=100, dt=1, st=None)
@@ -337,6 +360,8 @@ def test_no_device_is_reported(L):
     assert L.h2o_kv_scatter(P, P, P, 1, 2, 16, 4, 64, 1, None) == H.H2O_ENODEVICE
     for pol in (0, 1, 2):
         assert _step_if(L, pol=pol) == H.H2O_ENODEVICE
+    assert _noalloc(L) == H.H2O_ENODEVICE
+    assert _noalloc(L, B=8, Hq=32, Hkv=8, T=1, M=4096, d=64) == H.H2O_ENODEVICE
 
 
 def test_binding_raises_typed_errors(L):

@@ -220,21 +220,25 @@ int check_sdpa(const void* q, const void* k_cache, const void* v_cache, const vo
   return H2O_OK;
 }
 
+// scores_acc (may be nullptr): scores to which the summed weights of the M
+// cache slots are added in the column-sum pass (not on the decode path, whose
+// T == 1 step has its own fused kernels).
 hipError_t launch_sdpa(const Shape& s, const Plan& p, int dtype, const void* q,
                        const void* k_cache, const void* v_cache, const void* k_new,
                        const void* v_new, void* out, float* lse, float* wsum, void* workspace,
-                       float scale, hipStream_t st, KeyPos kp = KeyPos{nullptr, 0}) {
+                       float scale, hipStream_t st, KeyPos kp = KeyPos{nullptr, 0},
+                       float* scores_acc = nullptr) {
   char* ws = reinterpret_cast<char*>(workspace);
   switch (p.path) {
     case 1:
       return launch_sdpa_mfma(s, p, q, k_cache, v_cache, k_new, v_new, out, lse, wsum, ws,
-                              scale, kp, st);
+                              scale, kp, st, scores_acc);
     case 2:
       return launch_sdpa_decode(s, p, q, k_cache, v_cache, k_new, v_new, out, lse, wsum, ws,
                                 scale, kp, st);
     default:
       return launch_sdpa_generic(s, p, dtype, q, k_cache, v_cache, k_new, v_new, out, lse,
-                                 wsum, ws, scale, kp, st);
+                                 wsum, ws, scale, kp, st, scores_acc);
   }
 }
 
@@ -387,11 +391,15 @@ int chunk_step(StepPart part, const void* q, void* k_cache, void* v_cache, float
                               evict_idx, pos0, ws, scale, st);
   } else {
     const int rows = B * Hkv, eb = dtype == H2O_F32 ? 4 : 2;
+    // the whole step adds the summed weights to the scores in the column-sum
+    // pass of the attention; the evict half (after an attend call) adds them
+    // on its own
     if (part != STEP_EVICT)
       e = launch_sdpa(s, p, dtype, q, k_cache, v_cache, k_new, v_new, out, lse, wsum, workspace,
-                      scale, st);
+                      scale, st, KeyPos{nullptr, 0}, part == STEP_ALL ? scores : nullptr);
     if (part != STEP_ATTEND) {
-      if (e == hipSuccess) e = launch_accumulate(scores, wsum, rows, M, T, st);
+      if (e == hipSuccess && part == STEP_EVICT)
+        e = launch_accumulate(scores, wsum, rows, M, T, st);
       if (e == hipSuccess && T == 1) {
         e = launch_argmin_insert(k_cache, v_cache, scores, scores, 0, token_pos, k_new, v_new,
                                  wsum, evict_idx, rows, M, T, d, pos0, eb, st);
@@ -657,9 +665,10 @@ int h2o_chunk_step_insert_first(const void* q, void* k_cache, void* v_cache, flo
     e = launch_sdpa_decode(s, p, q, k_cache, v_cache, nullptr, nullptr, out, lse, wsum, ws,
                            scale, KeyPos{token_pos, pos0}, st, scores);
   } else if (e == hipSuccess) {
+    // the attention over the cache adds the summed weights to the scores in
+    // its column-sum pass
     e = launch_sdpa(s, p, dtype, q, k_cache, v_cache, nullptr, nullptr, out, lse, wsum, ws,
-                    scale, st, KeyPos{token_pos, pos0});
-    if (e == hipSuccess) e = launch_accumulate(scores, wsum, B * Hkv, M, 0, st);
+                    scale, st, KeyPos{token_pos, pos0}, scores);
   }
   if (e != hipSuccess) return fail(H2O_ELAUNCH, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();

@@ -144,14 +144,18 @@ hipError_t launch_kernel(int kernel_id, F kern, dim3 grid, dim3 block, hipStream
 // Each returns hipSuccess or the launch error. They assume validated inputs.
 // In cache mode (s.cache_only) kn and vn are unused and kp holds the token
 // positions; in chunk mode kp.tp is nullptr.
+// scores_acc (may be nullptr): the scores the summed weights are added to in
+// the column-sum pass (a chunk step's accumulation, bits of the separate
+// accumulate kernel).
 hipError_t launch_sdpa_generic(const Shape& s, const Plan& p, int dtype, const void* q,
                                const void* kc, const void* vc, const void* kn,
                                const void* vn, void* out, float* lse, float* wsum,
-                               char* ws, float scale, KeyPos kp, hipStream_t st);
+                               char* ws, float scale, KeyPos kp, hipStream_t st,
+                               float* scores_acc = nullptr);
 hipError_t launch_sdpa_mfma(const Shape& s, const Plan& p, const void* q, const void* kc,
                             const void* vc, const void* kn, const void* vn, void* out,
                             float* lse, float* wsum, char* ws, float scale, KeyPos kp,
-                            hipStream_t st);
+                            hipStream_t st, float* scores_acc = nullptr);
 // scores_acc (cache mode only, may be nullptr): scores to which the summed
 // weights are added in the same pass (the accumulate of an insert-first step).
 hipError_t launch_sdpa_decode(const Shape& s, const Plan& p, const void* q, const void* kc,
@@ -185,8 +189,10 @@ hipError_t launch_decode_step_insert_first(const Shape& s, const Plan& p, const 
                                            const void* kn, const void* vn, void* out, float* lse,
                                            float* wsum, int32_t* evict_idx, int32_t pos0,
                                            char* ws, float scale, hipStream_t st);
+// scores_acc (may be nullptr): scores[bh][j] += wsum[bh][j] for j < M in the
+// same pass (a chunk step's accumulation).
 hipError_t launch_colsum_reduce(const Shape& s, const Plan& p, const float* parts,
-                                float* wsum, hipStream_t st);
+                                float* wsum, hipStream_t st, float* scores_acc = nullptr);
 hipError_t launch_accumulate(float* scores, const float* wsum, int rows, int M, int T,
                              hipStream_t st);
 hipError_t launch_bottomk(const float* scores, int rows, int M, int k, int32_t* idx,

@@ -6,15 +6,22 @@ namespace {
 
 // ------------------------------------------------------------ colsum reduce
 // wsum[bh][j] = sum over the partial slots p (in increasing p, so the result
-// is bitwise reproducible) whose rows can see column j.
+// is bitwise reproducible) whose rows can see column j. With scores
+// non-null, a chunk step's accumulation in the same pass: scores[bh][j] +=
+// wsum[bh][j] for j < M, one float32 addition of the stored value (the bits
+// of the separate accumulate kernel).
 __global__ __launch_bounds__(256) void colsum_reduce_kernel(const float* __restrict__ parts,
-                                                            float* __restrict__ wsum, int nparts,
+                                                            float* __restrict__ wsum,
+                                                            float* __restrict__ scores, int nparts,
                                                             int rows_per_part, int BH, int Nk,
                                                             int ld, int G, int T, int M,
                                                             int Tk) {
   const int j = blockIdx.x * blockDim.x + threadIdx.x;
   const int bh = blockIdx.y;
   if (j >= Nk) return;
+  // the score is requested with the partials, not after them
+  float* sc = scores && j < M ? scores + (size_t)bh * M + j : nullptr;
+  const float s_old = sc ? *sc : 0.f;
   // The partials that see column j are p0 .. nparts-1 (kv_end grows with
   // p): all of them for a cache column, and for chunk key i = j - M those
   // whose last row (r1 - 1) / G reaches i, i.e. (p + 1) * rows_per_part > i * G.
@@ -34,6 +41,7 @@ __global__ __launch_bounds__(256) void colsum_reduce_kernel(const float* __restr
   }
   for (; p < nparts; ++p, src += stride) s += src[0];
   wsum[(size_t)bh * Nk + j] = s;
+  if (sc) *sc = s_old + s;
 }
 
 // ---------------------------------------------------------------- accumulate
@@ -53,6 +61,8 @@ constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / 64;
 
 // Exclusive prefix sum over the block (thread order); also returns the total.
+__device__ __forceinline__ uint32_t umin(uint32_t a, uint32_t b) { return a < b ? a : b; }
+
 __device__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* tmp, uint32_t* total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   uint32_t x = v;
@@ -88,105 +98,189 @@ __device__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* tmp, uint32_t* to
 constexpr int kSelLdsMax = 32768;
 __device__ __forceinline__ int sel_lds_index(int j) { return j + (j >> 5); }
 
-// hist[bin] += 1 for every active lane. Lanes of a wave that share a bin are
-// counted with one atomic (the leading bins of a wave first, at most four
-// rounds; the rest add one each): the first radix passes put most keys of a
-// row into a few bins, where plain LDS atomics would serialise.
+// hist[bin] += 1 for every active lane: plain LDS atomics. With 12-bit
+// digits the keys of a row spread over many bins; measured on score rows,
+// aggregating the lanes of a wave that share a bin (ballots, readlane) cost
+// more than the conflicts it saves. A row of equal scores puts every lane of
+// a wave on one bin, which serialises those atomics but stays correct.
 __device__ __forceinline__ void hist_add(uint32_t* hist, uint32_t bin, bool active) {
-  const int lane = threadIdx.x & 63;
-  uint64_t pending = __ballot(active);
-#pragma unroll
-  for (int it = 0; it < 4 && pending; ++it) {
-    const int leader = __ffsll((unsigned long long)pending) - 1;
-    const uint32_t lb = __shfl(bin, leader, 64);
-    const uint64_t same = __ballot(((pending >> lane) & 1ull) && bin == lb);
-    if (lane == leader) atomicAdd(&hist[lb], (uint32_t)__popcll(same));
-    pending &= ~same;
-  }
-  if ((pending >> lane) & 1ull) atomicAdd(&hist[bin], 1u);
+  if (active) atomicAdd(&hist[bin], 1u);
 }
 
-// One block per row. Radix-select the k-th smallest key tau (8 bits per pass,
-// most significant first), then emit, in ascending slot order, every slot with
-// key < tau and the lowest-index (k - #less) slots with key == tau.
+// Radix digits of the 32-bit order key, most significant first.
+constexpr int kSelBins = 4096;
+constexpr int kSelShift[3] = {20, 8, 0};
+constexpr uint32_t kSelDigitMask[3] = {0xFFFu, 0xFFFu, 0xFFu};
+// A round of the block covers 4 consecutive slots per thread.
+constexpr int kSelRound = 4 * kSelThreads;
+constexpr int kSelChunkRounds = kSelLdsMax / kSelRound;   // rounds whose loads go out together
+
+// Given the histogram of the current digit, the bin that holds the krem-th
+// smallest key of the prefix, and the keys of the prefix below that bin:
+// every thread sums four consecutive bins, a block scan gives each thread
+// the count before its bins, and the one thread whose range holds the
+// krem-th key writes the extended prefix and the rest of krem. Ends synced.
+__device__ __forceinline__ void select_bin(const uint32_t* hist, uint32_t* tmp, int shift,
+                                           uint32_t prefix, uint32_t krem, uint32_t* sh_prefix,
+                                           uint32_t* sh_krem) {
+  const int t = threadIdx.x;
+  const uint32_t c0 = hist[4 * t], c1 = hist[4 * t + 1], c2 = hist[4 * t + 2],
+                 c3 = hist[4 * t + 3];
+  const uint32_t c = c0 + c1 + c2 + c3;
+  uint32_t total;
+  const uint32_t before = block_exclusive_scan(c, tmp, &total);
+  if (before < krem && before + c >= krem) {
+    uint32_t b = before, bin = 4u * t;
+    if (b + c0 < krem) { b += c0; ++bin;
+      if (b + c1 < krem) { b += c1; ++bin;
+        if (b + c2 < krem) { b += c2; ++bin; } } }
+    *sh_prefix = prefix | (bin << shift);
+    *sh_krem = krem - b;
+  }
+  __syncthreads();
+}
+
+// The four scores of a thread in round r of a chunk: slots base + r *
+// kSelRound + 4 * t .. + 3 (16-byte loads where the row allows; slots past
+// the row read as +inf and are not used).
+__device__ __forceinline__ float4 load4(const float* s, int M, int j) {
+  if (j + 3 < M && ((reinterpret_cast<uintptr_t>(s + j) & 15u) == 0))
+    return *reinterpret_cast<const float4*>(s + j);
+  float4 v;
+  v.x = j < M ? s[j] : INFINITY;
+  v.y = j + 1 < M ? s[j + 1] : INFINITY;
+  v.z = j + 2 < M ? s[j + 2] : INFINITY;
+  v.w = j + 3 < M ? s[j + 3] : INFINITY;
+  return v;
+}
+
+// One block per row. Radix-select the k-th smallest key tau (digits of 12,
+// 12 and 8 bits, most significant first; the first digit's histogram is
+// taken while the row is staged), then emit, in ascending slot order, every
+// slot with key < tau and the lowest-index (k - #less) slots with key == tau.
+// Rows of up to kSelLdsMax slots are staged in LDS; longer rows are read
+// from global memory in every pass. Every loop over the row takes rounds of
+// the whole block (uniform trip counts: hist_add is a wave-level operation)
+// with 4 slots per thread, so a thread has 4 independent reads in flight.
 template <bool LDS>
 __global__ __launch_bounds__(kSelThreads) void bottomk_kernel(const float* __restrict__ scores,
                                                               int M, int k,
                                                               int32_t* __restrict__ idx) {
+  static_assert(kSelBins == 4 * kSelThreads, "four bins per thread in select_bin");
   __shared__ uint32_t keys[LDS ? kSelLdsMax + kSelLdsMax / 32 : 1];
-  __shared__ uint32_t hist[256];
+  __shared__ uint32_t hist[kSelBins];
   __shared__ uint32_t tmp[2 * kSelWaves + 1];
   __shared__ uint32_t sh_prefix, sh_krem;
   const float* s = scores + (size_t)blockIdx.x * M;
   int32_t* out = idx + (size_t)blockIdx.x * k;
   if (k <= 0) return;
-  if (LDS) {
-    for (int j = threadIdx.x; j < M; j += kSelThreads) keys[sel_lds_index(j)] = order_key(s[j]);
-  }
+  const int t4 = 4 * (int)threadIdx.x;
   auto key_at = [&](int j) { return LDS ? keys[sel_lds_index(j)] : order_key(s[j]); };
-  uint32_t prefix = 0, mask = 0, krem = (uint32_t)k;
-  for (int shift = 24; shift >= 0; shift -= 8) {
-    for (int b = threadIdx.x; b < 256; b += kSelThreads) hist[b] = 0u;
-    __syncthreads();
-    // rounds of the whole block (the trip count is uniform: hist_add is a
-    // wave-level operation)
-    for (int j0 = 0; j0 < M; j0 += kSelThreads) {
-      const int j = j0 + (int)threadIdx.x;
-      const uint32_t key = j < M ? key_at(j) : 0u;
-      hist_add(hist, (key >> shift) & 255u, j < M && (key & mask) == prefix);
-    }
-    __syncthreads();
-    if (threadIdx.x < 64) {
-      const int lane = threadIdx.x;
-      const uint32_t c0 = hist[4 * lane], c1 = hist[4 * lane + 1], c2 = hist[4 * lane + 2],
-                     c3 = hist[4 * lane + 3];
-      const uint32_t c = c0 + c1 + c2 + c3;
-      uint32_t inc = c;
+  for (int b = threadIdx.x; b < kSelBins; b += kSelThreads) hist[b] = 0u;
+  __syncthreads();
+  // first digit while the keys are staged: the loads of a chunk of rounds
+  // (the whole row when it fits LDS) are issued before their keys are used
+  for (int base = 0; base < M; base += kSelLdsMax) {
+    float4 v[kSelChunkRounds];
 #pragma unroll
-      for (int o = 1; o < 64; o <<= 1) {
-        uint32_t y = __shfl_up(inc, o, 64);
-        if (lane >= o) inc += y;
-      }
-      const uint32_t exc = inc - c;
-      // the lane whose range holds the krem-th element
-      const unsigned long long hit = __ballot(inc >= krem && exc < krem);
-      const int src = __ffsll(hit) - 1;
-      if (lane == src) {
-        uint32_t before = exc, bin = 4u * lane;
-        if (before + c0 < krem) { before += c0; ++bin;
-          if (before + c1 < krem) { before += c1; ++bin;
-            if (before + c2 < krem) { before += c2; ++bin; } } }
-        sh_prefix = prefix | (bin << shift);
-        sh_krem = krem - before;
+    for (int r = 0; r < kSelChunkRounds; ++r)
+      if (base + r * kSelRound < M) v[r] = load4(s, M, base + r * kSelRound + t4);
+#pragma unroll
+    for (int r = 0; r < kSelChunkRounds; ++r) {
+      if (base + r * kSelRound >= M) break;   // uniform
+      const float f[4] = {v[r].x, v[r].y, v[r].z, v[r].w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int j = base + r * kSelRound + t4 + e;
+        const uint32_t key = order_key(f[e]);
+        if (LDS && j < M) keys[sel_lds_index(j)] = key;
+        hist_add(hist, key >> kSelShift[0], j < M);
       }
     }
+  }
+  __syncthreads();
+  select_bin(hist, tmp, kSelShift[0], 0u, (uint32_t)k, &sh_prefix, &sh_krem);
+  uint32_t prefix = sh_prefix, krem = sh_krem;
+  uint32_t mask = kSelDigitMask[0] << kSelShift[0];
+#pragma unroll
+  for (int d = 1; d < 3; ++d) {
+    for (int b = threadIdx.x; b < kSelBins; b += kSelThreads) hist[b] = 0u;
     __syncthreads();
+    for (int j0 = 0; j0 < M; j0 += kSelRound) {
+      uint32_t kk[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int j = j0 + t4 + e;
+        kk[e] = j < M ? key_at(j) : 0u;
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        hist_add(hist, (kk[e] >> kSelShift[d]) & kSelDigitMask[d],
+                 j0 + t4 + e < M && (kk[e] & mask) == prefix);
+    }
+    __syncthreads();
+    select_bin(hist, tmp, kSelShift[d], prefix, krem, &sh_prefix, &sh_krem);
     prefix = sh_prefix;
     krem = sh_krem;
-    mask |= 255u << shift;
-    __syncthreads();
+    mask |= kSelDigitMask[d] << kSelShift[d];
   }
   const uint32_t tau = prefix, need_eq = krem;
-  // Compaction in slot order: thread t owns the contiguous chunk [t*C, (t+1)*C).
+  // Compaction in slot order: thread t owns the contiguous chunk [t*C,
+  // (t+1)*C). The slots of a chunk below tau come first in it, and the keys
+  // equal to tau of lowest slot are taken first, so a thread writes at
+  //   (slots below tau in earlier chunks) + min(keys equal to tau in earlier
+  //   chunks, need_eq)
+  // - one block scan of both counts, packed in 16-bit halves when the row is
+  // shorter than 65536 slots. Chunks of at most 32 slots keep the slots
+  // below and equal to tau as bit masks, so the emit does not read the keys
+  // again.
   const int C = (M + kSelThreads - 1) / kSelThreads;
   const int j0 = min(M, (int)threadIdx.x * C), j1 = min(M, j0 + C);
-  uint32_t n_less = 0, n_eq = 0;
+  const bool masks = C <= 32;
+  uint32_t n_less = 0, n_eq = 0, lt_mask = 0, eq_mask = 0;
+#pragma unroll 4
   for (int j = j0; j < j1; ++j) {
     const uint32_t key = key_at(j);
-    n_less += key < tau;
-    n_eq += key == tau;
+    const uint32_t bit = 1u << ((j - j0) & 31);
+    if (key < tau) { ++n_less; lt_mask |= bit; }
+    if (key == tau) { ++n_eq; eq_mask |= bit; }
   }
-  uint32_t tot;
-  const uint32_t eq_before = block_exclusive_scan(n_eq, tmp, &tot);
-  uint32_t take_eq = 0;
-  if (eq_before < need_eq) take_eq = min(n_eq, need_eq - eq_before);
-  const uint32_t pos = block_exclusive_scan(n_less + take_eq, tmp, &tot);
-  uint32_t w = pos, eq_seen = 0;
-  for (int j = j0; j < j1; ++j) {
-    const uint32_t key = key_at(j);
-    bool sel = key < tau;
-    if (key == tau) { sel = eq_seen < take_eq; ++eq_seen; }
-    if (sel && w < (uint32_t)k) out[w++] = j;
+  uint32_t tot, less_before, eq_before;
+  if (M < 65536) {
+    const uint32_t both = block_exclusive_scan(n_less | (n_eq << 16), tmp, &tot);
+    less_before = both & 0xFFFFu;
+    eq_before = both >> 16;
+  } else {
+    less_before = block_exclusive_scan(n_less, tmp, &tot);
+    eq_before = block_exclusive_scan(n_eq, tmp, &tot);
+  }
+  // keys equal to tau taken before this chunk, and by it (the difference
+  // need_eq - eq_taken never wraps, so no guarded subtraction is needed: a
+  // guarded one let the optimiser drop the cap below)
+  const uint32_t eq_taken = umin(eq_before, need_eq);
+  const uint32_t take_eq = umin(n_eq, need_eq - eq_taken);
+  uint32_t w = less_before + eq_taken;
+  if (masks) {
+    // the lowest take_eq bits of eq_mask
+    uint32_t em = eq_mask, sel = lt_mask;
+    for (uint32_t i = 0; i < take_eq; ++i) {
+      const uint32_t low = em & (0u - em);
+      sel |= low;
+      em ^= low;
+    }
+    while (sel) {
+      const int b = __ffs((int)sel) - 1;
+      sel &= sel - 1;
+      if (w < (uint32_t)k) out[w++] = j0 + b;
+    }
+  } else {
+    uint32_t eq_seen = 0;
+    for (int j = j0; j < j1; ++j) {
+      const uint32_t key = key_at(j);
+      bool sel = key < tau;
+      if (key == tau) { sel = eq_seen < take_eq; ++eq_seen; }
+      if (sel && w < (uint32_t)k) out[w++] = j;
+    }
   }
 }
 
@@ -363,10 +457,10 @@ hipError_t launch_broadcast_rows(const int32_t* src, int32_t* dst, int B, int n,
 }
 
 hipError_t launch_colsum_reduce(const Shape& s, const Plan& p, const float* parts, float* wsum,
-                                hipStream_t st) {
+                                hipStream_t st, float* scores_acc) {
   dim3 grid((s.Nk() + 255) / 256, s.BH());
   return launch_kernel(K_COLSUM_REDUCE, colsum_reduce_kernel, grid, dim3(256), st, parts, wsum,
-                       p.nparts, p.rows_per_part, s.BH(), s.Nk(), p.parts_ld, s.G(), s.T, s.M,
+                       scores_acc, p.nparts, p.rows_per_part, s.BH(), s.Nk(), p.parts_ld, s.G(), s.T, s.M,
                        s.Tk());
 }
 

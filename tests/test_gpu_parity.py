@@ -123,8 +123,11 @@ def test_tiny_f32_full_step():
 @pytest.mark.parametrize("rows,M,k,quant", [
     (1, 1, 1, None), (3, 10, 10, None), (4, 300, 64, None), (4, 300, 64, 2),
     (8, 8192, 1024, None), (8, 8192, 1024, 3), (2, 16384, 2048, 0), (64, 4096, 1, None),
-    (64, 4096, 1, 0), (5, 33, 32, 1), (2, 32768, 512, None), (3, 4097, 4096, 5)])
+    (64, 4096, 1, 0), (5, 33, 32, 1), (2, 32768, 512, None), (3, 4097, 4096, 5),
+    (32, 32768, 512, 8), (2, 40000, 300, None), (1, 65537, 5000, 2), (1, 50000, 50000, 0)])
 def test_bottomk_exact(rows, M, k, quant):
+    """Rows past 32768 slots take the kernel that reads the keys from global
+    memory in every pass; quantised scores force ties at the k-th key."""
     say(f"bottomk rows {rows} M {M} k {k} quant {quant}")
     rng = np.random.default_rng(rows * M + k)
     s = rng.standard_exponential((rows, M)).astype(np.float32)

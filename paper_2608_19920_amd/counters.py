@@ -9,7 +9,8 @@ dispatch:
     decode   one token step (h2o_chunk_step, B8 Hq32 Hkv8 d64 M4096, bf16) on
              each of 8 layer states, 3 times over, so every launch streams
              its cache from HBM
-    prefill  the chunked-prefill attention of one prefill workload (bf16)
+    prefill  the chunk step (attention, accumulate, evict, insert) of one
+             chunked-prefill workload (bf16)
     copy     a plain device-to-device copy of 1 GiB, the calibration: its
              algorithmic traffic is exactly 1 GiB read and 1 GiB written
 
@@ -38,6 +39,9 @@ KERNELS = {
     "decode_finish": ("decode_finish<", ["decode.hip"]),
     "mfma_lse": ("lse_pass<", ["sdpa_mfma.hip"]),
     "mfma_main": ("main_pass<", ["sdpa_mfma.hip"]),
+    "colsum_reduce": ("colsum_reduce_kernel", ["select.hip"]),
+    "bottomk": ("bottomk_kernel<", ["select.hip"]),
+    "insert": ("insert_kernel", ["select.hip"]),
 }
 
 
@@ -85,11 +89,7 @@ def _run(what: str, workload: str) -> None:
     torch.cuda.synchronize()
     for _ in range(3 if what == "decode" else 2):
         for st, q, kn, vn, pos0, scale, bufs in states:
-            if what == "decode":
-                H.step(st, q, kn, vn, bufs, pos0, scale)
-            else:
-                H.h2o_sdpa_chunk(q, st["k_cache"], st["v_cache"], kn, vn, bufs["out"],
-                                 bufs["lse"], bufs["wsum"], bufs["workspace"], scale)
+            H.step(st, q, kn, vn, bufs, pos0, scale)
     torch.cuda.synchronize()
     print(f"{what} {w.describe()}: done", flush=True)
 

@@ -319,6 +319,9 @@ STEP_SHAPES = [  # B, Hq, Hkv, d, M, T, dtype
     (1, 4, 2, 64, 256, 64, "f32"),
     (1, 8, 2, 128, 300, 70, "bf16"),
     (2, 4, 2, 64, 500, 1, "f32"),
+    (1, 4, 1, 64, 40000, 300, "bf16"),   # rows longer than the selection stages in LDS
+    (40, 4, 4, 64, 96, 33, "bf16"),      # 160 rows: one block per row in the fused selection
+    (1, 4, 1, 64, 4500, 4200, "bf16"),   # k above the fused selection's limit: separate kernels
 ]
 
 

@@ -220,7 +220,7 @@ def bench_prefill(name, args, torch, H, W):
     torch.cuda.synchronize()
     kt = {k: H.h2o_debug_kernel_time(k) for k in
           ("mfma_lse", "mfma_main", "split_reduce", "colsum_reduce", "accumulate", "bottomk",
-           "insert")}
+           "insert", "bottomk_insert")}
     H.h2o_debug_timing(False)
     Wf = attention_flops(w)
     tf = Wf / (ms * 1e-3) / 1e12

@@ -354,7 +354,8 @@ int h2o_debug_force_path(int path);
  *  13 score-variant keys and index broadcast (h2o_evict_insert_policy)
  *  14 backward dQ (VALU: and the rows' D)  15 backward dK/dV
  *  16 KV gather / scatter   17 backward rows' D (MFMA path)
- *  18 backward dQ split reduce (MFMA path) */
+ *  18 backward dQ split reduce (MFMA path)
+ *  19 bottom-k and insert in one launch (h2o_chunk_step, 1 < T <= 4096) */
 int h2o_debug_timing(int on);
 int h2o_debug_kernel_time(int kernel_id, double* total_ms, long* count);
 

@@ -41,6 +41,7 @@ KERNELS = {
     "mfma_main": ("main_pass<", ["sdpa_mfma.hip"]),
     "colsum_reduce": ("colsum_reduce_kernel", ["select.hip"]),
     "bottomk": ("bottomk_kernel<", ["select.hip"]),
+    "bottomk_insert": ("bottomk_insert_kernel<", ["select.hip"]),
     "insert": ("insert_kernel", ["select.hip"]),
 }
 

@@ -183,6 +183,8 @@ Plan make_plan(const Shape& s, int dtype) {
   p.off_opart = off;
   if (p.nsplit > 1) off = align256(off + (size_t)p.nsplit * BH * R * s.d * sizeof(float));
   p.off_logits = off;
+  p.off_keys = off;
+  off = align256(off + BH * (size_t)s.M * sizeof(float));
   p.bytes = off;
   return p;
 }
@@ -220,25 +222,25 @@ int check_sdpa(const void* q, const void* k_cache, const void* v_cache, const vo
   return H2O_OK;
 }
 
-// scores_acc (may be nullptr): scores to which the summed weights of the M
-// cache slots are added in the column-sum pass (not on the decode path, whose
+// acc: the scores to which the summed weights of the M cache slots are added
+// in the column-sum pass, with an optional copy (not on the decode path, whose
 // T == 1 step has its own fused kernels).
 hipError_t launch_sdpa(const Shape& s, const Plan& p, int dtype, const void* q,
                        const void* k_cache, const void* v_cache, const void* k_new,
                        const void* v_new, void* out, float* lse, float* wsum, void* workspace,
                        float scale, hipStream_t st, KeyPos kp = KeyPos{nullptr, 0},
-                       float* scores_acc = nullptr) {
+                       ScoreAcc acc = ScoreAcc{}) {
   char* ws = reinterpret_cast<char*>(workspace);
   switch (p.path) {
     case 1:
       return launch_sdpa_mfma(s, p, q, k_cache, v_cache, k_new, v_new, out, lse, wsum, ws,
-                              scale, kp, st, scores_acc);
+                              scale, kp, st, acc);
     case 2:
       return launch_sdpa_decode(s, p, q, k_cache, v_cache, k_new, v_new, out, lse, wsum, ws,
                                 scale, kp, st);
     default:
       return launch_sdpa_generic(s, p, dtype, q, k_cache, v_cache, k_new, v_new, out, lse,
-                                 wsum, ws, scale, kp, st, scores_acc);
+                                 wsum, ws, scale, kp, st, acc);
   }
 }
 
@@ -391,18 +393,26 @@ int chunk_step(StepPart part, const void* q, void* k_cache, void* v_cache, float
                               evict_idx, pos0, ws, scale, st);
   } else {
     const int rows = B * Hkv, eb = dtype == H2O_F32 ? 4 : 2;
-    // the whole step adds the summed weights to the scores in the column-sum
-    // pass of the attention; the evict half (after an attend call) adds them
-    // on its own
+    // The whole step adds the summed weights to the scores in the column-sum
+    // pass of the attention, which also leaves a copy of the accumulated
+    // scores in the workspace for a selection and insert in one launch (the
+    // copy is ranked, the scores are written). The evict half (after an
+    // attend call) adds them on its own.
+    const bool fused = part == STEP_ALL && T > 1 && bottomk_insert_supported(T);
+    float* keys = reinterpret_cast<float*>(ws + p.off_keys);
     if (part != STEP_EVICT)
       e = launch_sdpa(s, p, dtype, q, k_cache, v_cache, k_new, v_new, out, lse, wsum, workspace,
-                      scale, st, KeyPos{nullptr, 0}, part == STEP_ALL ? scores : nullptr);
+                      scale, st, KeyPos{nullptr, 0},
+                      ScoreAcc{part == STEP_ALL ? scores : nullptr, fused ? keys : nullptr});
     if (part != STEP_ATTEND) {
       if (e == hipSuccess && part == STEP_EVICT)
         e = launch_accumulate(scores, wsum, rows, M, T, st);
       if (e == hipSuccess && T == 1) {
         e = launch_argmin_insert(k_cache, v_cache, scores, scores, 0, token_pos, k_new, v_new,
                                  wsum, evict_idx, rows, M, T, d, pos0, eb, st);
+      } else if (e == hipSuccess && fused) {
+        e = launch_bottomk_insert(keys, scores, token_pos, k_cache, v_cache, k_new, v_new, wsum,
+                                  evict_idx, rows, M, T, d, T, pos0, eb, st);
       } else if (e == hipSuccess) {
         e = launch_bottomk(scores, rows, M, T, evict_idx, st);
         if (e == hipSuccess)
@@ -668,7 +678,7 @@ int h2o_chunk_step_insert_first(const void* q, void* k_cache, void* v_cache, flo
     // the attention over the cache adds the summed weights to the scores in
     // its column-sum pass
     e = launch_sdpa(s, p, dtype, q, k_cache, v_cache, nullptr, nullptr, out, lse, wsum, ws,
-                    scale, st, KeyPos{token_pos, pos0}, scores);
+                    scale, st, KeyPos{token_pos, pos0}, ScoreAcc{scores, nullptr});
   }
   if (e != hipSuccess) return fail(H2O_ELAUNCH, "kernel launch failed: %s", hipGetErrorString(e));
   return ok();

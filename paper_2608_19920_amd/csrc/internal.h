@@ -69,6 +69,16 @@ struct KeyPos {
   int32_t pos0;
 };
 
+// The H2O score accumulation a column-sum pass can carry out for a chunk
+// step (Eq. h2o-score): scores[bh][j] += wsum[bh][j] for the M cache slots,
+// and, with copy non-null, the accumulated value also written to
+// copy[bh][j] (the ranking input of the fused selection, which must not
+// change while that kernel runs). scores null: no accumulation.
+struct ScoreAcc {
+  float* scores = nullptr;
+  float* copy = nullptr;
+};
+
 // Packed row r of a KV head is (chunk position i = r / G, group member g = r % G).
 // In chunk mode the keys a chunk position i may see are columns [0, M + i + 1).
 // A partial-sum slot that covers packed rows [r0, r1) therefore sees key
@@ -103,6 +113,7 @@ struct Plan {
   size_t off_parts;    // float colsum partials [nparts][BH][Nk]; decode: 1 KiB store sink
   size_t off_opart;    // float O partials [nsplit][BH][R][d] (nsplit > 1)
   size_t off_logits;   // decode: float logits [BH][G][Nk]
+  size_t off_keys;     // float accumulated scores [BH][M], the ranking copy of a chunk step
   size_t bytes;
 };
 Plan make_plan(const Shape& s, int dtype);
@@ -116,7 +127,8 @@ bool decode_supports(int d, int G);   // (d, G) pairs the decode kernels handle
 enum KernelId {
   K_GENERIC_LSE = 0, K_GENERIC_MAIN, K_MFMA_LSE, K_MFMA_MAIN, K_SPLIT_REDUCE, K_COLSUM_REDUCE,
   K_ACCUMULATE, K_BOTTOMK, K_INSERT, K_DECODE_SPLIT, K_DECODE_COMBINE, K_ARGMIN_INSERT,
-  K_DECODE_FINISH, K_KEYS, K_BWD_DQ, K_BWD_DKDV, K_KV_COPY, K_BWD_DOT, K_BWD_DQ_REDUCE, K_COUNT
+  K_DECODE_FINISH, K_KEYS, K_BWD_DQ, K_BWD_DKDV, K_KV_COPY, K_BWD_DOT, K_BWD_DQ_REDUCE,
+  K_BOTTOMK_INSERT, K_COUNT
 };
 // While timing is switched on (h2o_debug_timing), kernels go out through
 // hipExtLaunchKernel with a start and a stop event: the runtime stamps them
@@ -144,18 +156,17 @@ hipError_t launch_kernel(int kernel_id, F kern, dim3 grid, dim3 block, hipStream
 // Each returns hipSuccess or the launch error. They assume validated inputs.
 // In cache mode (s.cache_only) kn and vn are unused and kp holds the token
 // positions; in chunk mode kp.tp is nullptr.
-// scores_acc (may be nullptr): the scores the summed weights are added to in
-// the column-sum pass (a chunk step's accumulation, bits of the separate
-// accumulate kernel).
+// acc: the score accumulation of a chunk step, done in the column-sum pass
+// (the bits of the separate accumulate kernel); none by default.
 hipError_t launch_sdpa_generic(const Shape& s, const Plan& p, int dtype, const void* q,
                                const void* kc, const void* vc, const void* kn,
                                const void* vn, void* out, float* lse, float* wsum,
                                char* ws, float scale, KeyPos kp, hipStream_t st,
-                               float* scores_acc = nullptr);
+                               ScoreAcc acc = ScoreAcc{});
 hipError_t launch_sdpa_mfma(const Shape& s, const Plan& p, const void* q, const void* kc,
                             const void* vc, const void* kn, const void* vn, void* out,
                             float* lse, float* wsum, char* ws, float scale, KeyPos kp,
-                            hipStream_t st, float* scores_acc = nullptr);
+                            hipStream_t st, ScoreAcc acc = ScoreAcc{});
 // scores_acc (cache mode only, may be nullptr): scores to which the summed
 // weights are added in the same pass (the accumulate of an insert-first step).
 hipError_t launch_sdpa_decode(const Shape& s, const Plan& p, const void* q, const void* kc,
@@ -189,14 +200,22 @@ hipError_t launch_decode_step_insert_first(const Shape& s, const Plan& p, const 
                                            const void* kn, const void* vn, void* out, float* lse,
                                            float* wsum, int32_t* evict_idx, int32_t pos0,
                                            char* ws, float scale, hipStream_t st);
-// scores_acc (may be nullptr): scores[bh][j] += wsum[bh][j] for j < M in the
-// same pass (a chunk step's accumulation).
+// acc: scores[bh][j] += wsum[bh][j] for j < M in the same pass (a chunk
+// step's accumulation), with the optional copy.
 hipError_t launch_colsum_reduce(const Shape& s, const Plan& p, const float* parts,
-                                float* wsum, hipStream_t st, float* scores_acc = nullptr);
+                                float* wsum, hipStream_t st, ScoreAcc acc = ScoreAcc{});
 hipError_t launch_accumulate(float* scores, const float* wsum, int rows, int M, int T,
                              hipStream_t st);
 hipError_t launch_bottomk(const float* scores, int rows, int M, int k, int32_t* idx,
                           hipStream_t st);
+// Bottom-k of keys (row pitch M; not written while the kernel runs, and
+// another array than scores) and the insert of the chunk (as launch_insert)
+// in one launch, for the k that bottomk_insert_supported() accepts.
+bool bottomk_insert_supported(int k);
+hipError_t launch_bottomk_insert(const float* keys, float* scores, int32_t* token_pos, void* kc,
+                                 void* vc, const void* kn, const void* vn, const float* wsum,
+                                 int32_t* idx, int rows, int M, int T, int d, int k,
+                                 int32_t pos0, int elem_bytes, hipStream_t st);
 hipError_t launch_argmin_insert(void* kc, void* vc, float* scores, const float* keys,
                                 int key_rows, int32_t* token_pos, const void* kn, const void* vn,
                                 const float* wsum, int32_t* idx, int rows, int M, int T, int d,

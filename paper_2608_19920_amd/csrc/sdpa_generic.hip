@@ -155,7 +155,7 @@ __global__ __launch_bounds__(kRows) void pass_b(const E* __restrict__ q, const E
 template <typename E, int D>
 hipError_t run(const Shape& s, const Plan& p, const void* q, const void* kc, const void* vc,
                const void* kn, const void* vn, void* out, float* lse, float* wsum, char* ws,
-               float scale, KeyPos kp, hipStream_t st, float* scores_acc) {
+               float scale, KeyPos kp, hipStream_t st, ScoreAcc acc) {
   dim3 grid((s.R() + kRows - 1) / kRows, s.BH());
   float* lse_ws = reinterpret_cast<float*>(ws + p.off_stats);
   float* parts = reinterpret_cast<float*>(ws + p.off_parts);
@@ -167,7 +167,7 @@ hipError_t run(const Shape& s, const Plan& p, const void* q, const void* kc, con
                     (const E*)kc, (const E*)vc, (const E*)kn, (const E*)vn, (E*)out,
                     (const float*)lse_ws, parts, s.Hq, s.Hkv, s.T, s.M, s.Tk(), scale, kp);
   if (e != hipSuccess) return e;
-  return launch_colsum_reduce(s, p, parts, wsum, st, scores_acc);
+  return launch_colsum_reduce(s, p, parts, wsum, st, acc);
 }
 
 }  // namespace
@@ -175,9 +175,9 @@ hipError_t run(const Shape& s, const Plan& p, const void* q, const void* kc, con
 hipError_t launch_sdpa_generic(const Shape& s, const Plan& p, int dtype, const void* q,
                                const void* kc, const void* vc, const void* kn, const void* vn,
                                void* out, float* lse, float* wsum, char* ws, float scale,
-                               KeyPos kp, hipStream_t st, float* scores_acc) {
+                               KeyPos kp, hipStream_t st, ScoreAcc acc) {
   auto go = [&](auto run_fn) {
-    return run_fn(s, p, q, kc, vc, kn, vn, out, lse, wsum, ws, scale, kp, st, scores_acc);
+    return run_fn(s, p, q, kc, vc, kn, vn, out, lse, wsum, ws, scale, kp, st, acc);
   };
   if (dtype == 0) return s.d == 64 ? go(run<float, 64>) : go(run<float, 128>);
   return s.d == 64 ? go(run<bf16_t, 64>) : go(run<bf16_t, 128>);

@@ -783,7 +783,7 @@ static_assert(kLseWaves * kLseQB == kMainWaves * kMainQB, "one row tiling");
 template <int D>
 hipError_t run(const Shape& s, const Plan& p, const void* q, const void* kc, const void* vc,
                const void* kn, const void* vn, void* out, float* lse, float* wsum, char* ws,
-               float scale, KeyPos kp, hipStream_t st, float* scores_acc) {
+               float scale, KeyPos kp, hipStream_t st, ScoreAcc acc) {
   constexpr int ROWS = kMainWaves * kMainQB * 16;
   Geo g{s.G(), s.T, s.M, s.R(), s.Nk(), s.Tk(), (const bf16_t*)q, (const bf16_t*)kc,
         (const bf16_t*)vc, (const bf16_t*)kn, (const bf16_t*)vn, kp.tp, kp.pos0};
@@ -813,7 +813,7 @@ hipError_t run(const Shape& s, const Plan& p, const void* q, const void* kc, con
                       s.R(), s.BH(), p.nsplit);
     if (e != hipSuccess) return e;
   }
-  return launch_colsum_reduce(s, p, parts, wsum, st, scores_acc);
+  return launch_colsum_reduce(s, p, parts, wsum, st, acc);
 }
 
 }  // namespace
@@ -826,10 +826,10 @@ int mfma_rows_per_part() { return kMainWaves * kMainQB * 16; }
 hipError_t launch_sdpa_mfma(const Shape& s, const Plan& p, const void* q, const void* kc,
                             const void* vc, const void* kn, const void* vn, void* out, float* lse,
                             float* wsum, char* ws, float scale, KeyPos kp, hipStream_t st,
-                            float* scores_acc) {
+                            ScoreAcc acc) {
   if (s.d == 64)
-    return run<64>(s, p, q, kc, vc, kn, vn, out, lse, wsum, ws, scale, kp, st, scores_acc);
-  return run<128>(s, p, q, kc, vc, kn, vn, out, lse, wsum, ws, scale, kp, st, scores_acc);
+    return run<64>(s, p, q, kc, vc, kn, vn, out, lse, wsum, ws, scale, kp, st, acc);
+  return run<128>(s, p, q, kc, vc, kn, vn, out, lse, wsum, ws, scale, kp, st, acc);
 }
 
 }  // namespace h2o

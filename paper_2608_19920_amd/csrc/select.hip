@@ -9,10 +9,12 @@ namespace {
 // is bitwise reproducible) whose rows can see column j. With scores
 // non-null, a chunk step's accumulation in the same pass: scores[bh][j] +=
 // wsum[bh][j] for j < M, one float32 addition of the stored value (the bits
-// of the separate accumulate kernel).
+// of the separate accumulate kernel); with copy non-null the sum is also
+// written to copy[bh][j], the ranking input of the fused selection.
 __global__ __launch_bounds__(256) void colsum_reduce_kernel(const float* __restrict__ parts,
                                                             float* __restrict__ wsum,
-                                                            float* __restrict__ scores, int nparts,
+                                                            float* __restrict__ scores,
+                                                            float* __restrict__ copy, int nparts,
                                                             int rows_per_part, int BH, int Nk,
                                                             int ld, int G, int T, int M,
                                                             int Tk) {
@@ -41,7 +43,11 @@ __global__ __launch_bounds__(256) void colsum_reduce_kernel(const float* __restr
   }
   for (; p < nparts; ++p, src += stride) s += src[0];
   wsum[(size_t)bh * Nk + j] = s;
-  if (sc) *sc = s_old + s;
+  if (sc) {
+    const float acc = s_old + s;
+    *sc = acc;
+    if (copy) copy[(size_t)bh * M + j] = acc;
+  }
 }
 
 // ---------------------------------------------------------------- accumulate
@@ -154,26 +160,36 @@ __device__ __forceinline__ float4 load4(const float* s, int M, int j) {
   return v;
 }
 
-// One block per row. Radix-select the k-th smallest key tau (digits of 12,
-// 12 and 8 bits, most significant first; the first digit's histogram is
-// taken while the row is staged), then emit, in ascending slot order, every
-// slot with key < tau and the lowest-index (k - #less) slots with key == tau.
+// Radix selection of one row by one block: the k-th smallest key tau
+// (digits of 12, 12 and 8 bits, most significant first; the first digit's
+// histogram is taken while the row is staged), then the compaction scan.
 // Rows of up to kSelLdsMax slots are staged in LDS; longer rows are read
 // from global memory in every pass. Every loop over the row takes rounds of
 // the whole block (uniform trip counts: hist_add is a wave-level operation)
 // with 4 slots per thread, so a thread has 4 independent reads in flight.
+//
+// Compaction in slot order: thread t owns the contiguous chunk [t*C,
+// (t+1)*C). The slots of a chunk below tau come first in it, and the keys
+// equal to tau of lowest slot are taken first, so a thread writes at
+//   (slots below tau in earlier chunks) + min(keys equal to tau in earlier
+//   chunks, need_eq)
+// - one block scan of both counts, packed in 16-bit halves when the row is
+// shorter than 65536 slots. Chunks of at most 32 slots keep the slots below
+// and equal to tau as bit masks, so the emit does not read the keys again.
+struct SelChunk {
+  uint32_t tau;       // the k-th smallest key
+  uint32_t take_eq;   // keys equal to tau this chunk contributes
+  uint32_t w;         // output position of the chunk's first chosen slot
+  int j0, j1;         // the chunk
+  bool masks;         // lt_mask / eq_mask hold the chunk's keys (C <= 32)
+  uint32_t lt_mask, eq_mask;
+};
+
 template <bool LDS>
-__global__ __launch_bounds__(kSelThreads) void bottomk_kernel(const float* __restrict__ scores,
-                                                              int M, int k,
-                                                              int32_t* __restrict__ idx) {
+__device__ __forceinline__ SelChunk bottomk_select(const float* s, int M, int k, uint32_t* keys,
+                                                   uint32_t* hist, uint32_t* tmp,
+                                                   uint32_t* sh_prefix, uint32_t* sh_krem) {
   static_assert(kSelBins == 4 * kSelThreads, "four bins per thread in select_bin");
-  __shared__ uint32_t keys[LDS ? kSelLdsMax + kSelLdsMax / 32 : 1];
-  __shared__ uint32_t hist[kSelBins];
-  __shared__ uint32_t tmp[2 * kSelWaves + 1];
-  __shared__ uint32_t sh_prefix, sh_krem;
-  const float* s = scores + (size_t)blockIdx.x * M;
-  int32_t* out = idx + (size_t)blockIdx.x * k;
-  if (k <= 0) return;
   const int t4 = 4 * (int)threadIdx.x;
   auto key_at = [&](int j) { return LDS ? keys[sel_lds_index(j)] : order_key(s[j]); };
   for (int b = threadIdx.x; b < kSelBins; b += kSelThreads) hist[b] = 0u;
@@ -199,8 +215,8 @@ __global__ __launch_bounds__(kSelThreads) void bottomk_kernel(const float* __res
     }
   }
   __syncthreads();
-  select_bin(hist, tmp, kSelShift[0], 0u, (uint32_t)k, &sh_prefix, &sh_krem);
-  uint32_t prefix = sh_prefix, krem = sh_krem;
+  select_bin(hist, tmp, kSelShift[0], 0u, (uint32_t)k, sh_prefix, sh_krem);
+  uint32_t prefix = *sh_prefix, krem = *sh_krem;
   uint32_t mask = kSelDigitMask[0] << kSelShift[0];
 #pragma unroll
   for (int d = 1; d < 3; ++d) {
@@ -219,32 +235,28 @@ __global__ __launch_bounds__(kSelThreads) void bottomk_kernel(const float* __res
                  j0 + t4 + e < M && (kk[e] & mask) == prefix);
     }
     __syncthreads();
-    select_bin(hist, tmp, kSelShift[d], prefix, krem, &sh_prefix, &sh_krem);
-    prefix = sh_prefix;
-    krem = sh_krem;
+    select_bin(hist, tmp, kSelShift[d], prefix, krem, sh_prefix, sh_krem);
+    prefix = *sh_prefix;
+    krem = *sh_krem;
     mask |= kSelDigitMask[d] << kSelShift[d];
   }
-  const uint32_t tau = prefix, need_eq = krem;
-  // Compaction in slot order: thread t owns the contiguous chunk [t*C,
-  // (t+1)*C). The slots of a chunk below tau come first in it, and the keys
-  // equal to tau of lowest slot are taken first, so a thread writes at
-  //   (slots below tau in earlier chunks) + min(keys equal to tau in earlier
-  //   chunks, need_eq)
-  // - one block scan of both counts, packed in 16-bit halves when the row is
-  // shorter than 65536 slots. Chunks of at most 32 slots keep the slots
-  // below and equal to tau as bit masks, so the emit does not read the keys
-  // again.
+  SelChunk c;
+  c.tau = prefix;
+  const uint32_t need_eq = krem;
   const int C = (M + kSelThreads - 1) / kSelThreads;
-  const int j0 = min(M, (int)threadIdx.x * C), j1 = min(M, j0 + C);
-  const bool masks = C <= 32;
+  c.j0 = min(M, (int)threadIdx.x * C);
+  c.j1 = min(M, c.j0 + C);
+  c.masks = C <= 32;
   uint32_t n_less = 0, n_eq = 0, lt_mask = 0, eq_mask = 0;
 #pragma unroll 4
-  for (int j = j0; j < j1; ++j) {
+  for (int j = c.j0; j < c.j1; ++j) {
     const uint32_t key = key_at(j);
-    const uint32_t bit = 1u << ((j - j0) & 31);
-    if (key < tau) { ++n_less; lt_mask |= bit; }
-    if (key == tau) { ++n_eq; eq_mask |= bit; }
+    const uint32_t bit = 1u << ((j - c.j0) & 31);
+    if (key < c.tau) { ++n_less; lt_mask |= bit; }
+    if (key == c.tau) { ++n_eq; eq_mask |= bit; }
   }
+  c.lt_mask = lt_mask;
+  c.eq_mask = eq_mask;
   uint32_t tot, less_before, eq_before;
   if (M < 65536) {
     const uint32_t both = block_exclusive_scan(n_less | (n_eq << 16), tmp, &tot);
@@ -258,12 +270,22 @@ __global__ __launch_bounds__(kSelThreads) void bottomk_kernel(const float* __res
   // need_eq - eq_taken never wraps, so no guarded subtraction is needed: a
   // guarded one let the optimiser drop the cap below)
   const uint32_t eq_taken = umin(eq_before, need_eq);
-  const uint32_t take_eq = umin(n_eq, need_eq - eq_taken);
-  uint32_t w = less_before + eq_taken;
-  if (masks) {
+  c.take_eq = umin(n_eq, need_eq - eq_taken);
+  c.w = less_before + eq_taken;
+  return c;
+}
+
+// Calls f(slot, position) for every chosen slot of the thread's chunk, in
+// increasing slot order, with consecutive positions from c.w on (positions
+// below k only).
+template <bool LDS, typename F>
+__device__ __forceinline__ void bottomk_emit(const SelChunk& c, const float* s,
+                                             const uint32_t* keys, int k, F&& f) {
+  uint32_t w = c.w;
+  if (c.masks) {
     // the lowest take_eq bits of eq_mask
-    uint32_t em = eq_mask, sel = lt_mask;
-    for (uint32_t i = 0; i < take_eq; ++i) {
+    uint32_t em = c.eq_mask, sel = c.lt_mask;
+    for (uint32_t i = 0; i < c.take_eq; ++i) {
       const uint32_t low = em & (0u - em);
       sel |= low;
       em ^= low;
@@ -271,15 +293,102 @@ __global__ __launch_bounds__(kSelThreads) void bottomk_kernel(const float* __res
     while (sel) {
       const int b = __ffs((int)sel) - 1;
       sel &= sel - 1;
-      if (w < (uint32_t)k) out[w++] = j0 + b;
+      if (w < (uint32_t)k) f(c.j0 + b, w++);
     }
   } else {
     uint32_t eq_seen = 0;
-    for (int j = j0; j < j1; ++j) {
-      const uint32_t key = key_at(j);
-      bool sel = key < tau;
-      if (key == tau) { sel = eq_seen < take_eq; ++eq_seen; }
-      if (sel && w < (uint32_t)k) out[w++] = j;
+    for (int j = c.j0; j < c.j1; ++j) {
+      const uint32_t key = LDS ? keys[sel_lds_index(j)] : order_key(s[j]);
+      bool sel = key < c.tau;
+      if (key == c.tau) { sel = eq_seen < c.take_eq; ++eq_seen; }
+      if (sel && w < (uint32_t)k) f(j, w++);
+    }
+  }
+}
+
+// One block per row: emit, in ascending slot order, every slot with key <
+// tau and the lowest-index (k - #less) slots with key == tau.
+template <bool LDS>
+__global__ __launch_bounds__(kSelThreads) void bottomk_kernel(const float* __restrict__ scores,
+                                                              int M, int k,
+                                                              int32_t* __restrict__ idx) {
+  __shared__ uint32_t keys[LDS ? kSelLdsMax + kSelLdsMax / 32 : 1];
+  __shared__ uint32_t hist[kSelBins];
+  __shared__ uint32_t tmp[2 * kSelWaves + 1];
+  __shared__ uint32_t sh_prefix, sh_krem;
+  const float* s = scores + (size_t)blockIdx.x * M;
+  int32_t* out = idx + (size_t)blockIdx.x * k;
+  if (k <= 0) return;
+  const SelChunk c = bottomk_select<LDS>(s, M, k, keys, hist, tmp, &sh_prefix, &sh_krem);
+  bottomk_emit<LDS>(c, s, keys, k, [&](int j, uint32_t w) { out[w] = j; });
+}
+
+// Selection and insert in one launch. Block (row, x), x < X = gridDim.y,
+// ranks the row's keys (which no kernel writes while it runs: a copy of the
+// accumulated scores), every one of the X blocks of a row computing the same
+// selection, so they need no communication. The X blocks of a row are
+// dispatched `rows` slots apart, so with a row count that is a multiple of
+// 8 they land on one XCD (dispatch goes round-robin over the 8) and read
+// the row through one L2. The chunk of thread t is
+// written out (evict_idx, the inserted slots' scores and token positions)
+// by block t % X; block x copies the K/V rows of chunk tokens [x*k/X,
+// (x+1)*k/X) into their slots, whose indices every block keeps in LDS (the
+// histogram array, free after the selection; k <= kSelBins). Same results
+// as bottomk_kernel followed by insert_kernel.
+template <bool LDS>
+__global__ __launch_bounds__(kSelThreads) void bottomk_insert_kernel(
+    const float* __restrict__ keys_in, float* __restrict__ scores,
+    int32_t* __restrict__ token_pos, uint4* __restrict__ kc, uint4* __restrict__ vc,
+    const uint4* __restrict__ kn, const uint4* __restrict__ vn, const float* __restrict__ wsum,
+    int32_t* __restrict__ idx, int M, int T, int k, int vecs, int32_t pos0) {
+  __shared__ uint32_t keys[LDS ? kSelLdsMax + kSelLdsMax / 32 : 1];
+  __shared__ uint32_t hist[kSelBins];
+  __shared__ uint32_t tmp[2 * kSelWaves + 1];
+  __shared__ uint32_t sh_prefix, sh_krem;
+  const size_t row = blockIdx.x;
+  const int X = gridDim.y, x = blockIdx.y;
+  const float* s = keys_in + row * M;
+  if (k <= 0) return;
+  const SelChunk c = bottomk_select<LDS>(s, M, k, keys, hist, tmp, &sh_prefix, &sh_krem);
+  uint32_t* sidx = hist;   // k <= kSelBins
+  const bool own = (int)threadIdx.x % X == x;
+  bottomk_emit<LDS>(c, s, keys, k, [&](int j, uint32_t w) {
+    sidx[w] = (uint32_t)j;
+    if (own) {
+      idx[row * k + w] = j;
+      scores[row * M + j] = wsum ? wsum[row * (size_t)(M + T) + M + w] : 0.f;
+      if (token_pos) token_pos[row * M + j] = pos0 + (int32_t)w;
+    }
+  });
+  __syncthreads();
+  // chunk tokens [i0, i1) of this block: 16-byte vectors, four loads of each
+  // tensor in flight per thread before the stores
+  const int i0 = (int)((long long)k * x / X), i1 = (int)((long long)k * (x + 1) / X);
+  const int n = (i1 - i0) * vecs;
+  constexpr int U = 4;
+  for (int e0 = threadIdx.x; e0 < n; e0 += U * kSelThreads) {
+    uint4 kv[U], vv[U];
+    uint32_t slot[U];
+    int cc[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int e = e0 + u * kSelThreads;
+      slot[u] = 0xFFFFFFFFu;
+      cc[u] = 0;
+      if (e < n) {
+        const int i = i0 + e / vecs;
+        cc[u] = e % vecs;
+        kv[u] = kn[(row * T + i) * vecs + cc[u]];
+        vv[u] = vn[(row * T + i) * vecs + cc[u]];
+        slot[u] = sidx[i];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (slot[u] < (uint32_t)M) {
+        kc[(row * M + slot[u]) * vecs + cc[u]] = kv[u];
+        vc[(row * M + slot[u]) * vecs + cc[u]] = vv[u];
+      }
     }
   }
 }
@@ -457,11 +566,11 @@ hipError_t launch_broadcast_rows(const int32_t* src, int32_t* dst, int B, int n,
 }
 
 hipError_t launch_colsum_reduce(const Shape& s, const Plan& p, const float* parts, float* wsum,
-                                hipStream_t st, float* scores_acc) {
+                                hipStream_t st, ScoreAcc acc) {
   dim3 grid((s.Nk() + 255) / 256, s.BH());
   return launch_kernel(K_COLSUM_REDUCE, colsum_reduce_kernel, grid, dim3(256), st, parts, wsum,
-                       scores_acc, p.nparts, p.rows_per_part, s.BH(), s.Nk(), p.parts_ld, s.G(), s.T, s.M,
-                       s.Tk());
+                       acc.scores, acc.scores ? acc.copy : nullptr, p.nparts, p.rows_per_part,
+                       s.BH(), s.Nk(), p.parts_ld, s.G(), s.T, s.M, s.Tk());
 }
 
 hipError_t launch_accumulate(float* scores, const float* wsum, int rows, int M, int T,
@@ -480,6 +589,31 @@ hipError_t launch_bottomk(const float* scores, int rows, int M, int k, int32_t* 
                          scores, M, k, idx);
   return launch_kernel(K_BOTTOMK, bottomk_kernel<false>, dim3(rows), dim3(kSelThreads), st,
                        scores, M, k, idx);
+}
+
+bool bottomk_insert_supported(int k) { return k >= 1 && k <= kSelBins; }
+
+hipError_t launch_bottomk_insert(const float* keys, float* scores, int32_t* token_pos, void* kc,
+                                 void* vc, const void* kn, const void* vn, const float* wsum,
+                                 int32_t* idx, int rows, int M, int T, int d, int k,
+                                 int32_t pos0, int elem_bytes, hipStream_t st) {
+  if (rows == 0 || k == 0) return hipSuccess;
+  if (!bottomk_insert_supported(k)) return hipErrorInvalidValue;
+  // about one block per CU in all: the X blocks of a row repeat its
+  // selection and share its inserts (8 to 32 blocks per row measured: the
+  // copy, not the repeated selection, decides)
+  int X = 256 / rows;
+  if (X > 32) X = 32;
+  if (X < 1) X = 1;
+  const int vecs = d * elem_bytes / 16;
+  const dim3 grid(rows, X);
+  if (M <= kSelLdsMax)
+    return launch_kernel(K_BOTTOMK_INSERT, bottomk_insert_kernel<true>, grid, dim3(kSelThreads), st,
+                         keys, scores, token_pos, (uint4*)kc, (uint4*)vc, (const uint4*)kn,
+                         (const uint4*)vn, wsum, idx, M, T, k, vecs, pos0);
+  return launch_kernel(K_BOTTOMK_INSERT, bottomk_insert_kernel<false>, grid, dim3(kSelThreads), st,
+                       keys, scores, token_pos, (uint4*)kc, (uint4*)vc, (const uint4*)kn,
+                       (const uint4*)vn, wsum, idx, M, T, k, vecs, pos0);
 }
 
 hipError_t launch_insert(void* kc, void* vc, float* scores, int32_t* token_pos, const void* kn,

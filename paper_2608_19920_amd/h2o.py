@@ -35,7 +35,7 @@ KERNEL_IDS = {"generic_lse": 0, "generic_main": 1, "mfma_lse": 2, "mfma_main": 3
               "insert": 8, "decode_split": 9, "decode_combine": 10,
               "argmin_insert": 11, "decode_finish": 12, "variant_keys": 13,
               "bwd_dq": 14, "bwd_dkdv": 15, "kv_copy": 16, "bwd_dot": 17,
-              "bwd_dq_reduce": 18}
+              "bwd_dq_reduce": 18, "bottomk_insert": 19}
 # eviction rankings (Sec. "Variants of Heavy-Hitter Oracle"), as h2o_policy
 POLICIES = {"h2o": 0, "h2o_norm": 1, "h2o_orig": 2}
 

@@ -42,7 +42,7 @@ KERNELS = {
     "colsum_reduce": ("colsum_reduce_kernel", ["select.hip"]),
     "bottomk": ("bottomk_kernel<", ["select.hip"]),
     "bottomk_insert": ("bottomk_insert_kernel<", ["select.hip"]),
-    "insert": ("insert_kernel", ["select.hip"]),
+    "insert": ("::insert_kernel(", ["select.hip"]),
 }
 
 

@@ -322,6 +322,8 @@ STEP_SHAPES = [  # B, Hq, Hkv, d, M, T, dtype
     (1, 4, 1, 64, 40000, 300, "bf16"),   # rows longer than the selection stages in LDS
     (40, 4, 4, 64, 96, 33, "bf16"),      # 160 rows: one block per row in the fused selection
     (1, 4, 1, 64, 4500, 4200, "bf16"),   # k above the fused selection's limit: separate kernels
+    (1, 4, 2, 64, 64, 64, "bf16"),       # k = M: every slot is evicted
+    (2, 4, 1, 64, 1000, 2, "bf16"),      # the smallest k of the fused selection
 ]
 
 

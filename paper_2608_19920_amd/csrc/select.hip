@@ -185,10 +185,14 @@ struct SelChunk {
   uint32_t lt_mask, eq_mask;
 };
 
+// Keys of the first digit's chosen bin gathered into LDS, at most.
+constexpr int kSelCand = 2048;
+
 template <bool LDS>
 __device__ __forceinline__ SelChunk bottomk_select(const float* s, int M, int k, uint32_t* keys,
-                                                   uint32_t* hist, uint32_t* tmp,
-                                                   uint32_t* sh_prefix, uint32_t* sh_krem) {
+                                                   uint32_t* hist, uint32_t* tmp, uint32_t* cand,
+                                                   uint32_t* sh_ncand, uint32_t* sh_prefix,
+                                                   uint32_t* sh_krem) {
   static_assert(kSelBins == 4 * kSelThreads, "four bins per thread in select_bin");
   const int t4 = 4 * (int)threadIdx.x;
   auto key_at = [&](int j) { return LDS ? keys[sel_lds_index(j)] : order_key(s[j]); };
@@ -218,10 +222,18 @@ __device__ __forceinline__ SelChunk bottomk_select(const float* s, int M, int k,
   select_bin(hist, tmp, kSelShift[0], 0u, (uint32_t)k, sh_prefix, sh_krem);
   uint32_t prefix = *sh_prefix, krem = *sh_krem;
   uint32_t mask = kSelDigitMask[0] << kSelShift[0];
-#pragma unroll
-  for (int d = 1; d < 3; ++d) {
-    for (int b = threadIdx.x; b < kSelBins; b += kSelThreads) hist[b] = 0u;
+  // The keys of the chosen first-digit bin: in rows of 16,384 slots or more,
+  // when there are at most kSelCand of them (the usual case, 12-bit digits
+  // spreading a row over many bins), one pass over the row gathers them
+  // into LDS and the two remaining digits are histogrammed over that list
+  // instead of over the row (shorter rows: two passes cost no more than the
+  // gather). Each wave reserves its lanes' places with one atomic add.
+  const uint32_t nb = hist[prefix >> kSelShift[0]];
+  const bool gather = M >= 16 * kSelThreads && nb <= (uint32_t)kSelCand;   // uniform
+  if (gather) {
+    if (threadIdx.x == 0) *sh_ncand = 0u;
     __syncthreads();
+    const int lane = threadIdx.x & 63;
     for (int j0 = 0; j0 < M; j0 += kSelRound) {
       uint32_t kk[4];
 #pragma unroll
@@ -230,9 +242,41 @@ __device__ __forceinline__ SelChunk bottomk_select(const float* s, int M, int k,
         kk[e] = j < M ? key_at(j) : 0u;
       }
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        hist_add(hist, (kk[e] >> kSelShift[d]) & kSelDigitMask[d],
-                 j0 + t4 + e < M && (kk[e] & mask) == prefix);
+      for (int e = 0; e < 4; ++e) {
+        const bool in = j0 + t4 + e < M && (kk[e] & mask) == prefix;
+        const uint64_t bal = __ballot(in);
+        if (bal) {   // uniform over the wave
+          uint32_t base = 0u;
+          if (lane == 0) base = atomicAdd(sh_ncand, (uint32_t)__popcll(bal));
+          base = __builtin_amdgcn_readfirstlane(base);
+          if (in) cand[base + (uint32_t)__popcll(bal & ((1ull << lane) - 1ull))] = kk[e];
+        }
+      }
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int d = 1; d < 3; ++d) {
+    for (int b = threadIdx.x; b < kSelBins; b += kSelThreads) hist[b] = 0u;
+    __syncthreads();
+    if (gather) {
+      for (int i = threadIdx.x; i < (int)nb; i += kSelThreads) {
+        const uint32_t key = cand[i];
+        hist_add(hist, (key >> kSelShift[d]) & kSelDigitMask[d], (key & mask) == prefix);
+      }
+    } else {
+      for (int j0 = 0; j0 < M; j0 += kSelRound) {
+        uint32_t kk[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int j = j0 + t4 + e;
+          kk[e] = j < M ? key_at(j) : 0u;
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          hist_add(hist, (kk[e] >> kSelShift[d]) & kSelDigitMask[d],
+                   j0 + t4 + e < M && (kk[e] & mask) == prefix);
+      }
     }
     __syncthreads();
     select_bin(hist, tmp, kSelShift[d], prefix, krem, sh_prefix, sh_krem);
@@ -315,11 +359,13 @@ __global__ __launch_bounds__(kSelThreads) void bottomk_kernel(const float* __res
   __shared__ uint32_t keys[LDS ? kSelLdsMax + kSelLdsMax / 32 : 1];
   __shared__ uint32_t hist[kSelBins];
   __shared__ uint32_t tmp[2 * kSelWaves + 1];
-  __shared__ uint32_t sh_prefix, sh_krem;
+  __shared__ uint32_t cand[kSelCand];
+  __shared__ uint32_t sh_ncand, sh_prefix, sh_krem;
   const float* s = scores + (size_t)blockIdx.x * M;
   int32_t* out = idx + (size_t)blockIdx.x * k;
   if (k <= 0) return;
-  const SelChunk c = bottomk_select<LDS>(s, M, k, keys, hist, tmp, &sh_prefix, &sh_krem);
+  const SelChunk c =
+      bottomk_select<LDS>(s, M, k, keys, hist, tmp, cand, &sh_ncand, &sh_prefix, &sh_krem);
   bottomk_emit<LDS>(c, s, keys, k, [&](int j, uint32_t w) { out[w] = j; });
 }
 
@@ -344,12 +390,14 @@ __global__ __launch_bounds__(kSelThreads) void bottomk_insert_kernel(
   __shared__ uint32_t keys[LDS ? kSelLdsMax + kSelLdsMax / 32 : 1];
   __shared__ uint32_t hist[kSelBins];
   __shared__ uint32_t tmp[2 * kSelWaves + 1];
-  __shared__ uint32_t sh_prefix, sh_krem;
+  __shared__ uint32_t cand[kSelCand];
+  __shared__ uint32_t sh_ncand, sh_prefix, sh_krem;
   const size_t row = blockIdx.x;
   const int X = gridDim.y, x = blockIdx.y;
   const float* s = keys_in + row * M;
   if (k <= 0) return;
-  const SelChunk c = bottomk_select<LDS>(s, M, k, keys, hist, tmp, &sh_prefix, &sh_krem);
+  const SelChunk c =
+      bottomk_select<LDS>(s, M, k, keys, hist, tmp, cand, &sh_ncand, &sh_prefix, &sh_krem);
   uint32_t* sidx = hist;   // k <= kSelBins
   const bool own = (int)threadIdx.x % X == x;
   bottomk_emit<LDS>(c, s, keys, k, [&](int j, uint32_t w) {

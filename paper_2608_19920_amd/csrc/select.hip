@@ -66,27 +66,34 @@ __global__ __launch_bounds__(256) void accumulate_kernel(float* __restrict__ sco
 constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / 64;
 
-// Exclusive prefix sum over the block (thread order); also returns the total.
 __device__ __forceinline__ uint32_t umin(uint32_t a, uint32_t b) { return a < b ? a : b; }
 
-__device__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* tmp, uint32_t* total) {
+// Inclusive prefix sum over the 64 lanes of a wave with DPP moves: shifts by
+// 1, 2, 4 and 8 lanes inside each 16-lane row (lanes shifted in from outside
+// the row add 0), then the running total carried across rows by the
+// broadcasts of lane 15 (into rows 1 and 3) and of lane 31 (into rows 2 and
+// 3). Six VALU additions, no LDS permutes.
+__device__ __forceinline__ uint32_t wave_inclusive_scan(uint32_t x) {
+  constexpr bool kZero = true;   // out-of-row source lanes read 0
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x111, 0xF, 0xF, kZero);   // row_shr:1
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x112, 0xF, 0xF, kZero);   // row_shr:2
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x114, 0xF, 0xF, kZero);   // row_shr:4
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x118, 0xF, 0xF, kZero);   // row_shr:8
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x142, 0xA, 0xF, false);   // row_bcast:15
+  x += (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, 0x143, 0xC, 0xF, false);   // row_bcast:31
+  return x;
+}
+
+// Exclusive prefix sum over the block (thread order); also returns the total.
+__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t* tmp,
+                                                         uint32_t* total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  uint32_t x = v;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    uint32_t y = __shfl_up(x, o, 64);
-    if (lane >= o) x += y;
-  }
+  const uint32_t x = wave_inclusive_scan(v);
   if (lane == 63) tmp[wave] = x;
   __syncthreads();
   if (wave == 0) {
-    uint32_t w = lane < kSelWaves ? tmp[lane] : 0u;
-    uint32_t z = w;
-#pragma unroll
-    for (int o = 1; o < kSelWaves; o <<= 1) {
-      uint32_t y = __shfl_up(z, o, 64);
-      if (lane >= o) z += y;
-    }
+    const uint32_t w = lane < kSelWaves ? tmp[lane] : 0u;
+    const uint32_t z = wave_inclusive_scan(w);
     if (lane < kSelWaves) tmp[kSelWaves + lane] = z - w;   // exclusive wave offsets
     if (lane == kSelWaves - 1) tmp[2 * kSelWaves] = z;
   }
@@ -123,25 +130,30 @@ constexpr int kSelChunkRounds = kSelLdsMax / kSelRound;   // rounds whose loads 
 
 // Given the histogram of the current digit, the bin that holds the krem-th
 // smallest key of the prefix, and the keys of the prefix below that bin:
-// every thread sums four consecutive bins, a block scan gives each thread
-// the count before its bins, and the one thread whose range holds the
-// krem-th key writes the extended prefix and the rest of krem. Ends synced.
-__device__ __forceinline__ void select_bin(const uint32_t* hist, uint32_t* tmp, int shift,
+// every thread sums four consecutive bins (and clears them for the next
+// digit: only it reads them), a block scan gives each thread the count
+// before its bins, and the one thread whose range holds the krem-th key
+// writes the extended prefix, the rest of krem and the bin's count. Ends
+// synced.
+__device__ __forceinline__ void select_bin(uint32_t* hist, uint32_t* tmp, int shift,
                                            uint32_t prefix, uint32_t krem, uint32_t* sh_prefix,
-                                           uint32_t* sh_krem) {
+                                           uint32_t* sh_krem, uint32_t* sh_count) {
   const int t = threadIdx.x;
   const uint32_t c0 = hist[4 * t], c1 = hist[4 * t + 1], c2 = hist[4 * t + 2],
                  c3 = hist[4 * t + 3];
+  hist[4 * t] = hist[4 * t + 1] = hist[4 * t + 2] = hist[4 * t + 3] = 0u;
   const uint32_t c = c0 + c1 + c2 + c3;
   uint32_t total;
   const uint32_t before = block_exclusive_scan(c, tmp, &total);
   if (before < krem && before + c >= krem) {
     uint32_t b = before, bin = 4u * t;
-    if (b + c0 < krem) { b += c0; ++bin;
-      if (b + c1 < krem) { b += c1; ++bin;
-        if (b + c2 < krem) { b += c2; ++bin; } } }
+    uint32_t cb = c0;
+    if (b + c0 < krem) { b += c0; ++bin; cb = c1;
+      if (b + c1 < krem) { b += c1; ++bin; cb = c2;
+        if (b + c2 < krem) { b += c2; ++bin; cb = c3; } } }
     *sh_prefix = prefix | (bin << shift);
     *sh_krem = krem - b;
+    *sh_count = cb;
   }
   __syncthreads();
 }
@@ -219,7 +231,7 @@ __device__ __forceinline__ SelChunk bottomk_select(const float* s, int M, int k,
     }
   }
   __syncthreads();
-  select_bin(hist, tmp, kSelShift[0], 0u, (uint32_t)k, sh_prefix, sh_krem);
+  select_bin(hist, tmp, kSelShift[0], 0u, (uint32_t)k, sh_prefix, sh_krem, sh_ncand);
   uint32_t prefix = *sh_prefix, krem = *sh_krem;
   uint32_t mask = kSelDigitMask[0] << kSelShift[0];
   // The keys of the chosen first-digit bin: in rows of 16,384 slots or more,
@@ -228,9 +240,10 @@ __device__ __forceinline__ SelChunk bottomk_select(const float* s, int M, int k,
   // into LDS and the two remaining digits are histogrammed over that list
   // instead of over the row (shorter rows: two passes cost no more than the
   // gather). Each wave reserves its lanes' places with one atomic add.
-  const uint32_t nb = hist[prefix >> kSelShift[0]];
+  const uint32_t nb = *sh_ncand;   // keys in the chosen bin
   const bool gather = M >= 16 * kSelThreads && nb <= (uint32_t)kSelCand;   // uniform
   if (gather) {
+    __syncthreads();   // every thread has read nb
     if (threadIdx.x == 0) *sh_ncand = 0u;
     __syncthreads();
     const int lane = threadIdx.x & 63;
@@ -257,8 +270,7 @@ __device__ __forceinline__ SelChunk bottomk_select(const float* s, int M, int k,
   }
 #pragma unroll
   for (int d = 1; d < 3; ++d) {
-    for (int b = threadIdx.x; b < kSelBins; b += kSelThreads) hist[b] = 0u;
-    __syncthreads();
+    // (select_bin left the histogram cleared)
     if (gather) {
       for (int i = threadIdx.x; i < (int)nb; i += kSelThreads) {
         const uint32_t key = cand[i];
@@ -279,7 +291,7 @@ __device__ __forceinline__ SelChunk bottomk_select(const float* s, int M, int k,
       }
     }
     __syncthreads();
-    select_bin(hist, tmp, kSelShift[d], prefix, krem, sh_prefix, sh_krem);
+    select_bin(hist, tmp, kSelShift[d], prefix, krem, sh_prefix, sh_krem, sh_ncand);
     prefix = *sh_prefix;
     krem = *sh_krem;
     mask |= kSelDigitMask[d] << kSelShift[d];

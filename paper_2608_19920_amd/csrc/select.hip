@@ -174,11 +174,13 @@ __device__ __forceinline__ float4 load4(const float* s, int M, int j) {
 
 // Radix selection of one row by one block: the k-th smallest key tau
 // (digits of 12, 12 and 8 bits, most significant first; the first digit's
-// histogram is taken while the row is staged), then the compaction scan.
-// Rows of up to kSelLdsMax slots are staged in LDS; longer rows are read
-// from global memory in every pass. Every loop over the row takes rounds of
-// the whole block (uniform trip counts: hist_add is a wave-level operation)
-// with 4 slots per thread, so a thread has 4 independent reads in flight.
+// histogram is taken while the row is staged; in long rows the last two
+// digits are taken over the gathered keys of the first digit's bin), then
+// the compaction scan. Rows of up to kSelLdsMax slots are staged in LDS;
+// longer rows are read from global memory in every pass. Every loop over
+// the row takes rounds of the whole block (uniform trip counts: the gather
+// takes ballots) with 4 slots per thread, so a thread has 4 independent
+// reads in flight.
 //
 // Compaction in slot order: thread t owns the contiguous chunk [t*C,
 // (t+1)*C). The slots of a chunk below tau come first in it, and the keys

@@ -361,8 +361,9 @@ __device__ __forceinline__ void split_body(
   issue(0, 0);
   if (INS) {
     // (key, slot)-smallest, slots visited in increasing order per thread so
-    // that a strict < keeps the lowest slot among equal keys
-    uint32_t bk = 0xFFFFFFFFu, bj = 0xFFFFFFFFu;
+    // that a strict < keeps the lowest slot among equal keys; the start
+    // (max key, slot 0) is a real pair whenever every key is the maximum
+    uint32_t bk = 0xFFFFFFFFu, bj = 0u;
 #pragma unroll
     for (int u = 0; u < kScPre; ++u) {
       const int j = tid + u * kThreads;
@@ -732,7 +733,9 @@ __global__ __launch_bounds__(kFinThreads) void decode_finish(
   }
   // Passes in increasing slot order; a thread visits its slots in
   // increasing order, so a strict < keeps the lowest slot among equal keys.
-  uint32_t bk = 0xFFFFFFFFu, bj = 0xFFFFFFFFu;
+  // The start (max key, slot 0) is a real pair whenever every key is the
+  // maximum, so the choice is always a slot of the cache.
+  uint32_t bk = 0xFFFFFFFFu, bj = 0u;
   f32x4 wv, sa;
   int base = 0;
   for (;;) {

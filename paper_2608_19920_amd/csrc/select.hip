@@ -501,7 +501,9 @@ __global__ __launch_bounds__(kArgThreads) void argmin_insert_kernel(
   const size_t row = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const float* s = keys + (key_rows > 0 ? row % key_rows : row) * M;
-  uint32_t bk = 0xFFFFFFFFu, bj = 0xFFFFFFFFu;     // (key, slot), lexicographic
+  // (key, slot), lexicographic; the start (max key, slot 0) is a real pair
+  // whenever every key is the maximum, so the result is always a slot
+  uint32_t bk = 0xFFFFFFFFu, bj = 0u;
   // four independent loads per step; slots are visited in increasing order
   // per thread, so a strict < keeps the lowest slot among equal keys
   int j = tid;

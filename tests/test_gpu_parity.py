@@ -147,6 +147,29 @@ def test_bottomk_negative_and_huge_values():
         np.testing.assert_array_equal(U.gpu_bottomk(s, k), oracle.bottomk(s, k))
 
 
+def test_selection_with_every_key_at_the_top():
+    """Scores whose order key is the largest one (NaN with a full payload, a
+    value no arithmetic produces): the (key, slot) minimum is then the lowest
+    slots, so the selection and the decode step's argmin still choose slots
+    inside the cache."""
+    top = np.array([0x7FFFFFFF], np.uint32).view(np.float32)[0]
+    for M, k in ((1, 1), (4096, 1), (300, 4), (9000, 7)):
+        say(f"all-top keys M {M} k {k}")
+        s = np.full((3, M), top, np.float32)
+        np.testing.assert_array_equal(U.gpu_bottomk(s, k),
+                                      np.tile(np.arange(k, dtype=np.int32), (3, 1)))
+    B, Hq, Hkv, d, M = 2, 8, 2, 64, 512
+    wl = W.custom("top", B=B, Hq=Hq, Hkv=Hkv, d=d, M=M, T=1, dtype="bf16", heavy_frac=0.02)
+    x = W.make_inputs(wl, seed=17)
+    x["scores"] = np.full_like(x["scores"], top)
+    q, kn, vn = (U.to_dev(x[n], torch.bfloat16) for n in ("q", "k_new", "v_new"))
+    st = U.device_state(x, "bf16")
+    bufs = H.alloc_step(B, Hq, Hkv, 1, M, d, torch.bfloat16)
+    H.step(st, q, kn, vn, bufs, int(x["pos0"]), float(x["scale"]))
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(U.to_np(bufs["evict_idx"]).reshape(-1), np.zeros(B * Hkv))
+
+
 DECODE_SHAPES = [(2, 4, 4, 128, 129, 1), (1, 32, 8, 64, 513, 1), (8, 32, 8, 64, 4096, 1),
                  (3, 16, 2, 64, 1000, 1), (1, 2, 1, 64, 256, 1), (2, 8, 2, 128, 300, 1),
                  (1, 8, 8, 64, 1, 1), (1, 4, 2, 64, 0, 1)]

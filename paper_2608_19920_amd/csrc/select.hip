@@ -174,13 +174,14 @@ __device__ __forceinline__ float4 load4(const float* s, int M, int j) {
 
 // Radix selection of one row by one block: the k-th smallest key tau
 // (digits of 12, 12 and 8 bits, most significant first; the first digit's
-// histogram is taken while the row is staged; in long rows the last two
-// digits are taken over the gathered keys of the first digit's bin), then
-// the compaction scan. Rows of up to kSelLdsMax slots are staged in LDS;
-// longer rows are read from global memory in every pass. Every loop over
-// the row takes rounds of the whole block (uniform trip counts: the gather
-// takes ballots) with 4 slots per thread, so a thread has 4 independent
-// reads in flight.
+// histogram is taken while the row is staged; when the first digit's bin
+// holds few keys they are gathered and ranked against each other instead of
+// the last two digits, and in long rows those digits are taken over the
+// gathered keys), then the compaction scan. Rows of up to kSelLdsMax slots
+// are staged in LDS; longer rows are read from global memory in every pass.
+// Every loop over the row takes rounds of the whole block (uniform trip
+// counts: the gather takes ballots) with 4 slots per thread, so a thread
+// has 4 independent reads in flight.
 //
 // Compaction in slot order: thread t owns the contiguous chunk [t*C,
 // (t+1)*C). The slots of a chunk below tau come first in it, and the keys
@@ -201,7 +202,11 @@ struct SelChunk {
 
 // Keys of the first digit's chosen bin gathered into LDS, at most.
 constexpr int kSelCand = 2048;
+// Gathered keys ranked against each other instead of two more digits, at most.
+constexpr int kSelRankMax = 256;
 
+// sh_ncand[0] receives the count of the chosen bin, sh_ncand[1] is the
+// gather's counter.
 template <bool LDS>
 __device__ __forceinline__ SelChunk bottomk_select(const float* s, int M, int k, uint32_t* keys,
                                                    uint32_t* hist, uint32_t* tmp, uint32_t* cand,
@@ -211,6 +216,7 @@ __device__ __forceinline__ SelChunk bottomk_select(const float* s, int M, int k,
   const int t4 = 4 * (int)threadIdx.x;
   auto key_at = [&](int j) { return LDS ? keys[sel_lds_index(j)] : order_key(s[j]); };
   for (int b = threadIdx.x; b < kSelBins; b += kSelThreads) hist[b] = 0u;
+  if (threadIdx.x == 0) sh_ncand[1] = 0u;   // the gather's counter
   __syncthreads();
   // first digit while the keys are staged: the loads of a chunk of rounds
   // (the whole row when it fits LDS) are issued before their keys are used
@@ -236,18 +242,18 @@ __device__ __forceinline__ SelChunk bottomk_select(const float* s, int M, int k,
   select_bin(hist, tmp, kSelShift[0], 0u, (uint32_t)k, sh_prefix, sh_krem, sh_ncand);
   uint32_t prefix = *sh_prefix, krem = *sh_krem;
   uint32_t mask = kSelDigitMask[0] << kSelShift[0];
-  // The keys of the chosen first-digit bin: in rows of 16,384 slots or more,
-  // when there are at most kSelCand of them (the usual case, 12-bit digits
-  // spreading a row over many bins), one pass over the row gathers them
-  // into LDS and the two remaining digits are histogrammed over that list
-  // instead of over the row (shorter rows: two passes cost no more than the
-  // gather). Each wave reserves its lanes' places with one atomic add.
+  // The keys of the chosen first-digit bin: when there are at most
+  // kSelRankMax of them (the usual case, 12-bit digits spreading a row over
+  // many bins), or in rows of 16,384 slots or more at most kSelCand, one
+  // pass over the row gathers them into LDS. A few are ranked against each
+  // other; more take the two remaining digits, histogrammed over the list
+  // instead of over the row (in shorter rows two passes over the row cost
+  // no more than the gather). Each wave reserves its lanes' places with one
+  // atomic add.
   const uint32_t nb = *sh_ncand;   // keys in the chosen bin
-  const bool gather = M >= 16 * kSelThreads && nb <= (uint32_t)kSelCand;   // uniform
+  const bool rank = nb <= (uint32_t)kSelRankMax;                       // uniform
+  const bool gather = rank || (M >= 16 * kSelThreads && nb <= (uint32_t)kSelCand);
   if (gather) {
-    __syncthreads();   // every thread has read nb
-    if (threadIdx.x == 0) *sh_ncand = 0u;
-    __syncthreads();
     const int lane = threadIdx.x & 63;
     for (int j0 = 0; j0 < M; j0 += kSelRound) {
       uint32_t kk[4];
@@ -262,7 +268,7 @@ __device__ __forceinline__ SelChunk bottomk_select(const float* s, int M, int k,
         const uint64_t bal = __ballot(in);
         if (bal) {   // uniform over the wave
           uint32_t base = 0u;
-          if (lane == 0) base = atomicAdd(sh_ncand, (uint32_t)__popcll(bal));
+          if (lane == 0) base = atomicAdd(sh_ncand + 1, (uint32_t)__popcll(bal));
           base = __builtin_amdgcn_readfirstlane(base);
           if (in) cand[base + (uint32_t)__popcll(bal & ((1ull << lane) - 1ull))] = kk[e];
         }
@@ -270,8 +276,39 @@ __device__ __forceinline__ SelChunk bottomk_select(const float* s, int M, int k,
     }
     __syncthreads();
   }
+  if (rank) {
+    // tau is the gathered value x with fewer than krem smaller keys and at
+    // least krem keys <= x (the krem-th smallest of the bin); the threads
+    // holding a key equal to it write the same values
+    if (threadIdx.x < nb) {
+      const uint32_t x = cand[threadIdx.x];
+      uint32_t lt = 0u, le = 0u;
+      const uint4* c4 = reinterpret_cast<const uint4*>(cand);
+      const uint32_t nq = nb >> 2;
+      for (uint32_t i = 0; i < nq; ++i) {
+        const uint4 y = c4[i];
+        lt += (uint32_t)(y.x < x) + (uint32_t)(y.y < x) + (uint32_t)(y.z < x) +
+              (uint32_t)(y.w < x);
+        le += (uint32_t)(y.x <= x) + (uint32_t)(y.y <= x) + (uint32_t)(y.z <= x) +
+              (uint32_t)(y.w <= x);
+      }
+      for (uint32_t i = nq << 2; i < nb; ++i) {
+        const uint32_t y = cand[i];
+        lt += (uint32_t)(y < x);
+        le += (uint32_t)(y <= x);
+      }
+      if (lt < krem && krem <= le) {
+        *sh_prefix = x;
+        *sh_krem = krem - lt;
+      }
+    }
+    __syncthreads();
+    prefix = *sh_prefix;
+    krem = *sh_krem;
+  }
 #pragma unroll
   for (int d = 1; d < 3; ++d) {
+    if (rank) break;   // uniform
     // (select_bin left the histogram cleared)
     if (gather) {
       for (int i = threadIdx.x; i < (int)nb; i += kSelThreads) {
@@ -373,13 +410,13 @@ __global__ __launch_bounds__(kSelThreads) void bottomk_kernel(const float* __res
   __shared__ uint32_t keys[LDS ? kSelLdsMax + kSelLdsMax / 32 : 1];
   __shared__ uint32_t hist[kSelBins];
   __shared__ uint32_t tmp[2 * kSelWaves + 1];
-  __shared__ uint32_t cand[kSelCand];
-  __shared__ uint32_t sh_ncand, sh_prefix, sh_krem;
+  __shared__ __attribute__((aligned(16))) uint32_t cand[kSelCand];
+  __shared__ uint32_t sh_ncand[2], sh_prefix, sh_krem;
   const float* s = scores + (size_t)blockIdx.x * M;
   int32_t* out = idx + (size_t)blockIdx.x * k;
   if (k <= 0) return;
   const SelChunk c =
-      bottomk_select<LDS>(s, M, k, keys, hist, tmp, cand, &sh_ncand, &sh_prefix, &sh_krem);
+      bottomk_select<LDS>(s, M, k, keys, hist, tmp, cand, sh_ncand, &sh_prefix, &sh_krem);
   bottomk_emit<LDS>(c, s, keys, k, [&](int j, uint32_t w) { out[w] = j; });
 }
 
@@ -404,14 +441,14 @@ __global__ __launch_bounds__(kSelThreads) void bottomk_insert_kernel(
   __shared__ uint32_t keys[LDS ? kSelLdsMax + kSelLdsMax / 32 : 1];
   __shared__ uint32_t hist[kSelBins];
   __shared__ uint32_t tmp[2 * kSelWaves + 1];
-  __shared__ uint32_t cand[kSelCand];
-  __shared__ uint32_t sh_ncand, sh_prefix, sh_krem;
+  __shared__ __attribute__((aligned(16))) uint32_t cand[kSelCand];
+  __shared__ uint32_t sh_ncand[2], sh_prefix, sh_krem;
   const size_t row = blockIdx.x;
   const int X = gridDim.y, x = blockIdx.y;
   const float* s = keys_in + row * M;
   if (k <= 0) return;
   const SelChunk c =
-      bottomk_select<LDS>(s, M, k, keys, hist, tmp, cand, &sh_ncand, &sh_prefix, &sh_krem);
+      bottomk_select<LDS>(s, M, k, keys, hist, tmp, cand, sh_ncand, &sh_prefix, &sh_krem);
   uint32_t* sidx = hist;   // k <= kSelBins
   const bool own = (int)threadIdx.x % X == x;
   bottomk_emit<LDS>(c, s, keys, k, [&](int j, uint32_t w) {

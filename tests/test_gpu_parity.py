@@ -138,6 +138,21 @@ def test_bottomk_exact(rows, M, k, quant):
     np.testing.assert_array_equal(U.gpu_bottomk(s, k), oracle.bottomk(s, k))
 
 
+@pytest.mark.parametrize("M,k,nties", [(8192, 1024, 40), (8192, 1024, 1), (20000, 2048, 90),
+                                        (40000, 512, 7), (1000, 999, 3), (300, 1, 5)])
+def test_bottomk_few_keys_in_the_bin(M, k, nties):
+    """Rows whose first 12-bit digit leaves few keys in the chosen bin (the
+    keys are then ranked against each other), with nties copies of the k-th
+    value spread over the row so that some but not all equal keys are taken."""
+    say(f"bottomk few keys M {M} k {k} ties {nties}")
+    rng = np.random.default_rng(M + k + nties)
+    s = rng.standard_exponential((3, M)).astype(np.float32)
+    for r in range(3):
+        tau = np.sort(s[r])[k - 1]
+        s[r, rng.choice(M, nties, replace=False)] = tau
+    np.testing.assert_array_equal(U.gpu_bottomk(s, k), oracle.bottomk(s, k))
+
+
 def test_bottomk_negative_and_huge_values():
     s = np.array([[3.0, -1.0, np.inf, -np.inf, 0.0, -0.0, 1e-45, -1e-45, 3.4e38, 2.0]],
                  np.float32)

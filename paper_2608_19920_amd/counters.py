@@ -39,6 +39,7 @@ KERNELS = {
     "decode_finish": ("decode_finish<", ["decode.hip"]),
     "mfma_lse": ("lse_pass<", ["sdpa_mfma.hip"]),
     "mfma_main": ("main_pass<", ["sdpa_mfma.hip"]),
+    "split_reduce": ("split_reduce<", ["sdpa_mfma.hip"]),
     "colsum_reduce": ("colsum_reduce_kernel", ["select.hip"]),
     "bottomk": ("bottomk_kernel<", ["select.hip"]),
     "bottomk_insert": ("bottomk_insert_kernel<", ["select.hip"]),

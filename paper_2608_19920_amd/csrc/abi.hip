@@ -137,27 +137,42 @@ Plan make_plan(const Shape& s, int dtype) {
   p.parts_ld = (int)Nk;
   if (path == 1) {
     // Split the key range of each row tile when there are too few blocks to
-    // fill the CUs: two 4-wave blocks of the main pass fit one CU, and the
-    // lighter lse pass is given more. Keep at least 8 key tiles per split.
-    const int rows_blk = mfma_rows_per_block();
-    const long long nrt = (R + rows_blk - 1) / rows_blk;
-    const long long blocks = nrt * (long long)BH;
+    // fill the CUs (a round: the main-pass blocks resident at once, two
+    // 4-wave or one 8-wave block per CU; the lighter lse pass, four 4-wave
+    // blocks per CU, is given 1,024). Keep at least 8 key tiles per split.
+    const int rows_lse = mfma_lse_rows_per_block();
+    const long long blocks_lse = (long long)((R + rows_lse - 1) / rows_lse) * (long long)BH;
     const long long ntiles = (Nk + 31) / 32;
-    auto pick = [&](long long target, long long maxs) {
-      long long ns = (target + blocks - 1) / blocks;
+    auto pick = [&](long long nb, long long target, long long maxs) {
+      long long ns = (target + nb - 1) / nb;
       if (ns > ntiles / 8) ns = ntiles / 8;
       if (ns > maxs) ns = maxs;
       return (int)(ns < 1 ? 1 : ns);
     };
-    p.nsplit = pick(512, 8);
-    // Between one and two rounds of main-pass blocks the second round is
-    // partly filled and runs at the pace of its fullest CUs; halved blocks
-    // shorten it (896 row tiles of 128 rows at GQA 7:1: 1,150 -> 1,030 us
-    // for the pass, 22 us for the O partials' reduce).
-    if (p.nsplit == 1 && blocks > 512 && blocks < 1024 && ntiles >= 16) p.nsplit = 2;
-    p.nsplit_lse = pick(1024, 16);
-    p.rows_per_part = mfma_rows_per_part();
-    p.nparts = (int)(nrt * (rows_blk / p.rows_per_part));
+    // main-pass blocks of `waves` waves: their row-tile count and split
+    auto main_grid = [&](int waves, long long& nrt_w, int& ns_w) {
+      const long long rows_w = (long long)waves * mfma_rows_per_wave();
+      const long long round = 256LL * (8 / waves);
+      nrt_w = ((long long)R + rows_w - 1) / rows_w;
+      const long long nb = nrt_w * (long long)BH;
+      ns_w = pick(nb, round, 8);
+      // Between one and two rounds the second round is partly filled and
+      // runs at the pace of its fullest CUs; halved blocks shorten it (896
+      // row tiles of 128 rows at GQA 7:1: 1,150 -> 1,030 us for the pass,
+      // 22 us for the O partials' reduce).
+      if (ns_w == 1 && nb > round && nb < 2 * round && ntiles >= 16) ns_w = 2;
+      return nb * ns_w % round == 0;   // whole rounds
+    };
+    // 8-wave blocks where they fill whole rounds (two blocks sharing a CU
+    // advance unevenly; one block per CU leaves CUs idle in a partial round)
+    long long nrt = 0;
+    int ns = 1;
+    p.main_waves = s.d == 128 && main_grid(8, nrt, ns) ? 8 : 4;
+    if (p.main_waves == 4) main_grid(4, nrt, ns);
+    p.nsplit = ns;
+    p.nsplit_lse = pick(blocks_lse, 1024, 16);
+    p.rows_per_part = p.main_waves * mfma_rows_per_wave();
+    p.nparts = (int)nrt;
     p.parts_ld = (int)((Nk + 31) / 32 * 32);
   } else if (path == 2) {
     p.nsplit = s.M > 0 ? decode_max_split() : 0;   // capacity; the launch picks the count

@@ -777,19 +777,24 @@ __global__ __launch_bounds__(256) void split_reduce(const float* __restrict__ op
 // Both passes use 128-row blocks of 4 waves x 32 rows: few enough registers
 // per wave that two or more waves share each SIMD and hide each other's
 // latencies.
-constexpr int kLseWaves = 4, kLseQB = 2, kMainWaves = 4, kMainQB = 2;
-static_assert(kLseWaves * kLseQB == kMainWaves * kMainQB, "one row tiling");
+// The lse pass runs 128-row blocks of 4 waves x 32 rows; the main pass the
+// same, or at d = 128 256-row blocks of 8 waves (one block per CU, the two
+// waves of a SIMD from one block) where the plan finds those fill whole
+// rounds of the CUs.
+constexpr int kLseWaves = 4, kLseQB = 2, kMainQB = 2;
 
 template <int D>
 hipError_t run(const Shape& s, const Plan& p, const void* q, const void* kc, const void* vc,
                const void* kn, const void* vn, void* out, float* lse, float* wsum, char* ws,
                float scale, KeyPos kp, hipStream_t st, ScoreAcc acc) {
-  constexpr int ROWS = kMainWaves * kMainQB * 16;
+  const int main_waves = D == 128 && p.main_waves == 8 ? 8 : 4;
+  const int ROWS = main_waves * kMainQB * 16;
+  constexpr int LSE_ROWS = kLseWaves * kLseQB * 16;
   Geo g{s.G(), s.T, s.M, s.R(), s.Nk(), s.Tk(), (const bf16_t*)q, (const bf16_t*)kc,
         (const bf16_t*)vc, (const bf16_t*)kn, (const bf16_t*)vn, kp.tp, kp.pos0};
   const bool cache = s.cache_only;
-  const int nrt = (s.R() + ROWS - 1) / ROWS;
-  dim3 grid(nrt * p.nsplit, s.BH()), grid_lse(nrt * p.nsplit_lse, s.BH());
+  const int nrt = (s.R() + ROWS - 1) / ROWS, nrt_lse = (s.R() + LSE_ROWS - 1) / LSE_ROWS;
+  dim3 grid(nrt * p.nsplit, s.BH()), grid_lse(nrt_lse * p.nsplit_lse, s.BH());
   const float c = scale * kLog2e;
   float2* stats = reinterpret_cast<float2*>(ws + p.off_stats);
   float* parts = reinterpret_cast<float*>(ws + p.off_parts);
@@ -800,11 +805,19 @@ hipError_t run(const Shape& s, const Plan& p, const void* q, const void* kc, con
                                grid_lse, dim3(kLseWaves * 64), st, g, s.Hq, s.Hkv, p.nsplit_lse, c,
                                stats);
   if (e != hipSuccess) return e;
-  e = launch_kernel(K_MFMA_MAIN,
-                    cache ? main_pass<D, kMainWaves, kMainQB, true>
-                          : main_pass<D, kMainWaves, kMainQB, false>,
-                    grid, dim3(kMainWaves * 64), st, g, s.Hq, s.Hkv, p.nsplit, p.nsplit_lse, c,
-                    (const float2*)stats, parts, p.parts_ld, (bf16_t*)out, opart, lse);
+  auto main = [&](auto kern) {
+    return launch_kernel(K_MFMA_MAIN, kern, grid, dim3(main_waves * 64), st, g, s.Hq, s.Hkv,
+                         p.nsplit, p.nsplit_lse, c, (const float2*)stats, parts, p.parts_ld,
+                         (bf16_t*)out, opart, lse);
+  };
+  if constexpr (D == 128) {
+    if (main_waves == 8)
+      e = cache ? main(main_pass<D, 8, kMainQB, true>) : main(main_pass<D, 8, kMainQB, false>);
+    else
+      e = cache ? main(main_pass<D, 4, kMainQB, true>) : main(main_pass<D, 4, kMainQB, false>);
+  } else {
+    e = cache ? main(main_pass<D, 4, kMainQB, true>) : main(main_pass<D, 4, kMainQB, false>);
+  }
   if (e != hipSuccess) return e;
   if (p.nsplit > 1) {
     const size_t n4 = (size_t)s.BH() * s.R() * s.d / 4;
@@ -820,8 +833,8 @@ hipError_t run(const Shape& s, const Plan& p, const void* q, const void* kc, con
 
 // Rows of packed queries per workgroup of the MFMA kernels, and per colsum
 // partial (one partial per block).
-int mfma_rows_per_block() { return kMainWaves * kMainQB * 16; }
-int mfma_rows_per_part() { return kMainWaves * kMainQB * 16; }
+int mfma_rows_per_wave() { return kMainQB * 16; }
+int mfma_lse_rows_per_block() { return kLseWaves * kLseQB * 16; }
 
 hipError_t launch_sdpa_mfma(const Shape& s, const Plan& p, const void* q, const void* kc,
                             const void* vc, const void* kn, const void* vn, void* out, float* lse,

@@ -137,11 +137,9 @@ Plan make_plan(const Shape& s, int dtype) {
   p.parts_ld = (int)Nk;
   if (path == 1) {
     // Split the key range of each row tile when there are too few blocks to
-    // fill the CUs (a round: the main-pass blocks resident at once, two
-    // 4-wave or one 8-wave block per CU; the lighter lse pass, four 4-wave
-    // blocks per CU, is given 1,024). Keep at least 8 key tiles per split.
-    const int rows_lse = mfma_lse_rows_per_block();
-    const long long blocks_lse = (long long)((R + rows_lse - 1) / rows_lse) * (long long)BH;
+    // fill the CUs (a round: the blocks resident at once; the main pass fits
+    // two 4-wave or one 8-wave block per CU, the lighter lse pass four
+    // 4-wave or two 8-wave blocks). Keep at least 8 key tiles per split.
     const long long ntiles = (Nk + 31) / 32;
     auto pick = [&](long long nb, long long target, long long maxs) {
       long long ns = (target + nb - 1) / nb;
@@ -170,7 +168,20 @@ Plan make_plan(const Shape& s, int dtype) {
     p.main_waves = s.d == 128 && main_grid(8, nrt, ns) ? 8 : 4;
     if (p.main_waves == 4) main_grid(4, nrt, ns);
     p.nsplit = ns;
-    p.nsplit_lse = pick(blocks_lse, 1024, 16);
+    // the lse pass: 1,024 blocks of 4 waves, or 512 of 8 where those fill
+    // whole rounds (long cache: the pass 580 against 610 us; more splits
+    // than one round's worth cost the main pass as much in statistics
+    // reads)
+    auto lse_grid = [&](int waves, int target, int& ns_w) {
+      const long long rows_w = (long long)waves * mfma_rows_per_wave();
+      const long long nb = (((long long)R + rows_w - 1) / rows_w) * (long long)BH;
+      ns_w = pick(nb, target, 16);
+      return nb * ns_w % (256LL * (16 / waves)) == 0;
+    };
+    int nl = 1;
+    p.lse_waves = s.d == 128 && lse_grid(8, 512, nl) ? 8 : 4;
+    if (p.lse_waves == 4) lse_grid(4, 1024, nl);
+    p.nsplit_lse = nl;
     p.rows_per_part = p.main_waves * mfma_rows_per_wave();
     p.nparts = (int)nrt;
     p.parts_ld = (int)((Nk + 31) / 32 * 32);

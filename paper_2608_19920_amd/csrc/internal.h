@@ -109,6 +109,7 @@ struct Plan {
   int nsplit;          // key-range splits per row tile of the main pass (MFMA path)
   int nsplit_lse;      // key-range splits per row tile of the lse pass (MFMA path)
   int main_waves;      // waves per main-pass block, 4 or 8 (MFMA path)
+  int lse_waves;       // waves per lse-pass block, 4 or 8 (MFMA path)
   int parts_ld;        // floats per colsum partial row (>= Nk)
   size_t off_stats;    // float2 (m, l) per (split, bh, row)  or lse per (bh,row)
   size_t off_parts;    // float colsum partials [nparts][BH][Nk]; decode: 1 KiB store sink
@@ -119,7 +120,6 @@ struct Plan {
 };
 Plan make_plan(const Shape& s, int dtype);
 int mfma_rows_per_wave();        // packed rows per wave of the MFMA kernels
-int mfma_lse_rows_per_block();   // packed rows per workgroup of the MFMA lse pass
 int decode_max_split();      // largest split-block count per head of the decode kernels
 bool decode_supports(int d, int G);   // (d, G) pairs the decode kernels handle
 

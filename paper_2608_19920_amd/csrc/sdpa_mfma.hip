@@ -777,11 +777,10 @@ __global__ __launch_bounds__(256) void split_reduce(const float* __restrict__ op
 // Both passes use 128-row blocks of 4 waves x 32 rows: few enough registers
 // per wave that two or more waves share each SIMD and hide each other's
 // latencies.
-// The lse pass runs 128-row blocks of 4 waves x 32 rows; the main pass the
-// same, or at d = 128 256-row blocks of 8 waves (one block per CU, the two
-// waves of a SIMD from one block) where the plan finds those fill whole
-// rounds of the CUs.
-constexpr int kLseWaves = 4, kLseQB = 2, kMainQB = 2;
+// Both passes run 128-row blocks of 4 waves x 32 rows, or at d = 128
+// 256-row blocks of 8 waves where the plan finds those fill whole rounds of
+// the CUs (so the waves that share a SIMD come from fewer blocks).
+constexpr int kLseQB = 2, kMainQB = 2;
 
 template <int D>
 hipError_t run(const Shape& s, const Plan& p, const void* q, const void* kc, const void* vc,
@@ -789,7 +788,8 @@ hipError_t run(const Shape& s, const Plan& p, const void* q, const void* kc, con
                float scale, KeyPos kp, hipStream_t st, ScoreAcc acc) {
   const int main_waves = D == 128 && p.main_waves == 8 ? 8 : 4;
   const int ROWS = main_waves * kMainQB * 16;
-  constexpr int LSE_ROWS = kLseWaves * kLseQB * 16;
+  const int lse_waves = D == 128 && p.lse_waves == 8 ? 8 : 4;
+  const int LSE_ROWS = lse_waves * kLseQB * 16;
   Geo g{s.G(), s.T, s.M, s.R(), s.Nk(), s.Tk(), (const bf16_t*)q, (const bf16_t*)kc,
         (const bf16_t*)vc, (const bf16_t*)kn, (const bf16_t*)vn, kp.tp, kp.pos0};
   const bool cache = s.cache_only;
@@ -799,11 +799,19 @@ hipError_t run(const Shape& s, const Plan& p, const void* q, const void* kc, con
   float2* stats = reinterpret_cast<float2*>(ws + p.off_stats);
   float* parts = reinterpret_cast<float*>(ws + p.off_parts);
   float* opart = reinterpret_cast<float*>(ws + p.off_opart);
-  hipError_t e = launch_kernel(K_MFMA_LSE,
-                               cache ? lse_pass<D, kLseWaves, kLseQB, true>
-                                     : lse_pass<D, kLseWaves, kLseQB, false>,
-                               grid_lse, dim3(kLseWaves * 64), st, g, s.Hq, s.Hkv, p.nsplit_lse, c,
-                               stats);
+  auto lse_k = [&](auto kern) {
+    return launch_kernel(K_MFMA_LSE, kern, grid_lse, dim3(lse_waves * 64), st, g, s.Hq, s.Hkv,
+                         p.nsplit_lse, c, stats);
+  };
+  hipError_t e;
+  if constexpr (D == 128) {
+    if (lse_waves == 8)
+      e = cache ? lse_k(lse_pass<D, 8, kLseQB, true>) : lse_k(lse_pass<D, 8, kLseQB, false>);
+    else
+      e = cache ? lse_k(lse_pass<D, 4, kLseQB, true>) : lse_k(lse_pass<D, 4, kLseQB, false>);
+  } else {
+    e = cache ? lse_k(lse_pass<D, 4, kLseQB, true>) : lse_k(lse_pass<D, 4, kLseQB, false>);
+  }
   if (e != hipSuccess) return e;
   auto main = [&](auto kern) {
     return launch_kernel(K_MFMA_MAIN, kern, grid, dim3(main_waves * 64), st, g, s.Hq, s.Hkv,
@@ -834,7 +842,6 @@ hipError_t run(const Shape& s, const Plan& p, const void* q, const void* kc, con
 // Rows of packed queries per workgroup of the MFMA kernels, and per colsum
 // partial (one partial per block).
 int mfma_rows_per_wave() { return kMainQB * 16; }
-int mfma_lse_rows_per_block() { return kLseWaves * kLseQB * 16; }
 
 hipError_t launch_sdpa_mfma(const Shape& s, const Plan& p, const void* q, const void* kc,
                             const void* vc, const void* kn, const void* vn, void* out, float* lse,

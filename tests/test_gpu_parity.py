@@ -82,6 +82,33 @@ def test_sdpa_bf16(shape, path):
     _check_attention(x, "bf16", res, extra=f"path {path}")
 
 
+@pytest.mark.parametrize("shape", [(1, 8, 1, 128, 2048, 2048), (1, 8, 1, 128, 1024, 1024)],
+                         ids=lambda s: "B%dHq%dHkv%dd%dM%dT%d" % s)
+def test_sdpa_bf16_whole_round_grids(shape):
+    """Shapes whose grids fill whole rounds of the CUs, so the plan takes
+    256-row blocks of 8 waves: both passes at the first shape, the main pass
+    at the second; all heads against the oracle, and the chunk step against
+    the three calls."""
+    say(f"sdpa bf16 whole-round grids {shape}")
+    w = W.custom(**dict(zip("B Hq Hkv d M T".split(), shape)), dtype="bf16", heavy_frac=0.02)
+    x = W.make_inputs(w, seed=5)
+    res = U.run_sdpa(x["q"], x["k_cache"], x["v_cache"], x["k_new"], x["v_new"], x["scale"],
+                     "bf16")
+    _check_attention(x, "bf16", res, extra="whole-round grids")
+    B, Hq, Hkv, d, M, T = shape
+    q, kn, vn = (U.to_dev(x[n], torch.bfloat16) for n in ("q", "k_new", "v_new"))
+    out = []
+    for fused in (False, True):
+        st = U.device_state(x, "bf16")
+        bufs = H.alloc_step(B, Hq, Hkv, T, M, d, torch.bfloat16)
+        H.step(st, q, kn, vn, bufs, int(x["pos0"]), float(x["scale"]), fused=fused)
+        torch.cuda.synchronize()
+        out.append([U.to_np(bufs[n]) for n in ("out", "wsum", "evict_idx")] +
+                   [U.to_np(st[n]) for n in ("k_cache", "scores")])
+    for a, b in zip(*out):
+        np.testing.assert_array_equal(a, b)
+
+
 def test_tiny_f32_full_step():
     """The 1x4x2, d64, M256, T64 float32 step: attention, accumulate, evict, insert."""
     wl = W.WORKLOADS["tiny_f32"]

@@ -122,6 +122,26 @@ void timing_end(int kid, hipEvent_t a, hipEvent_t b) {
   g_pending.push_back({kid, a, b});
 }
 
+// Compute units of the current device (cached per device; 256, the MI355X
+// count, where no device answers, e.g. a size query on a host without one).
+static int device_cus() {
+  static std::atomic<int> cached[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) {
+    (void)hipGetLastError();
+    return 256;
+  }
+  int n = cached[dev].load();
+  if (n > 0) return n;
+  if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      n < 1) {
+    (void)hipGetLastError();
+    return 256;
+  }
+  cached[dev].store(n);
+  return n;
+}
+
 Plan make_plan(const Shape& s, int dtype) {
   Plan p{};
   const size_t BH = s.BH(), R = s.R(), Nk = s.Nk();
@@ -141,6 +161,7 @@ Plan make_plan(const Shape& s, int dtype) {
     // two 4-wave or one 8-wave block per CU, the lighter lse pass four
     // 4-wave or two 8-wave blocks). Keep at least 8 key tiles per split.
     const long long ntiles = (Nk + 31) / 32;
+    const long long cus = device_cus();
     auto pick = [&](long long nb, long long target, long long maxs) {
       long long ns = (target + nb - 1) / nb;
       if (ns > ntiles / 8) ns = ntiles / 8;
@@ -150,7 +171,7 @@ Plan make_plan(const Shape& s, int dtype) {
     // main-pass blocks of `waves` waves: their row-tile count and split
     auto main_grid = [&](int waves, long long& nrt_w, int& ns_w) {
       const long long rows_w = (long long)waves * mfma_rows_per_wave();
-      const long long round = 256LL * (8 / waves);
+      const long long round = cus * (8 / waves);
       nrt_w = ((long long)R + rows_w - 1) / rows_w;
       const long long nb = nrt_w * (long long)BH;
       ns_w = pick(nb, round, 8);
@@ -168,19 +189,19 @@ Plan make_plan(const Shape& s, int dtype) {
     p.main_waves = s.d == 128 && main_grid(8, nrt, ns) ? 8 : 4;
     if (p.main_waves == 4) main_grid(4, nrt, ns);
     p.nsplit = ns;
-    // the lse pass: 1,024 blocks of 4 waves, or 512 of 8 where those fill
-    // whole rounds (long cache: the pass 580 against 610 us; more splits
-    // than one round's worth cost the main pass as much in statistics
-    // reads)
+    // the lse pass: a round of 4-wave blocks (1,024 on 256 CUs), or of
+    // 8-wave blocks where those fill whole rounds (long cache: the pass 580
+    // against 610 us; more splits than one round's worth cost the main pass
+    // as much in statistics reads)
     auto lse_grid = [&](int waves, int target, int& ns_w) {
       const long long rows_w = (long long)waves * mfma_rows_per_wave();
       const long long nb = (((long long)R + rows_w - 1) / rows_w) * (long long)BH;
       ns_w = pick(nb, target, 16);
-      return nb * ns_w % (256LL * (16 / waves)) == 0;
+      return nb * ns_w % (cus * (16 / waves)) == 0;
     };
     int nl = 1;
-    p.lse_waves = s.d == 128 && lse_grid(8, 512, nl) ? 8 : 4;
-    if (p.lse_waves == 4) lse_grid(4, 1024, nl);
+    p.lse_waves = s.d == 128 && lse_grid(8, (int)(2 * cus), nl) ? 8 : 4;
+    if (p.lse_waves == 4) lse_grid(4, (int)(4 * cus), nl);
     p.nsplit_lse = nl;
     p.rows_per_part = p.main_waves * mfma_rows_per_wave();
     p.nparts = (int)nrt;

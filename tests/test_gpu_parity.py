@@ -180,6 +180,27 @@ def test_bottomk_few_keys_in_the_bin(M, k, nties):
     np.testing.assert_array_equal(U.gpu_bottomk(s, k), oracle.bottomk(s, k))
 
 
+@pytest.mark.parametrize("M,nbin", [(8192, 256), (8192, 257), (20000, 256), (20000, 2049),
+                                    (40000, 200), (40000, 300)])
+def test_bottomk_bin_size_limits(M, nbin):
+    """The k-th key's first-digit bin holds exactly nbin keys: at most 256
+    are ranked against each other, more take the remaining digits (over the
+    gathered keys up to 2,048 of them in rows of 16,384 slots or more, over
+    the row beyond)."""
+    say(f"bottomk bin size M {M} bin {nbin}")
+    rng = np.random.default_rng(M + nbin)
+    below = 900
+    s = np.empty((2, M), np.float32)
+    for r in range(2):
+        low = rng.uniform(1e-3, 2e-3, below)                 # below the bin
+        inbin = 1.0 + rng.integers(0, 200, nbin) / 2048.0    # [1, 1.1): one first-digit bin, ties
+        high = rng.uniform(100.0, 200.0, M - below - nbin)   # above it
+        row = np.concatenate([low, inbin, high]).astype(np.float32)
+        s[r] = row[rng.permutation(M)]
+    for k in (below + 1, below + nbin // 2, below + nbin):
+        np.testing.assert_array_equal(U.gpu_bottomk(s, k), oracle.bottomk(s, k))
+
+
 def test_bottomk_negative_and_huge_values():
     s = np.array([[3.0, -1.0, np.inf, -np.inf, 0.0, -0.0, 1e-45, -1e-45, 3.4e38, 2.0]],
                  np.float32)

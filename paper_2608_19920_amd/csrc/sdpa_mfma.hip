@@ -208,11 +208,17 @@ __device__ __forceinline__ bool visible(int j, int M, int i) { return j < M || j
 // cache mode, where each key's position relative to the chunk, rp =
 // token_pos - pos0 (a value above every chunk position past the cache), is
 // staged in LDS with the tile and the key is visible to position i iff
-// rp <= i. Rel holds the rp of this lane's 8 keys of the tile.
+// rp <= i; 3 cache mode on a tile every row of the wave sees (positions
+// still staged for the tiles ahead, no mask). Rel holds the rp of this
+// lane's 8 keys of the tile.
 struct Rel {
   int rp[2][4];
 };
 constexpr int kRpFar = 1 << 30;   // above every chunk position
+// ints per staged row of relative positions: the tile's BN positions, then
+// (at index BN) their maximum, which lets a wave whose rows all see every
+// key of the tile skip the mask (16-byte aligned rows)
+constexpr int kRpPitch = BN + 4;
 
 __device__ __forceinline__ void load_rel(Rel& rl, const int* rps, int lane) {
 #pragma unroll
@@ -240,16 +246,31 @@ __device__ __forceinline__ int32_t load_tp(const int32_t* tp_bh, int j0, int M) 
   const int j = j0 + (int)threadIdx.x;
   return (threadIdx.x < BN && j < M) ? tp_bh[j] : 0;
 }
+template <bool MAX>
 __device__ __forceinline__ void store_rp(int* rps, int32_t tpj, int32_t pos0, int j0, int M) {
   // an empty asm that takes and returns the value: the conversion below
   // cannot be moved (or folded into the load) ahead of this point
   asm volatile("" : "+v"(tpj));
+  int v = -kRpFar;
   if (threadIdx.x < BN) {
     const int j = j0 + (int)threadIdx.x;
     const long long r = (long long)tpj - pos0;
-    rps[threadIdx.x] =
-        j >= M ? kRpFar : (r > kRpFar ? kRpFar : (r < -kRpFar ? -kRpFar : (int)r));
+    v = j >= M ? kRpFar : (r > kRpFar ? kRpFar : (r < -kRpFar ? -kRpFar : (int)r));
+    rps[threadIdx.x] = v;
   }
+  if (MAX && threadIdx.x < 64) {   // wave 0: the maximum over lanes 0 .. BN-1
+#pragma unroll
+    for (int o = 1; o < BN; o <<= 1) v = max(v, __shfl_xor(v, o, 64));
+    if (threadIdx.x == 0) rps[BN] = v;
+  }
+}
+
+// Cache mode: whether some row of the wave cannot see some key of the tile
+// (its largest relative position exceeds the wave's first chunk position,
+// qi[0] of lane 0). Wave-uniform.
+template <int NQB>
+__device__ __forceinline__ bool tile_needs_mask(const int* rps, const int (&qi)[NQB]) {
+  return __builtin_amdgcn_readfirstlane(rps[BN]) > __builtin_amdgcn_readfirstlane(qi[0]);
 }
 
 // Tiles [t0, t1) of a row tile's key range [0, ntiles*BN) for split sp.
@@ -326,7 +347,7 @@ template <int MK, int NQB>
 __device__ __forceinline__ void lse_update(const f32x4 (&sacc)[2][NQB], float (&m)[NQB],
                                            float (&l)[NQB], const int (&qi)[NQB], int j0, int M,
                                            int lane, float c, const Rel& rl) {
-  constexpr bool MASKED = MK != 0;
+  constexpr bool MASKED = MK == 1 || MK == 2;
 #pragma unroll
   for (int qb = 0; qb < NQB; ++qb) {
     float x[8];
@@ -365,12 +386,12 @@ struct LseState {
 // S(t+1) and the update with S(t) run; then tile t+2 (in `put`) goes to the
 // LDS buffer tile t-1 used. The loads of tile t+3 are waited for only one
 // tile later.
-template <int MK, int D, int NT, int NQB>
+template <int MK, bool SEL, int D, int NT, int NQB>
 __device__ __forceinline__ void lse_tile(int t, int t0, int t1, const f32x4 (&s_cur)[2][NQB],
                                          f32x4 (&s_nxt)[2][NQB], u32x4 (&fill)[Tile<D, NT>::N],
                                          const u32x4 (&put)[Tile<D, NT>::N], int& rfill,
                                          int rput, const Tile<D, NT>& tl,
-                                         bf16_t (*Ks)[BN * kstride(D)], int (*rps)[BN],
+                                         bf16_t (*Ks)[BN * kstride(D)], int (*rps)[kRpPitch],
                                          const bf16x8 (&qf)[NQB][D / 32], float (&m)[NQB],
                                          float (&l)[NQB], const int (&qi)[NQB],
                                          const bf16_t* kc_bh, const bf16_t* kn_bh,
@@ -378,37 +399,61 @@ __device__ __forceinline__ void lse_tile(int t, int t0, int t1, const f32x4 (&s_
   const int b0 = (t - t0) % NBUF, b1 = (t + 1 - t0) % NBUF, b2 = (t + 2 - t0) % NBUF;
   const int jn = min(t + 3, t1 - 1) * BN;
   load_tile<D, NT>(fill, tl, kc_bh, kn_bh, jn, g.M, g.Nk);
-  if (MK == 2) rfill = load_tp(tp_bh, jn, g.M);
+  if (MK >= 2) rfill = load_tp(tp_bh, jn, g.M);
   Rel rl;
   if (MK == 2) load_rel(rl, rps[b0], lane);
   scores_tile<D, NQB>(s_nxt, Ks[b1], qf, lane);
   lse_update<MK, NQB>(s_cur, m, l, qi, t * BN, g.M, lane, c, rl);
   interleave<2 * NQB * (D / 32), MK ? 8 : 5>();
   store_tile<D, NT>(Ks[b2], tl.loff, put);
-  if (MK == 2) store_rp(rps[b2], rput, g.pos0, min(t + 2, t1 - 1) * BN, g.M);
+  if (MK >= 2) store_rp<SEL>(rps[b2], rput, g.pos0, min(t + 2, t1 - 1) * BN, g.M);
   __syncthreads();
+}
+
+// Cache mode with SEL (MK 2): a tile every row of the wave sees runs the
+// body without the mask (MK 3). The choice is wave-uniform and made per
+// tile, between two straight-line bodies.
+template <int MK, bool SEL, int D, int NT, int NQB>
+__device__ __forceinline__ void lse_tile_sel(int t, int t0, int t1, const f32x4 (&s_cur)[2][NQB],
+                                             f32x4 (&s_nxt)[2][NQB],
+                                             u32x4 (&fill)[Tile<D, NT>::N],
+                                             const u32x4 (&put)[Tile<D, NT>::N], int& rfill,
+                                             int rput, const Tile<D, NT>& tl,
+                                             bf16_t (*Ks)[BN * kstride(D)],
+                                             int (*rps)[kRpPitch],
+                                             const bf16x8 (&qf)[NQB][D / 32], float (&m)[NQB],
+                                             float (&l)[NQB], const int (&qi)[NQB],
+                                             const bf16_t* kc_bh, const bf16_t* kn_bh,
+                                             const int32_t* tp_bh, const Geo& g, int lane,
+                                             float c) {
+  if (SEL && MK == 2 && !tile_needs_mask<NQB>(rps[(t - t0) % NBUF], qi))
+    lse_tile<3, SEL, D, NT, NQB>(t, t0, t1, s_cur, s_nxt, fill, put, rfill, rput, tl, Ks, rps,
+                                 qf, m, l, qi, kc_bh, kn_bh, tp_bh, g, lane, c);
+  else
+    lse_tile<MK, SEL, D, NT, NQB>(t, t0, t1, s_cur, s_nxt, fill, put, rfill, rput, tl, Ks, rps,
+                                  qf, m, l, qi, kc_bh, kn_bh, tp_bh, g, lane, c);
 }
 
 // Tiles [ta, tb): two tiles per trip with the roles of the register sets
 // swapped, so no accumulator or staging register is copied; an odd last
 // tile restores the state invariant with one copy.
-template <int MK, int D, int NT, int NQB>
+template <int MK, bool SEL, int D, int NT, int NQB>
 __device__ __forceinline__ void lse_loop(int ta, int tb, int t0, int t1, LseState<D, NT, NQB>& S,
                                          const Tile<D, NT>& tl,
-                                         bf16_t (*Ks)[BN * kstride(D)], int (*rps)[BN],
+                                         bf16_t (*Ks)[BN * kstride(D)], int (*rps)[kRpPitch],
                                          const bf16x8 (&qf)[NQB][D / 32], float (&m)[NQB],
                                          float (&l)[NQB], const int (&qi)[NQB],
                                          const bf16_t* kc_bh, const bf16_t* kn_bh,
                                          const int32_t* tp_bh, const Geo& g, int lane, float c) {
   int t = ta;
   for (; t + 1 < tb; t += 2) {
-    lse_tile<MK, D, NT, NQB>(t, t0, t1, S.sa, S.sb, S.kb, S.ka, S.rb, S.ra, tl, Ks, rps, qf, m, l,
+    lse_tile_sel<MK, SEL, D, NT, NQB>(t, t0, t1, S.sa, S.sb, S.kb, S.ka, S.rb, S.ra, tl, Ks, rps, qf, m, l,
                              qi, kc_bh, kn_bh, tp_bh, g, lane, c);
-    lse_tile<MK, D, NT, NQB>(t + 1, t0, t1, S.sb, S.sa, S.ka, S.kb, S.ra, S.rb, tl, Ks, rps, qf,
+    lse_tile_sel<MK, SEL, D, NT, NQB>(t + 1, t0, t1, S.sb, S.sa, S.ka, S.kb, S.ra, S.rb, tl, Ks, rps, qf,
                              m, l, qi, kc_bh, kn_bh, tp_bh, g, lane, c);
   }
   if (t < tb) {
-    lse_tile<MK, D, NT, NQB>(t, t0, t1, S.sa, S.sb, S.kb, S.ka, S.rb, S.ra, tl, Ks, rps, qf, m, l,
+    lse_tile_sel<MK, SEL, D, NT, NQB>(t, t0, t1, S.sa, S.sb, S.kb, S.ka, S.rb, S.ra, tl, Ks, rps, qf, m, l,
                              qi, kc_bh, kn_bh, tp_bh, g, lane, c);
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -429,13 +474,14 @@ __device__ __forceinline__ int mask_start(const Geo& g, int row0, int t0, int t1
   return min(t1, max(t0, first_masked_tile(g.M, min(row0, g.R - 1) / g.G)));
 }
 
-template <int D, int NW, int NQB, bool CACHE>
+// SEL (cache mode only): tiles every row of a wave sees skip the mask.
+template <int D, int NW, int NQB, bool CACHE, bool SEL>
 __global__ __launch_bounds__(NW * 64) void lse_pass(Geo g, int Hq, int Hkv, int nsplit,
                                                     float c_log2, float2* __restrict__ stats) {
   constexpr int NT = NW * 64, ROWS = NW * NQB * 16;
   constexpr int MKM = CACHE ? 2 : 1;   // mask mode of the masked tiles
   __shared__ __attribute__((aligned(16))) bf16_t Ks[NBUF][BN * kstride(D)];
-  __shared__ __attribute__((aligned(16))) int rps[NBUF][BN];
+  __shared__ __attribute__((aligned(16))) int rps[NBUF][kRpPitch];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const BlockId id = block_id(nsplit);
   const int rt = id.rt, sp = id.sp;
@@ -468,8 +514,8 @@ __global__ __launch_bounds__(NW * 64) void lse_pass(Geo g, int Hq, int Hkv, int 
     load_tile<D, NT>(S.ka, tl, kc_bh, kn_bh, t0 * BN, g.M, g.Nk);
     load_tile<D, NT>(S.kb, tl, kc_bh, kn_bh, j1, g.M, g.Nk);
     if (CACHE) {
-      store_rp(rps[0], load_tp(tp_bh, t0 * BN, g.M), g.pos0, t0 * BN, g.M);
-      store_rp(rps[1], load_tp(tp_bh, j1, g.M), g.pos0, j1, g.M);
+      store_rp<SEL>(rps[0], load_tp(tp_bh, t0 * BN, g.M), g.pos0, t0 * BN, g.M);
+      store_rp<SEL>(rps[1], load_tp(tp_bh, j1, g.M), g.pos0, j1, g.M);
       S.ra = load_tp(tp_bh, j2, g.M);
     }
     store_tile<D, NT>(Ks[0], tl.loff, S.ka);
@@ -477,9 +523,9 @@ __global__ __launch_bounds__(NW * 64) void lse_pass(Geo g, int Hq, int Hkv, int 
     load_tile<D, NT>(S.ka, tl, kc_bh, kn_bh, j2, g.M, g.Nk);
     __syncthreads();
     scores_tile<D, NQB>(S.sa, Ks[0], qf, lane);
-    lse_loop<0, D, NT, NQB>(t0, t_mask, t0, t1, S, tl, Ks, rps, qf, m, l, qi, kc_bh, kn_bh,
+    lse_loop<0, false, D, NT, NQB>(t0, t_mask, t0, t1, S, tl, Ks, rps, qf, m, l, qi, kc_bh, kn_bh,
                             tp_bh, g, lane, c_log2);
-    lse_loop<MKM, D, NT, NQB>(t_mask, t1, t0, t1, S, tl, Ks, rps, qf, m, l, qi, kc_bh, kn_bh,
+    lse_loop<MKM, SEL, D, NT, NQB>(t_mask, t1, t0, t1, S, tl, Ks, rps, qf, m, l, qi, kc_bh, kn_bh,
                               tp_bh, g, lane, c_log2);
   }
   // merge the four lane groups (disjoint key subsets of the same query)
@@ -560,7 +606,7 @@ __device__ __forceinline__ void main_tile(
     f32x4 (&oacc)[D / 16][NQB], u32x4 (&kfill)[Tile<D, NT>::N],
     u32x4 (&vfill)[Tile<D, NT>::N], const u32x4 (&kput)[Tile<D, NT>::N],
     const u32x4 (&vput)[Tile<D, NT>::N], int& rfill, int rput, const Tile<D, NT>& tl,
-    bf16_t (*Ks)[BN * kstride(D)], bf16_t (*Vs)[BN * vstride(D)], int (*rps)[BN],
+    bf16_t (*Ks)[BN * kstride(D)], bf16_t (*Vs)[BN * vstride(D)], int (*rps)[kRpPitch],
     const bf16x8 (&qf)[NQB][D / 32], const float (&lam)[NQB], const int (&qi)[NQB],
     float (*cs_lds)[NT / 64][BN], float* prow, const bf16_t* kc_bh, const bf16_t* kn_bh,
     const bf16_t* vc_bh, const bf16_t* vn_bh, const int32_t* tp_bh, const Geo& g, int lane,
@@ -571,7 +617,7 @@ __device__ __forceinline__ void main_tile(
   const int jn = min(t + 3, t1 - 1) * BN;
   load_tile<D, NT>(kfill, tl, kc_bh, kn_bh, jn, g.M, g.Nk);
   load_tile<D, NT>(vfill, tl, vc_bh, vn_bh, jn, g.M, g.Nk);
-  if (MK == 2) rfill = load_tp(tp_bh, jn, g.M);
+  if (MK >= 2) rfill = load_tp(tp_bh, jn, g.M);
   Rel rl;
   if (MK == 2) load_rel(rl, rps[b0], lane);
   bf16x8 pb[NQB];
@@ -582,7 +628,7 @@ __device__ __forceinline__ void main_tile(
   interleave<NQB * (D / 16), 1>();
   store_tile<D, NT>(Ks[b2], tl.loff, kput);
   store_tile<D, NT>(Vs[b2], tl.vloff, vput);
-  if (MK == 2) store_rp(rps[b2], rput, g.pos0, min(t + 2, t1 - 1) * BN, g.M);
+  if (MK >= 2) store_rp<false>(rps[b2], rput, g.pos0, min(t + 2, t1 - 1) * BN, g.M);
   __syncthreads();
   if (threadIdx.x < BN) {
     const float (*cs)[BN] = cs_lds[(t - t0) & 1];
@@ -597,7 +643,7 @@ template <int MK, int D, int NT, int NQB>
 __device__ __forceinline__ void main_loop(int ta, int tb, int t0, int t1, MainState<D, NT, NQB>& S,
                                           const Tile<D, NT>& tl,
                                           bf16_t (*Ks)[BN * kstride(D)],
-                                          bf16_t (*Vs)[BN * vstride(D)], int (*rps)[BN],
+                                          bf16_t (*Vs)[BN * vstride(D)], int (*rps)[kRpPitch],
                                           const bf16x8 (&qf)[NQB][D / 32],
                                           const float (&lam)[NQB], const int (&qi)[NQB],
                                           float (*cs_lds)[NT / 64][BN], float* prow,
@@ -642,7 +688,7 @@ __global__ __launch_bounds__(NW * 64) void main_pass(Geo g, int Hq, int Hkv, int
   constexpr int MKM = CACHE ? 2 : 1;   // mask mode of the masked tiles
   __shared__ __attribute__((aligned(16))) bf16_t Ks[NBUF][BN * kstride(D)];
   __shared__ __attribute__((aligned(16))) bf16_t Vs[NBUF][BN * vstride(D)];
-  __shared__ __attribute__((aligned(16))) int rps[NBUF][BN];
+  __shared__ __attribute__((aligned(16))) int rps[NBUF][kRpPitch];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const BlockId id = block_id(nsplit);
   const int rt = id.rt, sp = id.sp;
@@ -707,8 +753,8 @@ __global__ __launch_bounds__(NW * 64) void main_pass(Geo g, int Hq, int Hkv, int
     load_tile<D, NT>(S.kb, tl, kc_bh, kn_bh, j1, g.M, g.Nk);
     load_tile<D, NT>(S.vb, tl, vc_bh, vn_bh, j1, g.M, g.Nk);
     if (CACHE) {
-      store_rp(rps[0], load_tp(tp_bh, t0 * BN, g.M), g.pos0, t0 * BN, g.M);
-      store_rp(rps[1], load_tp(tp_bh, j1, g.M), g.pos0, j1, g.M);
+      store_rp<false>(rps[0], load_tp(tp_bh, t0 * BN, g.M), g.pos0, t0 * BN, g.M);
+      store_rp<false>(rps[1], load_tp(tp_bh, j1, g.M), g.pos0, j1, g.M);
       S.ra = load_tp(tp_bh, j2, g.M);
     }
     store_tile<D, NT>(Ks[0], tl.loff, S.ka);
@@ -789,6 +835,9 @@ hipError_t run(const Shape& s, const Plan& p, const void* q, const void* kc, con
   const int main_waves = D == 128 && p.main_waves == 8 ? 8 : 4;
   const int ROWS = main_waves * kMainQB * 16;
   const int lse_waves = D == 128 && p.lse_waves == 8 ? 8 : 4;
+  // cache mode with few chunk tokens among the slots: most tiles hold no
+  // token some row of a wave cannot see, and the lse pass skips their mask
+  const bool sel = s.cache_only && (long long)s.T * 16 <= (long long)s.M;
   const int LSE_ROWS = lse_waves * kLseQB * 16;
   Geo g{s.G(), s.T, s.M, s.R(), s.Nk(), s.Tk(), (const bf16_t*)q, (const bf16_t*)kc,
         (const bf16_t*)vc, (const bf16_t*)kn, (const bf16_t*)vn, kp.tp, kp.pos0};
@@ -806,11 +855,17 @@ hipError_t run(const Shape& s, const Plan& p, const void* q, const void* kc, con
   hipError_t e;
   if constexpr (D == 128) {
     if (lse_waves == 8)
-      e = cache ? lse_k(lse_pass<D, 8, kLseQB, true>) : lse_k(lse_pass<D, 8, kLseQB, false>);
+      e = !cache ? lse_k(lse_pass<D, 8, kLseQB, false, false>)
+          : sel  ? lse_k(lse_pass<D, 8, kLseQB, true, true>)
+                 : lse_k(lse_pass<D, 8, kLseQB, true, false>);
     else
-      e = cache ? lse_k(lse_pass<D, 4, kLseQB, true>) : lse_k(lse_pass<D, 4, kLseQB, false>);
+      e = !cache ? lse_k(lse_pass<D, 4, kLseQB, false, false>)
+          : sel  ? lse_k(lse_pass<D, 4, kLseQB, true, true>)
+                 : lse_k(lse_pass<D, 4, kLseQB, true, false>);
   } else {
-    e = cache ? lse_k(lse_pass<D, 4, kLseQB, true>) : lse_k(lse_pass<D, 4, kLseQB, false>);
+    e = !cache ? lse_k(lse_pass<D, 4, kLseQB, false, false>)
+        : sel  ? lse_k(lse_pass<D, 4, kLseQB, true, true>)
+               : lse_k(lse_pass<D, 4, kLseQB, true, false>);
   }
   if (e != hipSuccess) return e;
   auto main = [&](auto kern) {

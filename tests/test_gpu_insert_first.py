@@ -32,6 +32,8 @@ SHAPES = [  # B, Hq, Hkv, d, M, T, dtype, forced path (-1 automatic)
     (1, 4, 1, 64, 37, 1, "bf16", -1),
     (2, 4, 2, 64, 500, 1, "f32", -1),
     (1, 8, 2, 128, 129, 1, "bf16", 1),         # MFMA kernels with one query
+    (2, 8, 2, 128, 2048, 96, "bf16", -1),      # few chunk tokens among the slots: the lse
+    (1, 8, 2, 64, 1500, 64, "bf16", -1),       #   pass skips the mask on tiles a wave sees
 ]
 
 
@@ -91,6 +93,7 @@ STEP_SHAPES = [  # B, Hq, Hkv, d, M, T, dtype
     (2, 8, 2, 64, 5000, 1, "bf16"),     # T = 1, more slots than the fused kernel prefetches
     (1, 8, 2, 128, 4133, 1, "bf16"),    # T = 1, d = 128, ragged last step
     (2, 8, 2, 128, 700, 64, "bf16"),
+    (1, 8, 2, 128, 2048, 96, "bf16"),   # T * 16 <= M: tiles without a mask in the lse pass
     (1, 4, 2, 64, 256, 64, "f32"),
     (2, 4, 2, 64, 300, 1, "f32"),
 ]

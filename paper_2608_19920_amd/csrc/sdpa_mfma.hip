@@ -835,9 +835,11 @@ hipError_t run(const Shape& s, const Plan& p, const void* q, const void* kc, con
   const int main_waves = D == 128 && p.main_waves == 8 ? 8 : 4;
   const int ROWS = main_waves * kMainQB * 16;
   const int lse_waves = D == 128 && p.lse_waves == 8 ? 8 : 4;
-  // cache mode with few chunk tokens among the slots: most tiles hold no
-  // token some row of a wave cannot see, and the lse pass skips their mask
-  const bool sel = s.cache_only && (long long)s.T * 16 <= (long long)s.M;
+  // cache mode: the lse pass skips the mask on tiles every row of a wave
+  // sees where the chunk's tokens are few among the slots (most tiles hold
+  // none some row cannot see), and in 8-wave blocks, whose kernel fits four
+  // waves per SIMD (116 registers) only in this form (130 without it)
+  const bool sel = s.cache_only && (lse_waves == 8 || (long long)s.T * 16 <= (long long)s.M);
   const int LSE_ROWS = lse_waves * kLseQB * 16;
   Geo g{s.G(), s.T, s.M, s.R(), s.Nk(), s.Tk(), (const bf16_t*)q, (const bf16_t*)kc,
         (const bf16_t*)vc, (const bf16_t*)kn, (const bf16_t*)vn, kp.tp, kp.pos0};

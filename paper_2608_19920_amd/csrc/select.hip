@@ -33,7 +33,14 @@ __global__ __launch_bounds__(256) void colsum_reduce_kernel(const float* __restr
   const size_t stride = (size_t)BH * ld;
   float s = 0.f;
   int p = p0;
-  // loads four ahead, additions in increasing p (bitwise reproducible)
+  // sixteen loads in flight, additions in increasing p (bitwise reproducible)
+  for (; p + 15 < nparts; p += 16, src += 16 * stride) {
+    float a[16];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) a[e] = src[e * stride];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) s += a[e];
+  }
   for (; p + 3 < nparts; p += 4, src += 4 * stride) {
     const float a0 = src[0], a1 = src[stride], a2 = src[2 * stride], a3 = src[3 * stride];
     s += a0;

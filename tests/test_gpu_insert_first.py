@@ -34,6 +34,7 @@ SHAPES = [  # B, Hq, Hkv, d, M, T, dtype, forced path (-1 automatic)
     (1, 8, 2, 128, 129, 1, "bf16", 1),         # MFMA kernels with one query
     (2, 8, 2, 128, 2048, 96, "bf16", -1),      # few chunk tokens among the slots: the lse
     (1, 8, 2, 64, 1500, 64, "bf16", -1),       #   pass skips the mask on tiles a wave sees
+    (1, 8, 1, 128, 4096, 2048, "bf16", -1),    # grids of whole rounds: 8-wave blocks
 ]
 
 

@@ -447,14 +447,14 @@ __device__ __forceinline__ void lse_loop(int ta, int tb, int t0, int t1, LseStat
                                          const int32_t* tp_bh, const Geo& g, int lane, float c) {
   int t = ta;
   for (; t + 1 < tb; t += 2) {
-    lse_tile_sel<MK, SEL, D, NT, NQB>(t, t0, t1, S.sa, S.sb, S.kb, S.ka, S.rb, S.ra, tl, Ks, rps, qf, m, l,
-                             qi, kc_bh, kn_bh, tp_bh, g, lane, c);
-    lse_tile_sel<MK, SEL, D, NT, NQB>(t + 1, t0, t1, S.sb, S.sa, S.ka, S.kb, S.ra, S.rb, tl, Ks, rps, qf,
-                             m, l, qi, kc_bh, kn_bh, tp_bh, g, lane, c);
+    lse_tile_sel<MK, SEL, D, NT, NQB>(t, t0, t1, S.sa, S.sb, S.kb, S.ka, S.rb, S.ra, tl, Ks, rps,
+                                      qf, m, l, qi, kc_bh, kn_bh, tp_bh, g, lane, c);
+    lse_tile_sel<MK, SEL, D, NT, NQB>(t + 1, t0, t1, S.sb, S.sa, S.ka, S.kb, S.ra, S.rb, tl, Ks,
+                                      rps, qf, m, l, qi, kc_bh, kn_bh, tp_bh, g, lane, c);
   }
   if (t < tb) {
-    lse_tile_sel<MK, SEL, D, NT, NQB>(t, t0, t1, S.sa, S.sb, S.kb, S.ka, S.rb, S.ra, tl, Ks, rps, qf, m, l,
-                             qi, kc_bh, kn_bh, tp_bh, g, lane, c);
+    lse_tile_sel<MK, SEL, D, NT, NQB>(t, t0, t1, S.sa, S.sb, S.kb, S.ka, S.rb, S.ra, tl, Ks, rps,
+                                      qf, m, l, qi, kc_bh, kn_bh, tp_bh, g, lane, c);
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -523,10 +523,10 @@ __global__ __launch_bounds__(NW * 64) void lse_pass(Geo g, int Hq, int Hkv, int 
     load_tile<D, NT>(S.ka, tl, kc_bh, kn_bh, j2, g.M, g.Nk);
     __syncthreads();
     scores_tile<D, NQB>(S.sa, Ks[0], qf, lane);
-    lse_loop<0, false, D, NT, NQB>(t0, t_mask, t0, t1, S, tl, Ks, rps, qf, m, l, qi, kc_bh, kn_bh,
-                            tp_bh, g, lane, c_log2);
-    lse_loop<MKM, SEL, D, NT, NQB>(t_mask, t1, t0, t1, S, tl, Ks, rps, qf, m, l, qi, kc_bh, kn_bh,
-                              tp_bh, g, lane, c_log2);
+    lse_loop<0, false, D, NT, NQB>(t0, t_mask, t0, t1, S, tl, Ks, rps, qf, m, l, qi, kc_bh,
+                                   kn_bh, tp_bh, g, lane, c_log2);
+    lse_loop<MKM, SEL, D, NT, NQB>(t_mask, t1, t0, t1, S, tl, Ks, rps, qf, m, l, qi, kc_bh,
+                                   kn_bh, tp_bh, g, lane, c_log2);
   }
   // merge the four lane groups (disjoint key subsets of the same query)
 #pragma unroll

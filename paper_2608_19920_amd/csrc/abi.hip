@@ -124,7 +124,7 @@ void timing_end(int kid, hipEvent_t a, hipEvent_t b) {
 
 // Compute units of the current device (cached per device; 256, the MI355X
 // count, where no device answers, e.g. a size query on a host without one).
-static int device_cus() {
+int device_cus() {
   static std::atomic<int> cached[64];
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) {

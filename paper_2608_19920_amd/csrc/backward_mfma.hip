@@ -140,27 +140,27 @@ __device__ __forceinline__ void store4(bf16_t* p, const f32x4& v, float mul) {
   *reinterpret_cast<u16x4*>(p) = r;
 }
 
-// 16-byte chunk e of a 32-row tile for this thread: row (tid + e*256) / (D/8),
-// part (tid + e*256) % (D/8).
-template <int D>
-constexpr int tile_chunks() { return kTile * (D / 8) / kNT; }
+// 16-byte chunk e of a 32-row tile for this thread of NT: row (tid + e*NT) /
+// (D/8), part (tid + e*NT) % (D/8).
+template <int D, int NT = kNT>
+constexpr int tile_chunks() { return kTile * (D / 8) / NT; }
 
 // Keys [j0, j0 + 32) of head bh into registers (zero past the keys); in
 // cache mode threads 0..31 also fetch the keys' token positions (turned into
 // rel only when stored, so that no wait for the loads happens here). The
 // four bases come in as values so that the cache/chunk choice stays a
 // register select.
-template <int D, bool CACHE>
-__device__ __forceinline__ void load_key_tile(u32x4 (&kr)[tile_chunks<D>()],
-                                              u32x4 (&vr)[tile_chunks<D>()], int& relr,
+template <int D, bool CACHE, int NT = kNT>
+__device__ __forceinline__ void load_key_tile(u32x4 (&kr)[(tile_chunks<D, NT>())],
+                                              u32x4 (&vr)[(tile_chunks<D, NT>())], int& relr,
                                               const bf16_t* kc, const bf16_t* kn,
                                               const bf16_t* vc, const bf16_t* vn, const BArgs& a,
                                               size_t bh, int j0) {
   constexpr int CH = D / 8;
   const int tid = threadIdx.x;
 #pragma unroll
-  for (int e = 0; e < tile_chunks<D>(); ++e) {
-    const int c = tid + e * kNT, j = j0 + c / CH, part = c % CH;
+  for (int e = 0; e < tile_chunks<D, NT>(); ++e) {
+    const int c = tid + e * NT, j = j0 + c / CH, part = c % CH;
     const bool ok = j < a.Nk;
     const int jj = ok ? j : 0;
     kr[e] = load16(key_ptr<D>(kc, kn, a.M, a.T, bh, jj) + part * 8, ok);
@@ -172,16 +172,16 @@ __device__ __forceinline__ void load_key_tile(u32x4 (&kr)[tile_chunks<D>()],
 // Packed rows [r0, r0 + 32) of head (b, h): q and dout into registers, and in
 // threads 0..31 the row's lse (raw, converted when stored), D and chunk
 // position.
-template <int D>
-__device__ __forceinline__ void load_row_tile(u32x4 (&qr)[tile_chunks<D>()],
-                                              u32x4 (&orr)[tile_chunks<D>()], float& lamr,
+template <int D, int NT = kNT>
+__device__ __forceinline__ void load_row_tile(u32x4 (&qr)[(tile_chunks<D, NT>())],
+                                              u32x4 (&orr)[(tile_chunks<D, NT>())], float& lamr,
                                               float& dotr, int& iposr, const BArgs& a, int b,
                                               int h, size_t bh, int r0) {
   constexpr int CH = D / 8;
   const int tid = threadIdx.x;
 #pragma unroll
-  for (int e = 0; e < tile_chunks<D>(); ++e) {
-    const int c = tid + e * kNT, r = r0 + c / CH, part = c % CH;
+  for (int e = 0; e < tile_chunks<D, NT>(); ++e) {
+    const int c = tid + e * NT, r = r0 + c / CH, part = c % CH;
     const bool ok = r < a.R;
     const size_t off = (ok ? row_off(a, b, h, r) : 0) * D + part * 8;
     qr[e] = load16(a.q + off, ok);
@@ -197,22 +197,26 @@ __device__ __forceinline__ void load_row_tile(u32x4 (&qr)[tile_chunks<D>()],
 }
 
 // Registers of a 32-row tile into two LDS tiles of pitch D + kPad.
-template <int D>
-__device__ __forceinline__ void store_tile(bf16_t* A, bf16_t* B, const u32x4 (&ra)[tile_chunks<D>()],
-                                           const u32x4 (&rb)[tile_chunks<D>()]) {
+template <int D, int NT = kNT>
+__device__ __forceinline__ void store_tile(bf16_t* A, bf16_t* B,
+                                           const u32x4 (&ra)[(tile_chunks<D, NT>())],
+                                           const u32x4 (&rb)[(tile_chunks<D, NT>())]) {
   constexpr int CH = D / 8, P = pitch<D>();
 #pragma unroll
-  for (int e = 0; e < tile_chunks<D>(); ++e) {
-    const int c = threadIdx.x + e * kNT, row = c / CH, part = c % CH;
+  for (int e = 0; e < tile_chunks<D, NT>(); ++e) {
+    const int c = threadIdx.x + e * NT, row = c / CH, part = c % CH;
     *reinterpret_cast<u32x4*>(&A[row * P + part * 8]) = ra[e];
     *reinterpret_cast<u32x4*>(&B[row * P + part * 8]) = rb[e];
   }
 }
 
 // ---------------------------------------------------------------- rows passes
-template <int D, bool DQ, bool CACHE>
-__global__ __launch_bounds__(kNT) void bwd_rows(BArgs a) {
-  constexpr int P = pitch<D>(), KS = D / 32, NL = tile_chunks<D>();
+// NW waves of 32 rows per block (4, or 8 for the dq pass where the plan
+// finds its grid fills whole rounds of the CUs).
+template <int D, bool DQ, bool CACHE, int NW = kW>
+__global__ __launch_bounds__(NW * 64) void bwd_rows(BArgs a) {
+  constexpr int NT = NW * 64, RB = NW * 32;
+  constexpr int P = pitch<D>(), KS = D / 32, NL = tile_chunks<D, NT>();
   __shared__ __attribute__((aligned(16))) bf16_t Ks[2][kTile * P];
   __shared__ __attribute__((aligned(16))) bf16_t Vs[2][kTile * P];
   __shared__ __attribute__((aligned(16))) int rel_s[2][kTile];
@@ -224,8 +228,8 @@ __global__ __launch_bounds__(kNT) void bwd_rows(BArgs a) {
   const int b = bhi / a.Hkv, h = bhi % a.Hkv;
   // x = split * (row tiles) + row tile: the blocks of one key range are
   // consecutive, so they share their K/V tiles in one L2
-  const int nrt = (a.R + kRB - 1) / kRB;
-  const int sp = xb / nrt, rblk = (xb % nrt) * kRB, wrow0 = rblk + wave * 32;
+  const int nrt = (a.R + RB - 1) / RB;
+  const int sp = xb / nrt, rblk = (xb % nrt) * RB, wrow0 = rblk + wave * 32;
   const bool live = wrow0 < a.R;
   const int imin = wrow0 / a.G;
 
@@ -253,7 +257,7 @@ __global__ __launch_bounds__(kNT) void bwd_rows(BArgs a) {
   }
 
   const int kv_end =
-      CACHE ? a.M : kv_end_for_rows(min(rblk + kRB, a.R), a.G, a.T, a.M, a.Nk - a.M);
+      CACHE ? a.M : kv_end_for_rows(min(rblk + RB, a.R), a.G, a.T, a.M, a.Nk - a.M);
   // this split's share of the block's key tiles (possibly none)
   const int ntiles_all = (kv_end + kTile - 1) / kTile;
   const int tb = (int)((long long)sp * ntiles_all / a.ns);
@@ -269,14 +273,16 @@ __global__ __launch_bounds__(kNT) void bwd_rows(BArgs a) {
     for (int qb = 0; qb < 2; ++qb) dqacc[db][qb] = f32x4{0.f, 0.f, 0.f, 0.f};
   float dsum[2] = {0.f, 0.f};
 
-  if (tb < te) load_key_tile<D, CACHE>(kr, vr, relr, a.kc, a.kn, a.vc, a.vn, a, bh, tb * kTile);
+  if (tb < te)
+    load_key_tile<D, CACHE, NT>(kr, vr, relr, a.kc, a.kn, a.vc, a.vn, a, bh, tb * kTile);
   for (int t = tb; t < te; ++t) {
     const int buf = (t - tb) & 1, j0 = t * kTile;
-    store_tile<D>(Ks[buf], Vs[buf], kr, vr);
+    store_tile<D, NT>(Ks[buf], Vs[buf], kr, vr);
     if (CACHE && tid < kTile) rel_s[buf][tid] = key_rel_of(a, j0 + tid, relr);
     __syncthreads();
     if (t + 1 < te)
-      load_key_tile<D, CACHE>(kr, vr, relr, a.kc, a.kn, a.vc, a.vn, a, bh, (t + 1) * kTile);
+      load_key_tile<D, CACHE, NT>(kr, vr, relr, a.kc, a.kn, a.vc, a.vn, a, bh,
+                                  (t + 1) * kTile);
     if (!live) continue;
     const bf16_t* Kt = Ks[buf];
     const bf16_t* Vt = Vs[buf];
@@ -357,9 +363,10 @@ __global__ __launch_bounds__(kNT) void bwd_rows(BArgs a) {
 
 // ------------------------------------------------------------------ keys pass
 // A wave owns NKB*16 keys (NKB key blocks of 16).
-template <int D, int NKB, bool CACHE>
-__global__ __launch_bounds__(kNT) void bwd_keys(BArgs a) {
-  constexpr int P = pitch<D>(), KS = D / 32, NL = tile_chunks<D>();
+template <int D, int NKB, bool CACHE, int NW = kW>
+__global__ __launch_bounds__(NW * 64) void bwd_keys(BArgs a) {
+  constexpr int NT = NW * 64;
+  constexpr int P = pitch<D>(), KS = D / 32, NL = tile_chunks<D, NT>();
   __shared__ __attribute__((aligned(16))) bf16_t Qs[2][kTile * P];
   __shared__ __attribute__((aligned(16))) bf16_t Os[2][kTile * P];
   __shared__ __attribute__((aligned(16))) float lam_s[2][kTile];
@@ -371,7 +378,7 @@ __global__ __launch_bounds__(kNT) void bwd_keys(BArgs a) {
   block_coords(xb, bhi);
   const size_t bh = bhi;
   const int b = bhi / a.Hkv, h = bhi % a.Hkv;
-  const int kblk = xb * (kW * 16 * NKB), kw0 = kblk + wave * 16 * NKB;
+  const int kblk = xb * (NW * 16 * NKB), kw0 = kblk + wave * 16 * NKB;
   const bool live = kw0 < a.Nk;
 
   // this lane's keys kw0 + 16kb + l16: K and V as B operands (k = features)
@@ -415,17 +422,18 @@ __global__ __launch_bounds__(kNT) void bwd_keys(BArgs a) {
 #pragma unroll
     for (int kb = 0; kb < NKB; ++kb) dkacc[db][kb] = dvacc[db][kb] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  if (t0 < t1) load_row_tile<D>(qr, orr, lamr, dotr, iposr, a, b, h, bh, t0 * kTile);
+  if (t0 < t1) load_row_tile<D, NT>(qr, orr, lamr, dotr, iposr, a, b, h, bh, t0 * kTile);
   for (int t = t0; t < t1; ++t) {
     const int buf = (t - t0) & 1;
-    store_tile<D>(Qs[buf], Os[buf], qr, orr);
+    store_tile<D, NT>(Qs[buf], Os[buf], qr, orr);
     if (tid < kTile) {
       lam_s[buf][tid] = lambda_of(lamr);
       dot_s[buf][tid] = dotr;
       ipos_s[buf][tid] = iposr;
     }
     __syncthreads();
-    if (t + 1 < t1) load_row_tile<D>(qr, orr, lamr, dotr, iposr, a, b, h, bh, (t + 1) * kTile);
+    if (t + 1 < t1)
+      load_row_tile<D, NT>(qr, orr, lamr, dotr, iposr, a, b, h, bh, (t + 1) * kTile);
     if (!live) continue;
     const bf16_t* Qt = Qs[buf];
     const bf16_t* Ot = Os[buf];
@@ -519,7 +527,18 @@ hipError_t run(const Shape& s, const BackwardPlan& pl, BArgs a, hipStream_t st) 
                                dim3(kNT), st, a);
   if (e != hipSuccess) return e;
   a.ns = pl.ns_dq;
-  e = launch_kernel(K_BWD_DQ, bwd_rows<D, true, CACHE>, dim3(nrt * a.ns, BH), dim3(kNT), st, a);
+  if constexpr (D == 128) {
+    if (pl.dq_waves == 8) {
+      const int nrt8 = (s.R() + 8 * 32 - 1) / (8 * 32);
+      e = launch_kernel(K_BWD_DQ, bwd_rows<D, true, CACHE, 8>, dim3(nrt8 * a.ns, BH), dim3(512),
+                        st, a);
+    } else {
+      e = launch_kernel(K_BWD_DQ, bwd_rows<D, true, CACHE>, dim3(nrt * a.ns, BH), dim3(kNT), st,
+                        a);
+    }
+  } else {
+    e = launch_kernel(K_BWD_DQ, bwd_rows<D, true, CACHE>, dim3(nrt * a.ns, BH), dim3(kNT), st, a);
+  }
   if (e != hipSuccess) return e;
   if (a.ns > 1) {
     const size_t n4 = (size_t)BH * s.R() * (D / 4);
@@ -539,19 +558,31 @@ hipError_t run(const Shape& s, const BackwardPlan& pl, BArgs a, hipStream_t st) 
 // the CUs (the D pass runs three 4-wave blocks per CU, the dq pass two);
 // at least 8 key tiles per split.
 BackwardPlan backward_plan(const Shape& s, int dtype) {
-  BackwardPlan p{1, 1, 0, 0};
+  BackwardPlan p{1, 1, 0, 0, 4};
   const size_t BH = s.BH(), R = s.R();
   size_t bytes = align256_size(BH * R * sizeof(float));
   if (dtype == 1 && R > 0) {
     const long long blocks = (long long)((R + kRB - 1) / kRB) * (long long)BH;
     const long long ntiles = (s.Nk() + kTile - 1) / kTile;
-    auto pick = [&](long long target) {
-      long long ns = (target + blocks - 1) / blocks;
+    const long long cus = device_cus();
+    auto pick = [&](long long nb, long long target) {
+      long long ns = (target + nb - 1) / nb;
       ns = std::min(ns, std::max(1LL, ntiles / 8));
       return (int)std::max(1LL, std::min(ns, 8LL));
     };
-    p.ns_dot = pick(3 * 256);
-    p.ns_dq = pick(2 * 256);
+    p.ns_dot = pick(blocks, 3 * cus);
+    p.ns_dq = pick(blocks, 2 * cus);
+    // at d = 128 the dq pass runs 8-wave blocks (256 rows, one per CU) where
+    // their grid fills whole rounds: the waves sharing a SIMD then come from
+    // one block and keep pace at its barriers
+    if (s.d == 128) {
+      const long long blocks8 = (long long)((R + 8 * 32 - 1) / (8 * 32)) * (long long)BH;
+      const int ns8 = pick(blocks8, cus);
+      if (blocks8 * ns8 % cus == 0) {
+        p.dq_waves = 8;
+        p.ns_dq = ns8;
+      }
+    }
     // the D partials, and the summed D after them when there are several
     bytes = align256_size((size_t)(p.ns_dot + (p.ns_dot > 1)) * BH * R * sizeof(float));
     if (p.ns_dq > 1) {

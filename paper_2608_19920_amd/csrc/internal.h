@@ -251,7 +251,9 @@ hipError_t launch_sdpa_backward(const Shape& s, int dtype, const void* q, const 
 struct BackwardPlan {
   int ns_dot, ns_dq;
   size_t off_part, bytes;
+  int dq_waves;   // waves per block of the dq pass, 4 or 8
 };
+int device_cus();   // compute units of the current device (256 where none answers)
 BackwardPlan backward_plan(const Shape& s, int dtype);
 // The same gradients on bf16 MFMA (bf16 data, d = 64 or 128): a rows pass
 // for D_r, a rows pass for dq (plus the reduce of its split partials), a

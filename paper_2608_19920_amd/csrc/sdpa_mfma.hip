@@ -26,6 +26,9 @@
 // software pipeline below).
 #include "internal.h"
 
+#include <climits>
+#include <type_traits>
+
 namespace h2o {
 namespace {
 
@@ -136,13 +139,15 @@ struct Tile {
   }
 };
 
-template <int D, int NT, int N>
+// PURE: the caller knows the tile is wholly inside the cache or wholly
+// inside the chunk, and the load takes no branch.
+template <int D, int NT, bool PURE = false, int N>
 __device__ __forceinline__ void load_tile(u32x4 (&r)[N], const Tile<D, NT>& tl,
                                           const bf16_t* cache_bh, const bf16_t* fresh_bh, int j0,
                                           int M, int Nk) {
   // Tiles wholly inside the cache or wholly inside the chunk have one base row.
   const bool in_cache = j0 + BN <= M, in_chunk = j0 >= M && j0 + BN <= Nk;
-  if (in_cache || in_chunk) {
+  if (PURE || in_cache || in_chunk) {
     const char* base = reinterpret_cast<const char*>(
         in_cache ? cache_bh + (size_t)j0 * D : fresh_bh + (size_t)(j0 - M) * D);
 #pragma unroll
@@ -434,6 +439,35 @@ __device__ __forceinline__ void lse_tile_sel(int t, int t0, int t1, const f32x4 
                                   qf, m, l, qi, kc_bh, kn_bh, tp_bh, g, lane, c);
 }
 
+// Runs the tiles [ta, tb) of a loop in pieces by the kind of load they
+// issue. The tile for t loads tile min(t+3, t1-1) ahead; a tile wholly inside
+// the cache or wholly inside the chunk loads from one base row (PURE, no
+// branch), while a tile holding keys of both (it starts below M and ends
+// above it) or a ragged last tile needs the per-row choice. The tile that
+// loads the tile across M, and the last four when tile t1-1 is ragged, run
+// the general body; the rest run straight-line bodies. run(pure, a, b) runs
+// tiles [a, b), with pure a std::true_type or std::false_type.
+template <class F>
+__device__ __forceinline__ void by_load_kind(int ta, int tb, int t1, int M, int Nk, F&& run) {
+  const auto mixed = [M, Nk](int t) {
+    const int j0 = t * BN;
+    return (j0 < M && j0 + BN > M) || j0 + BN > Nk;
+  };
+  const int tm = M / BN;   // the tile across M when M is not a multiple of BN
+  const int p = (tm < t1 - 1 && mixed(tm)) ? tm - 3 : INT_MAX;
+  const int z = mixed(t1 - 1) ? t1 - 4 : INT_MAX;   // p < z
+  int a = ta;
+  const auto piece = [&](auto pure, int e) {
+    e = min(e, tb);
+    if (a < e) run(pure, a, e);
+    a = max(a, e);
+  };
+  piece(std::true_type{}, min(p, z));
+  if (a == p) piece(std::false_type{}, p + 1);
+  piece(std::true_type{}, z);
+  piece(std::false_type{}, tb);
+}
+
 // Tiles [ta, tb): two tiles per trip with the roles of the register sets
 // swapped, so no accumulator or staging register is copied; an odd last
 // tile restores the state invariant with one copy.
@@ -600,7 +634,7 @@ struct MainState {
 // cs_lds[tile parity][wave]; after the tile's barrier, threads 0..BN-1 add
 // them in wave order and store the block's partial row (one partial per
 // block and row tile).
-template <int MK, int D, int NT, int NQB>
+template <int MK, bool PURE, int D, int NT, int NQB>
 __device__ __forceinline__ void main_tile(
     int t, int t0, int t1, const f32x4 (&s_cur)[2][NQB], f32x4 (&s_nxt)[2][NQB],
     f32x4 (&oacc)[D / 16][NQB], u32x4 (&kfill)[Tile<D, NT>::N],
@@ -615,8 +649,8 @@ __device__ __forceinline__ void main_tile(
   const int j0 = t * BN;
   const int b0 = (t - t0) % NBUF, b1 = (t + 1 - t0) % NBUF, b2 = (t + 2 - t0) % NBUF;
   const int jn = min(t + 3, t1 - 1) * BN;
-  load_tile<D, NT>(kfill, tl, kc_bh, kn_bh, jn, g.M, g.Nk);
-  load_tile<D, NT>(vfill, tl, vc_bh, vn_bh, jn, g.M, g.Nk);
+  load_tile<D, NT, PURE>(kfill, tl, kc_bh, kn_bh, jn, g.M, g.Nk);
+  load_tile<D, NT, PURE>(vfill, tl, vc_bh, vn_bh, jn, g.M, g.Nk);
   if (MK >= 2) rfill = load_tp(tp_bh, jn, g.M);
   Rel rl;
   if (MK == 2) load_rel(rl, rps[b0], lane);
@@ -639,7 +673,8 @@ __device__ __forceinline__ void main_tile(
   }
 }
 
-template <int MK, int D, int NT, int NQB>
+// Tiles [ta, tb) of pass B, with the trip structure of pass A.
+template <int MK, bool PURE, int D, int NT, int NQB>
 __device__ __forceinline__ void main_loop(int ta, int tb, int t0, int t1, MainState<D, NT, NQB>& S,
                                           const Tile<D, NT>& tl,
                                           bf16_t (*Ks)[BN * kstride(D)],
@@ -652,17 +687,17 @@ __device__ __forceinline__ void main_loop(int ta, int tb, int t0, int t1, MainSt
                                           const int32_t* tp_bh, const Geo& g, int lane, float c) {
   int t = ta;
   for (; t + 1 < tb; t += 2) {
-    main_tile<MK, D, NT, NQB>(t, t0, t1, S.sa, S.sb, S.oacc, S.kb, S.vb, S.ka, S.va, S.rb, S.ra,
-                              tl, Ks, Vs, rps, qf, lam, qi, cs_lds, prow, kc_bh, kn_bh, vc_bh,
-                              vn_bh, tp_bh, g, lane, c);
-    main_tile<MK, D, NT, NQB>(t + 1, t0, t1, S.sb, S.sa, S.oacc, S.ka, S.va, S.kb, S.vb, S.ra,
-                              S.rb, tl, Ks, Vs, rps, qf, lam, qi, cs_lds, prow, kc_bh, kn_bh,
-                              vc_bh, vn_bh, tp_bh, g, lane, c);
+    main_tile<MK, PURE, D, NT, NQB>(t, t0, t1, S.sa, S.sb, S.oacc, S.kb, S.vb, S.ka, S.va, S.rb,
+                                    S.ra, tl, Ks, Vs, rps, qf, lam, qi, cs_lds, prow, kc_bh, kn_bh,
+                                    vc_bh, vn_bh, tp_bh, g, lane, c);
+    main_tile<MK, PURE, D, NT, NQB>(t + 1, t0, t1, S.sb, S.sa, S.oacc, S.ka, S.va, S.kb, S.vb,
+                                    S.ra, S.rb, tl, Ks, Vs, rps, qf, lam, qi, cs_lds, prow, kc_bh,
+                                    kn_bh, vc_bh, vn_bh, tp_bh, g, lane, c);
   }
   if (t < tb) {
-    main_tile<MK, D, NT, NQB>(t, t0, t1, S.sa, S.sb, S.oacc, S.kb, S.vb, S.ka, S.va, S.rb, S.ra,
-                              tl, Ks, Vs, rps, qf, lam, qi, cs_lds, prow, kc_bh, kn_bh, vc_bh,
-                              vn_bh, tp_bh, g, lane, c);
+    main_tile<MK, PURE, D, NT, NQB>(t, t0, t1, S.sa, S.sb, S.oacc, S.kb, S.vb, S.ka, S.va, S.rb,
+                                    S.ra, tl, Ks, Vs, rps, qf, lam, qi, cs_lds, prow, kc_bh, kn_bh,
+                                    vc_bh, vn_bh, tp_bh, g, lane, c);
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
@@ -765,10 +800,16 @@ __global__ __launch_bounds__(NW * 64) void main_pass(Geo g, int Hq, int Hkv, int
     load_tile<D, NT>(S.va, tl, vc_bh, vn_bh, j2, g.M, g.Nk);
     __syncthreads();
     scores_tile<D, NQB>(S.sa, Ks[0], qf, lane);
-    main_loop<0, D, NT, NQB>(t0, t_mask, t0, t1, S, tl, Ks, Vs, rps, qf, lam, qi, cs_lds, prow,
-                             kc_bh, kn_bh, vc_bh, vn_bh, tp_bh, g, lane, c_log2);
-    main_loop<MKM, D, NT, NQB>(t_mask, t1, t0, t1, S, tl, Ks, Vs, rps, qf, lam, qi, cs_lds,
-                               prow, kc_bh, kn_bh, vc_bh, vn_bh, tp_bh, g, lane, c_log2);
+    by_load_kind(t0, t_mask, t1, g.M, g.Nk, [&](auto pure, int a, int e) {
+      main_loop<0, decltype(pure)::value, D, NT, NQB>(a, e, t0, t1, S, tl, Ks, Vs, rps, qf, lam,
+                                                      qi, cs_lds, prow, kc_bh, kn_bh, vc_bh,
+                                                      vn_bh, tp_bh, g, lane, c_log2);
+    });
+    by_load_kind(t_mask, t1, t1, g.M, g.Nk, [&](auto pure, int a, int e) {
+      main_loop<MKM, decltype(pure)::value, D, NT, NQB>(a, e, t0, t1, S, tl, Ks, Vs, rps, qf,
+                                                        lam, qi, cs_lds, prow, kc_bh, kn_bh,
+                                                        vc_bh, vn_bh, tp_bh, g, lane, c_log2);
+    });
   }
   // write O (lane: query qb*16 + l%16, d = db*16 + 4*(l/16) + r)
 #pragma unroll

@@ -323,9 +323,11 @@ __device__ __forceinline__ int first_masked_tile(int M, int i_min) {
 // Workgroups go to the 8 XCDs round-robin in dispatch order, and each XCD
 // has its own L2. The blocks that read the same K/V tiles - one (head, key
 // split) group, all its row tiles - are given consecutive dispatch slots of
-// one XCD, so they start together there and share that L2. Grid: (nrt *
-// nsplit, BH); falls back to the plain order when the groups do not divide
-// evenly over the XCDs.
+// one XCD, so they start together there and share that L2. Within a group
+// the row tiles go last to first: in a chunk the later rows see more keys,
+// so the longest blocks start first and the short ones fill the last round.
+// Grid: (nrt * nsplit, BH); falls back to the plain order when the groups do
+// not divide evenly over the XCDs.
 constexpr int kXcds = 8;
 struct BlockId { int rt, sp, bh; };
 __device__ __forceinline__ BlockId block_id(int nsplit) {
@@ -335,10 +337,10 @@ __device__ __forceinline__ BlockId block_id(int nsplit) {
   if (ngroups % kXcds == 0) {
     const int i = lin / kXcds;
     grp = (i / nrt) * kXcds + lin % kXcds;
-    rt = i % nrt;
+    rt = nrt - 1 - i % nrt;
   } else {
     grp = lin / nrt;
-    rt = lin % nrt;
+    rt = nrt - 1 - lin % nrt;
   }
   return BlockId{rt, grp % nsplit, grp / nsplit};
 }

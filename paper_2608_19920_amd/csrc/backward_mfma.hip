@@ -211,8 +211,8 @@ __device__ __forceinline__ void store_tile(bf16_t* A, bf16_t* B,
 }
 
 // ---------------------------------------------------------------- rows passes
-// NW waves of 32 rows per block (4, or 8 for the dq pass where the plan
-// finds its grid fills whole rounds of the CUs).
+// NW waves of 32 rows per block (4, or 8 where the plan finds the pass's
+// grid fills whole rounds of the CUs).
 template <int D, bool DQ, bool CACHE, int NW = kW>
 __global__ __launch_bounds__(NW * 64) void bwd_rows(BArgs a) {
   constexpr int NT = NW * 64, RB = NW * 32;
@@ -523,8 +523,20 @@ template <int D, bool CACHE>
 hipError_t run(const Shape& s, const BackwardPlan& pl, BArgs a, hipStream_t st) {
   const int BH = s.BH(), nrt = (s.R() + kRB - 1) / kRB;
   a.ns = pl.ns_dot;
-  hipError_t e = launch_kernel(K_BWD_DOT, bwd_rows<D, false, CACHE>, dim3(nrt * a.ns, BH),
-                               dim3(kNT), st, a);
+  hipError_t e;
+  if constexpr (D == 128) {
+    if (pl.dot_waves == 8) {
+      const int nrt8 = (s.R() + 8 * 32 - 1) / (8 * 32);
+      e = launch_kernel(K_BWD_DOT, bwd_rows<D, false, CACHE, 8>, dim3(nrt8 * a.ns, BH),
+                        dim3(512), st, a);
+    } else {
+      e = launch_kernel(K_BWD_DOT, bwd_rows<D, false, CACHE>, dim3(nrt * a.ns, BH), dim3(kNT),
+                        st, a);
+    }
+  } else {
+    e = launch_kernel(K_BWD_DOT, bwd_rows<D, false, CACHE>, dim3(nrt * a.ns, BH), dim3(kNT), st,
+                      a);
+  }
   if (e != hipSuccess) return e;
   a.ns = pl.ns_dq;
   if constexpr (D == 128) {
@@ -554,11 +566,15 @@ hipError_t run(const Shape& s, const BackwardPlan& pl, BArgs a, hipStream_t st) 
 
 }  // namespace
 
+#ifndef H2O_DOT8_PER_CU
+#define H2O_DOT8_PER_CU 1
+#endif
 // Splits of the key range of the two rows passes, so that their grids fill
 // the CUs (the D pass runs three 4-wave blocks per CU, the dq pass two);
-// at least 8 key tiles per split.
+// at least 8 key tiles per split. At d = 128 either pass runs 8-wave blocks
+// (one per CU) where those fill whole rounds of the CUs.
 BackwardPlan backward_plan(const Shape& s, int dtype) {
-  BackwardPlan p{1, 1, 0, 0, 4};
+  BackwardPlan p{1, 1, 0, 0, 4, 4};
   const size_t BH = s.BH(), R = s.R();
   size_t bytes = align256_size(BH * R * sizeof(float));
   if (dtype == 1 && R > 0) {
@@ -581,6 +597,12 @@ BackwardPlan backward_plan(const Shape& s, int dtype) {
       if (blocks8 * ns8 % cus == 0) {
         p.dq_waves = 8;
         p.ns_dq = ns8;
+      }
+      // the D pass likewise (three waves per SIMD fit, so one 8-wave block per CU)
+      const int nsd8 = pick(blocks8, H2O_DOT8_PER_CU * cus);
+      if (H2O_DOT8_PER_CU > 0 && blocks8 * nsd8 % (H2O_DOT8_PER_CU * cus) == 0) {
+        p.dot_waves = 8;
+        p.ns_dot = nsd8;
       }
     }
     // the D partials, and the summed D after them when there are several

@@ -252,6 +252,7 @@ struct BackwardPlan {
   int ns_dot, ns_dq;
   size_t off_part, bytes;
   int dq_waves;   // waves per block of the dq pass, 4 or 8
+  int dot_waves;  // waves per block of the D pass, 4 or 8
 };
 int device_cus();   // compute units of the current device (256 where none answers)
 BackwardPlan backward_plan(const Shape& s, int dtype);

@@ -31,6 +31,7 @@ SHAPES = [  # B, Hq, Hkv, d, M, T, dtype
     (8, 32, 8, 64, 512, 1, "bf16"),         # one query, heavy hitters
     (1, 8, 2, 128, 1000, 128, "bf16"),
     (2, 32, 8, 128, 700, 64, "bf16"),       # 16 heads: XCD-grouped block order
+    (1, 32, 8, 128, 2048, 256, "bf16"),     # rows passes in 8-wave blocks (whole rounds)
 ]
 # bf16 shapes run on the MFMA kernels (-1) and on the VALU kernels (0);
 # float32 has only the VALU kernels
@@ -83,7 +84,8 @@ def test_backward_chunk_mode(shape, path, force):
 
 
 CACHE_SHAPES = [(1, 4, 2, 64, 256, 64, "f32"), (2, 8, 2, 128, 300, 33, "bf16"),
-                (4, 8, 4, 64, 200, 1, "bf16"), (1, 32, 8, 128, 500, 40, "bf16")]
+                (4, 8, 4, 64, 200, 1, "bf16"), (1, 32, 8, 128, 500, 40, "bf16"),
+                (1, 32, 8, 128, 2048, 256, "bf16")]   # rows passes in 8-wave blocks
 
 
 @pytest.mark.parametrize("shape,path", [(sh, p) for sh in CACHE_SHAPES

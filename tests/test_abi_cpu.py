@@ -283,12 +283,13 @@ def test_backward_workspace_bytes(L):
     assert L.h2o_backward_workspace_bytes(2, 8, 2, 16, 100, 64, 1) == 1024
     assert L.h2o_backward_workspace_bytes(2, 8, 2, 16, 100, 64, 0) == 1024
     assert L.h2o_backward_workspace_bytes(2, 8, 3, 16, 100, 64, 1) == 0
-    # B1 Hq32 Hkv8 d128 M8192 T1024: 256 row blocks of 128 rows, so the bf16
-    # rows passes split the keys, 3 ways for D (plus a plane for the sum) and
-    # 2 ways for dq (float32 partials); float32 keeps one float per row
+    # B1 Hq32 Hkv8 d128 M8192 T1024: 128 blocks of 256 rows (8-wave blocks,
+    # one per CU on 256 CUs), so both bf16 rows passes split the keys 2 ways
+    # to fill one round: the D pass's two planes plus a plane for their sum,
+    # and the dq pass's float32 partials; float32 keeps one float per row
     rows = 8 * 4096
     assert L.h2o_backward_workspace_bytes(1, 32, 8, 1024, 8192, 128, 1) == \
-        (3 + 1) * rows * 4 + 2 * rows * 128 * 4
+        (2 + 1) * rows * 4 + 2 * rows * 128 * 4
     assert L.h2o_backward_workspace_bytes(1, 32, 8, 1024, 8192, 128, 0) == rows * 4
 
 

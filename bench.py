@@ -5,8 +5,11 @@ Default workload: token generation, B=8, Hq=32, Hkv=8, d=64, M=4096, T=1,
 bf16. One bench step is one token step (h2o_chunk_step: attention, score
 accumulation, eviction and insert) for each of 8 independent layer states, so the 8 x 69 MB
 working set exceeds the 256 MB Infinity Cache and the step streams from HBM.
-The steps are captured in one HIP graph and replayed; ``value`` is algorithmic
-bytes per second (GB/s) over the timed steps.
+Consecutive token steps (each with its own query, new key and value, drawn
+for the workload's 16-step trajectory) are captured in one HIP graph, up to 16
+steps of 8 layer states, and the graph is replayed so that exactly --steps
+token steps are timed; ``value`` is algorithmic bytes per second (GB/s) over
+the timed steps.
 
 The chunked-prefill shapes (d=128: B1 Hq32 Hkv8 M8192 T1024; B4 Hq32 Hkv8
 M32768 T512; B2 Hq28 Hkv4 M16384 T2048) are timed too and reported under
@@ -106,6 +109,13 @@ def _dev_state(x, torch):
                 token_pos=to(x["token_pos"], torch.int32))
 
 
+def graph_steps(steps: int, avail: int) -> int:
+    """Token steps per captured graph: the largest divisor of the timed step
+    count that is at most 16 and at most the token steps the workload draws,
+    so that the timed region is exactly `steps` token steps."""
+    return max(g for g in range(1, min(16, avail, steps) + 1) if steps % g == 0)
+
+
 def bench_decode(args, torch, H, W):
     w = W.WORKLOADS["decode_bf16"]
     bf = torch.bfloat16
@@ -114,32 +124,41 @@ def bench_decode(args, torch, H, W):
         x = W.make_inputs(w, seed=layer)
         st = _dev_state(x, torch)
         to = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to("cuda").to(bf)
-        inp = dict(q=to(x["q_steps"][0]), k_new=to(x["k_new_steps"][0]),
-                   v_new=to(x["v_new_steps"][0]), pos0=int(x["pos0"]), scale=float(x["scale"]))
+        # the workload's token steps: each its own query, new key and value
+        inp = dict(q=[to(a) for a in x["q_steps"]], k_new=[to(a) for a in x["k_new_steps"]],
+                   v_new=[to(a) for a in x["v_new_steps"]], pos0=int(x["pos0"]),
+                   scale=float(x["scale"]))
         bufs = H.alloc_step(w.B, w.Hq, w.Hkv, w.T, w.M, w.d, bf)
         layers.append((st, inp, bufs))
     del x
+    n_avail = len(layers[0][1]["q"])
+    gsteps = graph_steps(args.steps, n_avail)
 
-    def step():
+    def step(s):
+        """Token step s (mod the drawn steps) over the layer states, in order."""
+        s %= n_avail
         for st, inp, bufs in layers:
-            H.step(st, inp["q"], inp["k_new"], inp["v_new"], bufs, inp["pos0"], inp["scale"])
+            H.step(st, inp["q"][s], inp["k_new"][s], inp["v_new"][s], bufs, inp["pos0"] + s,
+                   inp["scale"])
 
     stream = torch.cuda.Stream()
     torch.cuda.synchronize()
     with torch.cuda.stream(stream):
-        step()                                   # eager warm-up on the capture stream
+        for s in range(args.warmup):             # eager warm-up on the capture stream
+            step(s)
     torch.cuda.synchronize()
+    # `gsteps` consecutive token steps x LAYERS layer states in one graph
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph, stream=stream):
-        step()
+        for s in range(gsteps):
+            step(s)
     torch.cuda.synchronize()
-    for _ in range(args.warmup):
-        graph.replay()
+    graph.replay()                               # untimed: the graph's first launch
     torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t_wall = time.perf_counter()
     e0.record()
-    for _ in range(args.steps):
+    for _ in range(args.steps // gsteps):
         graph.replay()
     e1.record()
     torch.cuda.synchronize()
@@ -149,8 +168,8 @@ def bench_decode(args, torch, H, W):
     # Per-kernel durations: the same steps once more, eager, with the library
     # bracketing each of its launches by events on the launch stream.
     H.h2o_debug_timing(True)
-    for _ in range(args.steps):
-        step()
+    for s in range(args.steps):
+        step(s)
     torch.cuda.synchronize()
     ktimes = {k: H.h2o_debug_kernel_time(k) for k in ("decode_split", "decode_finish")}
     H.h2o_debug_timing(False)
@@ -163,7 +182,7 @@ def bench_decode(args, torch, H, W):
     hot = torch.cuda.CUDAGraph()
     with torch.cuda.graph(hot, stream=stream):
         for _ in range(LAYERS):
-            H.step(st0, inp0["q"], inp0["k_new"], inp0["v_new"], bufs0, inp0["pos0"],
+            H.step(st0, inp0["q"][0], inp0["k_new"][0], inp0["v_new"][0], bufs0, inp0["pos0"],
                    inp0["scale"])
     torch.cuda.synchronize()
     for _ in range(args.warmup):
@@ -192,7 +211,7 @@ def bench_decode(args, torch, H, W):
                       "own begin and end) on the launch stream, over an eager pass of the "
                       "timed steps"}
     return dict(w=w, ms_step=ms_step, value=gbs, roofline=roof, wall_s=t_wall,
-                step_bytes=step_bytes, hot_mall=hot_mall)
+                step_bytes=step_bytes, hot_mall=hot_mall, graph_steps=gsteps)
 
 
 def bench_prefill(name, args, torch, H, W):
@@ -441,7 +460,8 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": f"decode_bf16 token step over {LAYERS} layer states "
-                               f"(hipGraph replay)", "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv,
+                               f"(hipGraphs of {dec['graph_steps']} token steps, replayed)",
+                   "B": w.B, "Hq": w.Hq, "Hkv": w.Hkv,
                    "d": w.d, "M": w.M, "T": w.T, "layers": LAYERS,
                    "bytes_per_step": dec["step_bytes"],
                    "frac_of_hbm_peak": round(dec["value"] / HBM_PEAK_GBS, 4)},

@@ -271,9 +271,9 @@ def insert_first_step_bytes(w) -> int:
 
 
 def bench_insert_first(args, torch, H, W):
-    """h2o_chunk_step_insert_first on the decode workload (8 layer states, one
-    HIP graph) and h2o_sdpa_cache / the whole insert-first step on the
-    prefill workloads."""
+    """h2o_chunk_step_insert_first on the decode workload (8 layer states,
+    consecutive token steps in one HIP graph, as in bench_decode) and
+    h2o_sdpa_cache / the whole insert-first step on the prefill workloads."""
     bf = torch.bfloat16
     w = W.WORKLOADS["decode_bf16"]
     layers = []
@@ -281,32 +281,38 @@ def bench_insert_first(args, torch, H, W):
         x = W.make_inputs(w, seed=layer)
         st = _dev_state(x, torch)
         to = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to("cuda").to(bf)
-        inp = (to(x["q_steps"][0]), to(x["k_new_steps"][0]), to(x["v_new_steps"][0]),
-               int(x["pos0"]), float(x["scale"]))
+        inp = ([to(a) for a in x["q_steps"]], [to(a) for a in x["k_new_steps"]],
+               [to(a) for a in x["v_new_steps"]], int(x["pos0"]), float(x["scale"]))
         layers.append((st, inp, H.alloc_step(w.B, w.Hq, w.Hkv, w.T, w.M, w.d, bf,
                                              insert_first=True)))
     del x
+    n_avail = len(layers[0][1][0])
+    gsteps = graph_steps(args.steps, n_avail)
 
-    def step():
+    def step(s):
+        s %= n_avail
         for st, (q, kn, vn, pos0, scale), b in layers:
-            H.h2o_chunk_step_insert_first(q, st["k_cache"], st["v_cache"], st["scores"],
-                                          st["token_pos"], kn, vn, b["out"], b["lse"], b["wsum"],
-                                          b["evict_idx"], b["workspace"], pos0, scale)
+            H.h2o_chunk_step_insert_first(q[s], st["k_cache"], st["v_cache"], st["scores"],
+                                          st["token_pos"], kn[s], vn[s], b["out"], b["lse"],
+                                          b["wsum"], b["evict_idx"], b["workspace"], pos0 + s,
+                                          scale)
 
     stream = torch.cuda.Stream()
     torch.cuda.synchronize()
     with torch.cuda.stream(stream):
-        step()
+        for s in range(args.warmup):
+            step(s)
     torch.cuda.synchronize()
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph, stream=stream):
-        step()
+        for s in range(gsteps):
+            step(s)
     torch.cuda.synchronize()
-    for _ in range(args.warmup):
-        graph.replay()
+    graph.replay()
+    torch.cuda.synchronize()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
-    for _ in range(args.steps):
+    for _ in range(args.steps // gsteps):
         graph.replay()
     e1.record()
     torch.cuda.synchronize()

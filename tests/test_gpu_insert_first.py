@@ -135,7 +135,8 @@ def test_step_insert_first(shape, policy):
     np.testing.assert_allclose(g[2].sum(-1), T * (Hq // Hkv), rtol=2e-3)
 
 
-@pytest.mark.parametrize("name,nheads", [("prefill_bf16", 2), ("decode_bf16", 3)])
+@pytest.mark.parametrize("name,nheads", [("prefill_bf16", 2), ("longcache_bf16", 1),
+                                         ("gqa7_bf16", 1), ("decode_bf16", 3)])
 def test_full_size_insert_first_sampled_heads(name, nheads):
     """The insert-first step at a full workload size; the oracle recomputes a
     sample of (b, kv-head) pairs."""

@@ -184,12 +184,13 @@ def test_backward_random_shapes(shape):
     _grads_check("bf16", [U.to_np(g) for g in grads], ref, names)
 
 
-def test_backward_full_size_sampled_head():
-    """The backward at the 1024-token prefill size (B1 Hq32 Hkv8 d128 M8192
-    T1024, bf16) in the launch configuration the benchmark times; the oracle
-    recomputes the gradients of one KV head (its group's query heads and its
-    keys) from that head's slice of the inputs."""
-    wl = W.WORKLOADS["prefill_bf16"]
+@pytest.mark.parametrize("name,b,h", [("prefill_bf16", 0, 5), ("longcache_bf16", 2, 3)])
+def test_backward_full_size_sampled_head(name, b, h):
+    """The backward at a full prefill size (the 1024-token shape the benchmark
+    times, and the long cache) in the launch configuration of that size; the
+    oracle recomputes the gradients of one KV head of one batch entry (its
+    group's query heads and its keys) from that slice of the inputs."""
+    wl = W.WORKLOADS[name]
     say(f"backward, full size {wl.describe()}")
     x = W.make_inputs(wl, seed=1)
     tdt = torch.bfloat16
@@ -198,23 +199,23 @@ def test_backward_full_size_sampled_head():
     do_np = W.bf16_bits_to_f32(W.f32_to_bf16_bits(
         np.random.default_rng(11).standard_normal(x["q"].shape).astype(np.float32)))
     dout = U.to_dev(do_np, tdt)
-    b = H.alloc_step(wl.B, wl.Hq, wl.Hkv, wl.T, wl.M, wl.d, tdt)
+    bufs = H.alloc_step(wl.B, wl.Hq, wl.Hkv, wl.T, wl.M, wl.d, tdt)
     scale = float(x["scale"])
-    H.h2o_sdpa_chunk(q, kc, vc, kn, vn, b["out"], b["lse"], b["wsum"], b["workspace"], scale)
+    H.h2o_sdpa_chunk(q, kc, vc, kn, vn, bufs["out"], bufs["lse"], bufs["wsum"], bufs["workspace"],
+                     scale)
     grads = [torch.empty_like(t) for t in (q, kc, vc, kn, vn)]
     ws = torch.empty(H.h2o_backward_workspace_bytes(wl.B, wl.Hq, wl.Hkv, wl.T, wl.M, wl.d, tdt),
                      dtype=torch.uint8, device=U.DEV)
-    H.h2o_sdpa_chunk_backward(q, kc, vc, kn, vn, b["lse"], dout, *grads, ws, scale)
+    H.h2o_sdpa_chunk_backward(q, kc, vc, kn, vn, bufs["lse"], dout, *grads, ws, scale)
     torch.cuda.synchronize()
     got = [U.to_np(g) for g in grads]
     for g in got:
         assert np.isfinite(g).all()
-    G, h = wl.G, 5
-    qs = slice(h * G, (h + 1) * G)
-    ref = oracle.sdpa_chunk_backward(x["q"][:, qs], x["k_cache"][:, h:h + 1],
-                                     x["v_cache"][:, h:h + 1], x["k_new"][:, h:h + 1],
-                                     x["v_new"][:, h:h + 1], do_np[:, qs], scale)
-    sel = [got[0][:, qs]] + [g[:, h:h + 1] for g in got[1:]]
+    G = wl.G
+    qs, bs, hs = slice(h * G, (h + 1) * G), slice(b, b + 1), slice(h, h + 1)
+    ref = oracle.sdpa_chunk_backward(x["q"][bs, qs], x["k_cache"][bs, hs], x["v_cache"][bs, hs],
+                                     x["k_new"][bs, hs], x["v_new"][bs, hs], do_np[bs, qs], scale)
+    sel = [got[0][bs, qs]] + [g[bs, hs] for g in got[1:]]
     _grads_check("bf16", sel, ref, ("dq", "dk_cache", "dv_cache", "dk_new", "dv_new"))
 
 

@@ -658,9 +658,10 @@ __global__ __launch_bounds__(kCombThreads) void decode_combine(
 // scores of the first pass of slots, 16 bytes per load, the split
 // statistics and O-partials, the query and the chunk's key and value rows)
 // is requested before the first value is used; slot groups past the cache
-// do no arithmetic; and the slots of the last pass (the only pass at the
-// decode shapes) are stored only after the slot is chosen, so that the
-// chosen slot's score is written once, with its new value.
+// do no arithmetic; and of the last pass (the only pass at the decode
+// shapes) the summed weights are stored before the block's argmin, the
+// scores only after the slot is chosen, so that the chosen slot's score is
+// written once, with its new value.
 constexpr int kFinThreads = 1024;
 constexpr int kFinVec = 4;                          // consecutive slots per thread and pass
 constexpr int kFinPass = kFinThreads * kFinVec;     // slots per pass
@@ -762,6 +763,14 @@ __global__ __launch_bounds__(kFinThreads) void decode_finish(
     base += kFinPass;
     load_pass(base);
   }
+  {
+    // the last pass's summed weights do not wait for the choice: stored
+    // before the block's argmin, they drain while it runs
+    const int j0 = base + kFinVec * tid;
+#pragma unroll
+    for (int r = 0; r < kFinVec; ++r)
+      if (j0 + r < M) w[j0 + r] = wv[r];
+  }
   wave_argmin(bk, bj);
   if (lane == 0) { red_k[wave] = bk; red_j[wave] = bj; }
   __syncthreads();
@@ -774,9 +783,6 @@ __global__ __launch_bounds__(kFinThreads) void decode_finish(
   const float wnew = chunk_weight(hs, G);
   {
     const int j0 = base + kFinVec * tid;
-#pragma unroll
-    for (int r = 0; r < kFinVec; ++r)
-      if (j0 + r < M) w[j0 + r] = wv[r];
 #pragma unroll
     for (int r = 0; r < kFinVec; ++r)
       if (j0 + r == slot) sa[r] = wnew;

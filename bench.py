@@ -389,6 +389,45 @@ def bench_backward(args, torch, H, W):
 
 
 # -------------------------------------------------------------- CPU baseline
+def bench_variants(args, torch, H, W):
+    """Eviction and insert under the paper's three score rankings (Sec.
+    "Variants of Heavy-Hitter Oracle"): h2o_evict_insert_policy with
+    h2o, h2o_norm (score over age) and h2o_orig (score summed over the batch,
+    one slot set per KV head) on the chunked-prefill shapes, interleaved,
+    median of PREFILL_REPS after PREFILL_WARMUP rounds. Each call evicts and
+    inserts for real; the position advances by T per call so that every
+    slot's age stays positive."""
+    bf = torch.bfloat16
+    out = []
+    for name in PREFILL:
+        w = W.WORKLOADS[name]
+        x = W.make_inputs(w, seed=0)
+        st = _dev_state(x, torch)
+        to = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to("cuda").to(bf)
+        kn, vn = to(x["k_new"]), to(x["v_new"])
+        pos = [int(x["pos0"])]
+        del x
+        bufs = H.alloc_step(w.B, w.Hq, w.Hkv, w.T, w.M, w.d, bf)
+        bufs["wsum"].uniform_(0.0, 1.0)
+        fns = {}
+        for policy in ("h2o", "h2o_norm", "h2o_orig"):
+            ws = torch.empty(max(H.h2o_evict_workspace_bytes(w.B, w.Hkv, w.M, w.T, policy), 16),
+                             dtype=torch.uint8, device="cuda")
+
+            def fn(policy=policy, ws=ws):
+                H.h2o_evict_insert_policy(st["k_cache"], st["v_cache"], st["scores"],
+                                          st["token_pos"], kn, vn, bufs["wsum"],
+                                          bufs["evict_idx"], pos[0], policy, ws)
+                pos[0] += w.T
+            fns[policy] = fn
+        med = interleaved_median_ms(fns, PREFILL_REPS, PREFILL_WARMUP, torch)
+        out.append({"workload": w.describe(), "k": w.T,
+                    "us": {k: round(v * 1e3, 1) for k, v in med.items()}})
+        del st, kn, vn, bufs
+        torch.cuda.empty_cache()
+    return out
+
+
 def cpu_baseline(w, budget_s, W):
     import oracle
     try:
@@ -449,6 +488,11 @@ def main():
         ins = bench_insert_first(args, torch, H, W)
         print(f"# insert-first decode: {ins['decode']['gbs']} GB/s; prefill "
               f"{[r['tflops'] for r in ins['prefill']]} TFLOP/s", file=sys.stderr, flush=True)
+    variants = None
+    if not args.no_prefill:
+        variants = bench_variants(args, torch, H, W)
+        print(f"# evict+insert by policy (us): {[v['us'] for v in variants]}", file=sys.stderr,
+              flush=True)
     bwd = None
     if not args.no_prefill:
         bwd = bench_backward(args, torch, H, W)
@@ -476,6 +520,7 @@ def main():
         "cpu_baseline": cpu,
         "prefill": prefill,
         "insert_first": ins,
+        "variants": variants,
         "backward": bwd,
     }
     print(json.dumps(rec))

@@ -227,9 +227,11 @@ __global__ __launch_bounds__(NW * 64) void bwd_rows(BArgs a) {
   const size_t bh = bhi;
   const int b = bhi / a.Hkv, h = bhi % a.Hkv;
   // x = split * (row tiles) + row tile: the blocks of one key range are
-  // consecutive, so they share their K/V tiles in one L2
+  // consecutive, so they share their K/V tiles in one L2; the row tiles go
+  // last to first (later chunk rows see more keys: the longest blocks start
+  // first and the shortest fill the last partial round)
   const int nrt = (a.R + RB - 1) / RB;
-  const int sp = xb / nrt, rblk = (xb % nrt) * RB, wrow0 = rblk + wave * 32;
+  const int sp = xb / nrt, rblk = (nrt - 1 - xb % nrt) * RB, wrow0 = rblk + wave * 32;
   const bool live = wrow0 < a.R;
   const int imin = wrow0 / a.G;
 
